@@ -1,0 +1,218 @@
+"""ctypes front end of the CPU oracle (smallkv_oracle.c).
+
+TEST INFRASTRUCTURE ONLY: imported by tests/, by ``__graft_entry__.smoke()``
+and by the CPU-baseline leg of ``bench.py``; the product path never imports
+it.  It shares nothing with the HIP library or its binding.
+
+Every array goes in as a contiguous numpy array (float32 for inputs that the
+device holds as bf16 or fp32 -- bf16 widens to fp32 exactly -- int32 for
+indices) and comes out as numpy arrays; floating-point outputs other than
+the fp32 logits are float64.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import subprocess
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+SRC = os.path.join(HERE, "smallkv_oracle.c")
+LIB = os.path.join(HERE, "libsmallkv_oracle.so")
+
+NORM_REMAINING, NORM_NONE, NORM_SLM_CRIT, NORM_RETAINED, NORM_MARG_FILL = range(5)
+MODES = (NORM_REMAINING, NORM_NONE, NORM_SLM_CRIT, NORM_RETAINED, NORM_MARG_FILL)
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (no fast-math, no fp contraction)."""
+    if force or not os.path.exists(LIB):
+        tmp = LIB + ".tmp"
+        subprocess.check_call([
+            "gcc", "-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math",
+            "-Wall", "-Wextra", "-fPIC", "-shared", SRC, "-o", tmp, "-lm"])
+        os.replace(tmp, LIB)
+    return LIB
+
+
+_lib = None
+_F = C.POINTER(C.c_float)
+_D = C.POINTER(C.c_double)
+_I = C.POINTER(C.c_int32)
+
+
+class StepIn(C.Structure):
+    _fields_ = [
+        ("batch", C.c_int32), ("n_cap", C.c_int32), ("kc_cap", C.c_int32), ("km_cap", C.c_int32),
+        ("seq_len", _I), ("k_crit", _I), ("k_marg", _I),
+        ("s_layers", C.c_int32), ("s_q_heads", C.c_int32), ("s_kv_heads", C.c_int32), ("s_dim", C.c_int32),
+        ("s_scale", C.c_float),
+        ("s_q", _F), ("s_k", _F), ("s_v", _F),
+        ("l_layers", C.c_int32), ("l_q_heads", C.c_int32), ("l_kv_heads", C.c_int32), ("l_dim", C.c_int32),
+        ("l_scale", C.c_float),
+        ("l_rows", C.c_int64),
+        ("l_q", _F), ("l_k", _F), ("l_v", _F),
+        ("k_slot", _I), ("v_slot", _I),
+        ("head_map", _I),
+        ("mode", C.c_int32),
+    ]
+
+
+class StepOut(C.Structure):
+    _fields_ = [
+        ("logits", _F),
+        ("row_max", _D), ("row_sum", _D), ("small_out", _D),
+        ("crit", _I), ("marg", _I),
+        ("marg_prob", _D), ("mass", _D), ("large_out", _D),
+    ]
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB) or os.path.getmtime(LIB) < os.path.getmtime(SRC):
+            build()
+        L = C.CDLL(LIB)
+        L.orc_logit.argtypes = [C.c_int, C.c_float, _F, _F]
+        L.orc_logit.restype = C.c_float
+        L.orc_key.argtypes = [C.c_float]
+        L.orc_key.restype = C.c_uint32
+        L.orc_small_head.argtypes = [C.c_int, C.c_int, C.c_float, _F, _F, _F, _F, _D, _D, _D]
+        L.orc_partition.argtypes = [C.c_int, C.c_int, C.c_int, _F, C.c_double, C.c_double,
+                                    _I, C.c_int, _I, _D, C.c_int, _D, C.POINTER(C.c_int),
+                                    C.POINTER(C.c_int)]
+        L.orc_hybrid_head.argtypes = [C.c_int, C.c_float, _F, _F, _F, _I, _I, C.c_int, _I,
+                                      C.c_int, _I, _D, _D, C.c_int, _D]
+        L.orc_step.argtypes = [C.POINTER(StepIn), C.POINTER(StepOut)]
+        for f in (L.orc_small_head, L.orc_partition, L.orc_hybrid_head, L.orc_step):
+            f.restype = C.c_int
+        _lib = L
+    return _lib
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+def _f32(a):
+    return np.ascontiguousarray(a, dtype=np.float32)
+
+
+def _i32(a):
+    return np.ascontiguousarray(a, dtype=np.int32)
+
+
+def _p(a, t):
+    return a.ctypes.data_as(t)
+
+
+def _check(rc, what):
+    if rc != 0:
+        raise OracleError(f"{what} returned {rc}")
+
+
+def logit(q, k, scale) -> np.float32:
+    q, k = _f32(q), _f32(k)
+    return np.float32(lib().orc_logit(q.size, C.c_float(scale), _p(q, _F), _p(k, _F)))
+
+
+def key(s) -> int:
+    return int(lib().orc_key(C.c_float(s)))
+
+
+def small_head(q, K, V, scale):
+    """Stage 1 for one small query head. Returns (logits f32[n], m, Z, O f64[d])."""
+    q, K, V = _f32(q), _f32(K), _f32(V)
+    n, d = K.shape
+    logits = np.empty(n, np.float32)
+    m, Z = C.c_double(), C.c_double()
+    O = np.empty(d, np.float64)
+    _check(lib().orc_small_head(n, d, C.c_float(scale), _p(q, _F), _p(K, _F), _p(V, _F),
+                                _p(logits, _F), C.byref(m), C.byref(Z), _p(O, _D)), "orc_small_head")
+    return logits, m.value, Z.value, O
+
+
+def partition(logits, k_crit, k_marg, m, Z, kc_cap=None, km_cap=None):
+    """Stage 2 for one small head. Returns (crit, marg, marg_prob, mass) with -1 padding."""
+    logits = _f32(logits)
+    n = logits.size
+    nc_ = min(k_crit, n)
+    nm_ = max(0, min(k_marg, n - nc_))
+    kc_cap = nc_ if kc_cap is None else kc_cap
+    km_cap = nm_ if km_cap is None else km_cap
+    crit = np.empty(max(kc_cap, 1), np.int32)
+    marg = np.empty(max(km_cap, 1), np.int32)
+    mp = np.empty(max(km_cap, 1), np.float64)
+    mass = np.empty(2, np.float64)
+    nc, nm = C.c_int(), C.c_int()
+    _check(lib().orc_partition(n, k_crit, k_marg, _p(logits, _F), m, Z, _p(crit, _I), kc_cap,
+                               _p(marg, _I), _p(mp, _D), km_cap, _p(mass, _D), C.byref(nc),
+                               C.byref(nm)), "orc_partition")
+    return crit[:kc_cap], marg[:km_cap], mp[:km_cap], mass
+
+
+def hybrid_head(q, K, V, crit, marg, marg_prob, mass, scale, mode=NORM_REMAINING,
+                k_slot=None, v_slot=None):
+    """Stage 3 for one large query head (crit/marg may carry -1 padding)."""
+    q, K, V = _f32(q), _f32(K), _f32(V)
+    crit = _i32(np.asarray(crit)[np.asarray(crit) >= 0])
+    marg = np.asarray(marg)
+    keep = marg >= 0
+    marg = _i32(marg[keep])
+    mp = np.ascontiguousarray(np.asarray(marg_prob, np.float64)[keep])
+    mass = np.ascontiguousarray(mass, np.float64)
+    d = q.size
+    O = np.empty(d, np.float64)
+    ks = _i32(k_slot) if k_slot is not None else None
+    vs = _i32(v_slot) if v_slot is not None else None
+    _check(lib().orc_hybrid_head(d, C.c_float(scale), _p(q, _F), _p(K, _F), _p(V, _F),
+                                 _p(ks, _I) if ks is not None else None,
+                                 _p(vs, _I) if vs is not None else None,
+                                 crit.size, _p(crit, _I), marg.size,
+                                 _p(marg, _I) if marg.size else None,
+                                 _p(mp, _D) if marg.size else None, _p(mass, _D), int(mode),
+                                 _p(O, _D)), "orc_hybrid_head")
+    return O
+
+
+def step(*, seq_len, k_crit, k_marg, kc_cap, km_cap, head_map, mode,
+         s_q, s_k, s_v, s_scale, l_q, l_k, l_v, l_scale, k_slot=None, v_slot=None):
+    """A whole decode step over the library layout (see smallkv_oracle.h).
+
+    Shapes: s_q [B,l,Hqs,ds], s_k/s_v [B,l,Hks,n_cap,ds], l_q [B,L,Hq,d],
+    l_k/l_v [B,L,Hk,n_rows,d], slots [B,L,Hk,n_cap] or None.
+    """
+    s_q, s_k, s_v, l_q, l_k, l_v = map(_f32, (s_q, s_k, s_v, l_q, l_k, l_v))
+    seq_len, k_crit, k_marg, head_map = map(_i32, (seq_len, k_crit, k_marg, head_map))
+    B, l, hqs, ds = s_q.shape
+    hks, ncap = s_k.shape[2], s_k.shape[3]
+    _, L, hq, d = l_q.shape
+    hk, nrows = l_k.shape[2], l_k.shape[3]
+    ks = _i32(k_slot) if k_slot is not None else None
+    vs = _i32(v_slot) if v_slot is not None else None
+    nsh = l * hqs
+    out = dict(
+        logits=np.zeros((B, nsh, ncap), np.float32),
+        row_max=np.empty((B, nsh)), row_sum=np.empty((B, nsh)),
+        small_out=np.empty((B, l, hqs, ds)),
+        crit=np.empty((B, nsh, max(kc_cap, 1)), np.int32),
+        marg=np.empty((B, nsh, max(km_cap, 1)), np.int32),
+        marg_prob=np.empty((B, nsh, max(km_cap, 1))),
+        mass=np.empty((B, nsh, 2)),
+        large_out=np.empty((B, L, hq, d)),
+    )
+    si = StepIn(B, ncap, kc_cap, km_cap, _p(seq_len, _I), _p(k_crit, _I), _p(k_marg, _I),
+                l, hqs, hks, ds, s_scale, _p(s_q, _F), _p(s_k, _F), _p(s_v, _F),
+                L, hq, hk, d, l_scale, nrows, _p(l_q, _F), _p(l_k, _F), _p(l_v, _F),
+                _p(ks, _I) if ks is not None else None,
+                _p(vs, _I) if vs is not None else None,
+                _p(head_map, _I), int(mode))
+    so = StepOut(_p(out["logits"], _F), _p(out["row_max"], _D), _p(out["row_sum"], _D),
+                 _p(out["small_out"], _D), _p(out["crit"], _I), _p(out["marg"], _I),
+                 _p(out["marg_prob"], _D), _p(out["mass"], _D), _p(out["large_out"], _D))
+    _check(lib().orc_step(C.byref(si), C.byref(so)), "orc_step")
+    out["crit"] = out["crit"][..., :kc_cap]
+    out["marg"] = out["marg"][..., :km_cap]
+    out["marg_prob"] = out["marg_prob"][..., :km_cap]
+    return out

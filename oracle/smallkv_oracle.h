@@ -1,0 +1,133 @@
+/*
+ * smallkv_oracle.h -- plain, slow, single-threaded CPU oracle of SmallKV's
+ * per-decode-step compensated attention (arXiv 2508.02751).
+ *
+ * TEST INFRASTRUCTURE ONLY.  The oracle is what the GPU library is checked
+ * against.  It is linked or called only by the test suite, by the package's
+ * smoke check and by the CPU-baseline leg of the benchmark; the product path
+ * never reaches it.  It shares no source, header, table or helper with the
+ * HIP library under paper_2508_02751_amd/csrc.
+ *
+ * Precision: the ranking key (a small-model logit) is an fp32 value with one
+ * defined evaluation order (see orc_logit); everything else is fp64.
+ *
+ * Paper passages followed:
+ *   - Method section, "Similarity Matching": attention rows A = softmax(QK^T/sqrt(d_h)),
+ *     accumulative score F (Eq. 1) and the head map f(i) (Eq. 3);
+ *   - "Saliency Shift Compensation": eviction keeps the top-scored tokens (Eq. 4)
+ *     and selection is made from the small model's full cache;
+ *   - "Marginal Information Compensation": the compensated row A* (Eq. 6), with
+ *     K critical tokens and P-K marginal tokens;
+ *   - Algorithm 1 (decode branch) and the implementation pseudocode of
+ *     Appendix D: critical output by exact attention over the selected keys,
+ *     marginal output by small-model probabilities times the large model's V,
+ *     summed.
+ */
+#ifndef SMALLKV_ORACLE_H
+#define SMALLKV_ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  ORC_OK = 0,
+  ORC_EINVAL = -1,     /* bad sizes / budgets / missing slot */
+  ORC_ENONFINITE = -2  /* a non-finite logit or input value */
+};
+
+/* Weighting of the two parts of the compensated row (alpha_C, alpha_M).
+ * S'_C and S'_M are the small model's probability mass on the critical and
+ * marginal sets. */
+enum {
+  ORC_NORM_REMAINING = 0, /* alpha_C = 1 - S'_M, alpha_M = 1 (default)          */
+  ORC_NORM_NONE = 1,      /* alpha_C = 1,       alpha_M = 1 (O_c + O_m literal) */
+  ORC_NORM_SLM_CRIT = 2,  /* alpha_C = S'_C,    alpha_M = 1 (Eq. 6, SLM mass)   */
+  ORC_NORM_RETAINED = 3,  /* alpha_C = S'_C/(S'_C+S'_M), alpha_M = 1/(S'_C+S'_M) */
+  ORC_NORM_MARG_FILL = 4  /* alpha_C = S'_C, alpha_M = (1-S'_C)/S'_M (0 if S'_M=0) */
+};
+
+/* The ranking key of one token for one small-model query head: an fp32
+ * logit computed as a sequential fp32 fused multiply-add chain over the head
+ * dimension, starting from +0, followed by one fp32 multiplication by
+ * `scale`; a zero result is returned as +0. */
+float orc_logit(int d, float scale, const float *q, const float *k);
+
+/* Order-preserving map of an fp32 logit to uint32 (larger key = larger
+ * logit); -0 and +0 map to the same key. */
+uint32_t orc_key(float s);
+
+/* Stage 1 for one small-model query head: logits[t] for t < n (fp32 keys),
+ * row max m, partition function Z = sum_t exp(s_t - m) and output
+ * O = sum_t p_t V_t with p_t = exp(s_t - m) / Z, all fp64.
+ * K and V are [n][d] row-major.  Returns ORC_ENONFINITE on a non-finite logit. */
+int orc_small_head(int n, int d, float scale, const float *q, const float *K,
+                   const float *V, float *logits, double *m, double *Z,
+                   double *O);
+
+/* Stage 2 for one small head: tokens ordered by (logit descending, index
+ * ascending); the first nc = min(k_crit, n) are critical, the next
+ * nm = min(k_marg, n - nc) are marginal, the rest evicted.  Both lists are
+ * emitted in ascending token order and padded with -1 up to kc_cap / km_cap.
+ * marg_prob[i] = exp(s - m)/Z for marg[i] (0 in padding); mass[0] = S'_C,
+ * mass[1] = S'_M.  Requires k_crit >= 1, k_marg >= 0, kc_cap >= nc,
+ * km_cap >= nm. */
+int orc_partition(int n, int k_crit, int k_marg, const float *logits, double m,
+                  double Z, int32_t *crit, int kc_cap, int32_t *marg,
+                  double *marg_prob, int km_cap, double *mass, int *n_crit,
+                  int *n_marg);
+
+/* Stage 3 for one large-model query head.  K, V are [n_rows][d]; token t's
+ * K row is k_slot[t] (t when k_slot is NULL), its V row v_slot[t].
+ *   s_t  = scale * <q, K_t>              for t in crit (fp64)
+ *   O_c  = sum_C exp(s_t - max s) V_t / sum_C exp(s_t - max s)
+ *   O_m  = sum_M marg_prob_t V_t
+ *   O    = alpha_C * O_c + alpha_M * O_m   (alphas from `mode`, mass)  */
+int orc_hybrid_head(int d, float scale, const float *q, const float *K,
+                    const float *V, const int32_t *k_slot,
+                    const int32_t *v_slot, int n_crit, const int32_t *crit,
+                    int n_marg, const int32_t *marg, const double *marg_prob,
+                    const double *mass, int mode, double *O);
+
+/* One whole decode step over the library's tensor layout (host arrays,
+ * bf16 inputs widened exactly to fp32 by the caller).
+ *   small q  [B][l][Hq_s][d_s]         small K,V [B][l][Hkv_s][n_cap][d_s]
+ *   large q  [B][L][Hq][d]             large K,V [B][L][Hkv][n_rows][d]
+ *   k_slot, v_slot [B][L][Hkv][n_cap] or NULL
+ *   head_map [L*Hq] -> small head id j = layer*Hq_s + head
+ * Outputs: logits [B][l*Hq_s][n_cap] (entries t >= seq_len untouched),
+ *   row_max, row_sum [B][l*Hq_s], small_out [B][l][Hq_s][d_s],
+ *   crit [B][l*Hq_s][kc_cap], marg/marg_prob [B][l*Hq_s][km_cap],
+ *   mass [B][l*Hq_s][2], large_out [B][L][Hq][d]. */
+typedef struct {
+  int32_t batch, n_cap, kc_cap, km_cap;
+  const int32_t *seq_len, *k_crit, *k_marg;
+  /* small model */
+  int32_t s_layers, s_q_heads, s_kv_heads, s_dim;
+  float s_scale;
+  const float *s_q, *s_k, *s_v;
+  /* large model */
+  int32_t l_layers, l_q_heads, l_kv_heads, l_dim;
+  float l_scale;
+  int64_t l_rows;
+  const float *l_q, *l_k, *l_v;
+  const int32_t *k_slot, *v_slot;
+  const int32_t *head_map;
+  int32_t mode;
+} orc_step_in;
+
+typedef struct {
+  float *logits;
+  double *row_max, *row_sum, *small_out;
+  int32_t *crit, *marg;
+  double *marg_prob, *mass, *large_out;
+} orc_step_out;
+
+int orc_step(const orc_step_in *in, const orc_step_out *out);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SMALLKV_ORACLE_H */

@@ -1,0 +1,394 @@
+"""Pins of the CPU oracle against facts fixed outside the oracle itself.
+
+Each test checks one oracle function against something it does not compute
+the same way: exact rational arithmetic with IEEE-754 binary32 rounding,
+O(N^2) rank counting, exhaustive enumeration of subsets, a textbook numpy
+attention in float64, closed forms of the compensated row in special cases,
+and invariants the method states (three disjoint token classes with the
+budgeted sizes, Top(P-K) following TopK in one order, full attention when
+every token is critical).
+"""
+import itertools
+import math
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import oracle as O
+
+SCALE128 = float(np.float32(1.0 / math.sqrt(128.0)))
+
+
+# ------------------------------------------------------------ helpers --
+
+def round_binary32(x: Fraction) -> Fraction:
+    """Round a rational to the nearest IEEE-754 binary32 value, ties to even."""
+    if x == 0:
+        return Fraction(0)
+    sign = -1 if x < 0 else 1
+    a = abs(x)
+    e = a.numerator.bit_length() - a.denominator.bit_length()
+    if Fraction(2) ** e > a:
+        e -= 1
+    q = Fraction(2) ** max(e - 23, -149)
+    m = a / q
+    n = m.numerator // m.denominator
+    rem = m - n
+    if rem > Fraction(1, 2) or (rem == Fraction(1, 2) and n % 2 == 1):
+        n += 1
+    r = n * q
+    assert r < Fraction(2) ** 128, "overflow not expected in these tests"
+    return sign * r
+
+
+def textbook_attention(q, K, V, scale):
+    """softmax(scale * q K^T) V in float64 (independent of the oracle)."""
+    s = scale * (K.astype(np.float64) @ q.astype(np.float64))
+    p = np.exp(s - s.max())
+    p /= p.sum()
+    return p @ V.astype(np.float64), p
+
+
+def rank_bruteforce(logits):
+    """rank_t = #{v : s_v > s_t or (s_v == s_t and v < t)}  (O(N^2))."""
+    s = [float(x) for x in logits]
+    n = len(s)
+    return [sum(1 for v in range(n) if s[v] > s[t] or (s[v] == s[t] and v < t))
+            for t in range(n)]
+
+
+def small_row(rng, n, d, ties=False, scale=0.125):
+    q = rng.standard_normal(d).astype(np.float32)
+    K = rng.standard_normal((n, d)).astype(np.float32)
+    if ties:  # duplicated key rows force equal logits
+        for t in range(0, n, 3):
+            K[t] = K[(t * 7 + 1) % n]
+    V = rng.standard_normal((n, d)).astype(np.float32)
+    return q, K, V
+
+
+# --------------------------------------------------------------- keys --
+
+@pytest.mark.parametrize("seed", range(20))
+def test_logit_is_sequential_binary32_fma_chain(seed):
+    """The key equals a sequential FMA chain evaluated in exact rationals
+    with binary32 rounding after every step, then one rounded multiply."""
+    rng = np.random.default_rng(seed)
+    d = int(rng.integers(1, 24))
+    q = (rng.standard_normal(d) * 10.0 ** rng.integers(-3, 3)).astype(np.float32)
+    k = (rng.standard_normal(d) * 10.0 ** rng.integers(-3, 3)).astype(np.float32)
+    scale = np.float32(rng.uniform(0.01, 1.0))
+    a = Fraction(0)
+    for c in range(d):
+        a = round_binary32(Fraction(float(q[c])) * Fraction(float(k[c])) + a)
+    want = float(round_binary32(a * Fraction(float(scale))))
+    got = O.logit(q, k, float(scale))
+    assert got == np.float32(want)
+
+
+def test_logit_order_is_observable():
+    """Summation order matters in fp32, so the chain order is part of the key:
+    [1e8, 1, -1e8] summed left to right loses the 1."""
+    q = np.array([1.0, 1.0, 1.0], np.float32)
+    k = np.array([1e8, 1.0, -1e8], np.float32)
+    assert O.logit(q, k, 1.0) == np.float32(0.0)
+    k2 = np.array([1e8, -1e8, 1.0], np.float32)
+    assert O.logit(q, k2, 1.0) == np.float32(1.0)
+
+
+def test_logit_exact_on_bf16_grid():
+    """bf16 inputs whose partial sums stay exact in fp32 give the exact dot
+    product times the scale (a closed form)."""
+    rng = np.random.default_rng(5)
+    for _ in range(50):
+        q = rng.integers(-64, 65, 64).astype(np.float32) / 8
+        k = rng.integers(-64, 65, 64).astype(np.float32) / 16
+        exact = sum(Fraction(float(a)) * Fraction(float(b)) for a, b in zip(q, k))
+        assert O.logit(q, k, 0.125) == np.float32(float(exact * Fraction(1, 8)))
+
+
+def test_logit_unit_vector_and_zero():
+    k = np.arange(1, 65, dtype=np.float32) * 0.37
+    for c in (0, 17, 63):
+        q = np.zeros(64, np.float32)
+        q[c] = 1.0
+        assert O.logit(q, k, 0.125) == np.float32(k[c] * np.float32(0.125))
+    # -0 canonicalises to +0
+    s = O.logit(np.array([-1.0], np.float32), np.array([0.0], np.float32), 1.0)
+    assert s == 0.0 and math.copysign(1.0, s) == 1.0
+
+
+def test_key_is_order_preserving():
+    rng = np.random.default_rng(1)
+    vals = np.concatenate([
+        rng.standard_normal(500).astype(np.float32) * 10.0 ** rng.integers(-40, 38, 500),
+        np.array([0.0, -0.0, 1e-45, -1e-45, 3.4e38, -3.4e38, 1.0, -1.0], np.float32)])
+    vals = vals[np.isfinite(vals)].astype(np.float32)
+    keys = np.array([O.key(float(v)) for v in vals], np.uint64)
+    for i in range(len(vals)):
+        for j in range(0, len(vals), 7):
+            assert (keys[i] > keys[j]) == (vals[i] > vals[j])
+            assert (keys[i] == keys[j]) == (vals[i] == vals[j])
+    assert O.key(0.0) == O.key(-0.0)
+
+
+# ------------------------------------------------------------ stage 1 --
+
+@pytest.mark.parametrize("n,d", [(1, 64), (7, 64), (300, 64), (129, 128)])
+def test_small_head_is_textbook_attention(n, d):
+    rng = np.random.default_rng(n * 31 + d)
+    q, K, V = small_row(rng, n, d)
+    scale = float(np.float32(1 / math.sqrt(d)))
+    logits, m, Z, Ohat = O.small_head(q, K, V, scale)
+    Oref, pref = textbook_attention(q, K, V, scale)
+    np.testing.assert_allclose(Ohat, Oref, rtol=1e-6, atol=1e-6)
+    p = np.exp(logits.astype(np.float64) - m) / Z
+    assert abs(p.sum() - 1.0) < 1e-12
+    np.testing.assert_allclose(p, pref, rtol=1e-5, atol=1e-9)
+    assert m == logits.max()
+
+
+# ------------------------------------------------------------ stage 2 --
+
+@pytest.mark.parametrize("seed", range(40))
+def test_partition_matches_bruteforce_ranks(seed):
+    rng = np.random.default_rng(100 + seed)
+    n = int(rng.integers(1, 33))
+    q, K, V = small_row(rng, n, 64, ties=bool(seed % 2))
+    if seed % 4 == 3:  # coarse values: many exact ties, mixed signs, zeros
+        q = np.round(q * 2) / 2
+        K = np.round(K * 2) / 2
+    logits, m, Z, _ = O.small_head(q, K, V, 0.125)
+    kc = int(rng.integers(1, n + 3))
+    km = int(rng.integers(0, n + 3))
+    crit, marg, mp, mass = O.partition(logits, kc, km, m, Z, kc_cap=n + 2, km_cap=n + 2)
+    rank = rank_bruteforce(logits)
+    nc = min(kc, n)
+    nm = min(km, n - nc)
+    want_c = sorted(t for t in range(n) if rank[t] < nc)
+    want_m = sorted(t for t in range(n) if nc <= rank[t] < nc + nm)
+    assert list(crit[:nc]) == want_c and all(crit[nc:] == -1)
+    assert list(marg[:nm]) == want_m and all(marg[nm:] == -1)
+    p = np.exp(logits.astype(np.float64) - m) / Z
+    np.testing.assert_allclose(mp[:nm], p[want_m], rtol=1e-13, atol=0)
+    assert all(mp[nm:] == 0)
+    np.testing.assert_allclose(mass, [p[want_c].sum(), p[want_m].sum()], rtol=1e-12, atol=1e-15)
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_partition_is_max_sum_lowest_index_subset(seed):
+    """Exhaustive: among all subsets of size k, C is the one with the largest
+    exact logit sum and, among equal sums, the lexicographically smallest
+    ascending index tuple; C u M is the same for size k + |M|."""
+    rng = np.random.default_rng(300 + seed)
+    n = int(rng.integers(2, 11))
+    q, K, V = small_row(rng, n, 64, ties=True)
+    if seed % 3 == 0:
+        q = np.round(q)
+        K = np.round(K)
+    logits, m, Z, _ = O.small_head(q, K, V, 0.125)
+    exact = [Fraction(float(x)) for x in logits]
+    kc = int(rng.integers(1, n + 1))
+    km = int(rng.integers(0, n - kc + 1))
+    crit, marg, _, _ = O.partition(logits, kc, km, m, Z)
+
+    def best(k):
+        return min(itertools.combinations(range(n), k),
+                   key=lambda S: (-sum(exact[t] for t in S), S))
+
+    assert tuple(crit) == best(kc)
+    assert tuple(sorted(list(crit) + list(marg))) == best(kc + km)
+
+
+@pytest.mark.parametrize("n,kc,km", [(5, 9, 4), (5, 5, 3), (5, 3, 9), (1, 1, 0), (1, 4, 4), (8, 2, 0)])
+def test_partition_budget_clamping(n, kc, km):
+    rng = np.random.default_rng(n + kc + km)
+    q, K, V = small_row(rng, n, 64)
+    logits, m, Z, _ = O.small_head(q, K, V, 0.125)
+    crit, marg, mp, mass = O.partition(logits, kc, km, m, Z, kc_cap=10, km_cap=10)
+    nc, nm = min(kc, n), min(km, n - min(kc, n))
+    assert (crit >= 0).sum() == nc and (marg >= 0).sum() == nm
+    assert set(crit[:nc]).isdisjoint(set(marg[:nm]))
+    if nc + nm == n:
+        assert abs(mass.sum() - 1.0) < 1e-12
+    with pytest.raises(O.OracleError):
+        O.partition(logits, 0, km, m, Z, kc_cap=10, km_cap=10)
+
+
+def test_partition_class_order_invariant():
+    """Every critical key >= every marginal key >= every evicted key."""
+    rng = np.random.default_rng(9)
+    q, K, V = small_row(rng, 4096, 64, ties=True)
+    logits, m, Z, _ = O.small_head(q, K, V, 0.125)
+    crit, marg, _, _ = O.partition(logits, 400, 900, m, Z)
+    ev = np.setdiff1d(np.arange(4096), np.concatenate([crit, marg]))
+    assert len(crit) == 400 and len(marg) == 900 and len(ev) == 4096 - 1300
+    assert np.all(np.diff(crit) > 0) and np.all(np.diff(marg) > 0)
+    assert logits[crit].min() >= logits[marg].max() >= logits[ev].max()
+    # ties across a boundary go to the lower index
+    for a, b in ((crit, marg), (marg, ev)):
+        t = logits[a].min()
+        if t in logits[b]:
+            assert a[logits[a] == t].max() < b[logits[b] == t].min()
+
+
+# ------------------------------------------------------------ stage 3 --
+
+def _hybrid_setup(seed, n, d=64):
+    """'Identical models': the large head sees the same q, K and scale as the
+    small head, so its exact attention is the small model's."""
+    rng = np.random.default_rng(seed)
+    q, K, V = small_row(rng, n, d, ties=False)
+    scale = float(np.float32(1 / math.sqrt(d)))
+    logits, m, Z, _ = O.small_head(q, K, V, scale)
+    Vl = rng.standard_normal((n, d)).astype(np.float32)  # the large model's V
+    return q, K, Vl, scale, logits, m, Z
+
+
+@pytest.mark.parametrize("mode", O.MODES)
+def test_hybrid_all_critical_is_full_attention(mode):
+    q, K, V, scale, logits, m, Z = _hybrid_setup(1, 200, 128)
+    crit, marg, mp, mass = O.partition(logits, 200, 50, m, Z, kc_cap=200, km_cap=50)
+    out = O.hybrid_head(q, K, V, crit, marg, mp, mass, scale, mode)
+    ref, _ = textbook_attention(q, K, V, scale)
+    np.testing.assert_allclose(out, ref, rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("mode", [O.NORM_REMAINING, O.NORM_SLM_CRIT, O.NORM_RETAINED, O.NORM_MARG_FILL])
+@pytest.mark.parametrize("kc", [1, 17, 150])
+def test_hybrid_identical_models_no_eviction_is_full_attention(mode, kc):
+    n = 160
+    q, K, V, scale, logits, m, Z = _hybrid_setup(2 + kc, n)
+    crit, marg, mp, mass = O.partition(logits, kc, n - kc, m, Z)
+    out = O.hybrid_head(q, K, V, crit, marg, mp, mass, scale, mode)
+    ref, _ = textbook_attention(q, K, V, scale)
+    np.testing.assert_allclose(out, ref, rtol=2e-6, atol=2e-6)
+
+
+def test_hybrid_literal_sum_overweights_marginal():
+    """O_c + O_m taken literally carries weight 1 + S'_M, so it misses full
+    attention even with nothing evicted (why it is not the default)."""
+    n = 160
+    q, K, V, scale, logits, m, Z = _hybrid_setup(7, n)
+    crit, marg, mp, mass = O.partition(logits, 10, n - 10, m, Z)
+    ones = np.ones_like(V)
+    w = O.hybrid_head(q, K, ones, crit, marg, mp, mass, scale, O.NORM_NONE)
+    np.testing.assert_allclose(w, 1.0 + mass[1], rtol=1e-12)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_hybrid_identical_models_with_eviction(seed):
+    """Eq. 6 with the small model exact: A on C, A' on M, 0 elsewhere.
+    SLM_CRIT reproduces it; RETAINED is softmax restricted to C u M."""
+    n = 240
+    q, K, V, scale, logits, m, Z = _hybrid_setup(20 + seed, n)
+    crit, marg, mp, mass = O.partition(logits, 30, 70, m, Z)
+    _, p = textbook_attention(q, K, V, scale)
+    keep = np.concatenate([crit, marg])
+    eq6 = p[keep] @ V[keep].astype(np.float64)
+    out = O.hybrid_head(q, K, V, crit, marg, mp, mass, scale, O.NORM_SLM_CRIT)
+    np.testing.assert_allclose(out, eq6, rtol=2e-6, atol=2e-6)
+    out = O.hybrid_head(q, K, V, crit, marg, mp, mass, scale, O.NORM_RETAINED)
+    np.testing.assert_allclose(out, eq6 / p[keep].sum(), rtol=2e-6, atol=2e-6)
+
+
+@pytest.mark.parametrize("mode,weight", [
+    (O.NORM_REMAINING, lambda sc, sm: 1.0), (O.NORM_NONE, lambda sc, sm: 1.0 + sm),
+    (O.NORM_SLM_CRIT, lambda sc, sm: sc + sm), (O.NORM_RETAINED, lambda sc, sm: 1.0),
+    (O.NORM_MARG_FILL, lambda sc, sm: 1.0)])
+def test_hybrid_weight_sum(mode, weight):
+    n = 300
+    rng = np.random.default_rng(77)
+    q, K, _ = small_row(rng, n, 128)
+    qs, Ks, Vs = small_row(rng, n, 64)
+    logits, m, Z, _ = O.small_head(qs, Ks, Vs, 0.125)
+    crit, marg, mp, mass = O.partition(logits, 40, 90, m, Z)
+    out = O.hybrid_head(q, K, np.ones((n, 128), np.float32), crit, marg, mp, mass, SCALE128, mode)
+    np.testing.assert_allclose(out, weight(mass[0], mass[1]), rtol=1e-12)
+
+
+def test_hybrid_single_critical_is_its_value_row():
+    n = 50
+    rng = np.random.default_rng(3)
+    q, K, V = small_row(rng, n, 128)
+    logits, m, Z, _ = O.small_head(*small_row(rng, n, 64), 0.125)
+    crit, marg, mp, mass = O.partition(logits, 1, 0, m, Z, km_cap=0)
+    for mode in (O.NORM_REMAINING, O.NORM_NONE, O.NORM_RETAINED):
+        out = O.hybrid_head(q, K, V, crit, marg, mp, mass, SCALE128, mode)
+        np.testing.assert_allclose(out, V[crit[0]].astype(np.float64), rtol=0, atol=0)
+
+
+def test_hybrid_uses_large_values_and_slots():
+    """Rows reached through slot maps give the same output as identity rows;
+    changing a V row outside C u M changes nothing, inside it does."""
+    n, d = 120, 128
+    rng = np.random.default_rng(4)
+    q, K, V = small_row(rng, n, d)
+    logits, m, Z, _ = O.small_head(*small_row(rng, n, 64), 0.125)
+    crit, marg, mp, mass = O.partition(logits, 12, 30, m, Z)
+    base = O.hybrid_head(q, K, V, crit, marg, mp, mass, SCALE128)
+    perm = rng.permutation(n).astype(np.int32)
+    Kp = np.empty_like(K)
+    Vp = np.empty_like(V)
+    Kp[perm] = K
+    Vp[perm] = V
+    out = O.hybrid_head(q, Kp, Vp, crit, marg, mp, mass, SCALE128, k_slot=perm, v_slot=perm)
+    np.testing.assert_allclose(out, base, rtol=1e-13, atol=1e-13)
+    ev = np.setdiff1d(np.arange(n), np.concatenate([crit, marg]))[0]
+    V2 = V.copy()
+    V2[ev] += 100
+    np.testing.assert_array_equal(O.hybrid_head(q, K, V2, crit, marg, mp, mass, SCALE128), base)
+    V3 = V.copy()
+    V3[marg[0]] += 100
+    assert np.abs(O.hybrid_head(q, K, V3, crit, marg, mp, mass, SCALE128) - base).max() > 1e-3
+    # a token the store does not hold is an error
+    vs = perm.copy()
+    vs[marg[0]] = -1
+    with pytest.raises(O.OracleError):
+        O.hybrid_head(q, Kp, Vp, crit, marg, mp, mass, SCALE128, k_slot=perm, v_slot=vs)
+
+
+# ----------------------------------------------------------- whole step --
+
+def test_step_composes_the_three_stages():
+    """orc_step over the tensor layout equals the per-head functions applied
+    one by one, and with every token critical both models' outputs are
+    textbook full attention."""
+    rng = np.random.default_rng(11)
+    B, ncap, l, hqs, hks, ds = 2, 40, 2, 4, 2, 64
+    L, hq, hk, d = 3, 6, 3, 128
+    sq = rng.standard_normal((B, l, hqs, ds)).astype(np.float32)
+    sk = rng.standard_normal((B, l, hks, ncap, ds)).astype(np.float32)
+    sv = rng.standard_normal((B, l, hks, ncap, ds)).astype(np.float32)
+    lq = rng.standard_normal((B, L, hq, d)).astype(np.float32)
+    lk = rng.standard_normal((B, L, hk, ncap, d)).astype(np.float32)
+    lv = rng.standard_normal((B, L, hk, ncap, d)).astype(np.float32)
+    seq = np.array([40, 23], np.int32)
+    hm = rng.integers(0, l * hqs, L * hq).astype(np.int32)
+    for kc, km in ((np.array([5, 3]), np.array([9, 30])), (np.array([40, 40]), np.array([0, 0]))):
+        r = O.step(seq_len=seq, k_crit=kc, k_marg=km, kc_cap=40, km_cap=30, head_map=hm,
+                   mode=O.NORM_REMAINING, s_q=sq, s_k=sk, s_v=sv, s_scale=0.125,
+                   l_q=lq, l_k=lk, l_v=lv, l_scale=SCALE128)
+        for b in range(B):
+            n = seq[b]
+            for j in range(l * hqs):
+                lay, h = divmod(j, hqs)
+                g = h // (hqs // hks)
+                lg, m, Z, Os = O.small_head(sq[b, lay, h], sk[b, lay, g, :n], sv[b, lay, g, :n], 0.125)
+                np.testing.assert_array_equal(r["logits"][b, j, :n], lg)
+                np.testing.assert_array_equal(r["small_out"][b, lay, h], Os)
+                c, mg, mp, ms = O.partition(lg, int(kc[b]), int(km[b]), m, Z, kc_cap=40, km_cap=30)
+                np.testing.assert_array_equal(r["crit"][b, j], c)
+                np.testing.assert_array_equal(r["marg"][b, j], mg)
+                np.testing.assert_array_equal(r["mass"][b, j], ms)
+            for lay in range(L):
+                for h in range(hq):
+                    j = hm[lay * hq + h]
+                    g = h // (hq // hk)
+                    o = O.hybrid_head(lq[b, lay, h], lk[b, lay, g], lv[b, lay, g], r["crit"][b, j],
+                                      r["marg"][b, j], r["marg_prob"][b, j], r["mass"][b, j], SCALE128)
+                    np.testing.assert_array_equal(r["large_out"][b, lay, h], o)
+                    if kc[0] == 40:
+                        ref, _ = textbook_attention(lq[b, lay, h], lk[b, lay, g, :n], lv[b, lay, g, :n], SCALE128)
+                        np.testing.assert_allclose(r["large_out"][b, lay, h], ref, rtol=1e-10, atol=1e-12)
