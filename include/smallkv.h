@@ -1,0 +1,193 @@
+/*
+ * smallkv.h -- C ABI of the MI355X (gfx950) library for SmallKV's
+ * per-decode-step compensated attention (arXiv 2508.02751).
+ *
+ * One decode step has three stages (Algorithm 1, decode branch):
+ *   1. smallkv_small_attn  -- the small model's full decode attention over
+ *      its uncompressed cache (the selection of the "Saliency Shift
+ *      Compensation" paragraph is made from this full small cache);
+ *   2. smallkv_partition   -- per small head, the tokens ordered by the small
+ *      model's attention split into critical (TopK), marginal (Top(P-K)) and
+ *      evicted sets (Eq. 4 read as "keep the top-scored tokens", Eq. 6);
+ *   3. smallkv_hybrid_attn -- each large head i reads the partition of small
+ *      head f(i) (Eq. 3): exact softmax attention over its critical keys
+ *      (O_c), the small model's probabilities times the large model's V for
+ *      the marginal tokens (O_m), evicted tokens contribute nothing, and the
+ *      output O_c + O_m as weighted by smallkv_norm_t (Eq. 6; Algorithm 1,
+ *      "Attention Output by O_c + O_m").
+ * smallkv_step runs all three for every layer of both models.
+ *
+ * Conventions shared by every entry point
+ *   - Pointers named in the structs and arguments are DEVICE pointers unless
+ *     stated otherwise; the descriptor structs themselves live in host memory
+ *     and are read only during the call.
+ *   - Ownership: the caller allocates and owns every buffer, including the
+ *     workspace.  The library allocates no device memory, keeps no state
+ *     between calls and never synchronises: work is enqueued on `stream`
+ *     (a hipStream_t; NULL is the null stream) and the call returns.
+ *   - Errors: a negative status is returned, before anything is enqueued,
+ *     for every condition visible on the host (null pointers, sizes, head
+ *     dims, dtype, workspace too small, head counts).  A kernel launch
+ *     failure returns SMALLKV_EDEVICE.  Values that live in device memory
+ *     (seq_len, k_crit, k_marg, head_map, indices) cannot be checked on the
+ *     host: the kernels clamp them into range (see smallkv_batch_t) so that no
+ *     access leaves its buffer, and results outside the stated
+ *     preconditions are unspecified.
+ *   - Layout: every tensor is dense row-major in the order its comment gives.
+ *   - Numerics: logits are fp32 and bit-reproducible: each is a sequential
+ *     fp32 fused multiply-add chain over the head dimension starting from +0,
+ *     then one fp32 multiply by `scale`, with -0 returned as +0.  The
+ *     partition ranks on these logits (larger first, equal logits by lower
+ *     token index), so it is exact and deterministic.  Softmax statistics,
+ *     probabilities and outputs are fp32 arithmetic, rounded to the model
+ *     dtype (round to nearest even) on output.
+ */
+#ifndef SMALLKV_H
+#define SMALLKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SMALLKV_ABI_VERSION 1
+
+typedef enum { SMALLKV_F32 = 0, SMALLKV_BF16 = 1 } smallkv_dtype_t;
+
+/* Weights of the two parts of the compensated row: O = alpha_C*O_c + alpha_M*O_m,
+ * with S'_C, S'_M the small head's probability mass on the critical and
+ * marginal sets.  O_c is the large head's softmax over its critical keys
+ * (weights summing to 1); O_m = sum over marginal t of p'_t * V_t. */
+typedef enum {
+  SMALLKV_NORM_REMAINING = 0, /* default: alpha_C = 1 - S'_M, alpha_M = 1.  The
+                                 marginal tokens keep the small model's
+                                 probabilities; the critical softmax fills the
+                                 remaining mass, so the weights sum to 1 */
+  SMALLKV_NORM_NONE = 1,      /* alpha_C = 1, alpha_M = 1: the sum O_c + O_m
+                                 exactly as the implementation pseudocode adds
+                                 them (weights sum to 1 + S'_M) */
+  SMALLKV_NORM_SLM_CRIT = 2,  /* alpha_C = S'_C, alpha_M = 1: Eq. 6 with the
+                                 large model's full-row denominator estimated
+                                 by the small model's */
+  SMALLKV_NORM_RETAINED = 3,  /* alpha_C = S'_C/(S'_C+S'_M), alpha_M = 1/(S'_C+S'_M) */
+  SMALLKV_NORM_MARG_FILL = 4  /* alpha_C = S'_C, alpha_M = (1-S'_C)/S'_M (0 if S'_M = 0) */
+} smallkv_norm_t;
+
+enum {
+  SMALLKV_OK = 0,
+  SMALLKV_EINVAL = -1,       /* a null pointer, a bad size or an inconsistent shape */
+  SMALLKV_EUNSUPPORTED = -2, /* a valid request outside what the kernels implement */
+  SMALLKV_EWORKSPACE = -3,   /* ws_bytes below smallkv_workspace_size() */
+  SMALLKV_EDEVICE = -4       /* a HIP launch error */
+};
+
+/* One model's attention operands for one decode step (all layers). */
+typedef struct {
+  int32_t n_layers;   /* l (small) or L (large) */
+  int32_t n_q_heads;  /* query heads per layer */
+  int32_t n_kv_heads; /* kv heads per layer; n_q_heads % n_kv_heads == 0, query
+                         head h reads kv head h / (n_q_heads / n_kv_heads) */
+  int32_t head_dim;   /* 64 or 128 */
+  int32_t dtype;      /* smallkv_dtype_t of q, k, v and out */
+  float scale;        /* softmax scale, normally 1/sqrt(head_dim) */
+  const void *q;      /* [B][n_layers][n_q_heads][head_dim] */
+  const void *k;      /* [B][n_layers][n_kv_heads][n_rows][head_dim] */
+  const void *v;      /* same layout as k */
+  int64_t n_rows;     /* rows per (sequence, layer, kv head): n_cap for a full
+                         cache, or the capacity of a compact store */
+  const int32_t *k_slot; /* large model only, optional: [B][n_layers][n_kv_heads][n_cap]
+                            token -> row of k (-1: not held); NULL means row = token */
+  const int32_t *v_slot; /* same for v */
+  void *out;          /* [B][n_layers][n_q_heads][head_dim] attention output */
+} smallkv_model_t;
+
+/* The batch of sequences and their budgets. */
+typedef struct {
+  int32_t batch;          /* B >= 1 */
+  int32_t n_cap;          /* max tokens per sequence (cache capacity) >= 1 */
+  const int32_t *seq_len; /* [B] current length N_b, the current token included;
+                             precondition 1 <= N_b <= n_cap (clamped on device) */
+  const int32_t *k_crit;  /* [B] critical budget K_b >= 1 */
+  const int32_t *k_marg;  /* [B] marginal budget >= 0 */
+  int32_t kc_cap;         /* host: width of the critical index rows, >= 1 */
+  int32_t km_cap;         /* host: width of the marginal index rows, >= 0 */
+  /* Set sizes, computed on device per sequence:
+   *   |C| = min(max(K_b, 1), N_b, kc_cap)
+   *   |M| = min(max(k_marg_b, 0), N_b - |C|, km_cap)
+   * Within the preconditions (K_b <= kc_cap, the marginal count <= km_cap)
+   * the caps never bind. */
+} smallkv_batch_t;
+
+/* Stage 1.  For every sequence b, small layer, small query head h (small head
+ * id j = layer * n_q_heads + h) and token t < N_b:
+ *   logits[b][j][t] = the fp32 logit described above (entries t >= N_b are
+ *                     not written)
+ *   row_max[b][j]   = max_t logits,  row_sum[b][j] = sum_t exp(logit - row_max)
+ *   small->out      = sum_t (exp(logit - row_max) / row_sum) * V_t
+ * logits: [B][n_layers*n_q_heads][n_cap] fp32; row_max, row_sum: [B][n_layers*n_q_heads]
+ * fp32.  small->k_slot and v_slot must be NULL and small->n_rows == n_cap. */
+int smallkv_small_attn(const smallkv_batch_t *batch, const smallkv_model_t *small,
+                       float *logits, float *row_max, float *row_sum, void *ws,
+                       size_t ws_bytes, void *stream);
+
+/* Stage 2.  For every row (b, j), j < n_small_heads: tokens t < N_b ordered by
+ * (logit descending, index ascending); the first |C| are critical, the next
+ * |M| marginal, the rest evicted.
+ *   crit_idx  [B][n_small_heads][kc_cap] int32, ascending, padded with -1
+ *   marg_idx  [B][n_small_heads][km_cap] int32, ascending, padded with -1
+ *   marg_prob [B][n_small_heads][km_cap] fp32, p'_t = exp(logit_t - row_max)/row_sum
+ *             for marg_idx's token (0 in padding)
+ *   mass      [B][n_small_heads][2] fp32, {S'_C, S'_M}: the sum of p' over each set
+ * Inputs are stage 1's logits, row_max and row_sum.  Deterministic. */
+int smallkv_partition(const smallkv_batch_t *batch, int32_t n_small_heads,
+                      const float *logits, const float *row_max,
+                      const float *row_sum, int32_t *crit_idx,
+                      int32_t *marg_idx, float *marg_prob, float *mass, void *ws,
+                      size_t ws_bytes, void *stream);
+
+/* Stage 3.  For every sequence b, large layer and large query head h, with
+ * j = head_map[layer * n_q_heads + h] (0 <= j < n_small_heads) and kv head
+ * g = h / (n_q_heads / n_kv_heads):
+ *   s_t = scale * <q, K_g[row(t)]> for t in crit_idx[b][j]
+ *   O_c = sum_C softmax_C(s)_t V_g[row(t)],  O_m = sum_M marg_prob_t V_g[row(t)]
+ *   large->out = alpha_C * O_c + alpha_M * O_m   (alphas from `mode` and mass[b][j])
+ * head_map: [n_layers * n_q_heads] int32 (device).  Rows come from
+ * large->k_slot / v_slot when given. */
+int smallkv_hybrid_attn(const smallkv_batch_t *batch, const smallkv_model_t *large,
+                        const int32_t *head_map, int32_t n_small_heads,
+                        const int32_t *crit_idx, const int32_t *marg_idx,
+                        const float *marg_prob, const float *mass, int32_t mode,
+                        void *ws, size_t ws_bytes, void *stream);
+
+/* A whole decode step: stage 1 over every small layer, stage 2 over every
+ * small head, stage 3 over every large layer, enqueued back to back on one
+ * stream.  The intermediate buffers are the caller's, laid out as above,
+ * with n_small_heads = small.n_layers * small.n_q_heads. */
+typedef struct {
+  smallkv_batch_t batch;
+  smallkv_model_t small, large;
+  const int32_t *head_map; /* [large.n_layers * large.n_q_heads] */
+  int32_t mode;            /* smallkv_norm_t */
+  float *logits, *row_max, *row_sum;
+  int32_t *crit_idx, *marg_idx;
+  float *marg_prob, *mass;
+} smallkv_step_t;
+
+int smallkv_step(const smallkv_step_t *step, void *ws, size_t ws_bytes, void *stream);
+
+/* Bytes of workspace that smallkv_step needs for `step`; the single-stage
+ * calls need no more than this for the same shapes.  Host only. */
+int smallkv_workspace_size(const smallkv_step_t *step, size_t *bytes);
+
+/* A static string for a status code. */
+const char *smallkv_status_string(int status);
+
+/* SMALLKV_ABI_VERSION of the loaded library. */
+int smallkv_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SMALLKV_H */

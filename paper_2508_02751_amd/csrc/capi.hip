@@ -1,0 +1,154 @@
+// The C ABI of include/smallkv.h: host-side validation, workspace planning
+// and launches.  Nothing here touches device memory or synchronises.
+#include <hip/hip_runtime.h>
+
+#include "launch.h"
+#include "smallkv.h"
+
+using namespace smallkv;
+
+namespace {
+
+bool model_ok(const smallkv_model_t *m) {
+  if (!m || !m->q || !m->k || !m->v || !m->out) return false;
+  if (m->n_layers < 1 || m->n_q_heads < 1 || m->n_kv_heads < 1) return false;
+  if (m->n_q_heads % m->n_kv_heads) return false;
+  if (m->dtype != SMALLKV_F32 && m->dtype != SMALLKV_BF16) return false;
+  if (m->n_rows < 1) return false;
+  if (!(m->scale == m->scale)) return false;  // NaN scale
+  return true;
+}
+
+bool batch_ok(const smallkv_batch_t *b) {
+  return b && b->batch >= 1 && b->n_cap >= 1 && b->seq_len && b->k_crit && b->k_marg &&
+         b->kc_cap >= 1 && b->km_cap >= 0;
+}
+
+bool dim_supported(const smallkv_model_t *m) { return m->head_dim == 64 || m->head_dim == 128; }
+
+int check_small(const smallkv_batch_t *b, const smallkv_model_t *s) {
+  if (!batch_ok(b) || !model_ok(s)) return SMALLKV_EINVAL;
+  if (s->k_slot || s->v_slot || s->n_rows != b->n_cap) return SMALLKV_EINVAL;
+  if (!dim_supported(s)) return SMALLKV_EUNSUPPORTED;
+  if (s->n_q_heads / s->n_kv_heads > 16) return SMALLKV_EUNSUPPORTED;
+  if ((int64_t)b->batch * s->n_layers * s->n_q_heads > INT32_MAX / 2) return SMALLKV_EUNSUPPORTED;
+  return SMALLKV_OK;
+}
+
+int check_large(const smallkv_batch_t *b, const smallkv_model_t *l, const int32_t *head_map,
+                int n_small_heads) {
+  if (!batch_ok(b) || !model_ok(l) || !head_map || n_small_heads < 1) return SMALLKV_EINVAL;
+  if (!l->k_slot != !l->v_slot) return SMALLKV_EINVAL;  // both maps or neither
+  if (!l->k_slot && l->n_rows != b->n_cap) return SMALLKV_EINVAL;
+  if (l->n_rows > INT32_MAX) return SMALLKV_EUNSUPPORTED;
+  if (!dim_supported(l)) return SMALLKV_EUNSUPPORTED;
+  if (b->kc_cap > kHybridMaxCrit) return SMALLKV_EUNSUPPORTED;
+  if ((int64_t)b->batch * l->n_layers * l->n_q_heads > INT32_MAX / 2) return SMALLKV_EUNSUPPORTED;
+  return SMALLKV_OK;
+}
+
+int check_mode(int mode) {
+  return (mode >= SMALLKV_NORM_REMAINING && mode <= SMALLKV_NORM_MARG_FILL) ? SMALLKV_OK
+                                                                            : SMALLKV_EINVAL;
+}
+
+int status_of(hipError_t e) { return e == hipSuccess ? SMALLKV_OK : SMALLKV_EDEVICE; }
+
+}  // namespace
+
+extern "C" {
+
+int smallkv_abi_version(void) { return SMALLKV_ABI_VERSION; }
+
+const char *smallkv_status_string(int status) {
+  switch (status) {
+    case SMALLKV_OK:
+      return "ok";
+    case SMALLKV_EINVAL:
+      return "invalid argument";
+    case SMALLKV_EUNSUPPORTED:
+      return "unsupported shape or type";
+    case SMALLKV_EWORKSPACE:
+      return "workspace too small";
+    case SMALLKV_EDEVICE:
+      return "HIP launch error";
+    default:
+      return "unknown status";
+  }
+}
+
+int smallkv_workspace_size(const smallkv_step_t *step, size_t *bytes) {
+  if (!step || !bytes) return SMALLKV_EINVAL;
+  int rc = check_small(&step->batch, &step->small);
+  if (rc) return rc;
+  const SmallPlan p = plan_small(step->batch, step->small);
+  *bytes = p.ws_bytes;
+  return SMALLKV_OK;
+}
+
+int smallkv_small_attn(const smallkv_batch_t *batch, const smallkv_model_t *small, float *logits,
+                       float *row_max, float *row_sum, void *ws, size_t ws_bytes, void *stream) {
+  int rc = check_small(batch, small);
+  if (rc) return rc;
+  if (!logits || !row_max || !row_sum) return SMALLKV_EINVAL;
+  const SmallPlan p = plan_small(*batch, *small);
+  if (p.ws_bytes && (!ws || ws_bytes < p.ws_bytes)) return SMALLKV_EWORKSPACE;
+  return status_of(launch_small_attn(*batch, *small, logits, row_max, row_sum,
+                                     static_cast<float *>(ws), p,
+                                     static_cast<hipStream_t>(stream)));
+}
+
+int smallkv_partition(const smallkv_batch_t *batch, int32_t n_small_heads, const float *logits,
+                      const float *row_max, const float *row_sum, int32_t *crit_idx,
+                      int32_t *marg_idx, float *marg_prob, float *mass, void *ws, size_t ws_bytes,
+                      void *stream) {
+  (void)ws;
+  (void)ws_bytes;
+  if (!batch_ok(batch) || n_small_heads < 1) return SMALLKV_EINVAL;
+  if (!logits || !row_max || !row_sum || !crit_idx || !mass) return SMALLKV_EINVAL;
+  if (batch->km_cap > 0 && (!marg_idx || !marg_prob)) return SMALLKV_EINVAL;
+  if ((int64_t)batch->batch * n_small_heads > INT32_MAX / 2) return SMALLKV_EUNSUPPORTED;
+  return status_of(launch_partition(*batch, n_small_heads, logits, row_max, row_sum, crit_idx,
+                                    marg_idx, marg_prob, mass,
+                                    static_cast<hipStream_t>(stream)));
+}
+
+int smallkv_hybrid_attn(const smallkv_batch_t *batch, const smallkv_model_t *large,
+                        const int32_t *head_map, int32_t n_small_heads, const int32_t *crit_idx,
+                        const int32_t *marg_idx, const float *marg_prob, const float *mass,
+                        int32_t mode, void *ws, size_t ws_bytes, void *stream) {
+  (void)ws;
+  (void)ws_bytes;
+  int rc = check_large(batch, large, head_map, n_small_heads);
+  if (rc) return rc;
+  if ((rc = check_mode(mode))) return rc;
+  if (!crit_idx || !mass) return SMALLKV_EINVAL;
+  if (batch->km_cap > 0 && (!marg_idx || !marg_prob)) return SMALLKV_EINVAL;
+  return status_of(launch_hybrid(*batch, *large, head_map, n_small_heads, crit_idx, marg_idx,
+                                 marg_prob, mass, mode, static_cast<hipStream_t>(stream)));
+}
+
+int smallkv_step(const smallkv_step_t *s, void *ws, size_t ws_bytes, void *stream) {
+  if (!s) return SMALLKV_EINVAL;
+  const int nsh = s->small.n_layers * s->small.n_q_heads;
+  int rc = check_small(&s->batch, &s->small);
+  if (rc) return rc;
+  if ((rc = check_large(&s->batch, &s->large, s->head_map, nsh))) return rc;
+  if ((rc = check_mode(s->mode))) return rc;
+  if (!s->logits || !s->row_max || !s->row_sum || !s->crit_idx || !s->mass) return SMALLKV_EINVAL;
+  if (s->batch.km_cap > 0 && (!s->marg_idx || !s->marg_prob)) return SMALLKV_EINVAL;
+  const SmallPlan p = plan_small(s->batch, s->small);
+  if (p.ws_bytes && (!ws || ws_bytes < p.ws_bytes)) return SMALLKV_EWORKSPACE;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e = launch_small_attn(s->batch, s->small, s->logits, s->row_max, s->row_sum,
+                                   static_cast<float *>(ws), p, st);
+  if (e != hipSuccess) return SMALLKV_EDEVICE;
+  e = launch_partition(s->batch, nsh, s->logits, s->row_max, s->row_sum, s->crit_idx,
+                       s->marg_idx, s->marg_prob, s->mass, st);
+  if (e != hipSuccess) return SMALLKV_EDEVICE;
+  e = launch_hybrid(s->batch, s->large, s->head_map, nsh, s->crit_idx, s->marg_idx, s->marg_prob,
+                    s->mass, s->mode, st);
+  return status_of(e);
+}
+
+}  // extern "C"

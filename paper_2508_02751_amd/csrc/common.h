@@ -1,0 +1,99 @@
+// Device helpers shared by the SmallKV HIP kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "smallkv.h"
+
+namespace smallkv {
+
+constexpr int kWave = 64;
+
+// bf16 is carried as its 16-bit pattern; widening to fp32 is exact.
+struct bf16_t {
+  uint16_t bits;
+};
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// fp32 -> bf16, round to nearest even (NaN kept quiet).
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+template <typename T> struct elem;
+template <> struct elem<float> {
+  static constexpr int per16 = 4;  // elements per 16-byte vector
+  // Unpack one 16-byte vector into per16 floats.
+  __device__ __forceinline__ static void unpack(const uint4 &v, float *o) {
+    o[0] = __uint_as_float(v.x);
+    o[1] = __uint_as_float(v.y);
+    o[2] = __uint_as_float(v.z);
+    o[3] = __uint_as_float(v.w);
+  }
+  __device__ __forceinline__ static float load1(const void *p, int64_t i) {
+    return reinterpret_cast<const float *>(p)[i];
+  }
+  __device__ __forceinline__ static void store1(void *p, int64_t i, float x) {
+    reinterpret_cast<float *>(p)[i] = x;
+  }
+};
+template <> struct elem<bf16_t> {
+  static constexpr int per16 = 8;
+  __device__ __forceinline__ static void unpack(const uint4 &v, float *o) {
+    o[0] = bf16_lo(v.x);
+    o[1] = bf16_hi(v.x);
+    o[2] = bf16_lo(v.y);
+    o[3] = bf16_hi(v.y);
+    o[4] = bf16_lo(v.z);
+    o[5] = bf16_hi(v.z);
+    o[6] = bf16_lo(v.w);
+    o[7] = bf16_hi(v.w);
+  }
+  __device__ __forceinline__ static float load1(const void *p, int64_t i) {
+    return __uint_as_float((uint32_t)reinterpret_cast<const uint16_t *>(p)[i] << 16);
+  }
+  __device__ __forceinline__ static void store1(void *p, int64_t i, float x) {
+    reinterpret_cast<uint16_t *>(p)[i] = f32_to_bf16(x);
+  }
+};
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
+  return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+
+__device__ __forceinline__ int clampi(int x, int lo, int hi) { return x < lo ? lo : (x > hi ? hi : x); }
+
+// Per-sequence set sizes, exactly as documented in smallkv.h.
+struct Sizes {
+  int n, nc, nm;
+};
+__device__ __forceinline__ Sizes set_sizes(const int32_t *seq_len, const int32_t *k_crit,
+                                           const int32_t *k_marg, int b, int n_cap, int kc_cap,
+                                           int km_cap) {
+  Sizes s;
+  s.n = clampi(seq_len[b], 1, n_cap);
+  s.nc = clampi(k_crit[b], 1, min(s.n, kc_cap));
+  s.nm = clampi(k_marg[b], 0, min(s.n - s.nc, km_cap));
+  return s;
+}
+
+// Order-preserving uint32 key of an fp32 logit; -0 and +0 share a key.
+__device__ __forceinline__ uint32_t logit_key(float s) {
+  uint32_t u = __float_as_uint(s == 0.0f ? 0.0f : s);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+}  // namespace smallkv

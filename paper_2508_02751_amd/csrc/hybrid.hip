@@ -1,0 +1,262 @@
+// Stage 3: the large model's hybrid decode attention (Eq. 6; Algorithm 1,
+// "Calculate attention output O_c of critical tokens ... O_m of marginal
+// tokens ... Attention Output by O_c + O_m").
+//
+// One workgroup per (sequence, layer, large query head).  Large head i reads
+// the partition of small head f(i) from head_map.
+//   Phase 1: gather the K rows of the critical tokens (LPR lanes per row,
+//            16 bytes per lane, so a wave reads 64/LPR rows per instruction),
+//            dot with q, reduce across the row's lanes -> logits in LDS.
+//   Phase 2: softmax over the critical logits (workgroup max and sum), then
+//            one gather of V rows for critical and marginal tokens with
+//            weights alpha_C*e_t/Z_C and alpha_M*p'_t into one accumulator.
+// Workgroups are numbered so that the query heads sharing a kv head land on
+// the same XCD back to back: their gathered rows overlap and hit in that
+// XCD's L2.
+#include "common.h"
+#include "launch.h"
+
+namespace smallkv {
+namespace {
+
+constexpr int kHT = 256;
+constexpr int kXcd = 8;
+
+struct HybArgs {
+  int n_cap, layers, hq, hkv, g, nsh, kc_cap, km_cap, mode, units;
+  int64_t n_rows;
+  float scale;
+  const int32_t *seq_len, *k_crit, *k_marg, *head_map;
+  const void *q, *k, *v;
+  const int32_t *k_slot, *v_slot;
+  const int32_t *crit, *marg;
+  const float *marg_prob, *mass;
+  void *out;
+};
+
+__device__ __forceinline__ void alphas(int mode, float sc, float sm, float &ac, float &am) {
+  switch (mode) {
+    case SMALLKV_NORM_NONE:
+      ac = 1.0f;
+      am = 1.0f;
+      break;
+    case SMALLKV_NORM_SLM_CRIT:
+      ac = sc;
+      am = 1.0f;
+      break;
+    case SMALLKV_NORM_RETAINED:
+      ac = sc / (sc + sm);
+      am = 1.0f / (sc + sm);
+      break;
+    case SMALLKV_NORM_MARG_FILL:
+      ac = sc;
+      am = sm > 0.0f ? (1.0f - sc) / sm : 0.0f;
+      break;
+    default:
+      ac = 1.0f - sm;
+      am = 1.0f;
+      break;
+  }
+}
+
+template <typename T, int D>
+__global__ __launch_bounds__(kHT) void hybrid_kernel(HybArgs a) {
+  constexpr int EPL = elem<T>::per16;        // elements per lane (one 16-byte load)
+  constexpr int LPR = D / EPL;               // lanes per row
+  constexpr int RPW = kWave / LPR;           // rows per wave instruction
+  constexpr int NW = kHT / kWave;
+  constexpr int RPB = RPW * NW;              // rows per workgroup step
+  extern __shared__ float s_crit[];          // [kc_cap] logits, then weights
+  __shared__ float red[NW];
+  __shared__ float accbuf[NW][D];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int sub = lane % LPR, rg = lane / LPR;
+  // XCD-aware numbering: x = ((u / 8) * g + hh) * 8 + u % 8
+  const int x = blockIdx.x;
+  const int rest = x / kXcd;
+  const int u = (rest / a.g) * kXcd + x % kXcd, hh = rest % a.g;
+  if (u >= a.units) return;
+  const int kvh = u % a.hkv, bl = u / a.hkv, layer = bl % a.layers, b = bl / a.layers;
+  const int h = kvh * a.g + hh;
+  const int j = clampi(a.head_map[layer * a.hq + h], 0, a.nsh - 1);
+  const int64_t row = (int64_t)b * a.nsh + j;
+  const Sizes sz = set_sizes(a.seq_len, a.k_crit, a.k_marg, b, a.n_cap, a.kc_cap, a.km_cap);
+  const int nc = sz.nc, nm = sz.nm;
+  const int32_t *crit = a.crit + row * a.kc_cap;
+  const int32_t *marg = a.marg + row * a.km_cap;
+  const float *mp = a.marg_prob + row * a.km_cap;
+
+  const int64_t qrow = ((int64_t)b * a.layers + layer) * a.hq + h;
+  float qv[EPL];
+  {
+    const uint4 w = *reinterpret_cast<const uint4 *>(reinterpret_cast<const unsigned char *>(a.q) +
+                                                     (qrow * D + sub * EPL) * (int64_t)sizeof(T));
+    elem<T>::unpack(w, qv);
+  }
+  const unsigned char *kb = reinterpret_cast<const unsigned char *>(a.k) +
+                            (int64_t)u * a.n_rows * D * (int64_t)sizeof(T) + sub * 16;
+  const unsigned char *vb = reinterpret_cast<const unsigned char *>(a.v) +
+                            (int64_t)u * a.n_rows * D * (int64_t)sizeof(T) + sub * 16;
+  const int32_t *ks = a.k_slot ? a.k_slot + (int64_t)u * a.n_cap : nullptr;
+  const int32_t *vs = a.v_slot ? a.v_slot + (int64_t)u * a.n_cap : nullptr;
+  const int64_t rowb = D * (int64_t)sizeof(T);
+  const int last_row = (int)(a.n_rows - 1);
+
+  // ---- phase 1: critical logits -----------------------------------------
+  float lmax = -INFINITY;
+  for (int i0 = wave * RPW; i0 < nc; i0 += RPB * 4) {
+    int r[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int i = i0 + k * RPB + rg;
+      int t = i < nc ? crit[i] : 0;
+      t = clampi(t, 0, a.n_cap - 1);
+      r[k] = clampi(ks ? ks[t] : t, 0, last_row);
+    }
+    uint4 w[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) w[k] = *reinterpret_cast<const uint4 *>(kb + r[k] * rowb);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      float kv[EPL];
+      elem<T>::unpack(w[k], kv);
+      float d = 0.0f;
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) d = __builtin_fmaf(qv[e], kv[e], d);
+#pragma unroll
+      for (int o = 1; o < LPR; o <<= 1) d += __shfl_xor(d, o, kWave);
+      const int i = i0 + k * RPB + rg;
+      if (i < nc) {
+        const float s = d * a.scale;
+        if (sub == 0) s_crit[i] = s;
+        lmax = fmaxf(lmax, s);
+      }
+    }
+  }
+  lmax = wave_max(lmax);
+  if (lane == 0) red[wave] = lmax;
+  __syncthreads();
+  float m = red[0];
+#pragma unroll
+  for (int w = 1; w < NW; ++w) m = fmaxf(m, red[w]);
+  __syncthreads();
+  float zl = 0.0f;
+  for (int i = tid; i < nc; i += kHT) {
+    const float e = __expf(s_crit[i] - m);
+    s_crit[i] = e;
+    zl += e;
+  }
+  zl = wave_sum(zl);
+  if (lane == 0) red[wave] = zl;
+  __syncthreads();
+  float z = 0.0f;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) z += red[w];
+  float ac, am;
+  alphas(a.mode, a.mass[2 * row], a.mass[2 * row + 1], ac, am);
+  const float wc = ac / z;
+
+  // ---- phase 2: one weighted gather of V rows -----------------------------
+  float acc[EPL];
+#pragma unroll
+  for (int e = 0; e < EPL; ++e) acc[e] = 0.0f;
+  const int ntot = nc + nm;
+  for (int i0 = wave * RPW; i0 < ntot; i0 += RPB * 4) {
+    int r[4];
+    float wt[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int i = i0 + k * RPB + rg;
+      int t = 0;
+      float wgt = 0.0f;
+      if (i < nc) {
+        t = crit[i];
+        wgt = s_crit[i] * wc;
+      } else if (i < ntot) {
+        t = marg[i - nc];
+        wgt = mp[i - nc] * am;
+      }
+      t = clampi(t, 0, a.n_cap - 1);
+      r[k] = clampi(vs ? vs[t] : t, 0, last_row);
+      wt[k] = wgt;
+    }
+    uint4 w[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) w[k] = *reinterpret_cast<const uint4 *>(vb + r[k] * rowb);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      float vv[EPL];
+      elem<T>::unpack(w[k], vv);
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) acc[e] = __builtin_fmaf(wt[k], vv[e], acc[e]);
+    }
+  }
+#pragma unroll
+  for (int o = LPR; o < kWave; o <<= 1)
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) acc[e] += __shfl_xor(acc[e], o, kWave);
+  if (lane < LPR) {
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) accbuf[wave][sub * EPL + e] = acc[e];
+  }
+  __syncthreads();
+  if (tid < D) {
+    float o = 0.0f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) o += accbuf[w][tid];
+    elem<T>::store1(a.out, qrow * D + tid, o);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_hybrid(const smallkv_batch_t &b, const smallkv_model_t &m,
+                         const int32_t *head_map, int n_small_heads, const int32_t *crit,
+                         const int32_t *marg, const float *marg_prob, const float *mass,
+                         int mode, hipStream_t st) {
+  HybArgs a;
+  a.n_cap = b.n_cap;
+  a.layers = m.n_layers;
+  a.hq = m.n_q_heads;
+  a.hkv = m.n_kv_heads;
+  a.g = m.n_q_heads / m.n_kv_heads;
+  a.nsh = n_small_heads;
+  a.kc_cap = b.kc_cap;
+  a.km_cap = b.km_cap;
+  a.mode = mode;
+  a.units = b.batch * m.n_layers * m.n_kv_heads;
+  a.n_rows = m.n_rows;
+  a.scale = m.scale;
+  a.seq_len = b.seq_len;
+  a.k_crit = b.k_crit;
+  a.k_marg = b.k_marg;
+  a.head_map = head_map;
+  a.q = m.q;
+  a.k = m.k;
+  a.v = m.v;
+  a.k_slot = m.k_slot;
+  a.v_slot = m.v_slot;
+  a.crit = crit;
+  a.marg = marg;
+  a.marg_prob = marg_prob;
+  a.mass = mass;
+  a.out = m.out;
+  const int groups = (a.units + kXcd - 1) / kXcd;
+  const dim3 grid(groups * kXcd * a.g);
+  const size_t shm = (size_t)b.kc_cap * sizeof(float);
+  if (m.dtype == SMALLKV_F32) {
+    if (m.head_dim == 64)
+      hipLaunchKernelGGL((hybrid_kernel<float, 64>), grid, dim3(kHT), shm, st, a);
+    else
+      hipLaunchKernelGGL((hybrid_kernel<float, 128>), grid, dim3(kHT), shm, st, a);
+  } else {
+    if (m.head_dim == 64)
+      hipLaunchKernelGGL((hybrid_kernel<bf16_t, 64>), grid, dim3(kHT), shm, st, a);
+    else
+      hipLaunchKernelGGL((hybrid_kernel<bf16_t, 128>), grid, dim3(kHT), shm, st, a);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace smallkv

@@ -1,0 +1,39 @@
+// Host-side launchers of the SmallKV kernels (internal to the library).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+
+#include "smallkv.h"
+
+namespace smallkv {
+
+// Split-K plan of stage 1: each workgroup covers `chunk` tokens of one
+// (sequence, layer, kv head) unit; n_split chunks cover n_cap.
+struct SmallPlan {
+  int tile;      // tokens staged in LDS per iteration
+  int chunk;     // tokens per workgroup (multiple of tile)
+  int n_split;   // workgroups per unit
+  int gp;        // padded query-group size (4, 8 or 16)
+  size_t ws_bytes;
+};
+
+SmallPlan plan_small(const smallkv_batch_t &b, const smallkv_model_t &m);
+
+hipError_t launch_small_attn(const smallkv_batch_t &b, const smallkv_model_t &m, float *logits,
+                             float *row_max, float *row_sum, float *ws, const SmallPlan &p,
+                             hipStream_t st);
+
+hipError_t launch_partition(const smallkv_batch_t &b, int n_small_heads, const float *logits,
+                            const float *row_max, const float *row_sum, int32_t *crit,
+                            int32_t *marg, float *marg_prob, float *mass, hipStream_t st);
+
+// Largest kc_cap the single-pass hybrid kernel keeps in LDS.
+constexpr int kHybridMaxCrit = 12288;
+
+hipError_t launch_hybrid(const smallkv_batch_t &b, const smallkv_model_t &m,
+                         const int32_t *head_map, int n_small_heads, const int32_t *crit,
+                         const int32_t *marg, const float *marg_prob, const float *mass,
+                         int mode, hipStream_t st);
+
+}  // namespace smallkv

@@ -1,0 +1,247 @@
+"""Python binding of libsmallkv.so (include/smallkv.h).
+
+Argument marshalling only: torch tensors are used for device memory and the
+current HIP stream, their pointers and shapes go through ctypes to the C ABI,
+and every step of the computation runs in the library's HIP kernels.  There
+is no fallback: if the library is not built, or a call fails, this module
+raises.
+
+Entry points mirror the C names: smallkv_small_attn, smallkv_partition,
+smallkv_hybrid_attn, smallkv_step, smallkv_workspace_size.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import dataclasses
+import os
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libsmallkv.so")
+
+F32, BF16 = 0, 1
+NORM_REMAINING, NORM_NONE, NORM_SLM_CRIT, NORM_RETAINED, NORM_MARG_FILL = range(5)
+OK, EINVAL, EUNSUPPORTED, EWORKSPACE, EDEVICE = 0, -1, -2, -3, -4
+
+
+class Batch(C.Structure):
+    _fields_ = [("batch", C.c_int32), ("n_cap", C.c_int32),
+                ("seq_len", C.c_void_p), ("k_crit", C.c_void_p), ("k_marg", C.c_void_p),
+                ("kc_cap", C.c_int32), ("km_cap", C.c_int32)]
+
+
+class Model(C.Structure):
+    _fields_ = [("n_layers", C.c_int32), ("n_q_heads", C.c_int32), ("n_kv_heads", C.c_int32),
+                ("head_dim", C.c_int32), ("dtype", C.c_int32), ("scale", C.c_float),
+                ("q", C.c_void_p), ("k", C.c_void_p), ("v", C.c_void_p),
+                ("n_rows", C.c_int64), ("k_slot", C.c_void_p), ("v_slot", C.c_void_p),
+                ("out", C.c_void_p)]
+
+
+class Step(C.Structure):
+    _fields_ = [("batch", Batch), ("small", Model), ("large", Model),
+                ("head_map", C.c_void_p), ("mode", C.c_int32),
+                ("logits", C.c_void_p), ("row_max", C.c_void_p), ("row_sum", C.c_void_p),
+                ("crit_idx", C.c_void_p), ("marg_idx", C.c_void_p),
+                ("marg_prob", C.c_void_p), ("mass", C.c_void_p)]
+
+
+EXPORTS = ("smallkv_small_attn", "smallkv_partition", "smallkv_hybrid_attn", "smallkv_step",
+           "smallkv_workspace_size", "smallkv_status_string", "smallkv_abi_version")
+
+_lib = None
+
+
+def lib():
+    """Load libsmallkv.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: run `python -m paper_2508_02751_amd.build`")
+        L = C.CDLL(LIB_PATH)
+        P = C.POINTER
+        L.smallkv_small_attn.argtypes = [P(Batch), P(Model), C.c_void_p, C.c_void_p, C.c_void_p,
+                                         C.c_void_p, C.c_size_t, C.c_void_p]
+        L.smallkv_partition.argtypes = [P(Batch), C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p,
+                                        C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
+                                        C.c_void_p, C.c_size_t, C.c_void_p]
+        L.smallkv_hybrid_attn.argtypes = [P(Batch), P(Model), C.c_void_p, C.c_int32, C.c_void_p,
+                                          C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32,
+                                          C.c_void_p, C.c_size_t, C.c_void_p]
+        L.smallkv_step.argtypes = [P(Step), C.c_void_p, C.c_size_t, C.c_void_p]
+        L.smallkv_workspace_size.argtypes = [P(Step), P(C.c_size_t)]
+        L.smallkv_status_string.argtypes = [C.c_int]
+        L.smallkv_status_string.restype = C.c_char_p
+        L.smallkv_abi_version.argtypes = []
+        for f in ("smallkv_small_attn", "smallkv_partition", "smallkv_hybrid_attn",
+                  "smallkv_step", "smallkv_workspace_size", "smallkv_abi_version"):
+            getattr(L, f).restype = C.c_int
+        _lib = L
+    return _lib
+
+
+class SmallKVError(RuntimeError):
+    def __init__(self, fn, status):
+        msg = lib().smallkv_status_string(status).decode()
+        super().__init__(f"{fn} failed with status {status} ({msg})")
+        self.status = status
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise ValueError("tensors passed to libsmallkv must be contiguous")
+    return t.data_ptr()
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise ValueError(f"unsupported dtype {t.dtype}")
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream
+
+
+@dataclasses.dataclass
+class BatchSpec:
+    """Sequences and budgets: seq_len/k_crit/k_marg are int32 device tensors [B]."""
+    seq_len: torch.Tensor
+    k_crit: torch.Tensor
+    k_marg: torch.Tensor
+    n_cap: int
+    kc_cap: int
+    km_cap: int
+
+    def c(self) -> Batch:
+        for t in (self.seq_len, self.k_crit, self.k_marg):
+            if t.dtype != torch.int32:
+                raise ValueError("seq_len, k_crit and k_marg must be int32")
+        return Batch(self.seq_len.numel(), self.n_cap, _ptr(self.seq_len), _ptr(self.k_crit),
+                     _ptr(self.k_marg), self.kc_cap, self.km_cap)
+
+
+@dataclasses.dataclass
+class ModelSpec:
+    """One model's operands: q [B][L][Hq][d], k/v [B][L][Hkv][n_rows][d], out like q."""
+    q: torch.Tensor
+    k: torch.Tensor
+    v: torch.Tensor
+    out: torch.Tensor
+    scale: float
+    k_slot: Optional[torch.Tensor] = None
+    v_slot: Optional[torch.Tensor] = None
+
+    def c(self) -> Model:
+        B, L, hq, d = self.q.shape
+        hkv, rows = self.k.shape[2], self.k.shape[3]
+        if self.k.shape != self.v.shape or self.out.shape != self.q.shape:
+            raise ValueError("k/v or out shape mismatch")
+        if not (self.q.dtype == self.k.dtype == self.v.dtype == self.out.dtype):
+            raise ValueError("q, k, v and out must share a dtype")
+        for t in (self.k_slot, self.v_slot):
+            if t is not None and t.dtype != torch.int32:
+                raise ValueError("slot maps must be int32")
+        return Model(L, hq, hkv, d, _dtype_code(self.q), self.scale, _ptr(self.q), _ptr(self.k),
+                     _ptr(self.v), rows, _ptr(self.k_slot), _ptr(self.v_slot), _ptr(self.out))
+
+
+def _check(fn, rc):
+    if rc != OK:
+        raise SmallKVError(fn, rc)
+
+
+def _ws(ws: Optional[torch.Tensor]):
+    return (None, 0) if ws is None else (_ptr(ws), ws.numel() * ws.element_size())
+
+
+def smallkv_workspace_size(batch: BatchSpec, small: ModelSpec) -> int:
+    st = Step()
+    st.batch = batch.c()
+    st.small = small.c()
+    n = C.c_size_t()
+    _check("smallkv_workspace_size", lib().smallkv_workspace_size(C.byref(st), C.byref(n)))
+    return n.value
+
+
+def smallkv_small_attn(batch: BatchSpec, small: ModelSpec, logits, row_max, row_sum,
+                       ws=None, stream=None):
+    b, m = batch.c(), small.c()
+    w, wb = _ws(ws)
+    _check("smallkv_small_attn", lib().smallkv_small_attn(
+        C.byref(b), C.byref(m), _ptr(logits), _ptr(row_max), _ptr(row_sum), w, wb,
+        _stream(stream)))
+
+
+def smallkv_partition(batch: BatchSpec, n_small_heads: int, logits, row_max, row_sum,
+                      crit_idx, marg_idx, marg_prob, mass, ws=None, stream=None):
+    b = batch.c()
+    w, wb = _ws(ws)
+    _check("smallkv_partition", lib().smallkv_partition(
+        C.byref(b), n_small_heads, _ptr(logits), _ptr(row_max), _ptr(row_sum), _ptr(crit_idx),
+        _ptr(marg_idx), _ptr(marg_prob), _ptr(mass), w, wb, _stream(stream)))
+
+
+def smallkv_hybrid_attn(batch: BatchSpec, large: ModelSpec, head_map, n_small_heads: int,
+                        crit_idx, marg_idx, marg_prob, mass, mode=NORM_REMAINING, ws=None,
+                        stream=None):
+    b, m = batch.c(), large.c()
+    w, wb = _ws(ws)
+    _check("smallkv_hybrid_attn", lib().smallkv_hybrid_attn(
+        C.byref(b), C.byref(m), _ptr(head_map), n_small_heads, _ptr(crit_idx), _ptr(marg_idx),
+        _ptr(marg_prob), _ptr(mass), int(mode), w, wb, _stream(stream)))
+
+
+def make_step(batch: BatchSpec, small: ModelSpec, large: ModelSpec, head_map, mode, logits,
+              row_max, row_sum, crit_idx, marg_idx, marg_prob, mass) -> Step:
+    """Build the C step descriptor once (it holds raw pointers: keep the tensors alive)."""
+    return Step(batch.c(), small.c(), large.c(), _ptr(head_map), int(mode), _ptr(logits),
+                _ptr(row_max), _ptr(row_sum), _ptr(crit_idx), _ptr(marg_idx), _ptr(marg_prob),
+                _ptr(mass))
+
+
+def smallkv_step(step: Step, ws=None, stream=None):
+    w, wb = _ws(ws)
+    _check("smallkv_step", lib().smallkv_step(C.byref(step), w, wb, _stream(stream)))
+
+
+@dataclasses.dataclass
+class StepBuffers:
+    """The caller-owned intermediates and outputs of one decode step."""
+    logits: torch.Tensor
+    row_max: torch.Tensor
+    row_sum: torch.Tensor
+    crit_idx: torch.Tensor
+    marg_idx: torch.Tensor
+    marg_prob: torch.Tensor
+    mass: torch.Tensor
+    small_out: torch.Tensor
+    large_out: torch.Tensor
+    ws: Optional[torch.Tensor]
+
+
+def alloc_step_buffers(batch: BatchSpec, s_q: torch.Tensor, l_q: torch.Tensor,
+                       ws_bytes: int) -> StepBuffers:
+    B, l, hqs, _ = s_q.shape
+    nsh = l * hqs
+    dev = s_q.device
+    return StepBuffers(
+        logits=torch.empty((B, nsh, batch.n_cap), dtype=torch.float32, device=dev),
+        row_max=torch.empty((B, nsh), dtype=torch.float32, device=dev),
+        row_sum=torch.empty((B, nsh), dtype=torch.float32, device=dev),
+        crit_idx=torch.empty((B, nsh, batch.kc_cap), dtype=torch.int32, device=dev),
+        marg_idx=torch.empty((B, nsh, max(batch.km_cap, 1)), dtype=torch.int32, device=dev),
+        marg_prob=torch.empty((B, nsh, max(batch.km_cap, 1)), dtype=torch.float32, device=dev),
+        mass=torch.empty((B, nsh, 2), dtype=torch.float32, device=dev),
+        small_out=torch.empty_like(s_q),
+        large_out=torch.empty_like(l_q),
+        ws=torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev) if ws_bytes else None,
+    )

@@ -1,0 +1,83 @@
+"""Parity helpers: run the oracle on host copies of the exact device bytes and
+compare with the library's outputs.
+
+Tolerances (per head vector, ||gpu - ref||_inf <= tol * ||ref||_inf):
+fp32 workloads 1e-5, bf16 workloads 2e-2.  Index lists and logits must be
+bit-identical; row_max is exact (the max of identical fp32 logits).
+"""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import torch
+
+import oracle as O
+
+TOL = {torch.float32: 1e-5, torch.bfloat16: 2e-2}
+
+
+def host(t: torch.Tensor) -> np.ndarray:
+    if t.dtype == torch.bfloat16:
+        t = t.float()
+    return t.detach().cpu().numpy()
+
+
+def log(msg: str):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def oracle_step(x: dict, mode: int, k_slot=None, v_slot=None, l_k=None, l_v=None):
+    """The oracle's whole step on host copies of the inputs in `x`."""
+    from paper_2508_02751_amd.pipeline import softmax_scale
+    l_k = x["l_k"] if l_k is None else l_k
+    l_v = x["l_v"] if l_v is None else l_v
+    return O.step(
+        seq_len=host(x["seq_len"]), k_crit=host(x["k_crit"]), k_marg=host(x["k_marg"]),
+        kc_cap=int(x["kc_cap"]), km_cap=int(x["km_cap"]), head_map=host(x["head_map"]),
+        mode=mode, s_q=host(x["s_q"]), s_k=host(x["s_k"]), s_v=host(x["s_v"]),
+        s_scale=softmax_scale(x["s_q"].shape[-1]), l_q=host(x["l_q"]), l_k=host(l_k),
+        l_v=host(l_v), l_scale=softmax_scale(x["l_q"].shape[-1]),
+        k_slot=None if k_slot is None else host(k_slot),
+        v_slot=None if v_slot is None else host(v_slot))
+
+
+def head_err(got: np.ndarray, ref: np.ndarray) -> float:
+    """max over heads of ||got - ref||_inf / ||ref||_inf (last axis = head dim)."""
+    num = np.abs(got.astype(np.float64) - ref).max(-1)
+    den = np.maximum(np.abs(ref).max(-1), 1e-30)
+    return float((num / den).max())
+
+
+def compare_step(buf, ref: dict, x: dict, dtype, what: str = "", check_logits=True):
+    """Assert parity of every output of one step; returns a dict of error figures."""
+    tol = TOL[dtype]
+    seq = host(x["seq_len"]).astype(np.int64)
+    B = seq.size
+    lg = host(buf.logits)
+    if check_logits:
+        for b in range(B):
+            n = seq[b]
+            bad = (lg[b, :, :n].view(np.uint32) != ref["logits"][b, :, :n].view(np.uint32))
+            assert not bad.any(), f"{what}: {int(bad.sum())} logits differ in sequence {b}"
+    rm = host(buf.row_max)
+    assert np.array_equal(rm, ref["row_max"].astype(np.float32)), f"{what}: row_max differs"
+    rs = host(buf.row_sum)
+    np.testing.assert_allclose(rs, ref["row_sum"], rtol=1e-5, err_msg=f"{what}: row_sum")
+    crit = host(buf.crit_idx)[..., : ref["crit"].shape[-1]]
+    assert np.array_equal(crit, ref["crit"]), f"{what}: critical index lists differ"
+    km = ref["marg"].shape[-1]
+    if km:
+        marg = host(buf.marg_idx)[..., :km]
+        assert np.array_equal(marg, ref["marg"]), f"{what}: marginal index lists differ"
+        mp = host(buf.marg_prob)[..., :km]
+        np.testing.assert_allclose(mp, ref["marg_prob"], rtol=2e-5, atol=1e-9,
+                                   err_msg=f"{what}: marg_prob")
+    np.testing.assert_allclose(host(buf.mass), ref["mass"], rtol=2e-5, atol=2e-7,
+                               err_msg=f"{what}: mass")
+    es = head_err(host(buf.small_out), ref["small_out"])
+    el = head_err(host(buf.large_out), ref["large_out"])
+    assert es <= tol, f"{what}: small-model output error {es:.3g} > {tol}"
+    assert el <= tol, f"{what}: large-model output error {el:.3g} > {tol}"
+    return {"small_out_err": es, "large_out_err": el}

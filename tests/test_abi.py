@@ -1,0 +1,101 @@
+"""The C-ABI library loads, exports every function include/smallkv.h declares,
+and rejects host-detectable misuse before touching the GPU (no compute calls
+here: this file runs without a GPU)."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+from paper_2508_02751_amd import smallkv as S
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "smallkv.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(smallkv_\w+)\s*\(", text, flags=re.M)))
+
+
+def test_header_declares_the_four_stage_calls():
+    names = declared_functions()
+    for f in ("smallkv_small_attn", "smallkv_partition", "smallkv_hybrid_attn", "smallkv_step"):
+        assert f in names
+
+
+def test_library_exports_every_declared_symbol():
+    L = S.lib()
+    for name in declared_functions():
+        assert hasattr(L, name), name
+    assert set(S.EXPORTS) >= set(declared_functions())
+
+
+def test_abi_version_and_status_strings():
+    L = S.lib()
+    assert L.smallkv_abi_version() == 1
+    assert L.smallkv_status_string(0) == b"ok"
+    assert L.smallkv_status_string(-3) == b"workspace too small"
+    assert L.smallkv_status_string(123) == b"unknown status"
+
+
+def _fake_step(**over):
+    """A descriptor with plausible (never dereferenced) pointers."""
+    p = 0x1000
+    b = S.Batch(1, 512, p, p, p, 64, 128)
+    sm = S.Model(1, 14, 2, 64, S.BF16, 0.125, p, p, p, 512, None, None, p)
+    lg = S.Model(1, 28, 4, 128, S.BF16, 0.088, p, p, p, 512, None, None, p)
+    st = S.Step(b, sm, lg, p, 0, p, p, p, p, p, p, p)
+    for k, v in over.items():
+        obj, field = k.split("__")
+        setattr({"b": st.batch, "s": st.small, "l": st.large, "st": st}[obj], field, v)
+    return st
+
+
+@pytest.mark.parametrize("over,status", [
+    ({"s__head_dim": 96}, S.EUNSUPPORTED),
+    ({"s__n_q_heads": 13}, S.EINVAL),
+    ({"s__dtype": 7}, S.EINVAL),
+    ({"s__q": None}, S.EINVAL),
+    ({"b__batch": 0}, S.EINVAL),
+    ({"b__kc_cap": 0}, S.EINVAL),
+    ({"b__seq_len": None}, S.EINVAL),
+    ({"s__n_rows": 100}, S.EINVAL),
+    ({"s__k_slot": 0x1000}, S.EINVAL),
+    ({"s__n_q_heads": 34, "s__n_kv_heads": 2}, S.EUNSUPPORTED),
+])
+def test_workspace_size_rejects_bad_small_model(over, status):
+    n = C.c_size_t()
+    assert S.lib().smallkv_workspace_size(C.byref(_fake_step(**over)), C.byref(n)) == status
+
+
+@pytest.mark.parametrize("over,status", [
+    ({"l__head_dim": 80}, S.EUNSUPPORTED),
+    ({"l__n_kv_heads": 3}, S.EINVAL),
+    ({"st__mode": 9}, S.EINVAL),
+    ({"st__head_map": None}, S.EINVAL),
+    ({"st__logits": None}, S.EINVAL),
+    ({"l__k_slot": 0x1000}, S.EINVAL),          # one slot map without the other
+    ({"l__n_rows": 100}, S.EINVAL),             # compact rows need slot maps
+    ({"b__kc_cap": 20000}, S.EUNSUPPORTED),
+])
+def test_step_rejects_before_launch(over, status):
+    st = _fake_step(**over)
+    assert S.lib().smallkv_step(C.byref(st), None, 0, None) == status
+
+
+def test_step_needs_workspace():
+    st = _fake_step()
+    n = C.c_size_t()
+    assert S.lib().smallkv_workspace_size(C.byref(st), C.byref(n)) == 0 and n.value > 0
+    assert S.lib().smallkv_step(C.byref(st), None, 0, None) == S.EWORKSPACE
+    assert S.lib().smallkv_step(C.byref(st), C.c_void_p(0x1000), n.value - 1, None) == S.EWORKSPACE
+
+
+def test_partition_and_hybrid_reject_nulls():
+    b = S.Batch(1, 512, 0x1000, 0x1000, 0x1000, 64, 128)
+    L = S.lib()
+    assert L.smallkv_partition(C.byref(b), 14, None, 1, 1, 1, 1, 1, 1, None, 0, None) == S.EINVAL
+    lg = S.Model(1, 28, 4, 128, S.BF16, 0.088, 1, 1, 1, 512, None, None, 1)
+    assert L.smallkv_hybrid_attn(C.byref(b), C.byref(lg), None, 14, 1, 1, 1, 1, 0, None, 0,
+                                 None) == S.EINVAL

@@ -1,0 +1,212 @@
+"""GPU parity: the library (through the C ABI) against the CPU oracle on the
+same seeded inputs.  Index sets and logits bit-exact, outputs within the
+per-dtype tolerance of tests/parity.py."""
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from parity import compare_step, host, log, oracle_step
+from paper_2508_02751_amd import smallkv as S
+from paper_2508_02751_amd import workloads as W
+from paper_2508_02751_amd.pipeline import prepare_step
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+def run_case(w, mode=S.NORM_REMAINING, mutate=None, step=0, what=None):
+    what = what or w.name
+    log(f"[parity] {what} mode={mode}")
+    x = W.make_step_inputs(w, DEV, step)
+    if mutate is not None:
+        mutate(x)
+    ps = prepare_step(x, mode)
+    ps.run()
+    torch.cuda.synchronize()
+    ref = oracle_step(x, mode)
+    errs = compare_step(ps.buf, ref, x, w.torch_dtype, what)
+    log(f"[parity] {what} ok {errs}")
+    return ps, x, ref
+
+
+def custom(name, wid, batch, n, dtype, small, large, crit, marg, **kw):
+    return W.Workload(wid, name, batch, n, dtype, small, large, crit, marg, **kw)
+
+
+# ---------------------------------------------------------------- configs --
+
+@pytest.mark.parametrize("mode", O.MODES)
+def test_config1_tiny_f32_all_modes(mode):
+    run_case(W.WORKLOADS[1], mode)
+
+
+def test_config2_qwen2_7b_full_step():
+    run_case(W.WORKLOADS[2])
+
+
+# ------------------------------------------------------------- edge cases --
+
+SMALL = W.ModelShape(2, 8, 2, 64)
+LARGE = W.ModelShape(3, 12, 4, 128)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_ragged_lengths_and_budget_clamps(dtype):
+    """Lengths from 1 to n_cap; budgets above some lengths (|C| = N, M empty)."""
+    w = custom(f"ragged-{dtype}", 101, 5, 700, dtype, SMALL, LARGE, ("abs", 40), ("abs", 70),
+               ragged_min=1)
+    run_case(w)
+
+
+def test_single_token_sequences():
+    w = custom("n1", 102, 3, 1, "bf16", SMALL, LARGE, ("abs", 4), ("abs", 4))
+    run_case(w)
+
+
+def test_no_marginal_budget():
+    w = custom("km0", 103, 2, 513, "bf16", SMALL, LARGE, ("abs", 33), ("abs", 0))
+    run_case(w)
+
+
+def test_everything_critical():
+    w = custom("all-crit", 104, 2, 300, "f32", SMALL, LARGE, ("abs", 300), ("abs", 50))
+    run_case(w)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_ties_from_duplicated_keys(dtype):
+    """Duplicated small-model key rows give equal logits; the lower index wins."""
+    w = custom(f"ties-{dtype}", 105, 2, 1500, dtype, SMALL, LARGE, ("pct", 10), ("pct", 25))
+
+    def dup(x):
+        k = x["s_k"]
+        src = torch.arange(k.shape[3], device=k.device)
+        src = torch.where(src % 3 == 0, (src * 7 + 1) % k.shape[3], src)
+        x["s_k"] = k[:, :, :, src].contiguous()
+
+    run_case(w, mutate=dup)
+
+
+@pytest.mark.parametrize("sd,ld", [(128, 64), (128, 128), (64, 64)])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_head_dims(sd, ld, dtype):
+    w = custom(f"dims-{sd}-{ld}-{dtype}", 106, 2, 600, dtype, W.ModelShape(2, 4, 1, sd),
+               W.ModelShape(2, 8, 2, ld), ("abs", 50), ("abs", 120), ragged_min=200)
+    run_case(w)
+
+
+@pytest.mark.parametrize("g", [1, 3, 5, 16])
+def test_small_group_sizes(g):
+    w = custom(f"group{g}", 107, 2, 900, "bf16", W.ModelShape(2, g * 2, 2, 64),
+               W.ModelShape(2, 8, 8, 128), ("abs", 90), ("abs", 100))
+    run_case(w)
+
+
+def test_long_rows_multi_chunk():
+    """Rows long enough to need several chunks per unit and several radix bins."""
+    w = custom("long", 108, 1, 40000, "bf16", W.ModelShape(1, 4, 1, 64),
+               W.ModelShape(1, 8, 2, 128), ("pct", 5), ("pct", 15))
+    run_case(w)
+
+
+def test_deterministic_repeat():
+    w = W.WORKLOADS[1]
+    x = W.make_step_inputs(w, DEV)
+    ps = prepare_step(x)
+    ps.run()
+    torch.cuda.synchronize()
+    first = {f.name: getattr(ps.buf, f.name).clone() for f in dataclasses.fields(ps.buf)
+             if f.name != "ws"}
+    for _ in range(3):
+        ps.run()
+    torch.cuda.synchronize()
+    for k, v in first.items():
+        assert torch.equal(v.view(torch.uint8), getattr(ps.buf, k).view(torch.uint8)), k
+
+
+# --------------------------------------------------- single-stage entries --
+
+def test_single_stage_calls_match_step():
+    w = custom("stages", 109, 3, 2000, "bf16", SMALL, LARGE, ("pct", 10), ("pct", 20),
+               ragged_min=500)
+    x = W.make_step_inputs(w, DEV)
+    ps = prepare_step(x)
+    ps.run()
+    b = ps.buf
+    nsh = SMALL.layers * SMALL.q_heads
+    lg, rm, rs = torch.empty_like(b.logits), torch.empty_like(b.row_max), torch.empty_like(b.row_sum)
+    small = S.ModelSpec(ps.small.q, ps.small.k, ps.small.v, torch.empty_like(ps.small.out),
+                        ps.small.scale)
+    S.smallkv_small_attn(ps.batch, small, lg, rm, rs, b.ws)
+    ci, mi = torch.empty_like(b.crit_idx), torch.empty_like(b.marg_idx)
+    mp, ms = torch.empty_like(b.marg_prob), torch.empty_like(b.mass)
+    S.smallkv_partition(ps.batch, nsh, lg, rm, rs, ci, mi, mp, ms)
+    large = S.ModelSpec(ps.large.q, ps.large.k, ps.large.v, torch.empty_like(ps.large.out),
+                        ps.large.scale)
+    S.smallkv_hybrid_attn(ps.batch, large, ps.head_map, nsh, ci, mi, mp, ms)
+    torch.cuda.synchronize()
+    seq = host(x["seq_len"])
+    for bi in range(3):
+        n = int(seq[bi])
+        assert torch.equal(lg[bi, :, :n], b.logits[bi, :, :n])
+    for got, want in ((rm, b.row_max), (rs, b.row_sum), (ci, b.crit_idx), (mi, b.marg_idx),
+                      (mp, b.marg_prob), (ms, b.mass), (small.out, b.small_out),
+                      (large.out, b.large_out)):
+        assert torch.equal(got, want)
+
+
+# ------------------------------------------------------- compact stores --
+
+def compact_store(x, ref):
+    """Large K held for union(C) and V for union(C u M) of the query heads of
+    each (sequence, layer, kv head), with token->row slot maps (test-side
+    bookkeeping from the oracle's partition)."""
+    l_k, l_v, hm = x["l_k"], x["l_v"], host(x["head_map"])
+    B, L, hk, n_cap, d = l_k.shape
+    hq = x["l_q"].shape[2]
+    g = hq // hk
+    ks = np.full((B, L, hk, n_cap), -1, np.int32)
+    vs = np.full((B, L, hk, n_cap), -1, np.int32)
+    kr, vr = [], []
+    for b in range(B):
+        for li in range(L):
+            for kv in range(hk):
+                js = [hm[li * hq + kv * g + i] for i in range(g)]
+                c = sorted(set(int(t) for j in js for t in ref["crit"][b, j] if t >= 0))
+                m = sorted(set(int(t) for j in js for t in ref["marg"][b, j] if t >= 0) | set(c))
+                kr.append(c)
+                vr.append(m)
+    R = max(max(len(r) for r in kr), max(len(r) for r in vr), 1)
+    ck = torch.zeros((B, L, hk, R, d), dtype=l_k.dtype, device=l_k.device)
+    cv = torch.zeros_like(ck)
+    u = 0
+    for b in range(B):
+        for li in range(L):
+            for kv in range(hk):
+                # rows in reverse token order so row != token
+                for rows, src, dst, slot in ((kr[u], l_k, ck, ks), (vr[u], l_v, cv, vs)):
+                    idx = torch.tensor(rows[::-1], dtype=torch.long, device=l_k.device)
+                    dst[b, li, kv, : len(rows)] = src[b, li, kv, idx]
+                    slot[b, li, kv, rows[::-1]] = np.arange(len(rows), dtype=np.int32)
+                u += 1
+    return ck, cv, torch.from_numpy(ks).to(l_k.device), torch.from_numpy(vs).to(l_k.device)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_compact_store_with_slot_maps(dtype):
+    w = custom(f"compact-{dtype}", 110, 2, 1200, dtype, SMALL, LARGE, ("pct", 5),
+               ("pct", 15), ragged_min=600)
+    x = W.make_step_inputs(w, DEV)
+    ref_full = oracle_step(x, S.NORM_REMAINING)
+    ck, cv, ks, vs = compact_store(x, ref_full)
+    log(f"[parity] compact store rows {ck.shape[3]} of {x['l_k'].shape[3]}")
+    ps = prepare_step(x, k_slot=ks, v_slot=vs, l_k=ck, l_v=cv)
+    ps.run()
+    torch.cuda.synchronize()
+    ref = oracle_step(x, S.NORM_REMAINING, k_slot=ks, v_slot=vs, l_k=ck, l_v=cv)
+    np.testing.assert_array_equal(ref["large_out"], ref_full["large_out"])
+    compare_step(ps.buf, ref, x, w.torch_dtype, f"compact-{dtype}")
