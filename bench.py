@@ -1,0 +1,241 @@
+"""Benchmark of one SmallKV decode step on one MI355X.
+
+A step is the whole hot path over one batch: stage 1 (small-model decode
+attention over all its layers), stage 2 (partition of every small head),
+stage 3 (hybrid attention of every large layer).  Workload: the Qwen2-7B
+(28 layers, 28q/4kv, d=128) + Qwen2-0.5B (24 layers, 14q/2kv, d=64) shapes,
+bf16, batch 1, context 8192, critical 10% / marginal 20%.
+
+Timing: inputs are resident in HBM; the step is captured in one HIP graph per
+input copy, and consecutive steps rotate over `--rotate` copies so that a
+step never finds the previous step's operands in the 256 MB MALL.  W warm-up
+steps, then exactly K timed steps between two synchronisations.  A second
+pass with HIP events between the stages (enqueued behind a sleep kernel so
+the host never starves the GPU) gives per-stage kernel durations for the
+roofline.  The CPU baseline is the oracle on one host core over whole steps.
+
+Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, 8 TB/s
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=100)
+    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--rotate", type=int, default=4, help="input copies cycled through")
+    p.add_argument("--workload", type=int, default=2, help=argparse.SUPPRESS)
+    p.add_argument("--eager", action="store_true", help="launch without HIP graphs")
+    p.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time budget")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--copy-probe-mib", type=int, default=0,
+                   help="first run a plain device copy of this many MiB (counter calibration)")
+    return p.parse_args()
+
+
+def source_hash(name: str) -> str:
+    path = os.path.join(ROOT, "paper_2508_02751_amd", "csrc", name)
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+
+
+def load_traffic(kernel_src: str, launches_per_step: int):
+    """HBM bytes per launch from committed rocprofv3 --pmc summaries, or None
+    when the kernel source changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        t = json.load(open(path))
+        e = t["kernels"][kernel_src]
+    except (KeyError, ValueError):
+        return None
+    if e.get("source_sha256_16") != source_hash(kernel_src):
+        return None
+    return e.get("hbm_bytes_per_launch")
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py: this build runs on one GPU only; the multi-GPU sharding is a design "
+              "(see the sharding section of DESIGN.md), so --gpus must be 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2508_02751_amd import smallkv as S
+    from paper_2508_02751_amd import workloads as W
+    from paper_2508_02751_amd.bytes_model import step_bytes
+    from paper_2508_02751_amd.pipeline import prepare_step
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = W.WORKLOADS[args.workload]
+    if args.copy_probe_mib:
+        src = torch.ones(args.copy_probe_mib << 18, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+    print(f"[bench] generating {w.name}", file=sys.stderr, flush=True)
+    x0 = W.make_step_inputs(w, dev)
+    copies = [x0]
+    for _ in range(args.rotate - 1):
+        copies.append({k: (v.clone() if torch.is_tensor(v) else v) for k, v in x0.items()})
+    preps = [prepare_step(x) for x in copies]
+    stream = torch.cuda.current_stream()
+
+    # warm-up (eager), also builds the partitions used for byte accounting
+    for i in range(max(args.warmup, 1)):
+        preps[i % len(preps)].run()
+    torch.cuda.synchronize()
+
+    graphs = None
+    if not args.eager:
+        graphs = []
+        for ps in preps:
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                ps.run()
+            graphs.append(g)
+        for i in range(max(args.warmup, 1)):
+            graphs[i % len(graphs)].replay()
+        torch.cuda.synchronize()
+
+    # ---- timed region: exactly K steps ------------------------------------
+    K = args.steps
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(K):
+        if graphs is not None:
+            graphs[i % len(graphs)].replay()
+        else:
+            preps[i % len(preps)].run()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_per_step = (t1 - t0) * 1e3 / K
+
+    # ---- per-stage kernel durations with HIP events -------------------------
+    nsh = w.small.layers * w.small.q_heads
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    torch.cuda._sleep(50_000_000)  # keep the GPU busy while the host enqueues
+    for i in range(K):
+        ps = preps[i % len(preps)]
+        b = ps.buf
+        e = ev[i]
+        e[0].record(stream)
+        S.smallkv_small_attn(ps.batch, ps.small, b.logits, b.row_max, b.row_sum, b.ws, stream)
+        e[1].record(stream)
+        S.smallkv_partition(ps.batch, nsh, b.logits, b.row_max, b.row_sum, b.crit_idx,
+                            b.marg_idx, b.marg_prob, b.mass, None, stream)
+        e[2].record(stream)
+        S.smallkv_hybrid_attn(ps.batch, ps.large, ps.head_map, nsh, b.crit_idx, b.marg_idx,
+                              b.marg_prob, b.mass, ps.mode, None, stream)
+        e[3].record(stream)
+    torch.cuda.synchronize()
+    stage_ms = [sum(ev[i][s].elapsed_time(ev[i][s + 1]) for i in range(K)) / K for s in range(3)]
+
+    # ---- bytes ------------------------------------------------------------
+    ps = preps[0]
+    sb = step_bytes(ps.inputs, ps.buf.crit_idx, ps.buf.marg_idx, ps.batch.km_cap)
+    stage_bytes = [sb.stage1, sb.stage2, sb.stage3]
+    stage_names = ["small_attn_split+small_attn_merge", "partition_kernel", "hybrid_kernel"]
+    stage_src = ["small_attn.hip", "partition.hip", "hybrid.hip"]
+    dom = max(range(3), key=lambda s: stage_ms[s])
+    achieved = stage_bytes[dom] / (stage_ms[dom] * 1e-3) / 1e9
+    traffic = load_traffic(stage_src[dom], 1)
+    step_gbs = sb.step_compulsory / (ms_per_step * 1e-3) / 1e9
+
+    # ---- CPU baseline: the oracle on one core ------------------------------
+    cpu = None
+    if not args.no_cpu_baseline:
+        sys.path.insert(0, os.path.join(ROOT, "oracle"))
+        import oracle as O
+        from paper_2508_02751_amd.pipeline import softmax_scale
+
+        def h(t):
+            return t.detach().float().cpu().numpy() if t.dtype == torch.bfloat16 else t.cpu().numpy()
+
+        x = ps.inputs
+        host = {k: h(x[k]) for k in ("seq_len", "k_crit", "k_marg", "head_map", "s_q", "s_k",
+                                     "s_v", "l_q", "l_k", "l_v")}
+        try:
+            os.sched_setaffinity(0, {sorted(os.sched_getaffinity(0))[0]})
+        except (AttributeError, OSError):
+            pass
+        print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
+        reps, spent = 0, 0.0
+        while reps < 1 or spent < args.cpu_seconds:
+            c0 = time.perf_counter()
+            O.step(seq_len=host["seq_len"], k_crit=host["k_crit"], k_marg=host["k_marg"],
+                   kc_cap=x["kc_cap"], km_cap=x["km_cap"], head_map=host["head_map"],
+                   mode=O.NORM_REMAINING, s_q=host["s_q"], s_k=host["s_k"], s_v=host["s_v"],
+                   s_scale=softmax_scale(w.small.head_dim), l_q=host["l_q"], l_k=host["l_k"],
+                   l_v=host["l_v"], l_scale=softmax_scale(w.large.head_dim))
+            spent += time.perf_counter() - c0
+            reps += 1
+        cpu = {"value": w.batch * reps / spent, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+               "sample": f"{reps} whole decode step(s) of the same workload, single-threaded C "
+                         f"oracle pinned to one core ({spent:.1f} s)"}
+
+    out = {
+        "metric": "SmallKV decode-step attention tokens/s at 1 MI355X; % of HBM roofline",
+        "value": w.batch * 1e3 / ms_per_step,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": w.name,
+            "large": "28 layers, 28q/4kv, d=128", "small": "24 layers, 14q/2kv, d=64",
+            "kv_dtype": "bf16", "batch": w.batch, "context": w.n_ctx,
+            "critical": "10%", "marginal": "20%", "launch": "eager" if args.eager else "hip-graph",
+            "rotated_input_copies": args.rotate,
+        },
+        "roofline": {
+            "kernel": stage_names[dom],
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS,
+            "traffic": traffic,
+        },
+        "step": {
+            "compulsory_bytes": sb.step_compulsory,
+            "achieved_GBs": step_gbs,
+            "hbm_frac": step_gbs / HBM_PEAK_GBS,
+            "stage_ms": stage_ms,
+            "stage_bytes": stage_bytes,
+            "stage_GBs": [stage_bytes[s] / (stage_ms[s] * 1e-3) / 1e9 for s in range(3)],
+            "large_rows_per_head_over_union": (sb.large_k_perhead + sb.large_v_perhead)
+            / max(1, sb.large_k_union + sb.large_v_union),
+            "index_metadata_bytes": sb.index_meta,
+        },
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

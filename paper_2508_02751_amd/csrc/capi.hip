@@ -140,11 +140,11 @@ int smallkv_step(const smallkv_step_t *s, void *ws, size_t ws_bytes, void *strea
   const SmallPlan p = plan_small(s->batch, s->small);
   if (p.ws_bytes && (!ws || ws_bytes < p.ws_bytes)) return SMALLKV_EWORKSPACE;
   hipStream_t st = static_cast<hipStream_t>(stream);
-  hipError_t e = launch_small_attn(s->batch, s->small, s->logits, s->row_max, s->row_sum,
-                                   static_cast<float *>(ws), p, st);
+  hipError_t e = launch_small_split(s->batch, s->small, s->logits, static_cast<float *>(ws), p, st);
   if (e != hipSuccess) return SMALLKV_EDEVICE;
-  e = launch_partition(s->batch, nsh, s->logits, s->row_max, s->row_sum, s->crit_idx,
-                       s->marg_idx, s->marg_prob, s->mass, st);
+  e = launch_merge_partition(s->batch, s->small, p, static_cast<const float *>(ws), s->logits,
+                             s->row_max, s->row_sum, s->crit_idx, s->marg_idx, s->marg_prob,
+                             s->mass, st);
   if (e != hipSuccess) return SMALLKV_EDEVICE;
   e = launch_hybrid(s->batch, s->large, s->head_map, nsh, s->crit_idx, s->marg_idx, s->marg_prob,
                     s->mass, s->mode, st);

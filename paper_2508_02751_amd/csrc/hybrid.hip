@@ -2,14 +2,17 @@
 // "Calculate attention output O_c of critical tokens ... O_m of marginal
 // tokens ... Attention Output by O_c + O_m").
 //
-// One workgroup per (sequence, layer, large query head).  Large head i reads
-// the partition of small head f(i) from head_map.
-//   Phase 1: gather the K rows of the critical tokens (LPR lanes per row,
-//            16 bytes per lane, so a wave reads 64/LPR rows per instruction),
-//            dot with q, reduce across the row's lanes -> logits in LDS.
+// One workgroup per (sequence, layer, large query head); large head i reads
+// the partition of small head f(i) through head_map.
+//   Phase 1: the K rows of the critical tokens are gathered, LPR lanes per
+//            row and 16 bytes per lane; each wave takes a block of entries,
+//            loads their indices with one coalesced load, hands them out
+//            with lane shuffles and keeps a whole block of row loads in
+//            flight; the row's lanes reduce their partial dots with DPP and
+//            the logits go to LDS.
 //   Phase 2: softmax over the critical logits (workgroup max and sum), then
-//            one gather of V rows for critical and marginal tokens with
-//            weights alpha_C*e_t/Z_C and alpha_M*p'_t into one accumulator.
+//            one gather of V rows for critical and marginal tokens, weights
+//            alpha_C*e_t/Z_C and alpha_M*p'_t, into one accumulator.
 // Workgroups are numbered so that the query heads sharing a kv head land on
 // the same XCD back to back: their gathered rows overlap and hit in that
 // XCD's L2.
@@ -20,6 +23,7 @@ namespace smallkv {
 namespace {
 
 constexpr int kHT = 256;
+constexpr int kNW = kHT / kWave;
 constexpr int kXcd = 8;
 
 struct HybArgs {
@@ -59,16 +63,35 @@ __device__ __forceinline__ void alphas(int mode, float sc, float sm, float &ac, 
   }
 }
 
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xf, 0xf, false));
+}
+
+// Sum over the LPR consecutive lanes that hold one row; every lane of the
+// group ends with the sum.  DPP inside 16-lane rows, one shuffle beyond.
+template <int LPR>
+__device__ __forceinline__ float row_reduce(float x) {
+  x += dpp<0xB1>(x);   // quad_perm [1,0,3,2]: lane ^ 1
+  x += dpp<0x4E>(x);   // quad_perm [2,3,0,1]: lane ^ 2
+  x += dpp<0x141>(x);  // row_half_mirror: lane i <-> 7-i inside 8
+  if constexpr (LPR >= 16) x += dpp<0x140>(x);  // row_mirror: lane i <-> 15-i inside 16
+  if constexpr (LPR >= 32) x += __shfl_xor(x, 16, kWave);
+  return x;
+}
+
 template <typename T, int D>
 __global__ __launch_bounds__(kHT) void hybrid_kernel(HybArgs a) {
-  constexpr int EPL = elem<T>::per16;        // elements per lane (one 16-byte load)
-  constexpr int LPR = D / EPL;               // lanes per row
-  constexpr int RPW = kWave / LPR;           // rows per wave instruction
-  constexpr int NW = kHT / kWave;
-  constexpr int RPB = RPW * NW;              // rows per workgroup step
-  extern __shared__ float s_crit[];          // [kc_cap] logits, then weights
-  __shared__ float red[NW];
-  __shared__ float accbuf[NW][D];
+  constexpr int EPL = elem<T>::per16;            // elements per lane (one 16-byte load)
+  constexpr int LPR = D / EPL;                   // lanes per row
+  constexpr int RPW = kWave / LPR;               // rows per wave instruction
+  constexpr int NSUB = 16;                       // row loads in flight per lane
+  constexpr int BE = RPW * NSUB < kWave ? RPW * NSUB : kWave;  // entries per wave block
+  constexpr int NS = BE / RPW;                   // sub-steps per block
+  static_assert(LPR >= 8 && LPR <= 32, "lane group size");
+  extern __shared__ float s_crit[];  // [kc_cap] logits, then exp weights
+  __shared__ float red[kNW];
+  __shared__ float accbuf[kNW][D];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int sub = lane % LPR, rg = lane / LPR;
@@ -82,51 +105,47 @@ __global__ __launch_bounds__(kHT) void hybrid_kernel(HybArgs a) {
   const int j = clampi(a.head_map[layer * a.hq + h], 0, a.nsh - 1);
   const int64_t row = (int64_t)b * a.nsh + j;
   const Sizes sz = set_sizes(a.seq_len, a.k_crit, a.k_marg, b, a.n_cap, a.kc_cap, a.km_cap);
-  const int nc = sz.nc, nm = sz.nm;
+  const int nc = sz.nc, nm = sz.nm, ntot = sz.nc + sz.nm;
   const int32_t *crit = a.crit + row * a.kc_cap;
   const int32_t *marg = a.marg + row * a.km_cap;
   const float *mp = a.marg_prob + row * a.km_cap;
 
   const int64_t qrow = ((int64_t)b * a.layers + layer) * a.hq + h;
   float qv[EPL];
-  {
-    const uint4 w = *reinterpret_cast<const uint4 *>(reinterpret_cast<const unsigned char *>(a.q) +
-                                                     (qrow * D + sub * EPL) * (int64_t)sizeof(T));
-    elem<T>::unpack(w, qv);
-  }
-  const unsigned char *kb = reinterpret_cast<const unsigned char *>(a.k) +
-                            (int64_t)u * a.n_rows * D * (int64_t)sizeof(T) + sub * 16;
-  const unsigned char *vb = reinterpret_cast<const unsigned char *>(a.v) +
-                            (int64_t)u * a.n_rows * D * (int64_t)sizeof(T) + sub * 16;
+  elem<T>::unpack(*reinterpret_cast<const uint4 *>(reinterpret_cast<const unsigned char *>(a.q) +
+                                                   (qrow * D + sub * EPL) * (int64_t)sizeof(T)),
+                  qv);
+  const int64_t rowb = D * (int64_t)sizeof(T);
+  const unsigned char *kb = reinterpret_cast<const unsigned char *>(a.k) + (int64_t)u * a.n_rows * rowb + sub * 16;
+  const unsigned char *vb = reinterpret_cast<const unsigned char *>(a.v) + (int64_t)u * a.n_rows * rowb + sub * 16;
   const int32_t *ks = a.k_slot ? a.k_slot + (int64_t)u * a.n_cap : nullptr;
   const int32_t *vs = a.v_slot ? a.v_slot + (int64_t)u * a.n_cap : nullptr;
-  const int64_t rowb = D * (int64_t)sizeof(T);
   const int last_row = (int)(a.n_rows - 1);
 
   // ---- phase 1: critical logits -----------------------------------------
   float lmax = -INFINITY;
-  for (int i0 = wave * RPW; i0 < nc; i0 += RPB * 4) {
-    int r[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int i = i0 + k * RPB + rg;
-      int t = i < nc ? crit[i] : 0;
-      t = clampi(t, 0, a.n_cap - 1);
-      r[k] = clampi(ks ? ks[t] : t, 0, last_row);
+  for (int base = wave * BE; base < nc; base += kNW * BE) {
+    const int my = base + lane;
+    int r = 0;
+    if (lane < BE && my < nc) {
+      const int t = clampi(crit[my], 0, a.n_cap - 1);
+      r = clampi(ks ? ks[t] : t, 0, last_row);
     }
-    uint4 w[4];
+    uint4 w[NS];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) w[k] = *reinterpret_cast<const uint4 *>(kb + r[k] * rowb);
+    for (int k = 0; k < NS; ++k) {
+      const int rk = __shfl(r, k * RPW + rg, kWave);
+      w[k] = *reinterpret_cast<const uint4 *>(kb + rk * rowb);
+    }
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
+    for (int k = 0; k < NS; ++k) {
       float kv[EPL];
       elem<T>::unpack(w[k], kv);
       float d = 0.0f;
 #pragma unroll
       for (int e = 0; e < EPL; ++e) d = __builtin_fmaf(qv[e], kv[e], d);
-#pragma unroll
-      for (int o = 1; o < LPR; o <<= 1) d += __shfl_xor(d, o, kWave);
-      const int i = i0 + k * RPB + rg;
+      d = row_reduce<LPR>(d);
+      const int i = base + k * RPW + rg;
       if (i < nc) {
         const float s = d * a.scale;
         if (sub == 0) s_crit[i] = s;
@@ -139,7 +158,7 @@ __global__ __launch_bounds__(kHT) void hybrid_kernel(HybArgs a) {
   __syncthreads();
   float m = red[0];
 #pragma unroll
-  for (int w = 1; w < NW; ++w) m = fmaxf(m, red[w]);
+  for (int w = 1; w < kNW; ++w) m = fmaxf(m, red[w]);
   __syncthreads();
   float zl = 0.0f;
   for (int i = tid; i < nc; i += kHT) {
@@ -152,7 +171,7 @@ __global__ __launch_bounds__(kHT) void hybrid_kernel(HybArgs a) {
   __syncthreads();
   float z = 0.0f;
 #pragma unroll
-  for (int w = 0; w < NW; ++w) z += red[w];
+  for (int w = 0; w < kNW; ++w) z += red[w];
   float ac, am;
   alphas(a.mode, a.mass[2 * row], a.mass[2 * row + 1], ac, am);
   const float wc = ac / z;
@@ -161,35 +180,37 @@ __global__ __launch_bounds__(kHT) void hybrid_kernel(HybArgs a) {
   float acc[EPL];
 #pragma unroll
   for (int e = 0; e < EPL; ++e) acc[e] = 0.0f;
-  const int ntot = nc + nm;
-  for (int i0 = wave * RPW; i0 < ntot; i0 += RPB * 4) {
-    int r[4];
-    float wt[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int i = i0 + k * RPB + rg;
-      int t = 0;
-      float wgt = 0.0f;
-      if (i < nc) {
-        t = crit[i];
-        wgt = s_crit[i] * wc;
-      } else if (i < ntot) {
-        t = marg[i - nc];
-        wgt = mp[i - nc] * am;
+  for (int base = wave * BE; base < ntot; base += kNW * BE) {
+    const int my = base + lane;
+    int r = 0;
+    float wt = 0.0f;
+    if (lane < BE && my < ntot) {
+      int t;
+      if (my < nc) {
+        t = crit[my];
+        wt = s_crit[my] * wc;
+      } else {
+        t = marg[my - nc];
+        wt = mp[my - nc] * am;
       }
       t = clampi(t, 0, a.n_cap - 1);
-      r[k] = clampi(vs ? vs[t] : t, 0, last_row);
-      wt[k] = wgt;
+      r = clampi(vs ? vs[t] : t, 0, last_row);
     }
-    uint4 w[4];
+    uint4 w[NS];
+    float wk[NS];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) w[k] = *reinterpret_cast<const uint4 *>(vb + r[k] * rowb);
+    for (int k = 0; k < NS; ++k) {
+      const int src = k * RPW + rg;
+      const int rk = __shfl(r, src, kWave);
+      wk[k] = __shfl(wt, src, kWave);
+      w[k] = *reinterpret_cast<const uint4 *>(vb + rk * rowb);
+    }
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
+    for (int k = 0; k < NS; ++k) {
       float vv[EPL];
       elem<T>::unpack(w[k], vv);
 #pragma unroll
-      for (int e = 0; e < EPL; ++e) acc[e] = __builtin_fmaf(wt[k], vv[e], acc[e]);
+      for (int e = 0; e < EPL; ++e) acc[e] = __builtin_fmaf(wk[k], vv[e], acc[e]);
     }
   }
 #pragma unroll
@@ -204,7 +225,7 @@ __global__ __launch_bounds__(kHT) void hybrid_kernel(HybArgs a) {
   if (tid < D) {
     float o = 0.0f;
 #pragma unroll
-    for (int w = 0; w < NW; ++w) o += accbuf[w][tid];
+    for (int w = 0; w < kNW; ++w) o += accbuf[w][tid];
     elem<T>::store1(a.out, qrow * D + tid, o);
   }
 }

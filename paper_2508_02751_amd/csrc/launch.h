@@ -24,6 +24,18 @@ hipError_t launch_small_attn(const smallkv_batch_t &b, const smallkv_model_t &m,
                              float *row_max, float *row_sum, float *ws, const SmallPlan &p,
                              hipStream_t st);
 
+// Stage 1 without the merge: per-chunk records only (smallkv_step merges
+// them inside the partition kernel).
+hipError_t launch_small_split(const smallkv_batch_t &b, const smallkv_model_t &m, float *logits,
+                              float *ws, const SmallPlan &p, hipStream_t st);
+
+// Stage 2 fused with stage 1's merge: writes row_max, row_sum and the small
+// model's output, then partitions.
+hipError_t launch_merge_partition(const smallkv_batch_t &b, const smallkv_model_t &m,
+                                  const SmallPlan &p, const float *ws, const float *logits,
+                                  float *row_max, float *row_sum, int32_t *crit, int32_t *marg,
+                                  float *marg_prob, float *mass, hipStream_t st);
+
 hipError_t launch_partition(const smallkv_batch_t &b, int n_small_heads, const float *logits,
                             const float *row_max, const float *row_sum, int32_t *crit,
                             int32_t *marg, float *marg_prob, float *mass, hipStream_t st);

@@ -2,32 +2,42 @@
 // cache (Algorithm 1, decode branch; the full small cache C^s_all of the
 // "Saliency Shift Compensation" paragraph).
 //
-// small_attn_split: one workgroup per (sequence, layer, kv head, token chunk).
-//   Pass 1 stages K tiles through LDS with coalesced 16-byte loads; each
-//   thread then owns one token and evaluates the logit of every query head
-//   of the GQA group as a sequential fp32 FMA chain (the bit-exact key), and
-//   writes it out.  Pass 2 stages V tiles, turns the thread's own logits into
-//   exp(s - chunk max) and accumulates P.V with threads laid over
-//   (dim group, token stripe).  Output: per chunk and head (max, sum, P.V).
-// small_attn_merge: log-sum-exp combine of the chunks of one small head into
-//   row_max, row_sum and the head's output.
+// One workgroup per (sequence, layer, kv head, token chunk); the chunk is
+// walked in LDS tiles with an online softmax, and the workgroup emits one
+// partial record per query head of the GQA group: (chunk max, sum, P.V).
+//
+// bf16 kernel (small_attn_mfma), per tile:
+//   * K rows are staged in LDS with coalesced 16-byte loads; the V rows of
+//     the tile are loaded into registers at the same time, 8 consecutive
+//     tokens x 8 dims per thread, so their latency hides behind QK;
+//   * each thread owns one token and evaluates the logit of every query head
+//     of the group as a sequential fp32 FMA chain over the head dimension
+//     (the bit-exact ranking key), and writes it out;
+//   * P = exp(s - running max) is split into bf16 hi + lo parts and V is
+//     transposed in registers (v_perm) into a token-contiguous LDS tile, so
+//     P.V runs on MFMA (v_mfma_f32_16x16x32_bf16): M = query heads (padded
+//     to 16), N = 16 dims per wave, K = 32 tokens per instruction, twice
+//     (hi, lo), which keeps ~16 bits of P.
+// fp32 kernel (small_attn_valu): the same tiling with P.V on fp32 FMA.
+// small_attn_merge: log-sum-exp combine of a head's chunk records.
 #include "common.h"
 #include "launch.h"
+#include "merge.h"
 
 namespace smallkv {
 namespace {
 
 constexpr int kThreads = 256;
 
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
+typedef __attribute__((ext_vector_type(4))) float f32x4_t;
+
 template <typename T, int D>
 struct SmallCfg {
-  static constexpr int ROWB = D * (int)sizeof(T);                   // bytes per K/V row
-  static constexpr int TILE = 32768 / ROWB < 256 ? 32768 / ROWB : 256;  // rows per LDS tile
-  static constexpr int ROWS = ROWB + 16;                            // padded LDS row stride
-  static constexpr int V16 = ROWB / 16;                             // 16-byte vectors per row
-  static constexpr int VD = 4;                                      // dims per thread in P.V
-  static constexpr int NDG = D / VD;                                // dim groups
-  static constexpr int NTP = kThreads / NDG;                        // token stripes
+  static constexpr int ROWB = D * (int)sizeof(T);                       // bytes per K/V row
+  static constexpr int TILE = 32768 / ROWB < 256 ? 32768 / ROWB : 256;  // tokens per tile
+  static constexpr int ROWS = ROWB + 16;                                // padded K row stride
+  static constexpr int V16 = ROWB / 16;                                 // 16-byte vectors per row
 };
 
 struct SmallArgs {
@@ -39,167 +49,346 @@ struct SmallArgs {
   float *logits, *row_max, *row_sum, *part;
 };
 
+struct UnitPos {
+  int unit, split, b, layer, kvh, n, t0, t1;
+  int64_t head0;  // q row (and logits row) of the group's first query head
+};
+
+__device__ __forceinline__ bool unit_pos(const SmallArgs &a, UnitPos &u) {
+  u.unit = blockIdx.x / a.n_split;
+  u.split = blockIdx.x % a.n_split;
+  u.kvh = u.unit % a.hkv;
+  const int bl = u.unit / a.hkv;
+  u.layer = bl % a.layers;
+  u.b = bl / a.layers;
+  u.n = clampi(a.seq_len[u.b], 1, a.n_cap);
+  u.t0 = u.split * a.chunk;
+  u.t1 = min(u.t0 + a.chunk, u.n);
+  u.head0 = ((int64_t)u.b * a.layers + u.layer) * a.hq + (int64_t)u.kvh * a.g;
+  return u.t0 < u.n;
+}
+
+// Sequential fp32 FMA chain over the head dimension, then one multiply by
+// the scale; -0 becomes +0.  This is the bit-exact ranking key.
+template <int D>
+__device__ __forceinline__ float chain_logit(const float *q, const float *k, float scale) {
+  float acc = 0.0f;
+#pragma unroll
+  for (int c = 0; c < D; ++c) acc = __builtin_fmaf(q[c], k[c], acc);
+  const float s = acc * scale;
+  return s == 0.0f ? 0.0f : s;
+}
+
+// The same chain with q read as bf16 pairs through the constant address
+// space: wave-uniform scalar loads, so every FMA takes q from an SGPR and the
+// query costs no LDS traffic.  Bit-identical to chain_logit.
+typedef const __attribute__((address_space(4))) uint32_t *const_u32_ptr;
+template <int D>
+__device__ __forceinline__ float chain_logit_sq(const_u32_ptr qw, const float *k, float scale) {
+  float acc = 0.0f;
+#pragma unroll
+  for (int c = 0; c < D; c += 2) {
+    const uint32_t w = qw[c / 2];
+    acc = __builtin_fmaf(bf16_lo(w), k[c], acc);
+    acc = __builtin_fmaf(bf16_hi(w), k[c + 1], acc);
+  }
+  const float s = acc * scale;
+  return s == 0.0f ? 0.0f : s;
+}
+
 template <typename T, int D>
-__device__ __forceinline__ void stage_rows(unsigned char *tile, const unsigned char *src, int nr) {
+__device__ __forceinline__ void stage_k(unsigned char *tile, const unsigned char *src, int nr) {
   using C = SmallCfg<T, D>;
-  for (int x = threadIdx.x; x < nr * C::V16; x += kThreads) {
-    const int r = x / C::V16, w = x % C::V16;
-    const uint4 v = *reinterpret_cast<const uint4 *>(src + (int64_t)r * C::ROWB + w * 16);
-    *reinterpret_cast<uint4 *>(tile + r * C::ROWS + w * 16) = v;
+#pragma unroll
+  for (int r = 0; r < C::TILE * C::V16 / kThreads; ++r) {
+    const int x = threadIdx.x + r * kThreads;
+    const int row = x / C::V16, w = x % C::V16;
+    if (row < nr)
+      *reinterpret_cast<uint4 *>(tile + row * C::ROWS + w * 16) =
+          *reinterpret_cast<const uint4 *>(src + (int64_t)row * C::ROWB + w * 16);
   }
 }
 
-template <typename T>
-__device__ __forceinline__ void load4(const unsigned char *p, float *o);
-template <>
-__device__ __forceinline__ void load4<float>(const unsigned char *p, float *o) {
-  const uint4 v = *reinterpret_cast<const uint4 *>(p);
-  elem<float>::unpack(v, o);
-}
-template <>
-__device__ __forceinline__ void load4<bf16_t>(const unsigned char *p, float *o) {
-  const uint2 v = *reinterpret_cast<const uint2 *>(p);
-  o[0] = bf16_lo(v.x);
-  o[1] = bf16_hi(v.x);
-  o[2] = bf16_lo(v.y);
-  o[3] = bf16_hi(v.y);
-}
+// ------------------------------------------------------------ bf16 / MFMA --
 
-template <typename T, int D, int GP>
-__global__ __launch_bounds__(kThreads) void small_attn_split(SmallArgs a) {
-  using C = SmallCfg<T, D>;
-  __shared__ __align__(16) unsigned char tile[C::TILE * C::ROWS];
-  __shared__ __align__(16) float sq[GP * D];
-  __shared__ __align__(16) float sp[C::TILE * GP];
+template <int D, int GP>
+__global__ __launch_bounds__(kThreads) void small_attn_mfma(SmallArgs a) {
+  using C = SmallCfg<bf16_t, D>;
+  constexpr int TILE = C::TILE;
+  constexpr int DC = D / 8;                   // 8-dim chunks per row
+  constexpr int TB = kThreads / DC;           // 8-token blocks per V load pass
+  static_assert(TB * 8 == TILE, "one V pass covers the tile");
+  constexpr int VTS = (TILE + 8) * 2;         // V^T and P row stride (bytes)
+  constexpr int NB = D / 16;                  // 16-dim MFMA blocks
+  constexpr int NBW = NB / 4;                 // blocks per wave
+  static_assert(C::TILE * C::ROWS >= D * VTS, "V^T aliases the K tile");
+
+  __shared__ __align__(16) unsigned char tile[TILE * C::ROWS];  // K tile, then V^T
+  __shared__ __align__(16) unsigned char pt[2][GP * VTS];       // P hi, P lo (bf16)
   __shared__ float red[4 * GP];
-  __shared__ float redz[4 * GP];
+  __shared__ float salpha[16];
 
+  UnitPos u;
+  if (!unit_pos(a, u)) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int unit = blockIdx.x / a.n_split, split = blockIdx.x % a.n_split;
-  const int kvh = unit % a.hkv, bl = unit / a.hkv, layer = bl % a.layers, b = bl / a.layers;
-  const int n = clampi(a.seq_len[b], 1, a.n_cap);
-  const int t0 = split * a.chunk;
-  if (t0 >= n) return;
-  const int t1 = min(t0 + a.chunk, n);
   const int g = a.g;
-  const int64_t head0 = ((int64_t)b * a.layers + layer) * a.hq + (int64_t)kvh * g;  // q row of head 0
-
-  for (int x = tid; x < GP * D; x += kThreads) {
-    const int i = x / D, c = x % D;
-    sq[x] = i < g ? elem<T>::load1(a.q, (head0 + i) * D + c) : 0.0f;
-  }
-  const int64_t row0 = (int64_t)unit * a.n_cap;  // K/V row of token 0 of this unit
+  const int64_t row0 = (int64_t)u.unit * a.n_cap;
   const unsigned char *kb = reinterpret_cast<const unsigned char *>(a.k) + row0 * C::ROWB;
   const unsigned char *vb = reinterpret_cast<const unsigned char *>(a.v) + row0 * C::ROWB;
-  float *lrow = a.logits + head0 * a.n_cap;  // logits [b][j][n_cap], j = layer*hq + kvh*g + i
+  float *lrow = a.logits + u.head0 * a.n_cap;
+  const int tb8 = tid / DC, dc = tid % DC;  // V: token block and dim chunk of this thread
 
-  // ---- pass 1: logits (the ranking key) and the chunk max -------------
-  float mx[GP];
+  float m_run[GP], z_thr[GP];
 #pragma unroll
-  for (int i = 0; i < GP; ++i) mx[i] = -INFINITY;
-  for (int tb = t0; tb < t1; tb += C::TILE) {
-    const int nr = min(C::TILE, t1 - tb);
-    stage_rows<T, D>(tile, kb + (int64_t)tb * C::ROWB, nr);
+  for (int i = 0; i < GP; ++i) {
+    m_run[i] = -INFINITY;
+    z_thr[i] = 0.0f;
+  }
+  f32x4_t acc[NBW];
+#pragma unroll
+  for (int nb = 0; nb < NBW; ++nb) acc[nb] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+
+  for (int tb = u.t0; tb < u.t1; tb += TILE) {
+    const int nr = min(TILE, u.t1 - tb);
+    // V rows of 8 consecutive tokens x one 8-dim chunk, into registers
+    uint4 vr[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int tok = tb8 * 8 + k;
+      vr[k] = tok < nr ? *reinterpret_cast<const uint4 *>(vb + (int64_t)(tb + tok) * C::ROWB + dc * 16)
+                       : make_uint4(0u, 0u, 0u, 0u);
+    }
+    stage_k<bf16_t, D>(tile, kb + (int64_t)tb * C::ROWB, nr);
     __syncthreads();
+
+    // ---- logits: one token per thread, sequential FMA chains ------------
+    float s[GP];
     if (tid < nr) {
       float kr[D];
 #pragma unroll
       for (int w = 0; w < C::V16; ++w) {
         const uint4 v = *reinterpret_cast<const uint4 *>(tile + tid * C::ROWS + w * 16);
-        elem<T>::unpack(v, kr + w * elem<T>::per16);
+        elem<bf16_t>::unpack(v, kr + w * 8);
       }
+      const_u32_ptr qw = (const_u32_ptr)(reinterpret_cast<uintptr_t>(a.q)) + u.head0 * (D / 2);
 #pragma unroll
       for (int i = 0; i < GP; ++i) {
+        s[i] = -INFINITY;
         if (i < g) {
-          float acc = 0.0f;
-#pragma unroll
-          for (int c = 0; c < D; ++c) acc = __builtin_fmaf(sq[i * D + c], kr[c], acc);
-          float s = acc * a.scale;
-          s = (s == 0.0f) ? 0.0f : s;
-          lrow[(int64_t)i * a.n_cap + tb + tid] = s;
-          mx[i] = fmaxf(mx[i], s);
+          s[i] = chain_logit_sq<D>(qw + i * (D / 2), kr, a.scale);
+          lrow[(int64_t)i * a.n_cap + tb + tid] = s[i];
         }
       }
+    } else {
+#pragma unroll
+      for (int i = 0; i < GP; ++i) s[i] = -INFINITY;
+    }
+#pragma unroll
+    for (int i = 0; i < GP; ++i) {
+      const float v = wave_max(s[i]);
+      if (lane == 0) red[wave * GP + i] = v;
+    }
+    __syncthreads();  // K tile no longer read; red visible
+
+    // ---- online softmax, P hi/lo and V^T into LDS -----------------------
+    float alpha[GP];
+#pragma unroll
+    for (int i = 0; i < GP; ++i) {
+      const float mt = fmaxf(fmaxf(red[i], red[GP + i]), fmaxf(red[2 * GP + i], red[3 * GP + i]));
+      const float mn = fmaxf(m_run[i], mt);
+      alpha[i] = i < g ? __expf(m_run[i] - mn) : 1.0f;  // 0 on the first tile
+      m_run[i] = mn;
+      const float e = (i < g && tid < nr) ? __expf(s[i] - mn) : 0.0f;
+      z_thr[i] = __builtin_fmaf(z_thr[i], alpha[i], e);
+      const uint16_t hi = f32_to_bf16(e);
+      const uint16_t lo = f32_to_bf16(e - __uint_as_float((uint32_t)hi << 16));
+      if (tid < TILE) {
+        *reinterpret_cast<uint16_t *>(pt[0] + i * VTS + tid * 2) = hi;
+        *reinterpret_cast<uint16_t *>(pt[1] + i * VTS + tid * 2) = lo;
+      }
+    }
+    if (tid < 16) {
+      float al = 1.0f;
+#pragma unroll
+      for (int i = 0; i < GP; ++i)
+        if (i == tid) al = alpha[i];
+      salpha[tid] = al;
+    }
+#pragma unroll
+    for (int d = 0; d < 8; ++d) {
+      const uint32_t sel = (d & 1) ? 0x07060302u : 0x05040100u;
+      uint32_t w[4];
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        const uint32_t x0 = (&vr[2 * p].x)[d >> 1], x1 = (&vr[2 * p + 1].x)[d >> 1];
+        w[p] = __builtin_amdgcn_perm(x1, x0, sel);
+      }
+      *reinterpret_cast<uint4 *>(tile + (dc * 8 + d) * VTS + tb8 * 16) = make_uint4(w[0], w[1], w[2], w[3]);
     }
     __syncthreads();
+
+    // ---- P.V on MFMA --------------------------------------------------------
+    const int mrow = lane & 15, kq = lane >> 4;
+#pragma unroll
+    for (int nb = 0; nb < NBW; ++nb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[nb][r] *= salpha[kq * 4 + r];
+#pragma unroll
+    for (int ks = 0; ks < TILE / 32; ++ks) {
+      const int tok = ks * 32 + kq * 8;
+      uint4 ah = make_uint4(0u, 0u, 0u, 0u), al = ah;
+      if (mrow < GP) {
+        ah = *reinterpret_cast<const uint4 *>(pt[0] + mrow * VTS + tok * 2);
+        al = *reinterpret_cast<const uint4 *>(pt[1] + mrow * VTS + tok * 2);
+      }
+#pragma unroll
+      for (int nb = 0; nb < NBW; ++nb) {
+        const int dim = (wave + 4 * nb) * 16 + mrow;
+        const uint4 bv = *reinterpret_cast<const uint4 *>(tile + dim * VTS + tok * 2);
+        const bf16x8_t B = __builtin_bit_cast(bf16x8_t, bv);
+        acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ah), B, acc[nb], 0, 0, 0);
+        acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, al), B, acc[nb], 0, 0, 0);
+      }
+    }
+    __syncthreads();  // before the next tile overwrites the K/V^T and P tiles
   }
+
+  // ---- chunk record: max, sum and P.V per query head ----------------------
 #pragma unroll
   for (int i = 0; i < GP; ++i) {
-    const float v = wave_max(mx[i]);
+    const float v = wave_sum(z_thr[i]);
     if (lane == 0) red[wave * GP + i] = v;
   }
   __syncthreads();
-  float m[GP];
+  float *part = a.part + (int64_t)blockIdx.x * GP * (D + 2);
+  const int kq = lane >> 4, ncol = lane & 15;
 #pragma unroll
-  for (int i = 0; i < GP; ++i)
-    m[i] = fmaxf(fmaxf(red[i], red[GP + i]), fmaxf(red[2 * GP + i], red[3 * GP + i]));
+  for (int nb = 0; nb < NBW; ++nb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int head = kq * 4 + r, dim = (wave + 4 * nb) * 16 + ncol;
+      if (head < g) part[head * (D + 2) + 2 + dim] = acc[nb][r];
+    }
+  if (tid == 0) {
+#pragma unroll
+    for (int i = 0; i < GP; ++i)
+      if (i < g) {
+        part[i * (D + 2)] = m_run[i];
+        part[i * (D + 2) + 1] = red[i] + red[GP + i] + red[2 * GP + i] + red[3 * GP + i];
+      }
+  }
+}
 
-  // ---- pass 2: exp(s - m) and P.V --------------------------------------
-  const int dg = tid % C::NDG, tp = tid / C::NDG;
-  float acc[GP][C::VD];
-  float zl[GP];
+// ---------------------------------------------------------------- fp32 --
+
+template <int D, int GP>
+__global__ __launch_bounds__(kThreads) void small_attn_valu(SmallArgs a) {
+  using C = SmallCfg<float, D>;
+  constexpr int TILE = C::TILE;
+  constexpr int VD = 4;              // dims per thread in P.V
+  constexpr int NDG = D / VD;        // dim groups
+  constexpr int NTP = kThreads / NDG;  // token stripes
+  __shared__ __align__(16) unsigned char tile[TILE * C::ROWS];
+  __shared__ __align__(16) float sq[GP * D];
+  __shared__ __align__(16) float sp[TILE * GP];
+  __shared__ float red[4 * GP];
+
+  UnitPos u;
+  if (!unit_pos(a, u)) return;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = a.g;
+  for (int x = tid; x < GP * D; x += kThreads) {
+    const int i = x / D, c = x % D;
+    sq[x] = i < g ? elem<float>::load1(a.q, (u.head0 + i) * D + c) : 0.0f;
+  }
+  const int64_t row0 = (int64_t)u.unit * a.n_cap;
+  const unsigned char *kb = reinterpret_cast<const unsigned char *>(a.k) + row0 * C::ROWB;
+  const unsigned char *vb = reinterpret_cast<const unsigned char *>(a.v) + row0 * C::ROWB;
+  float *lrow = a.logits + u.head0 * a.n_cap;
+  const int dg = tid % NDG, tp = tid / NDG;
+
+  float m_run[GP], z_thr[GP], acc[GP][VD];
 #pragma unroll
   for (int i = 0; i < GP; ++i) {
-    zl[i] = 0.0f;
+    m_run[i] = -INFINITY;
+    z_thr[i] = 0.0f;
 #pragma unroll
-    for (int c = 0; c < C::VD; ++c) acc[i][c] = 0.0f;
+    for (int c = 0; c < VD; ++c) acc[i][c] = 0.0f;
   }
-  for (int tb = t0; tb < t1; tb += C::TILE) {
-    const int nr = min(C::TILE, t1 - tb);
-    stage_rows<T, D>(tile, vb + (int64_t)tb * C::ROWB, nr);
-    if (tid < nr) {
-#pragma unroll
-      for (int i = 0; i < GP; ++i) {
-        float e = 0.0f;
-        if (i < g) {
-          e = __expf(lrow[(int64_t)i * a.n_cap + tb + tid] - m[i]);
-          zl[i] += e;
-        }
-        sp[tid * GP + i] = e;
-      }
-    }
+  for (int tb = u.t0; tb < u.t1; tb += TILE) {
+    const int nr = min(TILE, u.t1 - tb);
+    stage_k<float, D>(tile, kb + (int64_t)tb * C::ROWB, nr);
     __syncthreads();
-    for (int t = tp; t < nr; t += C::NTP) {
-      float vv[C::VD];
-      load4<T>(tile + t * C::ROWS + dg * C::VD * (int)sizeof(T), vv);
-      float p[GP];
+    float s[GP];
 #pragma unroll
-      for (int i = 0; i < GP; i += 4) {
-        const float4 w = *reinterpret_cast<const float4 *>(sp + t * GP + i);
-        p[i] = w.x;
-        p[i + 1] = w.y;
-        p[i + 2] = w.z;
-        p[i + 3] = w.w;
+    for (int i = 0; i < GP; ++i) s[i] = -INFINITY;
+    if (tid < nr) {
+      float kr[D];
+#pragma unroll
+      for (int w = 0; w < C::V16; ++w) {
+        const uint4 v = *reinterpret_cast<const uint4 *>(tile + tid * C::ROWS + w * 16);
+        elem<float>::unpack(v, kr + w * 4);
       }
 #pragma unroll
       for (int i = 0; i < GP; ++i)
         if (i < g) {
+          s[i] = chain_logit<D>(sq + i * D, kr, a.scale);
+          lrow[(int64_t)i * a.n_cap + tb + tid] = s[i];
+        }
+    }
 #pragma unroll
-          for (int c = 0; c < C::VD; ++c) acc[i][c] = __builtin_fmaf(p[i], vv[c], acc[i][c]);
+    for (int i = 0; i < GP; ++i) {
+      const float v = wave_max(s[i]);
+      if (lane == 0) red[wave * GP + i] = v;
+    }
+    __syncthreads();
+    float alpha[GP];
+#pragma unroll
+    for (int i = 0; i < GP; ++i) {
+      const float mt = fmaxf(fmaxf(red[i], red[GP + i]), fmaxf(red[2 * GP + i], red[3 * GP + i]));
+      const float mn = fmaxf(m_run[i], mt);
+      alpha[i] = i < g ? __expf(m_run[i] - mn) : 1.0f;
+      m_run[i] = mn;
+      const float e = (i < g && tid < nr) ? __expf(s[i] - mn) : 0.0f;
+      z_thr[i] = __builtin_fmaf(z_thr[i], alpha[i], e);
+      if (tid < TILE) sp[tid * GP + i] = e;
+#pragma unroll
+      for (int c = 0; c < VD; ++c) acc[i][c] *= alpha[i];
+    }
+    // V tile replaces the K tile
+    stage_k<float, D>(tile, vb + (int64_t)tb * C::ROWB, nr);
+    __syncthreads();
+    for (int t = tp; t < nr; t += NTP) {
+      float vv[VD];
+      elem<float>::unpack(*reinterpret_cast<const uint4 *>(tile + t * C::ROWS + dg * VD * 4), vv);
+#pragma unroll
+      for (int i = 0; i < GP; ++i)
+        if (i < g) {
+          const float p = sp[t * GP + i];
+#pragma unroll
+          for (int c = 0; c < VD; ++c) acc[i][c] = __builtin_fmaf(p, vv[c], acc[i][c]);
         }
     }
     __syncthreads();
   }
-
-  // ---- reductions: z over all threads, P.V over token stripes -----------
 #pragma unroll
   for (int i = 0; i < GP; ++i) {
-    const float v = wave_sum(zl[i]);
-    if (lane == 0) redz[wave * GP + i] = v;
+    const float v = wave_sum(z_thr[i]);
+    if (lane == 0) red[wave * GP + i] = v;
   }
-  // stripes inside one wave first
 #pragma unroll
-  for (int o = C::NDG; o < kWave; o <<= 1)
-#pragma unroll
-    for (int i = 0; i < GP; ++i)
-#pragma unroll
-      for (int c = 0; c < C::VD; ++c) acc[i][c] += __shfl_xor(acc[i][c], o, kWave);
-  float *buf = reinterpret_cast<float *>(tile);  // [4 waves][GP][D]; tile is free now
-  if (lane < C::NDG) {
+  for (int o = NDG; o < kWave; o <<= 1)
 #pragma unroll
     for (int i = 0; i < GP; ++i)
 #pragma unroll
-      for (int c = 0; c < C::VD; ++c) buf[(wave * GP + i) * D + dg * C::VD + c] = acc[i][c];
+      for (int c = 0; c < VD; ++c) acc[i][c] += __shfl_xor(acc[i][c], o, kWave);
+  float *buf = reinterpret_cast<float *>(tile);  // [4 waves][GP][D]
+  static_assert(4 * GP * D * 4 <= TILE * C::ROWS, "reduction buffer fits the tile");
+  if (lane < NDG) {
+#pragma unroll
+    for (int i = 0; i < GP; ++i)
+#pragma unroll
+      for (int c = 0; c < VD; ++c) buf[(wave * GP + i) * D + dg * VD + c] = acc[i][c];
   }
   __syncthreads();
   float *part = a.part + (int64_t)blockIdx.x * GP * (D + 2);
@@ -212,78 +401,65 @@ __global__ __launch_bounds__(kThreads) void small_attn_split(SmallArgs a) {
 #pragma unroll
     for (int i = 0; i < GP; ++i)
       if (i < g) {
-        part[i * (D + 2)] = m[i];
-        part[i * (D + 2) + 1] = redz[i] + redz[GP + i] + redz[2 * GP + i] + redz[3 * GP + i];
+        part[i * (D + 2)] = m_run[i];
+        part[i * (D + 2) + 1] = red[i] + red[GP + i] + red[2 * GP + i] + red[3 * GP + i];
       }
   }
 }
 
-// One workgroup of D threads per small head: combine its chunks.
+// ------------------------------------------------------------- merge --
+
 template <typename T, int D, int GP>
-__global__ __launch_bounds__(D) void small_attn_merge(SmallArgs a) {
+__global__ __launch_bounds__(kThreads) void small_attn_merge(SmallArgs a) {
+  __shared__ float mw[kMaxChunks];
+  __shared__ float mred[4 + kThreads];
   const int row = blockIdx.x;  // = b * (layers*hq) + layer*hq + h
   const int h = row % a.hq, bl = row / a.hq, layer = bl % a.layers, b = bl / a.layers;
   const int unit = (b * a.layers + layer) * a.hkv + h / a.g, i = h % a.g;
   const int n = clampi(a.seq_len[b], 1, a.n_cap);
-  const int nv = (n + a.chunk - 1) / a.chunk;
-  const float *p = a.part + (int64_t)unit * a.n_split * GP * (D + 2) + i * (D + 2);
-  const int64_t stride = (int64_t)GP * (D + 2);
-  float M = -INFINITY;
-  for (int s = 0; s < nv; ++s) M = fmaxf(M, p[s * stride]);
-  float Z = 0.0f, o = 0.0f;
-  const int c = threadIdx.x;
-  for (int s = 0; s < nv; ++s) {
-    const float w = __expf(p[s * stride] - M);
-    Z = __builtin_fmaf(p[s * stride + 1], w, Z);
-    o = __builtin_fmaf(p[s * stride + 2 + c], w, o);
-  }
-  if (c == 0) {
+  MergeIn in;
+  in.stride = (int64_t)GP * (D + 2);
+  in.part = a.part + (int64_t)unit * a.n_split * in.stride + i * (D + 2);
+  in.nv = (n + a.chunk - 1) / a.chunk;
+  float M, Z;
+  void *out = a.out;
+  merge_head<kThreads>(in, D, mw, mred, M, Z,
+                          [&](int c, float v) { elem<T>::store1(out, (int64_t)row * D + c, v); });
+  if (threadIdx.x == 0) {
     a.row_max[row] = M;
     a.row_sum[row] = Z;
   }
-  elem<T>::store1(a.out, (int64_t)row * D + c, o / Z);
 }
 
-template <typename T, int D, int GP>
-hipError_t launch_t(const SmallArgs &a, int units, hipStream_t st) {
-  hipLaunchKernelGGL((small_attn_split<T, D, GP>), dim3(units * a.n_split), dim3(kThreads), 0, st, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  const int rows = units / a.hkv * a.hq;
-  hipLaunchKernelGGL((small_attn_merge<T, D, GP>), dim3(rows), dim3(D), 0, st, a);
+template <int D, int GP>
+hipError_t launch_split_t(const SmallArgs &a, int units, bool f32, hipStream_t st) {
+  if (f32)
+    hipLaunchKernelGGL((small_attn_valu<D, GP>), dim3(units * a.n_split), dim3(kThreads), 0, st, a);
+  else
+    hipLaunchKernelGGL((small_attn_mfma<D, GP>), dim3(units * a.n_split), dim3(kThreads), 0, st, a);
   return hipGetLastError();
 }
 
+template <int D>
+hipError_t launch_split_gp(const SmallArgs &a, int units, int gp, bool f32, hipStream_t st) {
+  if (gp == 4) return launch_split_t<D, 4>(a, units, f32, st);
+  if (gp == 8) return launch_split_t<D, 8>(a, units, f32, st);
+  return launch_split_t<D, 16>(a, units, f32, st);
+}
+
 template <typename T, int D>
-hipError_t launch_gp(const SmallArgs &a, int units, int gp, hipStream_t st) {
-  if (gp == 4) return launch_t<T, D, 4>(a, units, st);
-  if (gp == 8) return launch_t<T, D, 8>(a, units, st);
-  return launch_t<T, D, 16>(a, units, st);
+hipError_t launch_merge_gp(const SmallArgs &a, int rows, int gp, hipStream_t st) {
+  if (gp == 4)
+    hipLaunchKernelGGL((small_attn_merge<T, D, 4>), dim3(rows), dim3(kThreads), 0, st, a);
+  else if (gp == 8)
+    hipLaunchKernelGGL((small_attn_merge<T, D, 8>), dim3(rows), dim3(kThreads), 0, st, a);
+  else
+    hipLaunchKernelGGL((small_attn_merge<T, D, 16>), dim3(rows), dim3(kThreads), 0, st, a);
+  return hipGetLastError();
 }
 
-}  // namespace
-
-SmallPlan plan_small(const smallkv_batch_t &b, const smallkv_model_t &m) {
-  SmallPlan p{};
-  const int esz = m.dtype == SMALLKV_F32 ? 4 : 2;
-  const int rowb = m.head_dim * esz;
-  p.tile = 32768 / rowb < 256 ? 32768 / rowb : 256;
-  const int64_t units = (int64_t)b.batch * m.n_layers * m.n_kv_heads;
-  const int max_split = (b.n_cap + p.tile - 1) / p.tile;
-  int want = (int)((4096 + units - 1) / units);
-  int ns = want < 1 ? 1 : (want > max_split ? max_split : want);
-  const int per = (b.n_cap + ns - 1) / ns;
-  p.chunk = (per + p.tile - 1) / p.tile * p.tile;
-  p.n_split = (b.n_cap + p.chunk - 1) / p.chunk;
-  const int g = m.n_q_heads / m.n_kv_heads;
-  p.gp = g <= 4 ? 4 : (g <= 8 ? 8 : 16);
-  p.ws_bytes = (size_t)units * p.n_split * p.gp * (m.head_dim + 2) * sizeof(float);
-  return p;
-}
-
-hipError_t launch_small_attn(const smallkv_batch_t &b, const smallkv_model_t &m, float *logits,
-                             float *row_max, float *row_sum, float *ws, const SmallPlan &p,
-                             hipStream_t st) {
+SmallArgs make_args(const smallkv_batch_t &b, const smallkv_model_t &m, float *logits,
+                    float *row_max, float *row_sum, float *ws, const SmallPlan &p) {
   SmallArgs a;
   a.n_cap = b.n_cap;
   a.layers = m.n_layers;
@@ -302,12 +478,51 @@ hipError_t launch_small_attn(const smallkv_batch_t &b, const smallkv_model_t &m,
   a.row_max = row_max;
   a.row_sum = row_sum;
   a.part = ws;
+  return a;
+}
+
+}  // namespace
+
+SmallPlan plan_small(const smallkv_batch_t &b, const smallkv_model_t &m) {
+  SmallPlan p{};
+  const int esz = m.dtype == SMALLKV_F32 ? 4 : 2;
+  const int rowb = m.head_dim * esz;
+  p.tile = 32768 / rowb < 256 ? 32768 / rowb : 256;
+  const int64_t units = (int64_t)b.batch * m.n_layers * m.n_kv_heads;
+  const int max_split = (b.n_cap + p.tile - 1) / p.tile;
+  const int want = (int)((4096 + units - 1) / units);
+  int ns = want < 1 ? 1 : (want > max_split ? max_split : want);
+  if (ns > kMaxChunks) ns = kMaxChunks;
+  const int per = (b.n_cap + ns - 1) / ns;
+  p.chunk = (per + p.tile - 1) / p.tile * p.tile;
+  p.n_split = (b.n_cap + p.chunk - 1) / p.chunk;
+  const int g = m.n_q_heads / m.n_kv_heads;
+  p.gp = g <= 4 ? 4 : (g <= 8 ? 8 : 16);
+  p.ws_bytes = (size_t)units * p.n_split * p.gp * (m.head_dim + 2) * sizeof(float);
+  return p;
+}
+
+hipError_t launch_small_split(const smallkv_batch_t &b, const smallkv_model_t &m, float *logits,
+                              float *ws, const SmallPlan &p, hipStream_t st) {
+  const SmallArgs a = make_args(b, m, logits, nullptr, nullptr, ws, p);
   const int units = b.batch * m.n_layers * m.n_kv_heads;
+  const bool f32 = m.dtype == SMALLKV_F32;
+  return m.head_dim == 64 ? launch_split_gp<64>(a, units, p.gp, f32, st)
+                          : launch_split_gp<128>(a, units, p.gp, f32, st);
+}
+
+hipError_t launch_small_attn(const smallkv_batch_t &b, const smallkv_model_t &m, float *logits,
+                             float *row_max, float *row_sum, float *ws, const SmallPlan &p,
+                             hipStream_t st) {
+  hipError_t e = launch_small_split(b, m, logits, ws, p, st);
+  if (e != hipSuccess) return e;
+  const SmallArgs a = make_args(b, m, logits, row_max, row_sum, ws, p);
+  const int rows = b.batch * m.n_layers * m.n_q_heads;
   if (m.dtype == SMALLKV_F32)
-    return m.head_dim == 64 ? launch_gp<float, 64>(a, units, p.gp, st)
-                            : launch_gp<float, 128>(a, units, p.gp, st);
-  return m.head_dim == 64 ? launch_gp<bf16_t, 64>(a, units, p.gp, st)
-                          : launch_gp<bf16_t, 128>(a, units, p.gp, st);
+    return m.head_dim == 64 ? launch_merge_gp<float, 64>(a, rows, p.gp, st)
+                            : launch_merge_gp<float, 128>(a, rows, p.gp, st);
+  return m.head_dim == 64 ? launch_merge_gp<bf16_t, 64>(a, rows, p.gp, st)
+                          : launch_merge_gp<bf16_t, 128>(a, rows, p.gp, st);
 }
 
 }  // namespace smallkv
