@@ -1,0 +1,137 @@
+"""Summaries of rocprofv3 output for the library's kernels.
+
+  python -m paper_2508_02751_amd.profiling stats DIR [--title T] [--cmd C]
+      per-kernel call count and average / min / max duration from a
+      `rocprofv3 --kernel-trace --stats --output-format csv` run.
+
+  python -m paper_2508_02751_amd.profiling traffic FETCH_DIR WRITE_DIR --copy-mib N
+      HBM bytes per dispatch of each library kernel from two `--pmc` runs
+      (FETCH_SIZE, WRITE_SIZE, KiB per dispatch).  Each counter is scaled by
+      what it reads for a plain device copy of N MiB in the same run (the
+      largest copy dispatch), so the result is in true bytes.  Prints JSON
+      keyed by source file, with that file's hash so that a reader can tell
+      when the kernel changed after the counters were taken.
+"""
+from __future__ import annotations
+
+import argparse
+import collections
+import csv
+import glob
+import hashlib
+import json
+import os
+import sys
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+CSRC = os.path.join(PKG, "csrc")
+
+# kernel-name fragment -> source file
+KERNEL_SOURCES = {
+    "small_attn_mfma": "small_attn.hip",
+    "small_attn_valu": "small_attn.hip",
+    "small_attn_merge": "small_attn.hip",
+    "partition_kernel": "partition.hip",
+    "hybrid_kernel": "hybrid.hip",
+}
+
+
+def source_hash(name: str) -> str:
+    return hashlib.sha256(open(os.path.join(CSRC, name), "rb").read()).hexdigest()[:16]
+
+
+def short_name(full: str) -> str:
+    for frag in KERNEL_SOURCES:
+        if frag in full:
+            i = full.index(frag)
+            j = full.find("(", i)
+            return full[i:j] if j > 0 else full[i:]
+    return full[:60]
+
+
+def _one(pattern: str) -> str:
+    files = sorted(glob.glob(pattern, recursive=True))
+    if not files:
+        raise SystemExit(f"no file matches {pattern}")
+    return files[-1]
+
+
+def stats(d: str, title: str, cmd: str) -> str:
+    rows = list(csv.DictReader(open(_one(os.path.join(d, "**", "*kernel_stats.csv")))))
+    out = [f"# {title}", "", f"command: `{cmd}`", "",
+           "| kernel | calls | avg us | min us | max us | share of GPU time |",
+           "|---|---|---|---|---|---|"]
+    for r in rows:
+        if "smallkv" not in r["Name"]:
+            continue
+        out.append(f"| {short_name(r['Name'])} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.1f} | "
+                   f"{float(r['MinNs']) / 1e3:.1f} | {float(r['MaxNs']) / 1e3:.1f} | "
+                   f"{float(r['Percentage']):.1f}% |")
+    return "\n".join(out) + "\n"
+
+
+def _counter(d: str, name: str):
+    rows = list(csv.DictReader(open(_one(os.path.join(d, "**", "*counter_collection.csv")))))
+    per = collections.defaultdict(list)
+    copy = 0.0
+    for r in rows:
+        if r["Counter_Name"] != name:
+            continue
+        v = float(r["Counter_Value"])
+        if "copyBuffer" in r["Kernel_Name"]:
+            copy = max(copy, v)
+        elif "smallkv" in r["Kernel_Name"]:
+            per[short_name(r["Kernel_Name"])].append(v)
+    return per, copy
+
+
+def traffic(fetch_dir: str, write_dir: str, copy_mib: int) -> dict:
+    fetch, copy_f = _counter(fetch_dir, "FETCH_SIZE")
+    write, copy_w = _counter(write_dir, "WRITE_SIZE")
+    true_kib = copy_mib * 1024.0
+    ff = true_kib / copy_f if copy_f else None
+    fw = true_kib / copy_w if copy_w else None
+    out = {"calibration": {"copy_mib": copy_mib, "fetch_kib_read_for_copy": copy_f,
+                           "write_kib_read_for_copy": copy_w, "fetch_factor": ff,
+                           "write_factor": fw},
+           "kernels": {}}
+    for k in sorted(set(fetch) | set(write)):
+        src = next(v for f, v in KERNEL_SOURCES.items() if f in k)
+        fk = sum(fetch.get(k, [0])) / max(1, len(fetch.get(k, [])))
+        wk = sum(write.get(k, [0])) / max(1, len(write.get(k, [])))
+        rb = fk * 1024 * (ff or 1.0)
+        wb = wk * 1024 * (fw or 1.0)
+        entry = {"kernel": k, "dispatches": len(fetch.get(k, [])),
+                 "fetch_kib": fk, "write_kib": wk, "read_bytes": rb, "write_bytes": wb,
+                 "hbm_bytes_per_launch": rb + wb, "source_sha256_16": source_hash(src)}
+        # one source file can hold several kernels: keep the largest by traffic
+        prev = out["kernels"].get(src)
+        if prev is None or entry["hbm_bytes_per_launch"] > prev["hbm_bytes_per_launch"]:
+            out["kernels"][src] = entry
+    return out
+
+
+def main(argv=None):
+    p = argparse.ArgumentParser()
+    sub = p.add_subparsers(dest="action", required=True)
+    s = sub.add_parser("stats")
+    s.add_argument("dir")
+    s.add_argument("--title", default="rocprofv3 kernel statistics")
+    s.add_argument("--cmd", default="")
+    t = sub.add_parser("traffic")
+    t.add_argument("fetch_dir")
+    t.add_argument("write_dir")
+    t.add_argument("--copy-mib", type=int, required=True)
+    t.add_argument("--cmd", default="")
+    a = p.parse_args(argv)
+    if a.action == "stats":
+        sys.stdout.write(stats(a.dir, a.title, a.cmd))
+    else:
+        res = traffic(a.fetch_dir, a.write_dir, a.copy_mib)
+        res["command"] = a.cmd
+        json.dump(res, sys.stdout, indent=1)
+        sys.stdout.write("\n")
+
+
+if __name__ == "__main__":
+    main()
