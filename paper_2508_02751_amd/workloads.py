@@ -211,6 +211,13 @@ def q_layer(w: Workload, which: str, layer: int, z: torch.Tensor, step: int, dev
     return q.to(w.torch_dtype)
 
 
+def step_queries(w: Workload, z: torch.Tensor, step: int, device):
+    """Queries of both models for one decode step: (s_q [B][l][Hqs][ds], l_q [B][L][Hq][d])."""
+    s_q = torch.stack([q_layer(w, "small", i, z, step, device) for i in range(w.small.layers)], 1)
+    l_q = torch.stack([q_layer(w, "large", i, z, step, device) for i in range(w.large.layers)], 1)
+    return s_q, l_q
+
+
 def make_step_inputs(w: Workload, device, step: int = 0, *, z=None, large=True):
     """All inputs of one decode step as torch tensors on `device`.
 

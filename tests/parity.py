@@ -81,3 +81,56 @@ def compare_step(buf, ref: dict, x: dict, dtype, what: str = "", check_logits=Tr
     assert es <= tol, f"{what}: small-model output error {es:.3g} > {tol}"
     assert el <= tol, f"{what}: large-model output error {el:.3g} > {tol}"
     return {"small_out_err": es, "large_out_err": el}
+
+
+# ------------------------------------------------- sampled (full-size) checks --
+
+def oracle_small_row(x, b: int, j: int):
+    """Oracle stages 1-2 for one small row (b, j) from host copies of its slices."""
+    from paper_2508_02751_amd.pipeline import softmax_scale
+    s_q, s_k, s_v = x["s_q"], x["s_k"], x["s_v"]
+    hqs, hks, ds = s_q.shape[2], s_k.shape[2], s_q.shape[3]
+    layer, h = divmod(j, hqs)
+    g = h // (hqs // hks)
+    n = int(x["seq_len"][b])
+    lg, m, Z, out = O.small_head(host(s_q[b, layer, h]), host(s_k[b, layer, g, :n]),
+                                 host(s_v[b, layer, g, :n]), softmax_scale(ds))
+    kc, km = int(x["k_crit"][b]), int(x["k_marg"][b])
+    crit, marg, mp, mass = O.partition(lg, kc, km, m, Z, kc_cap=int(x["kc_cap"]),
+                                       km_cap=int(x["km_cap"]))
+    return dict(logits=lg, m=m, Z=Z, out=out, crit=crit, marg=marg, marg_prob=mp, mass=mass)
+
+
+def check_small_row(buf, x, b, j, ref, tol, what=""):
+    n = int(x["seq_len"][b])
+    nsh = buf.logits.shape[1]
+    hqs = x["s_q"].shape[2]
+    layer, h = divmod(j, hqs)
+    got = host(buf.logits[b, j, :n])
+    assert np.array_equal(got.view(np.uint32), ref["logits"].view(np.uint32)), f"{what}: logits ({b},{j})"
+    assert np.float32(ref["m"]) == host(buf.row_max[b, j]), f"{what}: row_max ({b},{j})"
+    np.testing.assert_allclose(host(buf.row_sum[b, j]), ref["Z"], rtol=1e-5)
+    assert np.array_equal(host(buf.crit_idx[b, j]), ref["crit"]), f"{what}: crit ({b},{j})"
+    km = ref["marg"].shape[0]
+    if km:
+        assert np.array_equal(host(buf.marg_idx[b, j, :km]), ref["marg"]), f"{what}: marg ({b},{j})"
+        np.testing.assert_allclose(host(buf.marg_prob[b, j, :km]), ref["marg_prob"], rtol=2e-5, atol=1e-9)
+    np.testing.assert_allclose(host(buf.mass[b, j]), ref["mass"], rtol=2e-5, atol=2e-7)
+    e = head_err(host(buf.small_out[b, layer, h])[None], ref["out"][None])
+    assert e <= tol, f"{what}: small output ({b},{j}) error {e}"
+    assert nsh == x["s_q"].shape[1] * hqs
+
+
+def oracle_large_head(x, b, layer, h, part, mode, l_k=None, l_v=None, k_slot=None, v_slot=None):
+    """Oracle stage 3 for one large head, given the oracle's partition of its small head."""
+    from paper_2508_02751_amd.pipeline import softmax_scale
+    l_q = x["l_q"]
+    l_k = x["l_k"] if l_k is None else l_k
+    l_v = x["l_v"] if l_v is None else l_v
+    hq, hk, d = l_q.shape[2], l_k.shape[2], l_q.shape[3]
+    g = h // (hq // hk)
+    ks = None if k_slot is None else host(k_slot[b, layer, g])
+    vs = None if v_slot is None else host(v_slot[b, layer, g])
+    return O.hybrid_head(host(l_q[b, layer, h]), host(l_k[b, layer, g]), host(l_v[b, layer, g]),
+                         part["crit"], part["marg"], part["marg_prob"], part["mass"],
+                         softmax_scale(d), mode, k_slot=ks, v_slot=vs)

@@ -1,0 +1,177 @@
+"""GPU parity at the full sizes of the large workloads, in the launch
+configuration the benchmark uses (one smallkv_step over all layers).
+
+The oracle cannot redo these steps whole in test time, so each test checks
+sampled small-model rows (logits and index lists bit-exact) and sampled
+large-model heads, each against the oracle run on that row's or head's own
+slices; the tiny and Qwen2-7B-shaped workloads are checked whole in
+test_gpu_parity.py.
+"""
+import gc
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from parity import (TOL, check_small_row, head_err, host, log, oracle_large_head,
+                    oracle_small_row)
+from paper_2508_02751_amd import smallkv as S
+from paper_2508_02751_amd import workloads as W
+from paper_2508_02751_amd.pipeline import prepare_step
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+MODE = S.NORM_REMAINING
+
+
+def free():
+    gc.collect()
+    torch.cuda.empty_cache()
+
+
+def check_heads(ps, x, heads, small_refs, tol, what, **store):
+    hm = host(x["head_map"])
+    hq = x["l_q"].shape[2]
+    worst = 0.0
+    for (b, layer, h) in heads:
+        j = int(hm[layer * hq + h])
+        if (b, j) not in small_refs:
+            small_refs[(b, j)] = oracle_small_row(x, b, j)
+            check_small_row(ps.buf, x, b, j, small_refs[(b, j)], tol, what)
+        ref = oracle_large_head(x, b, layer, h, small_refs[(b, j)], MODE, **store)
+        e = head_err(host(ps.buf.large_out[b, layer, h])[None], ref[None])
+        assert e <= tol, f"{what}: large head ({b},{layer},{h}) error {e}"
+        worst = max(worst, e)
+    return worst
+
+
+def sample(rng, n, *dims):
+    return [tuple(int(rng.integers(0, d)) for d in dims) for _ in range(n)]
+
+
+def test_llama3_8b_n32768_b16_sampled():
+    w = W.WORKLOADS[3]
+    log(f"[fullsize] {w.name}: generating inputs")
+    x = W.make_step_inputs(w, DEV)
+    ps = prepare_step(x, MODE)
+    ps.run()
+    torch.cuda.synchronize()
+    log("[fullsize] step done; checking samples against the oracle")
+    rng = np.random.default_rng(3)
+    tol = TOL[w.torch_dtype]
+    refs = {}
+    nsh = w.small.layers * w.small.q_heads
+    for (b, j) in sample(rng, 24, w.batch, nsh):
+        refs[(b, j)] = oracle_small_row(x, b, j)
+        check_small_row(ps.buf, x, b, j, refs[(b, j)], tol, w.name)
+    worst = check_heads(ps, x, sample(rng, 24, w.batch, w.large.layers, w.large.q_heads), refs,
+                        tol, w.name)
+    log(f"[fullsize] {w.name} ok: {len(refs)} small rows, worst large-head error {worst:.3g}")
+    del ps, x
+    free()
+
+
+def test_ragged_b64_256_drifting_steps_sampled():
+    w = W.WORKLOADS[4]
+    log(f"[fullsize] {w.name}: generating inputs")
+    z = W.latents(w, DEV)
+    x = W.make_step_inputs(w, DEV, 0, z=z)
+    ps = prepare_step(x, MODE)
+    rng = np.random.default_rng(4)
+    tol = TOL[w.torch_dtype]
+    checked, prev, jac = 0, None, []
+    watch = torch.tensor(rng.choice(w.small.layers * w.small.q_heads, 8, replace=False), device=DEV)
+    for step in range(w.steps):
+        s_q, l_q = W.step_queries(w, z, step, DEV)
+        n, kc, km = W.budgets(w, step)
+        ps.with_query(s_q, l_q, n.to(DEV), kc.to(DEV), km.to(DEV))
+        ps.run()
+        # saliency shift: the critical sets are re-selected as the query drifts
+        cur = ps.buf.crit_idx[:, watch].cpu().numpy()
+        if prev is not None:
+            for b in range(0, w.batch, 8):
+                for r in range(cur.shape[1]):
+                    a, c = set(prev[b, r][prev[b, r] >= 0]), set(cur[b, r][cur[b, r] >= 0])
+                    jac.append(len(a & c) / len(a | c))
+        prev = cur
+        if step in (0, 1, 127, 255):
+            torch.cuda.synchronize()
+            x["s_q"], x["l_q"] = ps.small.q, ps.large.q
+            x["seq_len"], x["k_crit"], x["k_marg"] = ps.batch.seq_len, ps.batch.k_crit, ps.batch.k_marg
+            refs = {}
+            nsh = w.small.layers * w.small.q_heads
+            seqs = [int(s) for s in rng.choice(w.batch, 2, replace=False)]
+            for b in seqs:
+                for j in rng.choice(nsh, 24, replace=False):
+                    refs[(b, int(j))] = oracle_small_row(x, b, int(j))
+                    check_small_row(ps.buf, x, b, int(j), refs[(b, int(j))], tol, f"{w.name} step {step}")
+            heads = [(b, int(l), int(h)) for b in seqs
+                     for l, h in zip(rng.integers(0, w.large.layers, 12), rng.integers(0, w.large.q_heads, 12))]
+            worst = check_heads(ps, x, heads, refs, tol, f"{w.name} step {step}")
+            checked += 1
+            log(f"[fullsize] step {step}: lengths {int(n.min())}..{int(n.max())}, "
+                f"{len(refs)} small rows ok, worst large-head error {worst:.3g}")
+    torch.cuda.synchronize()
+    assert checked == 4
+    mj = float(np.mean(jac))
+    log(f"[fullsize] mean Jaccard of critical sets between consecutive steps: {mj:.3f}")
+    assert 0.3 < mj < 0.999
+    del ps, x, z
+    free()
+
+
+def test_qwen2_72b_n65536_compact_store_sampled():
+    w = W.WORKLOADS[5]
+    log(f"[fullsize] {w.name}: generating small-model inputs")
+    z = W.latents(w, DEV)
+    x = W.make_step_inputs(w, DEV, 0, z=z, large=False)
+    B, L, hk, d = w.batch, w.large.layers, w.large.kv_heads, w.large.head_dim
+    hq, nsh = w.large.q_heads, w.small.layers * w.small.q_heads
+    g = hq // hk
+    n_cap = w.n_cap
+    # the retained set comes from the oracle's partition of every small row
+    log("[fullsize] oracle partitions of all small rows")
+    refs = {(b, j): oracle_small_row(x, b, j) for b in range(B) for j in range(nsh)}
+    hm = host(x["head_map"]).reshape(L, hq)
+    kc_rows, vc_rows = {}, {}
+    for b in range(B):
+        for li in range(L):
+            for kv in range(hk):
+                js = hm[li, kv * g:(kv + 1) * g]
+                c = np.unique(np.concatenate([refs[(b, int(j))]["crit"] for j in js]))
+                m = np.unique(np.concatenate([refs[(b, int(j))]["marg"] for j in js] + [c]))
+                kc_rows[(b, li, kv)] = c[c >= 0]
+                vc_rows[(b, li, kv)] = m[m >= 0]
+    R = max(max(len(v) for v in kc_rows.values()), max(len(v) for v in vc_rows.values()))
+    log(f"[fullsize] compact store: {R} rows per kv head of {n_cap} "
+        f"(union of critical {np.mean([len(v) for v in kc_rows.values()]) / n_cap:.3f}, "
+        f"critical+marginal {np.mean([len(v) for v in vc_rows.values()]) / n_cap:.3f})")
+    ck = torch.zeros((B, L, hk, R, d), dtype=w.torch_dtype, device=DEV)
+    cv = torch.zeros_like(ck)
+    ks = torch.full((B, L, hk, n_cap), -1, dtype=torch.int32, device=DEV)
+    vs = torch.full_like(ks, -1)
+    heavy = W.heavy_positions(w, DEV)
+    for li in range(L):
+        k, v = W.kv_layer(w, "large", li, z, heavy, DEV)  # full layer, then only retained rows kept
+        for b in range(B):
+            for kv in range(hk):
+                for rows, src, dst, slot in ((kc_rows[(b, li, kv)], k, ck, ks),
+                                             (vc_rows[(b, li, kv)], v, cv, vs)):
+                    idx = torch.from_numpy(rows.astype(np.int64)).to(DEV)
+                    dst[b, li, kv, : len(rows)] = src[b, kv, idx]
+                    slot[b, li, kv, idx] = torch.arange(len(rows), dtype=torch.int32, device=DEV)
+        del k, v
+    ps = prepare_step(x, MODE, k_slot=ks, v_slot=vs, l_k=ck, l_v=cv)
+    ps.run()
+    torch.cuda.synchronize()
+    log("[fullsize] step done; checking every small row and sampled large heads")
+    tol = TOL[w.torch_dtype]
+    for (b, j), ref in refs.items():
+        check_small_row(ps.buf, x, b, j, ref, tol, w.name)
+    rng = np.random.default_rng(5)
+    worst = check_heads(ps, x, sample(rng, 32, B, L, hq), refs, tol, w.name,
+                        l_k=ck, l_v=cv, k_slot=ks, v_slot=vs)
+    log(f"[fullsize] {w.name} ok: {len(refs)} small rows, worst large-head error {worst:.3g}")
+    del ps, x, ck, cv, ks, vs, z
+    free()
