@@ -9,18 +9,22 @@
 //      to the row max in steps of 1/64 -- locates each target's bin without
 //      the atomic pile-up that raw key bits give (logits share their top
 //      bits);
-//   2. the keys of each target's bin are gathered into LDS and an exact
-//      11+11+10-bit radix select among them gives the target key T and how
-//      many tokens equal to T it takes (the lowest indices); a bin too full
-//      for LDS is selected from the whole row instead;
+//   2. the keys of each target's bin are gathered into LDS and ranked
+//      exactly: by counting all pairs when the bin is small, else by an
+//      11+11+10-bit radix select (over LDS, or over the row when the bin
+//      exceeds the LDS buffer).  This gives the target key T, how many
+//      tokens equal to T the set takes (the lowest indices) and how many
+//      tokens equal T in all;
 //   3. one ordered pass compacts C and M in ascending token order with
-//      workgroup prefix sums, computes p' for marginal tokens and the masses
-//      S'_C, S'_M.
-// Rows up to 16384 tokens are read once, 4 consecutive logits per thread
-// per 2048-token chunk, and kept in registers for all passes; longer rows
-// are re-read per pass, four chunks in flight at a time.  The fused variants first combine stage 1's per-chunk
-// partials of their head (row max, row sum, the head's output), so a step
-// needs no separate merge launch.  Deterministic.
+//      workgroup prefix sums (DPP wave scans), computes p' for marginal
+//      tokens and the masses S'_C, S'_M.  Tie ranks are scanned only when a
+//      threshold's ties are split between two sets.
+// Rows up to 8192 tokens are read once, 4 consecutive logits per thread per
+// 2048-token chunk, and kept in registers; their compaction needs a single
+// barrier.  Longer rows are re-read per pass, four chunks in flight.  The
+// fused variant first combines stage 1's per-chunk records of its head (row
+// max, row sum, the head's output), so a step needs no separate merge launch.
+// The result depends only on the logits: deterministic.
 #include "common.h"
 #include "launch.h"
 #include "merge.h"
@@ -31,8 +35,9 @@ namespace {
 constexpr int kPT = 512;  // threads per row
 constexpr int kWaves = kPT / kWave;
 constexpr int kBins = 2048;
-constexpr int kCap = 4096;  // candidate keys per target kept in LDS
-constexpr int kChunk = 4 * kPT;  // tokens per register chunk
+constexpr int kCap = 2048;       // candidate keys per target kept in LDS
+constexpr int kChunk = 4 * kPT;  // tokens per chunk (4 per thread)
+constexpr int kMaxNK = 4;        // chunks of a register-cached row
 
 struct PartArgs {
   int n_cap, nsh, kc_cap, km_cap;
@@ -61,10 +66,27 @@ __device__ __forceinline__ int logit_bin(float s, float M) {
   return 2047 - (int)d;
 }
 
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ uint32_t dpp_shift(uint32_t v) {
+  // lanes without a source (or outside ROW_MASK) read 0
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, ROW_MASK, 0xf, false);
+}
+
+// Inclusive prefix sum over the 64 lanes of a wave with DPP: shifts of 1, 2,
+// 4, 8 inside each 16-lane row, then the row ends broadcast to the next rows.
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v) {
+  v += dpp_shift<0x111, 0xf>(v);  // row_shr:1
+  v += dpp_shift<0x112, 0xf>(v);  // row_shr:2
+  v += dpp_shift<0x114, 0xf>(v);  // row_shr:4
+  v += dpp_shift<0x118, 0xf>(v);  // row_shr:8
+  v += dpp_shift<0x142, 0xa>(v);  // row_bcast:15 into rows 1 and 3
+  v += dpp_shift<0x143, 0xc>(v);  // row_bcast:31 into rows 2 and 3
+  return v;
+}
+
 // One wave: find the bin of hist[0..NB) (scanned from the top) holding the
 // rr-th element (1-based); returns the bin and the count strictly above it.
-// Each lane owns NB/64 consecutive bins (lane 0 the highest) and scans them
-// in registers.
+// Each lane owns NB/64 consecutive bins (lane 0 the highest) in registers.
 template <int NB>
 __device__ __forceinline__ void find_digit(const uint32_t *hist, uint32_t rr, int &digit,
                                            uint32_t &above) {
@@ -83,16 +105,10 @@ __device__ __forceinline__ void find_digit(const uint32_t *hist, uint32_t rr, in
   uint32_t s = 0;
 #pragma unroll
   for (int k = 0; k < PER; ++k) s += hv[k];
-  uint32_t inc = s;
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const uint32_t y = __shfl_up(inc, o, kWave);
-    if (lane >= o) inc += y;
-  }
+  const uint32_t inc = wave_incl_scan(s);
   const uint32_t exc = inc - s;  // elements in the bins above this lane's
   const uint64_t who = __ballot(exc < rr && rr <= inc);
   const int src = who ? __ffsll((unsigned long long)who) - 1 : 0;
-  // every lane scans its own bins from the top; lane src's answer is used
   uint32_t cum = exc, ab = exc;
   int dsel = lo;
   bool found = false;
@@ -108,31 +124,16 @@ __device__ __forceinline__ void find_digit(const uint32_t *hist, uint32_t rr, in
   above = __shfl(ab, src, kWave);
 }
 
-// Inclusive prefix sum over the wave (64 lanes).
-__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const uint32_t y = __shfl_up(v, o, kWave);
-    if (lane >= o) v += y;
-  }
-  return v;
-}
-
 struct alignas(16) PartShared {
   uint32_t hist[2][kBins];
-  union {  // the merge's chunk weights are dead before candidates are gathered
-    uint32_t cand[2][kCap];
-    float mw[kMaxChunks];
-  };
-  uint32_t sel[2][4];  // per target: prefix, mask, remaining rank, bin
-  uint32_t res[2][2];  // per target selected by counting: key, ties taken
+  uint32_t cand[2][kCap];
+  uint32_t sel[2][4];  // radix: prefix, mask, remaining rank, count of T
+  uint32_t res[2][4];  // counting: key, ties taken, ties in all
   uint32_t ncand[2];
-  uint32_t wtot[2][2][kWaves];
+  uint32_t wt[4][kMaxNK][kWaves];  // wave totals of the block scans
   float wsum[2][kWaves];
-  float mred[kWaves + kPT];
+  float mred[3 * kPT + 2];
 };
-static_assert(sizeof(float) * kMaxChunks <= sizeof(uint32_t) * 2 * kCap, "mw fits in cand");
 
 struct RowCtx {
   int row, n, nc, nm;
@@ -164,7 +165,7 @@ __device__ __forceinline__ void row_setup(const PartArgs &a, PartShared &sh, Row
     void *out = a.small_out;
     const int64_t o0 = (int64_t)r.row * a.d;
     const bool bf = a.out_bf16;
-    merge_head<kPT>(in, a.d, sh.mw, sh.mred, r.M, r.Z, [&](int c, float v) {
+    merge_head<kPT>(in, a.d, sh.mred, r.M, r.Z, [&](int c, float v) {
       if (bf)
         elem<bf16_t>::store1(out, o0 + c, v);
       else
@@ -189,7 +190,6 @@ struct Row {
   float s[R > 0 ? R : 4];
   const float *lg;
   int n;
-
   bool aligned;  // 16-byte aligned row: whole chunks load as one float4
 
   __device__ __forceinline__ float4 fetch(int k) const {
@@ -255,46 +255,47 @@ struct Row {
   }
 };
 
-// Steps 1 and 2: the two target keys and the ties each takes.
+struct Targets {
+  uint32_t T[2];     // key of the |C|-th / (|C|+|M|)-th token
+  uint32_t need[2];  // tokens equal to T that the set takes
+  uint32_t eq[2];    // tokens equal to T in the row
+};
+
+// Steps 1 and 2.
 template <typename Row>
-__device__ __forceinline__ void select_targets(PartShared &sh, const RowCtx &r, const Row &row,
-                                               uint32_t &TC, uint32_t &TP, uint32_t &needC,
-                                               uint32_t &needP) {
+__device__ __forceinline__ Targets select_targets(PartShared &sh, const RowCtx &r, const Row &row) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const float M = r.M;
   for (int x = tid; x < kBins; x += kPT) sh.hist[0][x] = 0;
-  if (tid < 2) {
-    sh.sel[tid][0] = 0;
-    sh.sel[tid][1] = 0;
-    sh.sel[tid][2] = (uint32_t)(tid == 0 ? r.nc : r.nc + r.nm);
-    sh.ncand[tid] = 0;
-  }
+  if (tid < 2) sh.ncand[tid] = 0;
   __syncthreads();
   row.each([&](float s, bool valid) {
     if (valid) atomicAdd(&sh.hist[0][logit_bin(s, M)], 1u);
   });
   __syncthreads();
-  if (wave < 2) {
-    int bin;
+  // every wave finds both targets' bins itself: no broadcast needed
+  uint32_t rr[2] = {(uint32_t)r.nc, (uint32_t)(r.nc + r.nm)};
+  int bin[2];
+  uint32_t cnt[2];
+#pragma unroll
+  for (int x = 0; x < 2; ++x) {
     uint32_t above;
-    find_digit<kBins>(sh.hist[0], sh.sel[wave][2], bin, above);
-    if (lane == 0) {
-      sh.sel[wave][2] -= above;
-      sh.sel[wave][3] = (uint32_t)bin;
-    }
+    find_digit<kBins>(sh.hist[0], rr[x], bin[x], above);
+    rr[x] -= above;
+    cnt[x] = sh.hist[0][bin[x]];
   }
-  __syncthreads();
-  const int bin0 = (int)sh.sel[0][3], bin1 = (int)sh.sel[1][3];
-  const bool lds0 = sh.hist[0][bin0] <= (uint32_t)kCap, lds1 = sh.hist[0][bin1] <= (uint32_t)kCap;
-  if (lds0 || lds1) {
-    // gather the candidate keys (order inside a bin does not matter here)
+  // 0: rank by counting, 1: radix over LDS candidates, 2: radix over the row
+  int mode[2];
+#pragma unroll
+  for (int x = 0; x < 2; ++x) mode[x] = cnt[x] <= (uint32_t)kPT ? 0 : (cnt[x] <= (uint32_t)kCap ? 1 : 2);
+  if (mode[0] < 2 || mode[1] < 2) {
     const uint64_t lt = lanemask_lt();
     row.each([&](float s, bool valid) {
       const int bn = valid ? logit_bin(s, M) : -1;
       const uint32_t u = logit_key(s);
 #pragma unroll
       for (int x = 0; x < 2; ++x) {
-        const bool take = (x == 0 ? lds0 : lds1) && bn == (x == 0 ? bin0 : bin1);
+        const bool take = mode[x] < 2 && bn == bin[x];
         const uint64_t bal = __ballot(take);
         if (bal) {  // one LDS atomic per wave
           uint32_t off = 0;
@@ -305,94 +306,114 @@ __device__ __forceinline__ void select_targets(PartShared &sh, const RowCtx &r, 
       }
     });
   }
-  __syncthreads();  // candidates and their counts visible
-  // few candidates: rank each one by counting (all pairs), no radix passes
-  const uint32_t nc0 = lds0 ? sh.ncand[0] : 0u, nc1 = lds1 ? sh.ncand[1] : 0u;
-  const bool cnt0 = lds0 && nc0 <= (uint32_t)kPT, cnt1 = lds1 && nc1 <= (uint32_t)kPT;
+  if (tid < 2) {
+    sh.sel[tid][0] = 0;
+    sh.sel[tid][1] = 0;
+    sh.sel[tid][2] = rr[tid];
+  }
+  __syncthreads();  // candidates visible
 #pragma unroll
   for (int x = 0; x < 2; ++x) {
-    const bool cnt = x == 0 ? cnt0 : cnt1;
-    const uint32_t nx = x == 0 ? nc0 : nc1;
-    if (cnt && (uint32_t)tid < nx) {
+    if (mode[x] == 0 && (uint32_t)tid < cnt[x]) {
       const uint32_t key = sh.cand[x][tid];
       uint32_t gt = 0, eq = 0;
-      for (uint32_t c = 0; c < nx; ++c) {
-        const uint32_t v = sh.cand[x][c];
-        gt += v > key ? 1u : 0u;
-        eq += v == key ? 1u : 0u;
+      for (uint32_t c0 = 0; c0 < cnt[x]; c0 += 8) {  // 8 keys per step, two 16-byte reads
+        const uint4 a = *reinterpret_cast<const uint4 *>(&sh.cand[x][c0]);
+        const uint4 b = *reinterpret_cast<const uint4 *>(&sh.cand[x][c0 + 4]);
+        const uint32_t vs[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const bool ok = c0 + e < cnt[x];
+          gt += ok && vs[e] > key ? 1u : 0u;
+          eq += ok && vs[e] == key ? 1u : 0u;
+        }
       }
-      const uint32_t rr = sh.sel[x][2];
-      if (gt < rr && rr <= gt + eq) {  // every tie of the target writes the same values
+      if (gt < rr[x] && rr[x] <= gt + eq) {  // every tie of the target writes the same
         sh.res[x][0] = key;
-        sh.res[x][1] = rr - gt;
+        sh.res[x][1] = rr[x] - gt;
+        sh.res[x][2] = eq;
       }
     }
   }
-  const bool lds0r = lds0 && !cnt0, lds1r = lds1 && !cnt1;  // radix over LDS candidates
-  const bool need_radix = !cnt0 || !cnt1;
-  for (int pass = 0; need_radix && pass < 3; ++pass) {  // digits of 11, 11 and 10 bits
-    const int shf = pass == 0 ? 21 : (pass == 1 ? 10 : 0), nb = pass < 2 ? 2048 : 1024;
-    const uint32_t dmask = (uint32_t)nb - 1u;
-    __syncthreads();  // candidates / previous selection visible; hist free
-    for (int x = tid; x < 2 * kBins; x += kPT) (&sh.hist[0][0])[x] = 0;
-    __syncthreads();
-    const uint32_t p0 = sh.sel[0][0], m0 = sh.sel[0][1], p1 = sh.sel[1][0], m1 = sh.sel[1][1];
-    if (lds0r)
-      for (int k = tid; k < (int)sh.ncand[0]; k += kPT) {
-        const uint32_t u = sh.cand[0][k];
-        if ((u & m0) == p0) atomicAdd(&sh.hist[0][(u >> shf) & dmask], 1u);
-      }
-    if (lds1r)
-      for (int k = tid; k < (int)sh.ncand[1]; k += kPT) {
-        const uint32_t u = sh.cand[1][k];
-        if ((u & m1) == p1) atomicAdd(&sh.hist[1][(u >> shf) & dmask], 1u);
-      }
-    if (!lds0 || !lds1)  // a bin too full for LDS: select it from the row
-      row.each([&](float s, bool valid) {
-        const int bn = valid ? logit_bin(s, M) : -1;
-        const uint32_t u = logit_key(s);
-        if (!lds0 && bn == bin0 && (u & m0) == p0) atomicAdd(&sh.hist[0][(u >> shf) & dmask], 1u);
-        if (!lds1 && bn == bin1 && (u & m1) == p1) atomicAdd(&sh.hist[1][(u >> shf) & dmask], 1u);
-      });
-    __syncthreads();
-    if (wave < 2) {
-      int digit;
-      uint32_t above;
-      if (pass < 2)
-        find_digit<2048>(sh.hist[wave], sh.sel[wave][2], digit, above);
-      else
-        find_digit<1024>(sh.hist[wave], sh.sel[wave][2], digit, above);
-      if (lane == 0) {
-        sh.sel[wave][0] |= (uint32_t)digit << shf;
-        sh.sel[wave][1] |= dmask << shf;
-        sh.sel[wave][2] -= above;
+  if (mode[0] != 0 || mode[1] != 0) {
+    for (int pass = 0; pass < 3; ++pass) {  // digits of 11, 11 and 10 bits
+      const int shf = pass == 0 ? 21 : (pass == 1 ? 10 : 0), nb = pass < 2 ? 2048 : 1024;
+      const uint32_t dmask = (uint32_t)nb - 1u;
+      __syncthreads();  // previous selection visible; hist free
+      for (int x = tid; x < 2 * kBins; x += kPT) (&sh.hist[0][0])[x] = 0;
+      __syncthreads();
+      const uint32_t p0 = sh.sel[0][0], m0 = sh.sel[0][1], p1 = sh.sel[1][0], m1 = sh.sel[1][1];
+      if (mode[0] == 1)
+        for (int k = tid; k < (int)cnt[0]; k += kPT) {
+          const uint32_t u = sh.cand[0][k];
+          if ((u & m0) == p0) atomicAdd(&sh.hist[0][(u >> shf) & dmask], 1u);
+        }
+      if (mode[1] == 1)
+        for (int k = tid; k < (int)cnt[1]; k += kPT) {
+          const uint32_t u = sh.cand[1][k];
+          if ((u & m1) == p1) atomicAdd(&sh.hist[1][(u >> shf) & dmask], 1u);
+        }
+      if (mode[0] == 2 || mode[1] == 2)
+        row.each([&](float s, bool valid) {
+          const int bn = valid ? logit_bin(s, M) : -1;
+          const uint32_t u = logit_key(s);
+          if (mode[0] == 2 && bn == bin[0] && (u & m0) == p0) atomicAdd(&sh.hist[0][(u >> shf) & dmask], 1u);
+          if (mode[1] == 2 && bn == bin[1] && (u & m1) == p1) atomicAdd(&sh.hist[1][(u >> shf) & dmask], 1u);
+        });
+      __syncthreads();
+      if (wave < 2 && mode[wave] != 0) {
+        int digit;
+        uint32_t above;
+        if (pass < 2)
+          find_digit<2048>(sh.hist[wave], sh.sel[wave][2], digit, above);
+        else
+          find_digit<1024>(sh.hist[wave], sh.sel[wave][2], digit, above);
+        if (lane == 0) {
+          sh.sel[wave][0] |= (uint32_t)digit << shf;
+          sh.sel[wave][1] |= dmask << shf;
+          sh.sel[wave][2] -= above;
+          sh.sel[wave][3] = sh.hist[wave][digit];  // after the last pass: count of T
+        }
       }
     }
   }
   __syncthreads();
-  TC = cnt0 ? sh.res[0][0] : sh.sel[0][0];
-  TP = cnt1 ? sh.res[1][0] : sh.sel[1][0];
-  needC = cnt0 ? sh.res[0][1] : sh.sel[0][2];
-  needP = cnt1 ? sh.res[1][1] : sh.sel[1][2];
+  Targets t;
+#pragma unroll
+  for (int x = 0; x < 2; ++x) {
+    const bool c = mode[x] == 0;
+    t.T[x] = c ? sh.res[x][0] : sh.sel[x][0];
+    t.need[x] = c ? sh.res[x][1] : sh.sel[x][2];
+    t.eq[x] = c ? sh.res[x][2] : sh.sel[x][3];
+  }
+  return t;
 }
 
-// Workgroup exclusive prefix of a packed pair of 16-bit counts (per chunk
-// totals stay below 65536); returns this thread's offset and the total.
-__device__ __forceinline__ void block_scan2(PartShared &sh, int par, int slot, uint32_t v,
-                                            uint32_t &excl, uint32_t &total) {
+// Workgroup exclusive prefix of NK packed values (two 16-bit counts each;
+// per-chunk totals stay below 65536) with one barrier.
+template <int NK>
+__device__ __forceinline__ void block_scan(PartShared &sh, int slot, const uint32_t *v,
+                                           uint32_t *excl, uint32_t *total) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const uint32_t inc = wave_incl_scan(v);
-  if (lane == 63) sh.wtot[par][slot][wave] = inc;
-  __syncthreads();
-  uint32_t off = 0, tot = 0;
+  uint32_t inc[NK];
 #pragma unroll
-  for (int w = 0; w < kWaves; ++w) {
-    const uint32_t x = sh.wtot[par][slot][w];
-    off += w < wave ? x : 0u;
-    tot += x;
+  for (int k = 0; k < NK; ++k) {
+    inc[k] = wave_incl_scan(v[k]);
+    if (lane == 63) sh.wt[slot][k][wave] = inc[k];
   }
-  excl = off + inc - v;
-  total = tot;
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < NK; ++k) {
+    uint32_t off = 0, tot = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      const uint32_t x = sh.wt[slot][k][w];
+      off += w < wave ? x : 0u;
+      tot += x;
+    }
+    excl[k] = off + inc[k] - v[k];
+    total[k] = tot;
+  }
 }
 
 __device__ __forceinline__ void finish_row(const PartArgs &a, PartShared &sh, const RowCtx &r,
@@ -421,10 +442,41 @@ __device__ __forceinline__ void finish_row(const PartArgs &a, PartShared &sh, co
   }
 }
 
+// Step 3 helpers: membership of one value and its output.
+struct Compactor {
+  const RowCtx &r;
+  Targets t;
+  float Zinv;
+  float sc = 0.0f, sm = 0.0f;
+
+  // rC / rP: the value's rank (0-based, token order) among the row's ties at T
+  __device__ __forceinline__ void classify(uint32_t u, bool valid, uint32_t rC, uint32_t rP,
+                                           bool &inC, bool &inM) const {
+    inC = valid && (u > t.T[0] || (u == t.T[0] && rC < t.need[0]));
+    const bool inP = valid && (u > t.T[1] || (u == t.T[1] && rP < t.need[1]));
+    inM = inP && !inC;
+  }
+  __device__ __forceinline__ void emit(float s, int tok, bool inC, bool inM, uint32_t &pc,
+                                       uint32_t &pm) {
+    const float p = (inC || inM) ? __expf(s - r.M) * Zinv : 0.0f;
+    sc += inC ? p : 0.0f;
+    sm += inM ? p : 0.0f;
+    // the guards only matter if the select were wrong: never write past a row
+    if (inC && pc < (uint32_t)r.nc) r.crit[pc] = tok;
+    if (inM && pm < (uint32_t)r.nm) {
+      r.marg[pm] = tok;
+      r.mp[pm] = p;
+    }
+    pc += inC ? 1u : 0u;
+    pm += inM ? 1u : 0u;
+  }
+};
+
 // ---------------------------------------------------------------- kernel --
 
 template <bool kMerge, int R>
-__global__ __launch_bounds__(kPT) void partition_kernel(PartArgs a) {
+__global__ __launch_bounds__(kPT) __attribute__((amdgpu_waves_per_eu(4)))
+void partition_kernel(PartArgs a) {
   __shared__ PartShared sh;
   RowCtx r;
   row_setup<kMerge>(a, sh, r);
@@ -434,80 +486,106 @@ __global__ __launch_bounds__(kPT) void partition_kernel(PartArgs a) {
   row.n = r.n;
   row.aligned = (reinterpret_cast<uintptr_t>(r.lg) & 15) == 0;
   row.load();
-  uint32_t TC, TP, needC, needP;
-  select_targets(sh, r, row, TC, TP, needC, needP);
+  Compactor cp{r, select_targets(sh, r, row), 1.0f / r.Z};
+  // ties at a threshold split between two sets need their ranks in token order
+  const bool split = cp.t.need[0] < cp.t.eq[0] || cp.t.need[1] < cp.t.eq[1];
 
-  // ordered compaction, one chunk at a time
-  const float Zinv = 1.0f / r.Z;
-  uint32_t carry_eqC = 0, carry_eqP = 0, carry_c = 0, carry_m = 0;
-  float sc = 0.0f, sm = 0.0f;
-  const int nk = row.chunks();
-  auto compact = [&](int k, const float4 cur) {
-    const float sv[4] = {cur.x, cur.y, cur.z, cur.w};
-    const int par = k & 1;
-    const int t0 = k * kChunk + 4 * tid;
-    uint32_t u[4];
-    bool eqC[4], eqP[4];
-    uint32_t cnt = 0;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const bool valid = t0 + e < r.n;
-      u[e] = logit_key(sv[e]);
-      eqC[e] = valid && u[e] == TC;
-      eqP[e] = valid && u[e] == TP;
-      cnt += (eqC[e] ? 1u : 0u) + (eqP[e] ? 0x10000u : 0u);
-    }
-    uint32_t ex, tot;
-    block_scan2(sh, par, 0, cnt, ex, tot);
-    uint32_t rC = carry_eqC + (ex & 0xffffu), rP = carry_eqP + (ex >> 16);
-    bool inC[4], inM[4];
-    uint32_t cm = 0;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const bool valid = t0 + e < r.n;
-      inC[e] = valid && (u[e] > TC || (eqC[e] && rC < needC));
-      const bool inP = valid && (u[e] > TP || (eqP[e] && rP < needP));
-      inM[e] = inP && !inC[e];
-      rC += eqC[e] ? 1u : 0u;
-      rP += eqP[e] ? 1u : 0u;
-      cm += (inC[e] ? 1u : 0u) + (inM[e] ? 0x10000u : 0u);
-    }
-    carry_eqC += tot & 0xffffu;
-    carry_eqP += tot >> 16;
-    block_scan2(sh, par, 1, cm, ex, tot);
-    uint32_t pc = carry_c + (ex & 0xffffu), pm = carry_m + (ex >> 16);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const float p = (inC[e] || inM[e]) ? __expf(sv[e] - r.M) * Zinv : 0.0f;
-      sc += inC[e] ? p : 0.0f;
-      sm += inM[e] ? p : 0.0f;
-      // the guards only matter if the select were wrong: never write past a row
-      if (inC[e] && pc < (uint32_t)r.nc) r.crit[pc] = t0 + e;
-      if (inM[e] && pm < (uint32_t)r.nm) {
-        r.marg[pm] = t0 + e;
-        r.mp[pm] = p;
-      }
-      pc += inC[e] ? 1u : 0u;
-      pm += inM[e] ? 1u : 0u;
-    }
-    carry_c += tot & 0xffffu;
-    carry_m += tot >> 16;
-  };
   if constexpr (R > 0) {
+    constexpr int NK = R / 4;
+    static_assert(NK <= kMaxNK, "register row too long");
+    uint32_t rank_base[NK];  // tie ranks (C low, P high) before this thread's values
 #pragma unroll
-    for (int k = 0; k < R / 4; ++k) {
-      if (k >= nk) break;
-      compact(k, row.chunk(k));
+    for (int k = 0; k < NK; ++k) rank_base[k] = 0;
+    if (split) {
+      uint32_t v[NK], ex[NK], tot[NK];
+#pragma unroll
+      for (int k = 0; k < NK; ++k) {
+        v[k] = 0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const bool ok = row.valid(k, e);
+          const uint32_t u = logit_key(row.s[4 * k + e]);
+          v[k] += (ok && u == cp.t.T[0] ? 1u : 0u) + (ok && u == cp.t.T[1] ? 0x10000u : 0u);
+        }
+      }
+      block_scan<NK>(sh, 0, v, ex, tot);
+      uint32_t carry = 0;
+#pragma unroll
+      for (int k = 0; k < NK; ++k) {
+        rank_base[k] = carry + ex[k];
+        carry += tot[k];
+      }
+    }
+    bool inC[R], inM[R];
+    uint32_t v[NK], ex[NK], tot[NK];
+#pragma unroll
+    for (int k = 0; k < NK; ++k) {
+      uint32_t rC = rank_base[k] & 0xffffu, rP = rank_base[k] >> 16;
+      v[k] = 0;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int i = 4 * k + e;
+        const bool ok = row.valid(k, e);
+        const uint32_t u = logit_key(row.s[i]);
+        cp.classify(u, ok, rC, rP, inC[i], inM[i]);
+        rC += ok && u == cp.t.T[0] ? 1u : 0u;
+        rP += ok && u == cp.t.T[1] ? 1u : 0u;
+        v[k] += (inC[i] ? 1u : 0u) + (inM[i] ? 0x10000u : 0u);
+      }
+    }
+    block_scan<NK>(sh, 1, v, ex, tot);
+    uint32_t carry_c = 0, carry_m = 0;
+#pragma unroll
+    for (int k = 0; k < NK; ++k) {
+      uint32_t pc = carry_c + (ex[k] & 0xffffu), pm = carry_m + (ex[k] >> 16);
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        cp.emit(row.s[4 * k + e], k * kChunk + 4 * tid + e, inC[4 * k + e], inM[4 * k + e], pc, pm);
+      carry_c += tot[k] & 0xffffu;
+      carry_m += tot[k] >> 16;
     }
   } else {
+    const int nk = row.chunks();
+    uint32_t carry_eq = 0, carry_c = 0, carry_m = 0;
     float4 nxt = row.chunk(0);
     for (int k = 0; k < nk; ++k) {
       const float4 cur = nxt;
       if (k + 1 < nk) nxt = row.chunk(k + 1);  // in flight during this chunk's scans
-      compact(k, cur);
+      const float sv[4] = {cur.x, cur.y, cur.z, cur.w};
+      const int par = 2 * (k & 1);
+      uint32_t u[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) u[e] = logit_key(sv[e]);
+      uint32_t rank = 0;
+      if (split) {
+        uint32_t v = 0, ex, tot;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          v += (row.valid(k, e) && u[e] == cp.t.T[0] ? 1u : 0u) +
+               (row.valid(k, e) && u[e] == cp.t.T[1] ? 0x10000u : 0u);
+        block_scan<1>(sh, par, &v, &ex, &tot);
+        rank = carry_eq + ex;
+        carry_eq += tot;
+      }
+      bool inC[4], inM[4];
+      uint32_t rC = rank & 0xffffu, rP = rank >> 16, v = 0, ex, tot;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const bool ok = row.valid(k, e);
+        cp.classify(u[e], ok, rC, rP, inC[e], inM[e]);
+        rC += ok && u[e] == cp.t.T[0] ? 1u : 0u;
+        rP += ok && u[e] == cp.t.T[1] ? 1u : 0u;
+        v += (inC[e] ? 1u : 0u) + (inM[e] ? 0x10000u : 0u);
+      }
+      block_scan<1>(sh, par + 1, &v, &ex, &tot);
+      uint32_t pc = carry_c + (ex & 0xffffu), pm = carry_m + (ex >> 16);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) cp.emit(sv[e], k * kChunk + 4 * tid + e, inC[e], inM[e], pc, pm);
+      carry_c += tot & 0xffffu;
+      carry_m += tot >> 16;
     }
   }
-  finish_row(a, sh, r, sc, sm);
+  finish_row(a, sh, r, cp.sc, cp.sm);
 }
 
 PartArgs base_args(const smallkv_batch_t &b, int n_small_heads, const float *logits,
@@ -541,8 +619,6 @@ hipError_t launch_rows(const PartArgs &a, int rows, hipStream_t st) {
     hipLaunchKernelGGL((partition_kernel<kMerge, 8>), grid, block, 0, st, a);
   else if (n <= 16 * kPT)
     hipLaunchKernelGGL((partition_kernel<kMerge, 16>), grid, block, 0, st, a);
-  else if (n <= 32 * kPT)
-    hipLaunchKernelGGL((partition_kernel<kMerge, 32>), grid, block, 0, st, a);
   else
     hipLaunchKernelGGL((partition_kernel<kMerge, 0>), grid, block, 0, st, a);
   return hipGetLastError();

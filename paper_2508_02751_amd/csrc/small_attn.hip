@@ -96,6 +96,77 @@ __device__ __forceinline__ float chain_logit_sq(const_u32_ptr qw, const float *k
   return s == 0.0f ? 0.0f : s;
 }
 
+// Max (or sum) over the wave of GP per-head values at once.  Halving
+// exchanges hand every lane group one head (head = lane >> (6 - log2 GP)):
+// across lane halves with v_permlane32_swap, across row pairs with
+// v_permlane16_swap, inside a row with DPP; then each group reduces alone
+// with DPP.  No LDS traffic and no per-lane selects above the row level.
+template <bool kMax>
+__device__ __forceinline__ float red_op(float x, float y) {
+  return kMax ? fmaxf(x, y) : x + y;
+}
+
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, true));
+}
+
+template <int GP, bool kMax>
+__device__ __forceinline__ float wave_reduce_heads(float (&v)[GP]) {
+  const int lane = threadIdx.x & 63;
+  int n = GP;
+  if (n >= 2) {  // lanes 0-31 keep heads [0, n/2), lanes 32-63 the rest
+#pragma unroll
+    for (int i = 0; i < GP / 2; ++i) {
+      const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v[i]), __float_as_uint(v[i + GP / 2]),
+                                                      false, false);
+      v[i] = red_op<kMax>(__uint_as_float(r[0]), __uint_as_float(r[1]));
+    }
+    n >>= 1;
+  }
+  if (n >= 2) {  // even rows keep the lower half of the heads, odd rows the upper
+#pragma unroll
+    for (int i = 0; i < GP / 4; ++i) {
+      const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v[i]), __float_as_uint(v[i + GP / 4]),
+                                                      false, false);
+      v[i] = red_op<kMax>(__uint_as_float(r[0]), __uint_as_float(r[1]));
+    }
+    n >>= 1;
+  }
+  if (n >= 2) {  // row halves: lane i pairs with i ^ 8 (row_ror:8)
+    const bool upper = (lane & 8) != 0;
+#pragma unroll
+    for (int i = 0; i < GP / 8; ++i) {
+      const float keep = upper ? v[i + GP / 8] : v[i];
+      const float send = upper ? v[i] : v[i + GP / 8];
+      v[i] = red_op<kMax>(keep, dpp<0x128>(send));
+    }
+    n >>= 1;
+  }
+  if (n >= 2) {  // 8-lane halves: lane i pairs with 7 - i (row_half_mirror)
+    const bool upper = (lane & 4) != 0;
+#pragma unroll
+    for (int i = 0; i < GP / 16; ++i) {
+      const float keep = upper ? v[i + GP / 16] : v[i];
+      const float send = upper ? v[i] : v[i + GP / 16];
+      v[i] = red_op<kMax>(keep, dpp<0x141>(send));
+    }
+    n >>= 1;
+  }
+  // the group of 64 / GP lanes now shares one head: reduce it
+  float x = v[0];
+  x = red_op<kMax>(x, dpp<0xB1>(x));                    // lane ^ 1
+  x = red_op<kMax>(x, dpp<0x4E>(x));                    // lane ^ 2
+  if (GP <= 8) x = red_op<kMax>(x, dpp<0x141>(x));      // 8-lane mirror
+  if (GP <= 4) x = red_op<kMax>(x, dpp<0x140>(x));      // 16-lane mirror
+  return x;  // the reduction of head (lane >> (6 - log2 GP))
+}
+
+template <int GP>
+constexpr int head_shift() {
+  return GP == 4 ? 4 : (GP == 8 ? 3 : 2);
+}
+
 template <typename T, int D>
 __device__ __forceinline__ void stage_k(unsigned char *tile, const unsigned char *src, int nr) {
   using C = SmallCfg<T, D>;
@@ -111,7 +182,9 @@ __device__ __forceinline__ void stage_k(unsigned char *tile, const unsigned char
 
 // ------------------------------------------------------------ bf16 / MFMA --
 
-template <int D, int GP>
+// G: the query-group size when known at compile time (0: runtime a.g, the
+// padded heads then run on zero queries instead of behind branches).
+template <int D, int GP, int G>
 __global__ __launch_bounds__(kThreads) void small_attn_mfma(SmallArgs a) {
   using C = SmallCfg<bf16_t, D>;
   constexpr int TILE = C::TILE;
@@ -131,7 +204,8 @@ __global__ __launch_bounds__(kThreads) void small_attn_mfma(SmallArgs a) {
   UnitPos u;
   if (!unit_pos(a, u)) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int g = a.g;
+  const int g = G > 0 ? G : a.g;
+  constexpr int GC = G > 0 ? G : GP;  // heads the chains run on
   const int64_t row0 = (int64_t)u.unit * a.n_cap;
   const unsigned char *kb = reinterpret_cast<const unsigned char *>(a.k) + row0 * C::ROWB;
   const unsigned char *vb = reinterpret_cast<const unsigned char *>(a.v) + row0 * C::ROWB;
@@ -150,6 +224,70 @@ __global__ __launch_bounds__(kThreads) void small_attn_mfma(SmallArgs a) {
 
   for (int tb = u.t0; tb < u.t1; tb += TILE) {
     const int nr = min(TILE, u.t1 - tb);
+    stage_k<bf16_t, D>(tile, kb + (int64_t)tb * C::ROWB, nr);
+    __syncthreads();
+
+    // ---- logits: one token per thread, sequential FMA chains ------------
+    // The chain of each head runs over dims 0..D-1 in order; the K row is
+    // unpacked half a row at a time to keep registers low.
+    float s[GP];
+#pragma unroll
+    for (int i = 0; i < GP; ++i) s[i] = 0.0f;
+    if (tid < nr) {
+      const_u32_ptr qw = (const_u32_ptr)(reinterpret_cast<uintptr_t>(a.q)) + u.head0 * (D / 2);
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        float kr[D / 2];
+#pragma unroll
+        for (int w = 0; w < C::V16 / 2; ++w) {
+          const uint4 v = *reinterpret_cast<const uint4 *>(tile + tid * C::ROWS + (half * C::V16 / 2 + w) * 16);
+          elem<bf16_t>::unpack(v, kr + w * 8);
+        }
+        // one head after another: q comes from SGPRs (scalar loads), and a
+        // wave64 issues dependent FMAs back to back, so the chains need no
+        // interleaving
+#pragma unroll
+        for (int i = 0; i < GC; ++i) {
+          if (G == 0 && i >= g) continue;
+          // the scalar loads of this head's q wait for the chain two heads
+          // back: q is fetched one head ahead instead of all at once (which
+          // would hold hundreds of SGPRs and spill them); the offset stays a
+          // constant so that it folds into the loads
+          const_u32_ptr qb = qw;
+          if (i >= 2) __asm__ volatile("" : "+s"(qb) : "v"(s[i - 2]));
+          else if (half > 0) __asm__ volatile("" : "+s"(qb) : "v"(s[GC - 2 + i]));
+          const_u32_ptr qh = qb + i * (D / 2) + half * (D / 4);
+#pragma unroll
+          for (int c = 0; c < D / 2; c += 2) {
+            const uint32_t w = qh[c / 2];
+            s[i] = __builtin_fmaf(bf16_lo(w), kr[c], s[i]);
+            s[i] = __builtin_fmaf(bf16_hi(w), kr[c + 1], s[i]);
+          }
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < GP; ++i) {
+        if (i < g) {
+          float x = s[i] * a.scale;
+          x = x == 0.0f ? 0.0f : x;
+          lrow[(int64_t)i * a.n_cap + tb + tid] = x;
+          s[i] = x;
+        } else {
+          s[i] = -INFINITY;
+        }
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < GP; ++i) s[i] = -INFINITY;
+    }
+    {
+      float t[GP];
+#pragma unroll
+      for (int i = 0; i < GP; ++i) t[i] = s[i];
+      const float mx = wave_reduce_heads<GP, true>(t);
+      constexpr int sh = head_shift<GP>();
+      if ((lane & ((1 << sh) - 1)) == 0) red[wave * GP + (lane >> sh)] = mx;
+    }
     // V rows of 8 consecutive tokens x one 8-dim chunk, into registers
     uint4 vr[8];
 #pragma unroll
@@ -157,36 +295,6 @@ __global__ __launch_bounds__(kThreads) void small_attn_mfma(SmallArgs a) {
       const int tok = tb8 * 8 + k;
       vr[k] = tok < nr ? *reinterpret_cast<const uint4 *>(vb + (int64_t)(tb + tok) * C::ROWB + dc * 16)
                        : make_uint4(0u, 0u, 0u, 0u);
-    }
-    stage_k<bf16_t, D>(tile, kb + (int64_t)tb * C::ROWB, nr);
-    __syncthreads();
-
-    // ---- logits: one token per thread, sequential FMA chains ------------
-    float s[GP];
-    if (tid < nr) {
-      float kr[D];
-#pragma unroll
-      for (int w = 0; w < C::V16; ++w) {
-        const uint4 v = *reinterpret_cast<const uint4 *>(tile + tid * C::ROWS + w * 16);
-        elem<bf16_t>::unpack(v, kr + w * 8);
-      }
-      const_u32_ptr qw = (const_u32_ptr)(reinterpret_cast<uintptr_t>(a.q)) + u.head0 * (D / 2);
-#pragma unroll
-      for (int i = 0; i < GP; ++i) {
-        s[i] = -INFINITY;
-        if (i < g) {
-          s[i] = chain_logit_sq<D>(qw + i * (D / 2), kr, a.scale);
-          lrow[(int64_t)i * a.n_cap + tb + tid] = s[i];
-        }
-      }
-    } else {
-#pragma unroll
-      for (int i = 0; i < GP; ++i) s[i] = -INFINITY;
-    }
-#pragma unroll
-    for (int i = 0; i < GP; ++i) {
-      const float v = wave_max(s[i]);
-      if (lane == 0) red[wave * GP + i] = v;
     }
     __syncthreads();  // K tile no longer read; red visible
 
@@ -200,11 +308,11 @@ __global__ __launch_bounds__(kThreads) void small_attn_mfma(SmallArgs a) {
       m_run[i] = mn;
       const float e = (i < g && tid < nr) ? __expf(s[i] - mn) : 0.0f;
       z_thr[i] = __builtin_fmaf(z_thr[i], alpha[i], e);
-      const uint16_t hi = f32_to_bf16(e);
-      const uint16_t lo = f32_to_bf16(e - __uint_as_float((uint32_t)hi << 16));
+      const __bf16 hi = (__bf16)e;  // v_cvt_pk_bf16_f32, round to nearest even
+      const __bf16 lo = (__bf16)(e - (float)hi);
       if (tid < TILE) {
-        *reinterpret_cast<uint16_t *>(pt[0] + i * VTS + tid * 2) = hi;
-        *reinterpret_cast<uint16_t *>(pt[1] + i * VTS + tid * 2) = lo;
+        *reinterpret_cast<__bf16 *>(pt[0] + i * VTS + tid * 2) = hi;
+        *reinterpret_cast<__bf16 *>(pt[1] + i * VTS + tid * 2) = lo;
       }
     }
     if (tid < 16) {
@@ -254,10 +362,10 @@ __global__ __launch_bounds__(kThreads) void small_attn_mfma(SmallArgs a) {
   }
 
   // ---- chunk record: max, sum and P.V per query head ----------------------
-#pragma unroll
-  for (int i = 0; i < GP; ++i) {
-    const float v = wave_sum(z_thr[i]);
-    if (lane == 0) red[wave * GP + i] = v;
+  {
+    const float zs = wave_reduce_heads<GP, false>(z_thr);
+    constexpr int sh = head_shift<GP>();
+    if ((lane & ((1 << sh) - 1)) == 0) red[wave * GP + (lane >> sh)] = zs;
   }
   __syncthreads();
   float *part = a.part + (int64_t)blockIdx.x * GP * (D + 2);
@@ -409,10 +517,13 @@ __global__ __launch_bounds__(kThreads) void small_attn_valu(SmallArgs a) {
 
 // ------------------------------------------------------------- merge --
 
+// Same workgroup shape as the merge fused into the partition kernel, so the
+// two entry points combine the records in the same order (bit-identical).
+constexpr int kMergeThreads = 512;
+
 template <typename T, int D, int GP>
-__global__ __launch_bounds__(kThreads) void small_attn_merge(SmallArgs a) {
-  __shared__ float mw[kMaxChunks];
-  __shared__ float mred[4 + kThreads];
+__global__ __launch_bounds__(kMergeThreads) void small_attn_merge(SmallArgs a) {
+  __shared__ float mred[3 * kMergeThreads + 2];
   const int row = blockIdx.x;  // = b * (layers*hq) + layer*hq + h
   const int h = row % a.hq, bl = row / a.hq, layer = bl % a.layers, b = bl / a.layers;
   const int unit = (b * a.layers + layer) * a.hkv + h / a.g, i = h % a.g;
@@ -423,7 +534,7 @@ __global__ __launch_bounds__(kThreads) void small_attn_merge(SmallArgs a) {
   in.nv = (n + a.chunk - 1) / a.chunk;
   float M, Z;
   void *out = a.out;
-  merge_head<kThreads>(in, D, mw, mred, M, Z,
+  merge_head<kMergeThreads>(in, D, mred, M, Z,
                           [&](int c, float v) { elem<T>::store1(out, (int64_t)row * D + c, v); });
   if (threadIdx.x == 0) {
     a.row_max[row] = M;
@@ -431,12 +542,26 @@ __global__ __launch_bounds__(kThreads) void small_attn_merge(SmallArgs a) {
   }
 }
 
+template <int D, int GP, int G>
+void launch_mfma(const SmallArgs &a, int units, hipStream_t st) {
+  hipLaunchKernelGGL((small_attn_mfma<D, GP, G>), dim3(units * a.n_split), dim3(kThreads), 0, st, a);
+}
+
 template <int D, int GP>
 hipError_t launch_split_t(const SmallArgs &a, int units, bool f32, hipStream_t st) {
-  if (f32)
+  if (f32) {
     hipLaunchKernelGGL((small_attn_valu<D, GP>), dim3(units * a.n_split), dim3(kThreads), 0, st, a);
-  else
-    hipLaunchKernelGGL((small_attn_mfma<D, GP>), dim3(units * a.n_split), dim3(kThreads), 0, st, a);
+  } else if constexpr (GP == 4) {
+    if (a.g == 4) launch_mfma<D, 4, 4>(a, units, st);
+    else launch_mfma<D, 4, 0>(a, units, st);
+  } else if constexpr (GP == 8) {
+    if (a.g == 7) launch_mfma<D, 8, 7>(a, units, st);
+    else if (a.g == 8) launch_mfma<D, 8, 8>(a, units, st);
+    else launch_mfma<D, 8, 0>(a, units, st);
+  } else {
+    if (a.g == 16) launch_mfma<D, 16, 16>(a, units, st);
+    else launch_mfma<D, 16, 0>(a, units, st);
+  }
   return hipGetLastError();
 }
 
@@ -450,11 +575,11 @@ hipError_t launch_split_gp(const SmallArgs &a, int units, int gp, bool f32, hipS
 template <typename T, int D>
 hipError_t launch_merge_gp(const SmallArgs &a, int rows, int gp, hipStream_t st) {
   if (gp == 4)
-    hipLaunchKernelGGL((small_attn_merge<T, D, 4>), dim3(rows), dim3(kThreads), 0, st, a);
+    hipLaunchKernelGGL((small_attn_merge<T, D, 4>), dim3(rows), dim3(kMergeThreads), 0, st, a);
   else if (gp == 8)
-    hipLaunchKernelGGL((small_attn_merge<T, D, 8>), dim3(rows), dim3(kThreads), 0, st, a);
+    hipLaunchKernelGGL((small_attn_merge<T, D, 8>), dim3(rows), dim3(kMergeThreads), 0, st, a);
   else
-    hipLaunchKernelGGL((small_attn_merge<T, D, 16>), dim3(rows), dim3(kThreads), 0, st, a);
+    hipLaunchKernelGGL((small_attn_merge<T, D, 16>), dim3(rows), dim3(kMergeThreads), 0, st, a);
   return hipGetLastError();
 }
 
