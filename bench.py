@@ -144,7 +144,7 @@ def main():
                             b.marg_idx, b.marg_prob, b.mass, None, stream)
         e[2].record(stream)
         S.smallkv_hybrid_attn(ps.batch, ps.large, ps.head_map, nsh, b.crit_idx, b.marg_idx,
-                              b.marg_prob, b.mass, ps.mode, None, stream)
+                              b.marg_prob, b.mass, ps.mode, b.ws, stream)
         e[3].record(stream)
     torch.cuda.synchronize()
     stage_ms = [sum(ev[i][s].elapsed_time(ev[i][s + 1]) for i in range(K)) / K for s in range(3)]

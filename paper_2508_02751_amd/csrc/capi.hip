@@ -42,7 +42,7 @@ int check_large(const smallkv_batch_t *b, const smallkv_model_t *l, const int32_
   if (!l->k_slot && l->n_rows != b->n_cap) return SMALLKV_EINVAL;
   if (l->n_rows > INT32_MAX) return SMALLKV_EUNSUPPORTED;
   if (!dim_supported(l)) return SMALLKV_EUNSUPPORTED;
-  if (b->kc_cap > kHybridMaxCrit) return SMALLKV_EUNSUPPORTED;
+  if (!plan_group(*b, *l, n_small_heads).use && b->kc_cap > kHybridMaxCrit) return SMALLKV_EUNSUPPORTED;
   if ((int64_t)b->batch * l->n_layers * l->n_q_heads > INT32_MAX / 2) return SMALLKV_EUNSUPPORTED;
   return SMALLKV_OK;
 }
@@ -53,6 +53,19 @@ int check_mode(int mode) {
 }
 
 int status_of(hipError_t e) { return e == hipSuccess ? SMALLKV_OK : SMALLKV_EDEVICE; }
+
+size_t max_sz(size_t x, size_t y) { return x > y ? x : y; }
+
+// Stage 3: the grouped kernel where it applies, the per-head kernel otherwise.
+hipError_t launch_stage3(const smallkv_batch_t &b, const smallkv_model_t &l, const int32_t *head_map,
+                         int nsh, const int32_t *crit, const int32_t *marg, const float *marg_prob,
+                         const float *mass, int mode, void *ws, hipStream_t st) {
+  const GroupPlan gp = plan_group(b, l, nsh);
+  if (gp.use)
+    return launch_hybrid_group(b, l, head_map, nsh, crit, marg, marg_prob, mass, mode, gp,
+                               static_cast<float *>(ws), st);
+  return launch_hybrid(b, l, head_map, nsh, crit, marg, marg_prob, mass, mode, st);
+}
 
 }  // namespace
 
@@ -81,8 +94,11 @@ int smallkv_workspace_size(const smallkv_step_t *step, size_t *bytes) {
   if (!step || !bytes) return SMALLKV_EINVAL;
   int rc = check_small(&step->batch, &step->small);
   if (rc) return rc;
+  const int nsh = step->small.n_layers * step->small.n_q_heads;
+  if ((rc = check_large(&step->batch, &step->large, step->head_map, nsh))) return rc;
   const SmallPlan p = plan_small(step->batch, step->small);
-  *bytes = p.ws_bytes;
+  const GroupPlan gp = plan_group(step->batch, step->large, nsh);
+  *bytes = max_sz(p.ws_bytes, gp.use ? gp.ws_bytes : 0);
   return SMALLKV_OK;
 }
 
@@ -117,15 +133,15 @@ int smallkv_hybrid_attn(const smallkv_batch_t *batch, const smallkv_model_t *lar
                         const int32_t *head_map, int32_t n_small_heads, const int32_t *crit_idx,
                         const int32_t *marg_idx, const float *marg_prob, const float *mass,
                         int32_t mode, void *ws, size_t ws_bytes, void *stream) {
-  (void)ws;
-  (void)ws_bytes;
   int rc = check_large(batch, large, head_map, n_small_heads);
   if (rc) return rc;
   if ((rc = check_mode(mode))) return rc;
   if (!crit_idx || !mass) return SMALLKV_EINVAL;
   if (batch->km_cap > 0 && (!marg_idx || !marg_prob)) return SMALLKV_EINVAL;
-  return status_of(launch_hybrid(*batch, *large, head_map, n_small_heads, crit_idx, marg_idx,
-                                 marg_prob, mass, mode, static_cast<hipStream_t>(stream)));
+  const GroupPlan gp = plan_group(*batch, *large, n_small_heads);
+  if (gp.use && gp.ws_bytes && (!ws || ws_bytes < gp.ws_bytes)) return SMALLKV_EWORKSPACE;
+  return status_of(launch_stage3(*batch, *large, head_map, n_small_heads, crit_idx, marg_idx,
+                                 marg_prob, mass, mode, ws, static_cast<hipStream_t>(stream)));
 }
 
 int smallkv_step(const smallkv_step_t *s, void *ws, size_t ws_bytes, void *stream) {
@@ -138,7 +154,9 @@ int smallkv_step(const smallkv_step_t *s, void *ws, size_t ws_bytes, void *strea
   if (!s->logits || !s->row_max || !s->row_sum || !s->crit_idx || !s->mass) return SMALLKV_EINVAL;
   if (s->batch.km_cap > 0 && (!s->marg_idx || !s->marg_prob)) return SMALLKV_EINVAL;
   const SmallPlan p = plan_small(s->batch, s->small);
-  if (p.ws_bytes && (!ws || ws_bytes < p.ws_bytes)) return SMALLKV_EWORKSPACE;
+  const GroupPlan gp = plan_group(s->batch, s->large, nsh);
+  const size_t need = max_sz(p.ws_bytes, gp.use ? gp.ws_bytes : 0);
+  if (need && (!ws || ws_bytes < need)) return SMALLKV_EWORKSPACE;
   hipStream_t st = static_cast<hipStream_t>(stream);
   hipError_t e = launch_small_split(s->batch, s->small, s->logits, static_cast<float *>(ws), p, st);
   if (e != hipSuccess) return SMALLKV_EDEVICE;
@@ -146,8 +164,9 @@ int smallkv_step(const smallkv_step_t *s, void *ws, size_t ws_bytes, void *strea
                              s->row_max, s->row_sum, s->crit_idx, s->marg_idx, s->marg_prob,
                              s->mass, st);
   if (e != hipSuccess) return SMALLKV_EDEVICE;
-  e = launch_hybrid(s->batch, s->large, s->head_map, nsh, s->crit_idx, s->marg_idx, s->marg_prob,
-                    s->mass, s->mode, st);
+  // stage 1's records are consumed by now: stage 3 reuses the workspace
+  e = launch_stage3(s->batch, s->large, s->head_map, nsh, s->crit_idx, s->marg_idx, s->marg_prob,
+                    s->mass, s->mode, ws, st);
   return status_of(e);
 }
 

@@ -1,0 +1,680 @@
+// Stage 3 for a whole GQA group at once: bf16, head_dim 128, up to 8 query
+// heads per kv head (Eq. 6; Algorithm 1, "O_c of critical tokens ... O_m of
+// marginal tokens ... O_c + O_m").
+//
+// The query heads that share a kv head read different small heads (Eq. 3),
+// so their critical and marginal sets differ but overlap heavily.  Reading
+// the rows head by head fetches every shared row once per head; here one
+// workgroup serves the whole group over a range of tokens and reads each
+// row of the union once:
+//   * per window of kWin tokens, the group's 2g sorted index lists (C and M
+//     of each head) are scanned from per-list cursors into an LDS membership
+//     word per token (bit h: critical for head h, bit 8+h: marginal), which
+//     is compacted into the ascending list of union rows;
+//   * each wave streams blocks of 32 union rows.  QK runs on MFMA
+//     (v_mfma_f32_16x16x32_bf16) with the K rows loaded straight from HBM as
+//     the A operand (M = 16 rows, K = 32 dims) and the group's queries as B
+//     (N = heads); K rows that no head holds critical are not read.  An
+//     online softmax per head masks the logits by the critical bits;
+//   * P.V runs on MFMA too: the rows of P are the 8 heads' critical weights
+//     exp(s - m) and their marginal weights alpha_M * p' (taken from the
+//     marginal lists by rank), split into bf16 hi + lo; V is transposed in
+//     registers (v_perm) into a per-wave LDS tile;
+//   * the waves' states merge in LDS; with one split the workgroup writes
+//     the output, otherwise a (max, sum, O_C, O_M) record per head that
+//     hybrid_group_merge combines.
+// The workgroups of one kv head's splits share an XCD, so the index lists
+// they all scan stay in that XCD's L2.
+#include <limits.h>
+
+#include "common.h"
+#include "launch.h"
+
+namespace smallkv {
+namespace {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
+typedef __attribute__((ext_vector_type(4))) float f32x4_t;
+typedef __attribute__((ext_vector_type(4))) unsigned int u32x4_t;
+
+constexpr int kGT = 256;                 // threads per workgroup
+constexpr int kGW = kGT / kWave;         // waves
+constexpr int kD = 128;                  // head dim
+constexpr int kRowB = kD * 2;            // bytes per bf16 K/V row
+constexpr int kWin = 2048;               // tokens per membership window
+constexpr int kPosBits = 11;             // log2(kWin)
+constexpr int kBR = 32;                  // union rows per wave block
+constexpr int kVTS = kBR * 2 + 16;       // V^T row stride in LDS (bytes)
+// V^T byte offset of (dim, 8-row group): every 8 dims shift by 16 bytes more,
+// so that the 16 lanes writing dims 8c + d (c = 0..15) and the 16 lanes
+// reading dims 16nb + 0..15 each spread over all banks (2-way, the minimum
+// for 16-byte accesses) instead of piling 16-deep on one.
+__device__ __forceinline__ int vt_off(int dim, int rg) { return dim * kVTS + (dim >> 3) * 16 + rg * 16; }
+constexpr int kVTBytes = 128 * kVTS + 16 * 16;
+constexpr int kPS = kBR + 4;             // P row stride (floats)
+constexpr int kMaxG = 8;
+constexpr int kXcd = 8;
+constexpr int kRec = 2 * kD + 2;         // floats per (split, head) record
+constexpr int kTargetWgs = 512;          // two resident workgroups per CU
+// Raw buffer loads: an offset at or past the resource's size returns zero
+// without touching memory, so masked lanes need no branch.
+constexpr uint32_t kOOB = 0x80000000u;
+constexpr int kBufWord3 = 0x00020000;    // gfx9 raw buffer descriptor word 3
+constexpr int64_t kMaxBuf = 0x7fffffff;
+
+struct GroupArgs {
+  int n_cap, layers, hq, hkv, g, nsh, kc_cap, km_cap, mode, units, n_split, span;
+  int mp_bytes;  // size of marg_prob in bytes (< 2^31)
+  int64_t n_rows;
+  float scale;
+  const int32_t *seq_len, *k_crit, *k_marg, *head_map;
+  const void *q, *k, *v;
+  const int32_t *k_slot, *v_slot;
+  const int32_t *crit, *marg;
+  const float *marg_prob, *mass;
+  float *rec;
+  void *out;
+};
+
+struct WaveTiles {
+  unsigned char vt[kVTBytes];   // V^T of the block (dims x rows), later the wave's O
+  float p[16][kPS];             // P: slot (C head h / M head 8+h) x row
+  float alpha[16];              // per-slot rescale of the accumulators
+};
+
+struct GroupShared {
+  uint32_t mem[kWin];           // membership bits per window position
+  uint32_t uni[kWin];           // union rows: (bits << kPosBits) | position
+  WaveTiles w[kGW];
+  int cur[2 * kMaxG];           // list cursors (first entry not yet consumed)
+  int mstart[kMaxG];            // M-list cursor at the window start
+  int wcnt[kGW][kMaxG];         // marginal entries per head in each wave's rows
+  int wsum[kGW];
+  int64_t hrow[kMaxG];          // small-model row (b, j) of each head
+  float ac[kMaxG], am[kMaxG];
+};
+
+__device__ __forceinline__ void alphas(int mode, float sc, float sm, float &ac, float &am) {
+  switch (mode) {
+    case SMALLKV_NORM_NONE:
+      ac = 1.0f;
+      am = 1.0f;
+      break;
+    case SMALLKV_NORM_SLM_CRIT:
+      ac = sc;
+      am = 1.0f;
+      break;
+    case SMALLKV_NORM_RETAINED:
+      ac = sc / (sc + sm);
+      am = 1.0f / (sc + sm);
+      break;
+    case SMALLKV_NORM_MARG_FILL:
+      ac = sc;
+      am = sm > 0.0f ? (1.0f - sc) / sm : 0.0f;
+      break;
+    default:
+      ac = 1.0f - sm;
+      am = 1.0f;
+      break;
+  }
+}
+
+// Orders the wave's own LDS writes before its later reads (and reads before
+// later writes): a wave's LDS instructions execute in order, so only the
+// compiler has to be kept from moving them.
+__device__ __forceinline__ void wave_lds_fence() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Max with the lane 32 (then 16) positions away.
+__device__ __forceinline__ float max_xor32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float max_xor16(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_xor32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float sum_xor16(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+__device__ __forceinline__ uint4 load16(const unsigned char *p) { return *reinterpret_cast<const uint4 *>(p); }
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_of(const void *p, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), 0, bytes, kBufWord3);
+}
+__device__ __forceinline__ uint4 bload16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+
+// The list a wave owns in slot i: L = wave + kGW * i; L < g is head L's
+// critical list, g <= L < 2g head (L - g)'s marginal list.
+struct ListRef {
+  const int32_t *p;
+  int len;
+  uint32_t bit;
+  bool on;
+};
+
+__device__ __forceinline__ ListRef list_ref(const GroupArgs &a, const GroupShared &sh, int L, int nc, int nm) {
+  ListRef r;
+  r.on = L < 2 * a.g;
+  r.p = a.crit;
+  r.len = 0;
+  r.bit = 0;
+  if (!r.on) return r;
+  if (L < a.g) {
+    r.p = a.crit + sh.hrow[L] * a.kc_cap;
+    r.len = nc;
+    r.bit = 1u << L;
+  } else {
+    r.p = a.marg + sh.hrow[L - a.g] * a.km_cap;
+    r.len = nm;
+    r.bit = 1u << (8 + L - a.g);
+  }
+  return r;
+}
+
+// First position of every list holding a token >= target (the lists are
+// ascending).  The wave runs one 64-way search per list, all lists in
+// lockstep so that their loads overlap: probes split [lo, hi) into 64
+// pieces, the ballot of "entry < target" picks the piece.
+constexpr int kLPW = 2 * kMaxG / kGW;  // lists per wave
+__device__ __forceinline__ void lower_bounds(const ListRef (&l)[kLPW], int target, int (&res)[kLPW]) {
+  const int lane = threadIdx.x & 63;
+  int lo[kLPW], hi[kLPW];
+#pragma unroll
+  for (int i = 0; i < kLPW; ++i) {
+    lo[i] = 0;
+    hi[i] = (l[i].on && target > 0) ? l[i].len : 0;
+  }
+  for (;;) {
+    bool more = false;
+#pragma unroll
+    for (int i = 0; i < kLPW; ++i) more |= hi[i] - lo[i] > kWave;
+    if (!more) break;
+    int v[kLPW];
+#pragma unroll
+    for (int i = 0; i < kLPW; ++i) {
+      const int span = hi[i] - lo[i];
+      v[i] = INT_MAX;
+      if (span > kWave) v[i] = l[i].p[lo[i] + (int)(((int64_t)lane * span) >> 6)];
+    }
+#pragma unroll
+    for (int i = 0; i < kLPW; ++i) {
+      const int span = hi[i] - lo[i];
+      if (span > kWave) {
+        const int c = __popcll(__ballot(v[i] < target));
+        const int nlo = c > 0 ? lo[i] + (int)(((int64_t)(c - 1) * span) >> 6) + 1 : lo[i];
+        const int nhi = c < kWave ? lo[i] + (int)(((int64_t)c * span) >> 6) : hi[i];
+        lo[i] = nlo;
+        hi[i] = nhi;
+      }
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < kLPW; ++i) {
+    const int q = lo[i] + lane;
+    const int v = q < hi[i] ? l[i].p[q] : INT_MAX;
+    res[i] = lo[i] + __popcll(__ballot(v < target));
+  }
+}
+
+__global__ __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2))) void hybrid_group_kernel(GroupArgs a) {
+  __shared__ __align__(16) GroupShared sh;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // XCD-aware numbering: x = ((u / 8) * n_split + sp) * 8 + u % 8
+  const int x = blockIdx.x;
+  const int rest = x / kXcd;
+  const int u = (rest / a.n_split) * kXcd + x % kXcd, sp = rest % a.n_split;
+  if (u >= a.units) return;
+  const int kvh = u % a.hkv, bl = u / a.hkv, layer = bl % a.layers, b = bl / a.layers;
+  const Sizes sz = set_sizes(a.seq_len, a.k_crit, a.k_marg, b, a.n_cap, a.kc_cap, a.km_cap);
+  const int t_begin = sp * a.span;
+  if (t_begin >= sz.n) return;
+  const int t_end = min(t_begin + a.span, sz.n);
+  const int g = a.g;
+  const int hc = lane & 15, lq = lane >> 4;  // MFMA column (head / slot) and lane quarter
+  WaveTiles &wt = sh.w[wave];
+
+  if (tid < g) {
+    const int j = clampi(a.head_map[layer * a.hq + kvh * g + tid], 0, a.nsh - 1);
+    const int64_t row = (int64_t)b * a.nsh + j;
+    sh.hrow[tid] = row;
+    float ac, am;
+    alphas(a.mode, a.mass[2 * row], a.mass[2 * row + 1], ac, am);
+    sh.ac[tid] = ac;
+    sh.am[tid] = am;
+  }
+  // P slots no head writes stay zero; slots 8..15 (marginal) never rescale
+  for (int i = lane; i < 16 * kPS; i += kWave) (&wt.p[0][0])[i] = 0.0f;
+  if (lane < 16) wt.alpha[lane] = 1.0f;
+  __syncthreads();
+
+  ListRef lists[kLPW];
+#pragma unroll
+  for (int i = 0; i < kLPW; ++i) lists[i] = list_ref(a, sh, wave + kGW * i, sz.nc, sz.nm);
+  {
+    int res[kLPW];
+    lower_bounds(lists, t_begin, res);
+    if (lane == 0)
+#pragma unroll
+      for (int i = 0; i < kLPW; ++i)
+        if (lists[i].on) sh.cur[wave + kGW * i] = res[i];
+  }
+
+  // the group's queries as the B operand of QK: lane holds head hc, dims 32ks + 8lq .. +7
+  const int64_t qrow0 = ((int64_t)b * a.layers + layer) * a.hq + (int64_t)kvh * g;
+  uint4 qb[kD / 32];
+#pragma unroll
+  for (int ks = 0; ks < kD / 32; ++ks)
+    qb[ks] = hc < g ? load16(reinterpret_cast<const unsigned char *>(a.q) + ((qrow0 + hc) * kD + ks * 32 + lq * 8) * 2)
+                    : make_uint4(0u, 0u, 0u, 0u);
+
+  const int64_t rowb = kRowB;
+  const unsigned char *kb = reinterpret_cast<const unsigned char *>(a.k) + (int64_t)u * a.n_rows * rowb;
+  const unsigned char *vb = reinterpret_cast<const unsigned char *>(a.v) + (int64_t)u * a.n_rows * rowb;
+  const __amdgpu_buffer_rsrc_t kbuf = buffer_of(kb, (int)(a.n_rows * rowb));
+  const __amdgpu_buffer_rsrc_t vbuf = buffer_of(vb, (int)(a.n_rows * rowb));
+  const __amdgpu_buffer_rsrc_t mbuf = buffer_of(a.marg_prob, a.mp_bytes);
+  const int32_t *ksl = a.k_slot ? a.k_slot + (int64_t)u * a.n_cap : nullptr;
+  const int32_t *vsl = a.v_slot ? a.v_slot + (int64_t)u * a.n_cap : nullptr;
+  const int last_row = (int)(a.n_rows - 1);
+
+  f32x4_t acc[kD / 16];
+#pragma unroll
+  for (int nb = 0; nb < kD / 16; ++nb) acc[nb] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+  float m_run = -INFINITY, z_lane = 0.0f;  // per column hc (a head for hc < g)
+
+  for (int ws = t_begin; ws < t_end; ws += kWin) {
+    const int we = min(ws + kWin, t_end);
+    for (int i = tid; i < kWin; i += kGT) sh.mem[i] = 0u;
+    __syncthreads();  // also: every wave is done with the previous window's union rows
+
+    // ---- membership: scan each owned list from its cursor up to we -------
+    {
+      int c[kLPW];
+      bool act[kLPW];
+#pragma unroll
+      for (int i = 0; i < kLPW; ++i) {
+        act[i] = lists[i].on;
+        c[i] = act[i] ? sh.cur[wave + kGW * i] : 0;
+        const int L = wave + kGW * i;
+        if (act[i] && L >= g && lane == 0) sh.mstart[L - g] = c[i];
+      }
+      for (;;) {
+        bool any = false;
+#pragma unroll
+        for (int i = 0; i < kLPW; ++i) any |= act[i];
+        if (!any) break;
+        int e[kLPW][4];
+#pragma unroll
+        for (int i = 0; i < kLPW; ++i)
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            const int pos = c[i] + lane + kWave * k;
+            e[i][k] = (act[i] && pos < lists[i].len) ? lists[i].p[pos] : INT_MAX;
+          }
+#pragma unroll
+        for (int i = 0; i < kLPW; ++i) {
+          if (!act[i]) continue;
+          int cnt = 0;
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            const bool in = e[i][k] < we;
+            if (in && e[i][k] >= ws) atomicOr(&sh.mem[e[i][k] - ws], lists[i].bit);
+            cnt += __popcll(__ballot(in));
+          }
+          c[i] += cnt;
+          if (cnt < 4 * kWave) act[i] = false;
+        }
+      }
+      if (lane == 0)
+#pragma unroll
+        for (int i = 0; i < kLPW; ++i)
+          if (lists[i].on) sh.cur[wave + kGW * i] = c[i];
+    }
+    __syncthreads();
+
+    // ---- compaction into ascending union rows ---------------------------
+    // Thread t takes pc consecutive positions, so wave w's rows are those
+    // of positions [w * 64 * pc, (w + 1) * 64 * pc): it streams exactly the
+    // rows its own threads compact, and counts their marginal bits here.
+    constexpr int PT = kWin / kGT;  // most positions per thread
+    const int pc = (we - ws + kGT - 1) / kGT;
+    uint32_t mv[PT];
+    int cnt = 0;
+#pragma unroll
+    for (int k = 0; k < PT; ++k) {
+      mv[k] = k < pc ? sh.mem[tid * pc + k] : 0u;
+      cnt += mv[k] != 0u;
+    }
+    int inc = cnt;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const int y = __shfl_up(inc, o, kWave);
+      if (lane >= o) inc += y;
+    }
+    if (lane == kWave - 1) sh.wsum[wave] = inc;
+    for (int h = 0; h < g; ++h) {
+      int c = 0;
+#pragma unroll
+      for (int k = 0; k < PT; ++k) c += __popcll(__ballot((mv[k] >> (8 + h)) & 1u));
+      if (lane == 0) sh.wcnt[wave][h] = c;
+    }
+    __syncthreads();
+    int r0 = 0;
+#pragma unroll
+    for (int w = 0; w < kGW; ++w) r0 += w < wave ? sh.wsum[w] : 0;
+    const int r1 = r0 + sh.wsum[wave];
+    {
+      int o = r0 + inc - cnt;
+#pragma unroll
+      for (int k = 0; k < PT; ++k)
+        if (mv[k]) sh.uni[o++] = (mv[k] << kPosBits) | (uint32_t)(tid * pc + k);
+    }
+    int mpos[kMaxG];
+#pragma unroll
+    for (int h = 0; h < kMaxG; ++h) {
+      mpos[h] = 0;
+      if (h < g) {
+        mpos[h] = sh.mstart[h];
+        for (int w = 0; w < wave; ++w) mpos[h] += sh.wcnt[w][h];
+      }
+    }
+    __syncthreads();
+
+    // ---- stream the rows: QK, online softmax, P.V -----------------------
+    for (int r = r0; r < r1; r += kBR) {
+      const int own = r + (lane & 31);
+      const bool valid = own < r1;
+      const uint32_t e = valid ? sh.uni[own] : 0u;
+      const uint32_t bits = e >> kPosBits;
+      const int tok = ws + (int)(e & (kWin - 1));
+      int rk = tok, rv = tok;
+      if (valid && ksl) {
+        rk = clampi(ksl[tok], 0, last_row);
+        rv = clampi(vsl[tok], 0, last_row);
+      }
+      rk = clampi(rk, 0, last_row);
+      rv = clampi(rv, 0, last_row);
+
+      // K rows (A operand of QK): lane holds row h*16 + hc, dims 32ks + 8lq .. +7
+      // (rows no head holds critical are not read: their offset is out of range)
+      uint4 kr[2][kD / 32];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int src = h * 16 + hc;
+        const int row = __shfl(rk, src, kWave);
+        const bool crit = (__shfl((int)bits, src, kWave) & 0xff) != 0;
+        const uint32_t off = crit ? (uint32_t)row * kRowB + lq * 16 : kOOB;
+#pragma unroll
+        for (int ks = 0; ks < kD / 32; ++ks) kr[h][ks] = bload16(kbuf, off + ks * 64);
+      }
+      // V rows: lane holds dims 8hc .. +7 of rows 8lq .. 8lq+7
+      uint4 vr[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int src = lq * 8 + k;
+        const int row = __shfl(rv, src, kWave);
+        vr[k] = bload16(vbuf, r + src < r1 ? (uint32_t)row * kRowB + hc * 16 : kOOB);
+      }
+      // marginal weights alpha_M * p', taken from each head's list by rank;
+      // all loads are issued here, the LDS writes wait until after QK
+      float wm[kMaxG];
+#pragma unroll
+      for (int h = 0; h < kMaxG; ++h) {
+        wm[h] = 0.0f;
+        if (h < g) {
+          const bool mb = lane < 32 && ((bits >> (8 + h)) & 1u);
+          const uint64_t mask = __ballot(mb);
+          const int rank = __popcll(mask & ((1ull << lane) - 1ull));
+          const int pos = clampi(mpos[h] + rank, 0, a.km_cap - 1);
+          const uint32_t off = mb ? (uint32_t)(sh.hrow[h] * a.km_cap + pos) * 4u : kOOB;
+          wm[h] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(mbuf, off, 0, 0));
+          mpos[h] += __popcll(mask);
+        }
+      }
+
+      // QK: S^T[row][head], lane holds rows h*16 + 4lq + i of head hc
+      f32x4_t s[2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) s[h] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+      for (int ks = 0; ks < kD / 32; ++ks)
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+          s[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kr[h][ks]),
+                                                         __builtin_bit_cast(bf16x8_t, qb[ks]), s[h], 0, 0, 0);
+      float sv[2][4];
+      float bmax = -INFINITY;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int rr = r + h * 16 + lq * 4;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const uint32_t uu = sh.uni[min(rr + i, kWin - 1)];
+          const bool cb = hc < g && rr + i < r1 && ((uu >> (kPosBits + hc)) & 1u);
+          sv[h][i] = cb ? s[h][i] * a.scale : -INFINITY;
+          bmax = fmaxf(bmax, sv[h][i]);
+        }
+      }
+      bmax = max_xor16(max_xor32(bmax));
+      const float mn = fmaxf(m_run, bmax);
+      const float alpha = mn == -INFINITY ? 1.0f : __expf(m_run - mn);
+      m_run = mn;
+      z_lane *= alpha;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        float ev[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          ev[i] = sv[h][i] == -INFINITY ? 0.0f : __expf(sv[h][i] - mn);
+          z_lane += ev[i];
+        }
+        if (hc < 8)
+          *reinterpret_cast<float4 *>(&wt.p[hc][h * 16 + lq * 4]) = make_float4(ev[0], ev[1], ev[2], ev[3]);
+      }
+      if (lane < 8) wt.alpha[lane] = alpha;
+      if (lane < 32)
+#pragma unroll
+        for (int h = 0; h < kMaxG; ++h)
+          if (h < g) wt.p[8 + h][lane] = wm[h] * sh.am[h];
+
+      // V^T into LDS: 8 dims x 8 rows per lane through v_perm
+#pragma unroll
+      for (int d = 0; d < 8; ++d) {
+        const uint32_t sel = (d & 1) ? 0x07060302u : 0x05040100u;
+        uint32_t w4[4];
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+          const uint32_t x0 = (&vr[2 * p].x)[d >> 1], x1 = (&vr[2 * p + 1].x)[d >> 1];
+          w4[p] = __builtin_amdgcn_perm(x1, x0, sel);
+        }
+        *reinterpret_cast<uint4 *>(wt.vt + vt_off(hc * 8 + d, lq)) = make_uint4(w4[0], w4[1], w4[2], w4[3]);
+      }
+      wave_lds_fence();
+
+      // P.V: O[slot][dim] += P[slot][rows] V[rows][dim]
+      if (__ballot(alpha != 1.0f)) {  // some head's max moved
+        const float4 al = *reinterpret_cast<const float4 *>(&wt.alpha[lq * 4]);
+#pragma unroll
+        for (int nb = 0; nb < kD / 16; ++nb) {
+          acc[nb][0] *= al.x;
+          acc[nb][1] *= al.y;
+          acc[nb][2] *= al.z;
+          acc[nb][3] *= al.w;
+        }
+      }
+      const float4 p0 = *reinterpret_cast<const float4 *>(&wt.p[hc][lq * 8]);
+      const float4 p1 = *reinterpret_cast<const float4 *>(&wt.p[hc][lq * 8 + 4]);
+      const float pf[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
+      bf16x8_t ph, pl;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const __bf16 hi = (__bf16)pf[i];
+        ph[i] = hi;
+        pl[i] = (__bf16)(pf[i] - (float)hi);
+      }
+      bf16x8_t B[kD / 16];
+#pragma unroll
+      for (int nb = 0; nb < kD / 16; ++nb)
+        B[nb] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4 *>(wt.vt + vt_off(nb * 16 + hc, lq)));
+      // hi for every block, then lo: no accumulator feeds the next MFMA directly
+#pragma unroll
+      for (int nb = 0; nb < kD / 16; ++nb)
+        acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph, B[nb], acc[nb], 0, 0, 0);
+#pragma unroll
+      for (int nb = 0; nb < kD / 16; ++nb)
+        acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pl, B[nb], acc[nb], 0, 0, 0);
+      wave_lds_fence();
+    }
+  }
+
+  // ---- merge the waves, then write the output or this split's record ----
+  const float z_col = sum_xor16(sum_xor32(z_lane));
+  __syncthreads();  // the V^T tiles are free
+  static_assert(16 * kD * 4 <= kVTBytes, "the wave's O fits the V^T tile");
+  float *wo = reinterpret_cast<float *>(wt.vt);  // [16 slots][kD]
+#pragma unroll
+  for (int nb = 0; nb < kD / 16; ++nb)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) wo[(lq * 4 + i) * kD + nb * 16 + hc] = acc[nb][i];
+  if (lane < 16) {
+    wt.p[0][lane] = m_run;
+    wt.p[1][lane] = z_col;
+  }
+  __syncthreads();
+  for (int idx = tid; idx < g * kD; idx += kGT) {
+    const int h = idx / kD, d = idx % kD;
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < kGW; ++w) M = fmaxf(M, sh.w[w].p[0][h]);
+    float Z = 0.0f, oc = 0.0f, om = 0.0f;
+#pragma unroll
+    for (int w = 0; w < kGW; ++w) {
+      const float mw = sh.w[w].p[0][h];
+      const float f = mw == -INFINITY ? 0.0f : __expf(mw - M);
+      const float *o = reinterpret_cast<const float *>(sh.w[w].vt);
+      Z = __builtin_fmaf(sh.w[w].p[1][h], f, Z);
+      oc = __builtin_fmaf(o[h * kD + d], f, oc);
+      om += o[(8 + h) * kD + d];
+    }
+    if (a.n_split == 1) {
+      const float o = (Z > 0.0f ? sh.ac[h] * (oc / Z) : 0.0f) + om;
+      elem<bf16_t>::store1(a.out, (qrow0 + h) * kD + d, o);
+    } else {
+      float *rec = a.rec + (((int64_t)u * a.n_split + sp) * g + h) * kRec;
+      if (d == 0) {
+        rec[0] = M;
+        rec[1] = Z;
+      }
+      rec[2 + d] = oc;
+      rec[2 + kD + d] = om;
+    }
+  }
+}
+
+// Combine the split records of one (sequence, layer, kv head): log-sum-exp
+// over the critical parts, plain sum over the marginal parts.
+__global__ __launch_bounds__(kGT) void hybrid_group_merge(GroupArgs a) {
+  const int u = blockIdx.x;
+  const int kvh = u % a.hkv, bl = u / a.hkv, layer = bl % a.layers, b = bl / a.layers;
+  const int n = clampi(a.seq_len[b], 1, a.n_cap);
+  const int ns = min(a.n_split, (n + a.span - 1) / a.span);
+  const int g = a.g;
+  const int64_t qrow0 = ((int64_t)b * a.layers + layer) * a.hq + (int64_t)kvh * g;
+  const float *rec0 = a.rec + (int64_t)u * a.n_split * g * kRec;
+  for (int idx = threadIdx.x; idx < g * kD; idx += kGT) {
+    const int h = idx / kD, d = idx % kD;
+    const int j = clampi(a.head_map[layer * a.hq + kvh * g + h], 0, a.nsh - 1);
+    const int64_t row = (int64_t)b * a.nsh + j;
+    float ac, am;
+    alphas(a.mode, a.mass[2 * row], a.mass[2 * row + 1], ac, am);
+    float M = -INFINITY;
+    for (int s = 0; s < ns; ++s) M = fmaxf(M, rec0[(s * g + h) * kRec]);
+    float Z = 0.0f, oc = 0.0f, om = 0.0f;
+    for (int s = 0; s < ns; ++s) {
+      const float *r = rec0 + (s * g + h) * kRec;
+      const float f = r[0] == -INFINITY ? 0.0f : __expf(r[0] - M);
+      Z = __builtin_fmaf(r[1], f, Z);
+      oc = __builtin_fmaf(r[2 + d], f, oc);
+      om += r[2 + kD + d];
+    }
+    const float o = (Z > 0.0f ? ac * (oc / Z) : 0.0f) + om;
+    elem<bf16_t>::store1(a.out, (qrow0 + h) * kD + d, o);
+  }
+}
+
+}  // namespace
+
+GroupPlan plan_group(const smallkv_batch_t &b, const smallkv_model_t &m, int n_small_heads) {
+  GroupPlan p{};
+  const int g = m.n_q_heads / m.n_kv_heads;
+  p.use = m.dtype == SMALLKV_BF16 && m.head_dim == kD && g <= kMaxG &&
+          m.n_rows * kRowB <= kMaxBuf &&
+          (int64_t)b.batch * n_small_heads * b.km_cap * (int64_t)sizeof(float) <= kMaxBuf;
+  if (!p.use) return p;
+  const int64_t units = (int64_t)b.batch * m.n_layers * m.n_kv_heads;
+  int64_t s = kTargetWgs / units;  // whole rounds only: a partial last round is a tail
+  s = s < 1 ? 1 : s;
+  const int64_t max_s = (b.n_cap + 255) / 256;  // at least 256 tokens per split
+  s = s > max_s ? max_s : s;
+  p.span = (int)((b.n_cap + s - 1) / s);
+  p.n_split = (int)((b.n_cap + p.span - 1) / p.span);
+  p.ws_bytes = p.n_split > 1 ? (size_t)units * p.n_split * g * kRec * sizeof(float) : 0;
+  return p;
+}
+
+hipError_t launch_hybrid_group(const smallkv_batch_t &b, const smallkv_model_t &m,
+                               const int32_t *head_map, int n_small_heads, const int32_t *crit,
+                               const int32_t *marg, const float *marg_prob, const float *mass,
+                               int mode, const GroupPlan &p, float *ws, hipStream_t st) {
+  GroupArgs a;
+  a.n_cap = b.n_cap;
+  a.layers = m.n_layers;
+  a.hq = m.n_q_heads;
+  a.hkv = m.n_kv_heads;
+  a.g = m.n_q_heads / m.n_kv_heads;
+  a.nsh = n_small_heads;
+  a.kc_cap = b.kc_cap;
+  a.km_cap = b.km_cap;
+  a.mode = mode;
+  a.units = b.batch * m.n_layers * m.n_kv_heads;
+  a.n_split = p.n_split;
+  a.span = p.span;
+  a.mp_bytes = (int)((int64_t)b.batch * n_small_heads * b.km_cap * (int64_t)sizeof(float));
+  a.n_rows = m.n_rows;
+  a.scale = m.scale;
+  a.seq_len = b.seq_len;
+  a.k_crit = b.k_crit;
+  a.k_marg = b.k_marg;
+  a.head_map = head_map;
+  a.q = m.q;
+  a.k = m.k;
+  a.v = m.v;
+  a.k_slot = m.k_slot;
+  a.v_slot = m.v_slot;
+  a.crit = crit;
+  a.marg = marg;
+  a.marg_prob = marg_prob;
+  a.mass = mass;
+  a.rec = ws;
+  a.out = m.out;
+  const int groups = (a.units + kXcd - 1) / kXcd;
+  hipLaunchKernelGGL(hybrid_group_kernel, dim3(groups * kXcd * a.n_split), dim3(kGT), 0, st, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.n_split == 1) return e;
+  hipLaunchKernelGGL(hybrid_group_merge, dim3(a.units), dim3(kGT), 0, st, a);
+  return hipGetLastError();
+}
+
+}  // namespace smallkv

@@ -40,8 +40,25 @@ hipError_t launch_partition(const smallkv_batch_t &b, int n_small_heads, const f
                             const float *row_max, const float *row_sum, int32_t *crit,
                             int32_t *marg, float *marg_prob, float *mass, hipStream_t st);
 
-// Largest kc_cap the single-pass hybrid kernel keeps in LDS.
+// Largest kc_cap the per-head hybrid kernel keeps in LDS.
 constexpr int kHybridMaxCrit = 12288;
+
+// Plan of the grouped stage-3 kernel (bf16, head_dim 128, group <= 8): each
+// (sequence, layer, kv head) is cut into n_split token ranges of `span`
+// tokens; with more than one, the workspace holds a record per range and
+// query head.
+struct GroupPlan {
+  bool use;
+  int n_split, span;
+  size_t ws_bytes;
+};
+
+GroupPlan plan_group(const smallkv_batch_t &b, const smallkv_model_t &m, int n_small_heads);
+
+hipError_t launch_hybrid_group(const smallkv_batch_t &b, const smallkv_model_t &m,
+                               const int32_t *head_map, int n_small_heads, const int32_t *crit,
+                               const int32_t *marg, const float *marg_prob, const float *mass,
+                               int mode, const GroupPlan &p, float *ws, hipStream_t st);
 
 hipError_t launch_hybrid(const smallkv_batch_t &b, const smallkv_model_t &m,
                          const int32_t *head_map, int n_small_heads, const int32_t *crit,

@@ -194,10 +194,13 @@ __global__ __launch_bounds__(kThreads) void small_attn_mfma(SmallArgs a) {
   constexpr int VTS = (TILE + 8) * 2;         // V^T and P row stride (bytes)
   constexpr int NB = D / 16;                  // 16-dim MFMA blocks
   constexpr int NBW = NB / 4;                 // blocks per wave
-  static_assert(C::TILE * C::ROWS >= D * VTS, "V^T aliases the K tile");
+  // V^T rows of 8-dim group c start 16*c bytes further, so that the lanes
+  // writing dims 8c + d for different c do not share a bank
+  constexpr int VTB = D * VTS + (D / 8) * 16;
+  constexpr int TB_BYTES = C::TILE * C::ROWS > VTB ? C::TILE * C::ROWS : VTB;
 
-  __shared__ __align__(16) unsigned char tile[TILE * C::ROWS];  // K tile, then V^T
-  __shared__ __align__(16) unsigned char pt[2][GP * VTS];       // P hi, P lo (bf16)
+  __shared__ __align__(16) unsigned char tile[TB_BYTES];  // K tile, then V^T
+  __shared__ __align__(16) unsigned char pt[2][GP * VTS];  // P hi, P lo (bf16)
   __shared__ float red[4 * GP];
   __shared__ float salpha[16];
 
@@ -331,7 +334,7 @@ __global__ __launch_bounds__(kThreads) void small_attn_mfma(SmallArgs a) {
         const uint32_t x0 = (&vr[2 * p].x)[d >> 1], x1 = (&vr[2 * p + 1].x)[d >> 1];
         w[p] = __builtin_amdgcn_perm(x1, x0, sel);
       }
-      *reinterpret_cast<uint4 *>(tile + (dc * 8 + d) * VTS + tb8 * 16) = make_uint4(w[0], w[1], w[2], w[3]);
+      *reinterpret_cast<uint4 *>(tile + (dc * 8 + d) * VTS + dc * 16 + tb8 * 16) = make_uint4(w[0], w[1], w[2], w[3]);
     }
     __syncthreads();
 
@@ -352,7 +355,7 @@ __global__ __launch_bounds__(kThreads) void small_attn_mfma(SmallArgs a) {
 #pragma unroll
       for (int nb = 0; nb < NBW; ++nb) {
         const int dim = (wave + 4 * nb) * 16 + mrow;
-        const uint4 bv = *reinterpret_cast<const uint4 *>(tile + dim * VTS + tok * 2);
+        const uint4 bv = *reinterpret_cast<const uint4 *>(tile + dim * VTS + (dim >> 3) * 16 + tok * 2);
         const bf16x8_t B = __builtin_bit_cast(bf16x8_t, bv);
         acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ah), B, acc[nb], 0, 0, 0);
         acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, al), B, acc[nb], 0, 0, 0);

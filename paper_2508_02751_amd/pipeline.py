@@ -61,11 +61,11 @@ def prepare_step(x: dict, mode: int = S.NORM_REMAINING,
                         softmax_scale(s_q.shape[-1]))
     large = S.ModelSpec(l_q.contiguous(), l_k, l_v, torch.empty_like(l_q),
                         softmax_scale(l_q.shape[-1]), k_slot, v_slot)
-    ws_bytes = S.smallkv_workspace_size(batch, small)
+    hm = x["head_map"].contiguous()
+    ws_bytes = S.smallkv_workspace_size(batch, small, large, hm)
     buf = S.alloc_step_buffers(batch, s_q, l_q, ws_bytes)
     buf.small_out = small.out
     buf.large_out = large.out
-    hm = x["head_map"].contiguous()
     desc = S.make_step(batch, small, large, hm, mode, buf.logits, buf.row_max, buf.row_sum,
                        buf.crit_idx, buf.marg_idx, buf.marg_prob, buf.mass)
     return PreparedStep(batch, small, large, hm, mode, buf, desc, x)

@@ -33,6 +33,8 @@ KERNEL_SOURCES = {
     "small_attn_merge": "small_attn.hip",
     "partition_kernel": "partition.hip",
     "hybrid_kernel": "hybrid.hip",
+    "hybrid_group_kernel": "hybrid_group.hip",
+    "hybrid_group_merge": "hybrid_group.hip",
 }
 
 

@@ -163,10 +163,13 @@ def _ws(ws: Optional[torch.Tensor]):
     return (None, 0) if ws is None else (_ptr(ws), ws.numel() * ws.element_size())
 
 
-def smallkv_workspace_size(batch: BatchSpec, small: ModelSpec) -> int:
+def smallkv_workspace_size(batch: BatchSpec, small: ModelSpec, large: ModelSpec,
+                           head_map) -> int:
     st = Step()
     st.batch = batch.c()
     st.small = small.c()
+    st.large = large.c()
+    st.head_map = _ptr(head_map)
     n = C.c_size_t()
     _check("smallkv_workspace_size", lib().smallkv_workspace_size(C.byref(st), C.byref(n)))
     return n.value

@@ -77,7 +77,7 @@ def test_workspace_size_rejects_bad_small_model(over, status):
     ({"st__logits": None}, S.EINVAL),
     ({"l__k_slot": 0x1000}, S.EINVAL),          # one slot map without the other
     ({"l__n_rows": 100}, S.EINVAL),             # compact rows need slot maps
-    ({"b__kc_cap": 20000}, S.EUNSUPPORTED),
+    ({"b__kc_cap": 20000, "l__dtype": S.F32}, S.EUNSUPPORTED),  # per-head kernel's LDS
 ])
 def test_step_rejects_before_launch(over, status):
     st = _fake_step(**over)

@@ -106,6 +106,22 @@ def test_small_group_sizes(g):
     run_case(w)
 
 
+@pytest.mark.parametrize("mode", O.MODES)
+def test_bf16_all_modes_group8(mode):
+    """Every normalisation mode on the grouped bf16 stage 3 (8 query heads per kv head)."""
+    w = custom("modes-g8", 111, 2, 1500, "bf16", SMALL, W.ModelShape(2, 16, 2, 128),
+               ("pct", 8), ("pct", 20), ragged_min=700)
+    run_case(w, mode)
+
+
+@pytest.mark.parametrize("g", [2, 4, 7, 8, 16])
+def test_large_group_sizes(g):
+    """Large-model query groups: up to 8 share one workgroup, 16 runs per head."""
+    w = custom(f"lgroup{g}", 112, 2, 1100, "bf16", SMALL, W.ModelShape(2, 2 * g, 2, 128),
+               ("pct", 10), ("pct", 25), ragged_min=300)
+    run_case(w)
+
+
 def test_long_rows_multi_chunk():
     """Rows long enough to need several chunks per unit and several radix bins."""
     w = custom("long", 108, 1, 40000, "bf16", W.ModelShape(1, 4, 1, 64),
@@ -147,7 +163,7 @@ def test_single_stage_calls_match_step():
     S.smallkv_partition(ps.batch, nsh, lg, rm, rs, ci, mi, mp, ms)
     large = S.ModelSpec(ps.large.q, ps.large.k, ps.large.v, torch.empty_like(ps.large.out),
                         ps.large.scale)
-    S.smallkv_hybrid_attn(ps.batch, large, ps.head_map, nsh, ci, mi, mp, ms)
+    S.smallkv_hybrid_attn(ps.batch, large, ps.head_map, nsh, ci, mi, mp, ms, ws=b.ws)
     torch.cuda.synchronize()
     seq = host(x["seq_len"])
     for bi in range(3):
