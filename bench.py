@@ -51,20 +51,24 @@ def source_hash(name: str) -> str:
     return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
 
 
-def load_traffic(kernel_src: str, launches_per_step: int):
-    """HBM bytes per launch from committed rocprofv3 --pmc summaries, or None
-    when the kernel source changed since the counters were taken."""
+def load_traffic(kernels):
+    """HBM bytes of one stage call (the sum over its kernels) from the committed
+    rocprofv3 --pmc summary, or None when a kernel is missing or its source
+    changed since the counters were taken."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
         return None
     try:
-        t = json.load(open(path))
-        e = t["kernels"][kernel_src]
-    except (KeyError, ValueError):
+        t = json.load(open(path))["kernels"]
+        total = 0.0
+        for k in kernels:
+            e = t[k]
+            if e.get("source_sha256_16") != source_hash(e["source"]):
+                return None
+            total += e["hbm_bytes_per_launch"]
+        return total
+    except (KeyError, ValueError, TypeError):
         return None
-    if e.get("source_sha256_16") != source_hash(kernel_src):
-        return None
-    return e.get("hbm_bytes_per_launch")
 
 
 def main():
@@ -153,11 +157,14 @@ def main():
     ps = preps[0]
     sb = step_bytes(ps.inputs, ps.buf.crit_idx, ps.buf.marg_idx, ps.batch.km_cap)
     stage_bytes = [sb.stage1, sb.stage2, sb.stage3]
-    stage_names = ["small_attn_split+small_attn_merge", "partition_kernel", "hybrid_kernel"]
-    stage_src = ["small_attn.hip", "partition.hip", "hybrid.hip"]
+    # kernels each single-stage call launches for this workload (bf16, large
+    # head_dim 128, 7 query heads per kv head, 112 kv-head units: stage 3 is
+    # the grouped kernel over token splits plus their merge)
+    stage_kernels = [["small_attn_mfma", "small_attn_merge"], ["partition_kernel"],
+                     ["hybrid_group_kernel", "hybrid_group_merge"]]
     dom = max(range(3), key=lambda s: stage_ms[s])
     achieved = stage_bytes[dom] / (stage_ms[dom] * 1e-3) / 1e9
-    traffic = load_traffic(stage_src[dom], 1)
+    traffic = load_traffic(stage_kernels[dom])
     step_gbs = sb.step_compulsory / (ms_per_step * 1e-3) / 1e9
 
     # ---- CPU baseline: the oracle on one core ------------------------------
@@ -203,7 +210,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": "bf16",
         "data": "synthetic",
         "config": {
             "workload": w.name,
@@ -213,7 +220,7 @@ def main():
             "rotated_input_copies": args.rotate,
         },
         "roofline": {
-            "kernel": stage_names[dom],
+            "kernel": "+".join(stage_kernels[dom]),
             "bound": "hbm",
             "achieved": achieved,
             "peak": HBM_PEAK_GBS,

@@ -17,8 +17,8 @@
 //     (N = heads); K rows that no head holds critical are not read.  An
 //     online softmax per head masks the logits by the critical bits;
 //   * P.V runs on MFMA too: the rows of P are the 8 heads' critical weights
-//     exp(s - m) and their marginal weights alpha_M * p' (taken from the
-//     marginal lists by rank), split into bf16 hi + lo; V is transposed in
+//     exp(s - m) and their marginal probabilities p' (taken from the marginal
+//     lists by rank), split into bf16 hi + lo; V is transposed in
 //     registers (v_perm) into a per-wave LDS tile;
 //   * the waves' states merge in LDS; with one split the workgroup writes
 //     the output, otherwise a (max, sum, O_C, O_M) record per head that
@@ -253,6 +253,10 @@ __global__ __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2))) void h
     alphas(a.mode, a.mass[2 * row], a.mass[2 * row + 1], ac, am);
     sh.ac[tid] = ac;
     sh.am[tid] = am;
+  } else if (tid < kMaxG) {
+    sh.hrow[tid] = 0;
+    sh.ac[tid] = 0.0f;
+    sh.am[tid] = 0.0f;
   }
   // P slots no head writes stay zero; slots 8..15 (marginal) never rescale
   for (int i = lane; i < 16 * kPS; i += kWave) (&wt.p[0][0])[i] = 0.0f;
@@ -381,35 +385,45 @@ __global__ __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2))) void h
       for (int k = 0; k < PT; ++k)
         if (mv[k]) sh.uni[o++] = (mv[k] << kPosBits) | (uint32_t)(tid * pc + k);
     }
+    // element index in marg_prob of the next marginal entry of each head
+    // (wave-uniform: kept in SGPRs)
     int mpos[kMaxG];
 #pragma unroll
     for (int h = 0; h < kMaxG; ++h) {
-      mpos[h] = 0;
+      int p = 0;
       if (h < g) {
-        mpos[h] = sh.mstart[h];
-        for (int w = 0; w < wave; ++w) mpos[h] += sh.wcnt[w][h];
+        p = (int)(sh.hrow[h] * a.km_cap) + sh.mstart[h];
+        for (int w = 0; w < wave; ++w) p += sh.wcnt[w][h];
       }
+      mpos[h] = __builtin_amdgcn_readfirstlane(p);
     }
     __syncthreads();
 
     // ---- stream the rows: QK, online softmax, P.V -----------------------
-    for (int r = r0; r < r1; r += kBR) {
-      const int own = r + (lane & 31);
+    // Software pipeline: the next block's K rows and marginal weights are
+    // requested as soon as this block's QK has consumed its K registers, its
+    // V rows as soon as this block's V is in LDS, so the gathers of block
+    // i + 1 overlap the arithmetic of block i.
+    uint4 kr[2][kD / 32];  // K rows (A operand of QK): row h*16 + hc, dims 32ks + 8lq .. +7
+    uint4 vr[8];           // V rows: dims 8hc .. +7 of rows 8lq .. 8lq+7
+    float wm[kMaxG];       // p' of the rows' marginal heads (lanes < 32 own the rows)
+    auto rows_of = [&](int rb, int &rk, int &rv, uint32_t &bits) {
+      const int own = rb + (lane & 31);
       const bool valid = own < r1;
       const uint32_t e = valid ? sh.uni[own] : 0u;
-      const uint32_t bits = e >> kPosBits;
+      bits = e >> kPosBits;
       const int tok = ws + (int)(e & (kWin - 1));
-      int rk = tok, rv = tok;
+      rk = tok;
+      rv = tok;
       if (valid && ksl) {
-        rk = clampi(ksl[tok], 0, last_row);
-        rv = clampi(vsl[tok], 0, last_row);
+        rk = ksl[tok];
+        rv = vsl[tok];
       }
       rk = clampi(rk, 0, last_row);
       rv = clampi(rv, 0, last_row);
-
-      // K rows (A operand of QK): lane holds row h*16 + hc, dims 32ks + 8lq .. +7
-      // (rows no head holds critical are not read: their offset is out of range)
-      uint4 kr[2][kD / 32];
+    };
+    // rows no head holds critical are not read: their offset is out of range
+    auto issue_k = [&](int rk, uint32_t bits) {
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         const int src = h * 16 + hc;
@@ -419,30 +433,41 @@ __global__ __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2))) void h
 #pragma unroll
         for (int ks = 0; ks < kD / 32; ++ks) kr[h][ks] = bload16(kbuf, off + ks * 64);
       }
-      // V rows: lane holds dims 8hc .. +7 of rows 8lq .. 8lq+7
-      uint4 vr[8];
+    };
+    // marginal weights p', taken from each head's list by rank (one load per
+    // head slot, out of range where the row is not marginal for that head);
+    // lanes 32..63 mirror lanes 0..31
+    auto issue_m = [&](uint32_t bits) {
+      const uint32_t below = (1u << (lane & 31)) - 1u;
+#pragma unroll
+      for (int h = 0; h < kMaxG; ++h) {
+        const bool mb = (bits >> (8 + h)) & 1u;
+        const uint32_t mask = (uint32_t)__ballot(mb);
+        const int rank = __popc(mask & below);
+        const uint32_t off = mb ? (uint32_t)(mpos[h] + rank) * 4u : kOOB;
+        wm[h] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(mbuf, off, 0, 0));
+        mpos[h] += __popc(mask);
+      }
+    };
+    auto issue_v = [&](int rb, int rv) {
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
         const int src = lq * 8 + k;
         const int row = __shfl(rv, src, kWave);
-        vr[k] = bload16(vbuf, r + src < r1 ? (uint32_t)row * kRowB + hc * 16 : kOOB);
+        vr[k] = bload16(vbuf, rb + src < r1 ? (uint32_t)row * kRowB + hc * 16 : kOOB);
       }
-      // marginal weights alpha_M * p', taken from each head's list by rank;
-      // all loads are issued here, the LDS writes wait until after QK
-      float wm[kMaxG];
-#pragma unroll
-      for (int h = 0; h < kMaxG; ++h) {
-        wm[h] = 0.0f;
-        if (h < g) {
-          const bool mb = lane < 32 && ((bits >> (8 + h)) & 1u);
-          const uint64_t mask = __ballot(mb);
-          const int rank = __popcll(mask & ((1ull << lane) - 1ull));
-          const int pos = clampi(mpos[h] + rank, 0, a.km_cap - 1);
-          const uint32_t off = mb ? (uint32_t)(sh.hrow[h] * a.km_cap + pos) * 4u : kOOB;
-          wm[h] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(mbuf, off, 0, 0));
-          mpos[h] += __popcll(mask);
-        }
-      }
+    };
+    if (r0 < r1) {
+      int rk, rv;
+      uint32_t bits;
+      rows_of(r0, rk, rv, bits);
+      issue_k(rk, bits);
+      issue_m(bits);
+      issue_v(r0, rv);
+    }
+    for (int r = r0; r < r1; r += kBR) {
+      const int rn = r + kBR;
+      const bool more = rn < r1;
 
       // QK: S^T[row][head], lane holds rows h*16 + 4lq + i of head hc
       f32x4_t s[2];
@@ -454,6 +479,18 @@ __global__ __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2))) void h
         for (int h = 0; h < 2; ++h)
           s[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kr[h][ks]),
                                                          __builtin_bit_cast(bf16x8_t, qb[ks]), s[h], 0, 0, 0);
+      // this block's marginal weights into P (frees wm; alpha_M is applied
+      // per head at the end), then the next block's K rows and weights go out
+#pragma unroll
+      for (int h = 0; h < kMaxG; ++h) wt.p[8 + h][lane & 31] = wm[h];
+      int rvn = 0;
+      if (more) {
+        int rkn;
+        uint32_t bitsn;
+        rows_of(rn, rkn, rvn, bitsn);
+        issue_k(rkn, bitsn);
+        issue_m(bitsn);
+      }
       float sv[2][4];
       float bmax = -INFINITY;
 #pragma unroll
@@ -484,10 +521,6 @@ __global__ __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2))) void h
           *reinterpret_cast<float4 *>(&wt.p[hc][h * 16 + lq * 4]) = make_float4(ev[0], ev[1], ev[2], ev[3]);
       }
       if (lane < 8) wt.alpha[lane] = alpha;
-      if (lane < 32)
-#pragma unroll
-        for (int h = 0; h < kMaxG; ++h)
-          if (h < g) wt.p[8 + h][lane] = wm[h] * sh.am[h];
 
       // V^T into LDS: 8 dims x 8 rows per lane through v_perm
 #pragma unroll
@@ -501,6 +534,7 @@ __global__ __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2))) void h
         }
         *reinterpret_cast<uint4 *>(wt.vt + vt_off(hc * 8 + d, lq)) = make_uint4(w4[0], w4[1], w4[2], w4[3]);
       }
+      if (more) issue_v(rn, rvn);
       wave_lds_fence();
 
       // P.V: O[slot][dim] += P[slot][rows] V[rows][dim]
@@ -524,17 +558,21 @@ __global__ __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2))) void h
         ph[i] = hi;
         pl[i] = (__bf16)(pf[i] - (float)hi);
       }
-      bf16x8_t B[kD / 16];
+      // four dim blocks at a time: hi for each, then lo, so that no
+      // accumulator feeds the very next MFMA
 #pragma unroll
-      for (int nb = 0; nb < kD / 16; ++nb)
-        B[nb] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4 *>(wt.vt + vt_off(nb * 16 + hc, lq)));
-      // hi for every block, then lo: no accumulator feeds the next MFMA directly
+      for (int nq = 0; nq < kD / 16; nq += 4) {
+        bf16x8_t B[4];
 #pragma unroll
-      for (int nb = 0; nb < kD / 16; ++nb)
-        acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph, B[nb], acc[nb], 0, 0, 0);
+        for (int i = 0; i < 4; ++i)
+          B[i] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4 *>(wt.vt + vt_off((nq + i) * 16 + hc, lq)));
 #pragma unroll
-      for (int nb = 0; nb < kD / 16; ++nb)
-        acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pl, B[nb], acc[nb], 0, 0, 0);
+        for (int i = 0; i < 4; ++i)
+          acc[nq + i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph, B[i], acc[nq + i], 0, 0, 0);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          acc[nq + i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pl, B[i], acc[nq + i], 0, 0, 0);
+      }
       wave_lds_fence();
     }
   }
@@ -568,6 +606,7 @@ __global__ __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2))) void h
       oc = __builtin_fmaf(o[h * kD + d], f, oc);
       om += o[(8 + h) * kD + d];
     }
+    om *= sh.am[h];
     if (a.n_split == 1) {
       const float o = (Z > 0.0f ? sh.ac[h] * (oc / Z) : 0.0f) + om;
       elem<bf16_t>::store1(a.out, (qrow0 + h) * kD + d, o);
@@ -583,35 +622,34 @@ __global__ __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2))) void h
   }
 }
 
-// Combine the split records of one (sequence, layer, kv head): log-sum-exp
-// over the critical parts, plain sum over the marginal parts.
-__global__ __launch_bounds__(kGT) void hybrid_group_merge(GroupArgs a) {
-  const int u = blockIdx.x;
+// Combine the split records of one (sequence, layer, kv head, query head):
+// log-sum-exp over the critical parts, plain sum over the marginal parts.
+// One workgroup per query head, one thread per dim.
+__global__ __launch_bounds__(kD) void hybrid_group_merge(GroupArgs a) {
+  const int u = blockIdx.x / a.g, h = blockIdx.x % a.g, d = threadIdx.x;
   const int kvh = u % a.hkv, bl = u / a.hkv, layer = bl % a.layers, b = bl / a.layers;
   const int n = clampi(a.seq_len[b], 1, a.n_cap);
   const int ns = min(a.n_split, (n + a.span - 1) / a.span);
   const int g = a.g;
-  const int64_t qrow0 = ((int64_t)b * a.layers + layer) * a.hq + (int64_t)kvh * g;
-  const float *rec0 = a.rec + (int64_t)u * a.n_split * g * kRec;
-  for (int idx = threadIdx.x; idx < g * kD; idx += kGT) {
-    const int h = idx / kD, d = idx % kD;
-    const int j = clampi(a.head_map[layer * a.hq + kvh * g + h], 0, a.nsh - 1);
-    const int64_t row = (int64_t)b * a.nsh + j;
-    float ac, am;
-    alphas(a.mode, a.mass[2 * row], a.mass[2 * row + 1], ac, am);
-    float M = -INFINITY;
-    for (int s = 0; s < ns; ++s) M = fmaxf(M, rec0[(s * g + h) * kRec]);
-    float Z = 0.0f, oc = 0.0f, om = 0.0f;
-    for (int s = 0; s < ns; ++s) {
-      const float *r = rec0 + (s * g + h) * kRec;
-      const float f = r[0] == -INFINITY ? 0.0f : __expf(r[0] - M);
-      Z = __builtin_fmaf(r[1], f, Z);
-      oc = __builtin_fmaf(r[2 + d], f, oc);
-      om += r[2 + kD + d];
-    }
-    const float o = (Z > 0.0f ? ac * (oc / Z) : 0.0f) + om;
-    elem<bf16_t>::store1(a.out, (qrow0 + h) * kD + d, o);
+  const int64_t qrow = ((int64_t)b * a.layers + layer) * a.hq + (int64_t)kvh * g + h;
+  const int j = clampi(a.head_map[layer * a.hq + kvh * g + h], 0, a.nsh - 1);
+  const int64_t row = (int64_t)b * a.nsh + j;
+  float ac, am;
+  alphas(a.mode, a.mass[2 * row], a.mass[2 * row + 1], ac, am);
+  const float *rec0 = a.rec + ((int64_t)u * a.n_split * g + h) * kRec;
+  const int64_t sstride = (int64_t)g * kRec;
+  float M = -INFINITY;
+  for (int s = 0; s < ns; ++s) M = fmaxf(M, rec0[s * sstride]);
+  float Z = 0.0f, oc = 0.0f, om = 0.0f;
+  for (int s = 0; s < ns; ++s) {
+    const float *r = rec0 + s * sstride;
+    const float f = r[0] == -INFINITY ? 0.0f : __expf(r[0] - M);
+    Z = __builtin_fmaf(r[1], f, Z);
+    oc = __builtin_fmaf(r[2 + d], f, oc);
+    om += r[2 + kD + d];
   }
+  const float o = (Z > 0.0f ? ac * (oc / Z) : 0.0f) + om;
+  elem<bf16_t>::store1(a.out, qrow * kD + d, o);
 }
 
 }  // namespace
@@ -673,7 +711,7 @@ hipError_t launch_hybrid_group(const smallkv_batch_t &b, const smallkv_model_t &
   hipLaunchKernelGGL(hybrid_group_kernel, dim3(groups * kXcd * a.n_split), dim3(kGT), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.n_split == 1) return e;
-  hipLaunchKernelGGL(hybrid_group_merge, dim3(a.units), dim3(kGT), 0, st, a);
+  hipLaunchKernelGGL(hybrid_group_merge, dim3(a.units * a.g), dim3(kD), 0, st, a);
   return hipGetLastError();
 }
 

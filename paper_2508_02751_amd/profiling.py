@@ -72,7 +72,16 @@ def stats(d: str, title: str, cmd: str) -> str:
     return "\n".join(out) + "\n"
 
 
+def _fragment(full: str):
+    for frag in KERNEL_SOURCES:
+        if frag in full:
+            return frag
+    return None
+
+
 def _counter(d: str, name: str):
+    """Counter values per dispatch, grouped by kernel (all template instances
+    of one kernel together), and the largest value a device copy read."""
     rows = list(csv.DictReader(open(_one(os.path.join(d, "**", "*counter_collection.csv")))))
     per = collections.defaultdict(list)
     copy = 0.0
@@ -83,7 +92,9 @@ def _counter(d: str, name: str):
         if "copyBuffer" in r["Kernel_Name"]:
             copy = max(copy, v)
         elif "smallkv" in r["Kernel_Name"]:
-            per[short_name(r["Kernel_Name"])].append(v)
+            frag = _fragment(r["Kernel_Name"])
+            if frag:
+                per[frag].append(v)
     return per, copy
 
 
@@ -98,18 +109,15 @@ def traffic(fetch_dir: str, write_dir: str, copy_mib: int) -> dict:
                            "write_factor": fw},
            "kernels": {}}
     for k in sorted(set(fetch) | set(write)):
-        src = next(v for f, v in KERNEL_SOURCES.items() if f in k)
+        src = KERNEL_SOURCES[k]
         fk = sum(fetch.get(k, [0])) / max(1, len(fetch.get(k, [])))
         wk = sum(write.get(k, [0])) / max(1, len(write.get(k, [])))
         rb = fk * 1024 * (ff or 1.0)
         wb = wk * 1024 * (fw or 1.0)
-        entry = {"kernel": k, "dispatches": len(fetch.get(k, [])),
-                 "fetch_kib": fk, "write_kib": wk, "read_bytes": rb, "write_bytes": wb,
-                 "hbm_bytes_per_launch": rb + wb, "source_sha256_16": source_hash(src)}
-        # one source file can hold several kernels: keep the largest by traffic
-        prev = out["kernels"].get(src)
-        if prev is None or entry["hbm_bytes_per_launch"] > prev["hbm_bytes_per_launch"]:
-            out["kernels"][src] = entry
+        out["kernels"][k] = {"source": src, "dispatches": len(fetch.get(k, [])),
+                             "fetch_kib": fk, "write_kib": wk, "read_bytes": rb,
+                             "write_bytes": wb, "hbm_bytes_per_launch": rb + wb,
+                             "source_sha256_16": source_hash(src)}
     return out
 
 
