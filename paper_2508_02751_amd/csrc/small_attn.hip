@@ -238,35 +238,47 @@ __global__ __launch_bounds__(kThreads) void small_attn_mfma(SmallArgs a) {
     for (int i = 0; i < GP; ++i) s[i] = 0.0f;
     if (tid < nr) {
       const_u32_ptr qw = (const_u32_ptr)(reinterpret_cast<uintptr_t>(a.q)) + u.head0 * (D / 2);
+      // q of one (half, head) step: QW words in SGPRs.  Scalar loads return
+      // out of order, so any use of one waits for all in flight: each step
+      // first touches its own q (one FMA, which waits), then requests the
+      // next step's q, then runs the rest of its chain while those arrive.
+      constexpr int QW = D / 4;
+      constexpr int NSTEP = 2 * GC;
+      auto q_at = [&](int st) { return qw + (st % GC) * (D / 2) + (st / GC) * QW; };
+      uint32_t qc[QW], qn[QW];
 #pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        float kr[D / 2];
+      for (int w = 0; w < QW; ++w) qc[w] = q_at(0)[w];
+      float kr[D / 2];
 #pragma unroll
-        for (int w = 0; w < C::V16 / 2; ++w) {
-          const uint4 v = *reinterpret_cast<const uint4 *>(tile + tid * C::ROWS + (half * C::V16 / 2 + w) * 16);
-          elem<bf16_t>::unpack(v, kr + w * 8);
+      for (int st = 0; st < NSTEP; ++st) {
+        const int i = st % GC, half = st / GC;
+        if (G == 0 && i >= g) {  // padded head slot of a runtime group size
+          if (st + 1 < NSTEP)
+#pragma unroll
+            for (int w = 0; w < QW; ++w) qc[w] = q_at(st + 1)[w];
+          continue;
         }
-        // one head after another: q comes from SGPRs (scalar loads), and a
-        // wave64 issues dependent FMAs back to back, so the chains need no
-        // interleaving
+        if (i == 0) {  // this half of the K row, unpacked
 #pragma unroll
-        for (int i = 0; i < GC; ++i) {
-          if (G == 0 && i >= g) continue;
-          // the scalar loads of this head's q wait for the chain two heads
-          // back: q is fetched one head ahead instead of all at once (which
-          // would hold hundreds of SGPRs and spill them); the offset stays a
-          // constant so that it folds into the loads
-          const_u32_ptr qb = qw;
-          if (i >= 2) __asm__ volatile("" : "+s"(qb) : "v"(s[i - 2]));
-          else if (half > 0) __asm__ volatile("" : "+s"(qb) : "v"(s[GC - 2 + i]));
-          const_u32_ptr qh = qb + i * (D / 2) + half * (D / 4);
-#pragma unroll
-          for (int c = 0; c < D / 2; c += 2) {
-            const uint32_t w = qh[c / 2];
-            s[i] = __builtin_fmaf(bf16_lo(w), kr[c], s[i]);
-            s[i] = __builtin_fmaf(bf16_hi(w), kr[c + 1], s[i]);
+          for (int w = 0; w < C::V16 / 2; ++w) {
+            const uint4 v = *reinterpret_cast<const uint4 *>(tile + tid * C::ROWS + (half * C::V16 / 2 + w) * 16);
+            elem<bf16_t>::unpack(v, kr + w * 8);
           }
         }
+        s[i] = __builtin_fmaf(bf16_lo(qc[0]), kr[0], s[i]);
+        __builtin_amdgcn_sched_barrier(0);
+        if (st + 1 < NSTEP)
+#pragma unroll
+          for (int w = 0; w < QW; ++w) qn[w] = q_at(st + 1)[w];
+        __builtin_amdgcn_sched_barrier(0);
+        s[i] = __builtin_fmaf(bf16_hi(qc[0]), kr[1], s[i]);
+#pragma unroll
+        for (int c = 2; c < D / 2; c += 2) {
+          s[i] = __builtin_fmaf(bf16_lo(qc[c / 2]), kr[c], s[i]);
+          s[i] = __builtin_fmaf(bf16_hi(qc[c / 2]), kr[c + 1], s[i]);
+        }
+#pragma unroll
+        for (int w = 0; w < QW; ++w) qc[w] = qn[w];
       }
 #pragma unroll
       for (int i = 0; i < GP; ++i) {
