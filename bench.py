@@ -37,7 +37,8 @@ def parse():
     p.add_argument("--steps", type=int, default=100)
     p.add_argument("--warmup", type=int, default=10)
     p.add_argument("--rotate", type=int, default=4, help="input copies cycled through")
-    p.add_argument("--workload", type=int, default=2, help=argparse.SUPPRESS)
+    p.add_argument("--workload", type=int, default=2,
+                   help="2: the Qwen2-7B + Qwen2-0.5B headline step; 3-5: the larger shapes")
     p.add_argument("--eager", action="store_true", help="launch without HIP graphs")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time budget")
     p.add_argument("--no-cpu-baseline", action="store_true")
@@ -51,15 +52,18 @@ def source_hash(name: str) -> str:
     return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
 
 
-def load_traffic(kernels):
+def load_traffic(kernels, workload: str):
     """HBM bytes of one stage call (the sum over its kernels) from the committed
-    rocprofv3 --pmc summary, or None when a kernel is missing or its source
-    changed since the counters were taken."""
+    rocprofv3 --pmc summary, or None when the counters were taken on another
+    workload, a kernel is missing, or its source changed since."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
         return None
     try:
-        t = json.load(open(path))["kernels"]
+        doc = json.load(open(path))
+        if doc.get("workload") != workload:
+            return None
+        t = doc["kernels"]
         total = 0.0
         for k in kernels:
             e = t[k]
@@ -69,6 +73,28 @@ def load_traffic(kernels):
         return total
     except (KeyError, ValueError, TypeError):
         return None
+
+
+def shape_text(m) -> str:
+    return f"{m.layers} layers, {m.q_heads}q/{m.kv_heads}kv, d={m.head_dim}"
+
+
+def budget_text(spec) -> str:
+    kind, v = spec
+    return f"{v}%" if kind == "pct" else f"{v} tokens"
+
+
+def stage3_kernels(w):
+    """Kernels one stage-3 call launches for workload w: the grouped kernel for
+    bf16, head_dim 128 and at most 8 query heads per kv head (plus the merge
+    of its token splits when there are fewer than 512 kv-head units, the
+    library's rule), the per-head kernel otherwise."""
+    L = w.large
+    if w.dtype != "bf16" or L.head_dim != 128 or L.group > 8:
+        return ["hybrid_kernel"]
+    units = w.batch * L.layers * L.kv_heads
+    splits = max(1, min(512 // units, (w.n_cap + 255) // 256))
+    return ["hybrid_group_kernel", "hybrid_group_merge"] if splits > 1 else ["hybrid_group_kernel"]
 
 
 def main():
@@ -97,6 +123,9 @@ def main():
         del src, dst
     print(f"[bench] generating {w.name}", file=sys.stderr, flush=True)
     x0 = W.make_step_inputs(w, dev)
+    copy_bytes = sum(v.numel() * v.element_size() for v in x0.values() if torch.is_tensor(v))
+    if copy_bytes > (16 << 30):  # far beyond the 256 MB MALL already; keep HBM free
+        args.rotate = 1
     copies = [x0]
     for _ in range(args.rotate - 1):
         copies.append({k: (v.clone() if torch.is_tensor(v) else v) for k, v in x0.items()})
@@ -161,10 +190,10 @@ def main():
     # head_dim 128, 7 query heads per kv head, 112 kv-head units: stage 3 is
     # the grouped kernel over token splits plus their merge)
     stage_kernels = [["small_attn_mfma", "small_attn_merge"], ["partition_kernel"],
-                     ["hybrid_group_kernel", "hybrid_group_merge"]]
+                     stage3_kernels(w)]
     dom = max(range(3), key=lambda s: stage_ms[s])
     achieved = stage_bytes[dom] / (stage_ms[dom] * 1e-3) / 1e9
-    traffic = load_traffic(stage_kernels[dom])
+    traffic = load_traffic(stage_kernels[dom], w.name)
     step_gbs = sb.step_compulsory / (ms_per_step * 1e-3) / 1e9
 
     # ---- CPU baseline: the oracle on one core ------------------------------
@@ -214,9 +243,10 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": w.name,
-            "large": "28 layers, 28q/4kv, d=128", "small": "24 layers, 14q/2kv, d=64",
-            "kv_dtype": "bf16", "batch": w.batch, "context": w.n_ctx,
-            "critical": "10%", "marginal": "20%", "launch": "eager" if args.eager else "hip-graph",
+            "large": shape_text(w.large), "small": shape_text(w.small),
+            "kv_dtype": w.dtype, "batch": w.batch, "context": w.n_ctx,
+            "critical": budget_text(w.crit), "marginal": budget_text(w.marg),
+            "launch": "eager" if args.eager else "hip-graph",
             "rotated_input_copies": args.rotate,
         },
         "roofline": {

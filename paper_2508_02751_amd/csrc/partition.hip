@@ -32,12 +32,16 @@
 namespace smallkv {
 namespace {
 
-constexpr int kPT = 512;  // threads per row
-constexpr int kWaves = kPT / kWave;
+// PT: threads per row (a template parameter: 256 when many rows share the
+// GPU, 512 or 1024 when a few rows must finish fast)
 constexpr int kBins = 2048;
 constexpr int kCap = 2048;       // candidate keys per target kept in LDS
-constexpr int kChunk = 4 * kPT;  // tokens per chunk (4 per thread)
 constexpr int kMaxNK = 4;        // chunks of a register-cached row
+template <int PT>
+struct PC {
+  static constexpr int waves = PT / kWave;
+  static constexpr int chunk = 4 * PT;  // tokens per chunk (4 per thread)
+};
 
 struct PartArgs {
   int n_cap, nsh, kc_cap, km_cap;
@@ -124,15 +128,16 @@ __device__ __forceinline__ void find_digit(const uint32_t *hist, uint32_t rr, in
   above = __shfl(ab, src, kWave);
 }
 
+template <int PT>
 struct alignas(16) PartShared {
   uint32_t hist[2][kBins];
   uint32_t cand[2][kCap];
   uint32_t sel[2][4];  // radix: prefix, mask, remaining rank, count of T
   uint32_t res[2][4];  // counting: key, ties taken, ties in all
   uint32_t ncand[2];
-  uint32_t wt[4][kMaxNK][kWaves];  // wave totals of the block scans
-  float wsum[2][kWaves];
-  float mred[3 * kPT + 2];
+  uint32_t wt[4][kMaxNK][PC<PT>::waves];  // wave totals of the block scans
+  float wsum[2][PC<PT>::waves];
+  float mred[3 * PT + 2];
 };
 
 struct RowCtx {
@@ -143,8 +148,8 @@ struct RowCtx {
   float M, Z;
 };
 
-template <bool kMerge>
-__device__ __forceinline__ void row_setup(const PartArgs &a, PartShared &sh, RowCtx &r) {
+template <bool kMerge, int PT>
+__device__ __forceinline__ void row_setup(const PartArgs &a, PartShared<PT> &sh, RowCtx &r) {
   r.row = blockIdx.x;
   const int b = r.row / a.nsh;
   const Sizes sz = set_sizes(a.seq_len, a.k_crit, a.k_marg, b, a.n_cap, a.kc_cap, a.km_cap);
@@ -165,7 +170,7 @@ __device__ __forceinline__ void row_setup(const PartArgs &a, PartShared &sh, Row
     void *out = a.small_out;
     const int64_t o0 = (int64_t)r.row * a.d;
     const bool bf = a.out_bf16;
-    merge_head<kPT>(in, a.d, sh.mred, r.M, r.Z, [&](int c, float v) {
+    merge_head<PT>(in, a.d, sh.mred, r.M, r.Z, [&](int c, float v) {
       if (bf)
         elem<bf16_t>::store1(out, o0 + c, v);
       else
@@ -185,8 +190,9 @@ __device__ __forceinline__ void row_setup(const PartArgs &a, PartShared &sh, Row
 // 4 consecutive tokens per thread (token of value e = k*kChunk + 4*tid + e).
 // R > 0: the row sits in R registers per thread, read from memory once.
 // R == 0: every pass reads it from memory, four chunks in flight at a time.
-template <int R>
+template <int R, int PT>
 struct Row {
+  static constexpr int kChunk = PC<PT>::chunk;
   float s[R > 0 ? R : 4];
   const float *lg;
   int n;
@@ -262,11 +268,11 @@ struct Targets {
 };
 
 // Steps 1 and 2.
-template <typename Row>
-__device__ __forceinline__ Targets select_targets(PartShared &sh, const RowCtx &r, const Row &row) {
+template <int PT, typename Row>
+__device__ __forceinline__ Targets select_targets(PartShared<PT> &sh, const RowCtx &r, const Row &row) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const float M = r.M;
-  for (int x = tid; x < kBins; x += kPT) sh.hist[0][x] = 0;
+  for (int x = tid; x < kBins; x += PT) sh.hist[0][x] = 0;
   if (tid < 2) sh.ncand[tid] = 0;
   __syncthreads();
   row.each([&](float s, bool valid) {
@@ -287,7 +293,7 @@ __device__ __forceinline__ Targets select_targets(PartShared &sh, const RowCtx &
   // 0: rank by counting, 1: radix over LDS candidates, 2: radix over the row
   int mode[2];
 #pragma unroll
-  for (int x = 0; x < 2; ++x) mode[x] = cnt[x] <= (uint32_t)kPT ? 0 : (cnt[x] <= (uint32_t)kCap ? 1 : 2);
+  for (int x = 0; x < 2; ++x) mode[x] = cnt[x] <= (uint32_t)PT ? 0 : (cnt[x] <= (uint32_t)kCap ? 1 : 2);
   if (mode[0] < 2 || mode[1] < 2) {
     const uint64_t lt = lanemask_lt();
     row.each([&](float s, bool valid) {
@@ -340,16 +346,16 @@ __device__ __forceinline__ Targets select_targets(PartShared &sh, const RowCtx &
       const int shf = pass == 0 ? 21 : (pass == 1 ? 10 : 0), nb = pass < 2 ? 2048 : 1024;
       const uint32_t dmask = (uint32_t)nb - 1u;
       __syncthreads();  // previous selection visible; hist free
-      for (int x = tid; x < 2 * kBins; x += kPT) (&sh.hist[0][0])[x] = 0;
+      for (int x = tid; x < 2 * kBins; x += PT) (&sh.hist[0][0])[x] = 0;
       __syncthreads();
       const uint32_t p0 = sh.sel[0][0], m0 = sh.sel[0][1], p1 = sh.sel[1][0], m1 = sh.sel[1][1];
       if (mode[0] == 1)
-        for (int k = tid; k < (int)cnt[0]; k += kPT) {
+        for (int k = tid; k < (int)cnt[0]; k += PT) {
           const uint32_t u = sh.cand[0][k];
           if ((u & m0) == p0) atomicAdd(&sh.hist[0][(u >> shf) & dmask], 1u);
         }
       if (mode[1] == 1)
-        for (int k = tid; k < (int)cnt[1]; k += kPT) {
+        for (int k = tid; k < (int)cnt[1]; k += PT) {
           const uint32_t u = sh.cand[1][k];
           if ((u & m1) == p1) atomicAdd(&sh.hist[1][(u >> shf) & dmask], 1u);
         }
@@ -391,9 +397,10 @@ __device__ __forceinline__ Targets select_targets(PartShared &sh, const RowCtx &
 
 // Workgroup exclusive prefix of NK packed values (two 16-bit counts each;
 // per-chunk totals stay below 65536) with one barrier.
-template <int NK>
-__device__ __forceinline__ void block_scan(PartShared &sh, int slot, const uint32_t *v,
+template <int NK, int PT>
+__device__ __forceinline__ void block_scan(PartShared<PT> &sh, int slot, const uint32_t *v,
                                            uint32_t *excl, uint32_t *total) {
+  constexpr int kWaves = PC<PT>::waves;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   uint32_t inc[NK];
 #pragma unroll
@@ -416,11 +423,13 @@ __device__ __forceinline__ void block_scan(PartShared &sh, int slot, const uint3
   }
 }
 
-__device__ __forceinline__ void finish_row(const PartArgs &a, PartShared &sh, const RowCtx &r,
+template <int PT>
+__device__ __forceinline__ void finish_row(const PartArgs &a, PartShared<PT> &sh, const RowCtx &r,
                                            float sc, float sm) {
+  constexpr int kWaves = PC<PT>::waves;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  for (int i = r.nc + tid; i < a.kc_cap; i += kPT) r.crit[i] = -1;
-  for (int i = r.nm + tid; i < a.km_cap; i += kPT) {
+  for (int i = r.nc + tid; i < a.kc_cap; i += PT) r.crit[i] = -1;
+  for (int i = r.nm + tid; i < a.km_cap; i += PT) {
     r.marg[i] = -1;
     r.mp[i] = 0.0f;
   }
@@ -474,14 +483,15 @@ struct Compactor {
 
 // ---------------------------------------------------------------- kernel --
 
-template <bool kMerge, int R>
-__global__ __launch_bounds__(kPT) __attribute__((amdgpu_waves_per_eu(4)))
+template <bool kMerge, int R, int PT>
+__global__ __launch_bounds__(PT) __attribute__((amdgpu_waves_per_eu(4)))
 void partition_kernel(PartArgs a) {
-  __shared__ PartShared sh;
+  constexpr int kChunk = PC<PT>::chunk;
+  __shared__ PartShared<PT> sh;
   RowCtx r;
   row_setup<kMerge>(a, sh, r);
   const int tid = threadIdx.x;
-  Row<R> row;
+  Row<R, PT> row;
   row.lg = r.lg;
   row.n = r.n;
   row.aligned = (reinterpret_cast<uintptr_t>(r.lg) & 15) == 0;
@@ -609,19 +619,29 @@ PartArgs base_args(const smallkv_batch_t &b, int n_small_heads, const float *log
   return a;
 }
 
+template <bool kMerge, int PT>
+hipError_t launch_pt(const PartArgs &a, int rows, hipStream_t st) {
+  const dim3 grid(rows), block(PT);
+  const int n = a.n_cap;
+  if (n <= 4 * PT)
+    hipLaunchKernelGGL((partition_kernel<kMerge, 4, PT>), grid, block, 0, st, a);
+  else if (n <= 8 * PT)
+    hipLaunchKernelGGL((partition_kernel<kMerge, 8, PT>), grid, block, 0, st, a);
+  else if (n <= 16 * PT)
+    hipLaunchKernelGGL((partition_kernel<kMerge, 16, PT>), grid, block, 0, st, a);
+  else
+    hipLaunchKernelGGL((partition_kernel<kMerge, 0, PT>), grid, block, 0, st, a);
+  return hipGetLastError();
+}
+
+// Many rows (several per CU): 256 threads each, so that more rows are
+// resident at once; few rows: 512 threads, so that each finishes sooner.
+constexpr int kManyRows = 4 * 256;
+
 template <bool kMerge>
 hipError_t launch_rows(const PartArgs &a, int rows, hipStream_t st) {
-  const dim3 grid(rows), block(kPT);
-  const int n = a.n_cap;
-  if (n <= 4 * kPT)
-    hipLaunchKernelGGL((partition_kernel<kMerge, 4>), grid, block, 0, st, a);
-  else if (n <= 8 * kPT)
-    hipLaunchKernelGGL((partition_kernel<kMerge, 8>), grid, block, 0, st, a);
-  else if (n <= 16 * kPT)
-    hipLaunchKernelGGL((partition_kernel<kMerge, 16>), grid, block, 0, st, a);
-  else
-    hipLaunchKernelGGL((partition_kernel<kMerge, 0>), grid, block, 0, st, a);
-  return hipGetLastError();
+  if (rows >= kManyRows) return launch_pt<kMerge, 256>(a, rows, st);
+  return launch_pt<kMerge, 512>(a, rows, st);
 }
 
 }  // namespace

@@ -4,13 +4,14 @@
       per-kernel call count and average / min / max duration from a
       `rocprofv3 --kernel-trace --stats --output-format csv` run.
 
-  python -m paper_2508_02751_amd.profiling traffic FETCH_DIR WRITE_DIR --copy-mib N
+  python -m paper_2508_02751_amd.profiling traffic FETCH_DIR WRITE_DIR --copy-mib N --workload W
       HBM bytes per dispatch of each library kernel from two `--pmc` runs
-      (FETCH_SIZE, WRITE_SIZE, KiB per dispatch).  Each counter is scaled by
-      what it reads for a plain device copy of N MiB in the same run (the
-      largest copy dispatch), so the result is in true bytes.  Prints JSON
-      keyed by source file, with that file's hash so that a reader can tell
-      when the kernel changed after the counters were taken.
+      (FETCH_SIZE, WRITE_SIZE, KiB per dispatch) of workload W.  Each counter
+      is scaled by what it reads for a plain device copy of N MiB in the same
+      run (the largest copy dispatch), so the result is in true bytes.  Prints
+      JSON keyed by kernel, with the hash of each kernel's source file so that
+      a reader can tell when the kernel changed after the counters were
+      taken.
 """
 from __future__ import annotations
 
@@ -133,11 +134,13 @@ def main(argv=None):
     t.add_argument("write_dir")
     t.add_argument("--copy-mib", type=int, required=True)
     t.add_argument("--cmd", default="")
+    t.add_argument("--workload", required=True, help="name of the workload the runs measured")
     a = p.parse_args(argv)
     if a.action == "stats":
         sys.stdout.write(stats(a.dir, a.title, a.cmd))
     else:
         res = traffic(a.fetch_dir, a.write_dir, a.copy_mib)
+        res["workload"] = a.workload
         res["command"] = a.cmd
         json.dump(res, sys.stdout, indent=1)
         sys.stdout.write("\n")

@@ -122,6 +122,13 @@ def test_large_group_sizes(g):
     run_case(w)
 
 
+def test_many_rows_narrow_partition():
+    """1024 small-head rows: the partition runs 256 threads per row."""
+    w = custom("many-rows", 113, 16, 1500, "bf16", W.ModelShape(4, 16, 4, 64),
+               W.ModelShape(2, 8, 2, 128), ("pct", 10), ("pct", 20), ragged_min=200)
+    run_case(w)
+
+
 def test_long_rows_multi_chunk():
     """Rows long enough to need several chunks per unit and several radix bins."""
     w = custom("long", 108, 1, 40000, "bf16", W.ModelShape(1, 4, 1, 64),
