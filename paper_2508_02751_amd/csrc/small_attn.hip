@@ -184,7 +184,10 @@ __device__ __forceinline__ void stage_k(unsigned char *tile, const unsigned char
 
 // G: the query-group size when known at compile time (0: runtime a.g, the
 // padded heads then run on zero queries instead of behind branches).
-template <int D, int GP, int G>
+// kPre: the chunk has several tiles; the next tile's K rows travel into
+// registers while this tile computes (costs registers, so single-tile chunks
+// go without).
+template <int D, int GP, int G, bool kPre>
 __global__ __launch_bounds__(kThreads) void small_attn_mfma(SmallArgs a) {
   using C = SmallCfg<bf16_t, D>;
   constexpr int TILE = C::TILE;
@@ -225,10 +228,40 @@ __global__ __launch_bounds__(kThreads) void small_attn_mfma(SmallArgs a) {
 #pragma unroll
   for (int nb = 0; nb < NBW; ++nb) acc[nb] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
 
+  constexpr int KR = C::TILE * C::V16 / kThreads;  // 16-byte K pieces per thread
+  uint4 kpre[kPre ? KR : 1];
+  auto load_k = [&](int t, int n) {
+#pragma unroll
+    for (int r = 0; r < KR; ++r) {
+      const int x = tid + r * kThreads;
+      const int row = x / C::V16, w = x % C::V16;
+      kpre[r] = row < n ? *reinterpret_cast<const uint4 *>(kb + (int64_t)(t + row) * C::ROWB + w * 16)
+                        : make_uint4(0u, 0u, 0u, 0u);
+    }
+  };
+  auto store_k = [&]() {
+#pragma unroll
+    for (int r = 0; r < KR; ++r) {
+      const int x = tid + r * kThreads;
+      const int row = x / C::V16, w = x % C::V16;
+      *reinterpret_cast<uint4 *>(tile + row * C::ROWS + w * 16) = kpre[r];
+    }
+  };
+  if constexpr (kPre) {
+    load_k(u.t0, min(TILE, u.t1 - u.t0));
+    store_k();
+  }
+
   for (int tb = u.t0; tb < u.t1; tb += TILE) {
     const int nr = min(TILE, u.t1 - tb);
-    stage_k<bf16_t, D>(tile, kb + (int64_t)tb * C::ROWB, nr);
-    __syncthreads();
+    const int tn = tb + TILE;
+    if constexpr (kPre) {
+      __syncthreads();  // this tile's K is in LDS
+      if (tn < u.t1) load_k(tn, min(TILE, u.t1 - tn));
+    } else {
+      stage_k<bf16_t, D>(tile, kb + (int64_t)tb * C::ROWB, nr);
+      __syncthreads();
+    }
 
     // ---- logits: one token per thread, sequential FMA chains ------------
     // The chain of each head runs over dims 0..D-1 in order; the K row is
@@ -374,6 +407,8 @@ __global__ __launch_bounds__(kThreads) void small_attn_mfma(SmallArgs a) {
       }
     }
     __syncthreads();  // before the next tile overwrites the K/V^T and P tiles
+    if constexpr (kPre)
+      if (tn < u.t1) store_k();
   }
 
   // ---- chunk record: max, sum and P.V per query head ----------------------
@@ -559,7 +594,10 @@ __global__ __launch_bounds__(kMergeThreads) void small_attn_merge(SmallArgs a) {
 
 template <int D, int GP, int G>
 void launch_mfma(const SmallArgs &a, int units, hipStream_t st) {
-  hipLaunchKernelGGL((small_attn_mfma<D, GP, G>), dim3(units * a.n_split), dim3(kThreads), 0, st, a);
+  if (a.chunk > SmallCfg<bf16_t, D>::TILE)
+    hipLaunchKernelGGL((small_attn_mfma<D, GP, G, true>), dim3(units * a.n_split), dim3(kThreads), 0, st, a);
+  else
+    hipLaunchKernelGGL((small_attn_mfma<D, GP, G, false>), dim3(units * a.n_split), dim3(kThreads), 0, st, a);
 }
 
 template <int D, int GP>

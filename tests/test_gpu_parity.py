@@ -129,6 +129,14 @@ def test_many_rows_narrow_partition():
     run_case(w)
 
 
+def test_multi_tile_chunks_prefetch():
+    """1024 small kv-head units: stage 1 gives each workgroup two 256-token
+    tiles and prefetches the second tile's K while the first computes."""
+    w = custom("multi-tile", 114, 16, 2048, "bf16", W.ModelShape(8, 8, 8, 64),
+               W.ModelShape(1, 8, 2, 128), ("pct", 10), ("pct", 20), ragged_min=700)
+    run_case(w)
+
+
 def test_long_rows_multi_chunk():
     """Rows long enough to need several chunks per unit and several radix bins."""
     w = custom("long", 108, 1, 40000, "bf16", W.ModelShape(1, 4, 1, 64),
