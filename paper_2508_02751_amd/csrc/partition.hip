@@ -19,11 +19,13 @@
 //      workgroup prefix sums (DPP wave scans), computes p' for marginal
 //      tokens and the masses S'_C, S'_M.  Tie ranks are scanned only when a
 //      threshold's ties are split between two sets.
-// Rows up to 8192 tokens are read once, 4 consecutive logits per thread per
-// 2048-token chunk, and kept in registers; their compaction needs a single
-// barrier.  Longer rows are re-read per pass, four chunks in flight.  The
-// fused variant first combines stage 1's per-chunk records of its head (row
-// max, row sum, the head's output), so a step needs no separate merge launch.
+// Rows of up to 16 (20 with 256 threads) logits per thread are read once,
+// 4 consecutive logits per thread per chunk, and kept in registers; their
+// compaction needs a single barrier.  Longer rows are re-read per pass, four
+// chunks in flight.  Many rows (several per CU) get 256 threads each, so
+// that more rows are resident; few rows get 512.  The fused variant first
+// combines stage 1's per-chunk records of its head (row max, row sum, the
+// head's output), so a step needs no separate merge launch.
 // The result depends only on the logits: deterministic.
 #include "common.h"
 #include "launch.h"
@@ -36,7 +38,7 @@ namespace {
 // GPU, 512 or 1024 when a few rows must finish fast)
 constexpr int kBins = 2048;
 constexpr int kCap = 2048;       // candidate keys per target kept in LDS
-constexpr int kMaxNK = 4;        // chunks of a register-cached row
+constexpr int kMaxNK = 5;        // chunks of a register-cached row
 template <int PT>
 struct PC {
   static constexpr int waves = PT / kWave;
@@ -629,6 +631,8 @@ hipError_t launch_pt(const PartArgs &a, int rows, hipStream_t st) {
     hipLaunchKernelGGL((partition_kernel<kMerge, 8, PT>), grid, block, 0, st, a);
   else if (n <= 16 * PT)
     hipLaunchKernelGGL((partition_kernel<kMerge, 16, PT>), grid, block, 0, st, a);
+  else if (PT == 256 && n <= 20 * PT)  // narrow rows: one more register chunk
+    hipLaunchKernelGGL((partition_kernel<kMerge, PT == 256 ? 20 : 16, PT>), grid, block, 0, st, a);
   else
     hipLaunchKernelGGL((partition_kernel<kMerge, 0, PT>), grid, block, 0, st, a);
   return hipGetLastError();
