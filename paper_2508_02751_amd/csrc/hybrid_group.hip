@@ -56,6 +56,7 @@ constexpr int kMaxG = 8;
 constexpr int kXcd = 8;
 constexpr int kRec = 2 * kD + 2;         // floats per (split, head) record
 constexpr int kTargetWgs = 512;          // two resident workgroups per CU
+constexpr int64_t kSetupTok = 384;       // per-workgroup setup, in streamed-token time
 // Raw buffer loads: an offset at or past the resource's size returns zero
 // without touching memory, so masked lanes need no branch.
 constexpr uint32_t kOOB = 0x80000000u;
@@ -662,10 +663,16 @@ GroupPlan plan_group(const smallkv_batch_t &b, const smallkv_model_t &m, int n_s
           (int64_t)b.batch * n_small_heads * b.km_cap * (int64_t)sizeof(float) <= kMaxBuf;
   if (!p.use) return p;
   const int64_t units = (int64_t)b.batch * m.n_layers * m.n_kv_heads;
-  int64_t s = kTargetWgs / units;  // whole rounds only: a partial last round is a tail
-  s = s < 1 ? 1 : s;
+  // splits per kv head: the fewest token-equivalents on the critical path,
+  // rounds of resident workgroups (a partial last round costs a whole one) x
+  // (span + the fixed per-workgroup setup); ties go to fewer splits
   const int64_t max_s = (b.n_cap + 255) / 256;  // at least 256 tokens per split
-  s = s > max_s ? max_s : s;
+  auto cost = [&](int64_t c) {
+    return (units * c + kTargetWgs - 1) / kTargetWgs * ((b.n_cap + c - 1) / c + kSetupTok);
+  };
+  int64_t s = 1;
+  for (int64_t c = 2; c <= 16 && c <= max_s; ++c)
+    if (cost(c) < cost(s)) s = c;
   p.span = (int)((b.n_cap + s - 1) / s);
   p.n_split = (int)((b.n_cap + p.span - 1) / p.span);
   p.ws_bytes = p.n_split > 1 ? (size_t)units * p.n_split * g * kRec * sizeof(float) : 0;
