@@ -150,8 +150,7 @@ struct RowCtx {
   float M, Z;
 };
 
-template <bool kMerge, int PT>
-__device__ __forceinline__ void row_setup(const PartArgs &a, PartShared<PT> &sh, RowCtx &r) {
+__device__ __forceinline__ void row_setup(const PartArgs &a, RowCtx &r) {
   r.row = blockIdx.x;
   const int b = r.row / a.nsh;
   const Sizes sz = set_sizes(a.seq_len, a.k_crit, a.k_marg, b, a.n_cap, a.kc_cap, a.km_cap);
@@ -162,8 +161,14 @@ __device__ __forceinline__ void row_setup(const PartArgs &a, PartShared<PT> &sh,
   r.crit = a.crit + (int64_t)r.row * a.kc_cap;
   r.marg = a.marg + (int64_t)r.row * a.km_cap;
   r.mp = a.marg_prob + (int64_t)r.row * a.km_cap;
+}
+
+// Row max and sum: combined from stage 1's chunk records (fused; also writes
+// the head's output) or read back.
+template <bool kMerge, int PT>
+__device__ __forceinline__ void row_stats(const PartArgs &a, PartShared<PT> &sh, RowCtx &r) {
   if constexpr (kMerge) {
-    const int j = r.row % a.nsh, layer = j / a.hq, h = j % a.hq;
+    const int b = r.row / a.nsh, j = r.row % a.nsh, layer = j / a.hq, h = j % a.hq;
     const int unit = (b * a.layers + layer) * a.hkv + h / a.g, i = h % a.g;
     MergeIn in;
     in.stride = (int64_t)a.gp * (a.d + 2);
@@ -491,13 +496,14 @@ void partition_kernel(PartArgs a) {
   constexpr int kChunk = PC<PT>::chunk;
   __shared__ PartShared<PT> sh;
   RowCtx r;
-  row_setup<kMerge>(a, sh, r);
+  row_setup(a, r);
   const int tid = threadIdx.x;
   Row<R, PT> row;
   row.lg = r.lg;
   row.n = r.n;
   row.aligned = (reinterpret_cast<uintptr_t>(r.lg) & 15) == 0;
-  row.load();
+  row.load();  // in flight while the row's statistics arrive
+  row_stats<kMerge>(a, sh, r);
   Compactor cp{r, select_targets(sh, r, row), 1.0f / r.Z};
   // ties at a threshold split between two sets need their ranks in token order
   const bool split = cp.t.need[0] < cp.t.eq[0] || cp.t.need[1] < cp.t.eq[1];

@@ -668,7 +668,9 @@ SmallPlan plan_small(const smallkv_batch_t &b, const smallkv_model_t &m) {
   p.tile = 32768 / rowb < 256 ? 32768 / rowb : 256;
   const int64_t units = (int64_t)b.batch * m.n_layers * m.n_kv_heads;
   const int max_split = (b.n_cap + p.tile - 1) / p.tile;
-  const int want = (int)((4096 + units - 1) / units);
+  // about two rounds of resident workgroups (three per CU): fewer, longer
+  // chunks pipeline their tiles, more of them only add merge records
+  const int want = (int)((1536 + units - 1) / units);
   int ns = want < 1 ? 1 : (want > max_split ? max_split : want);
   if (ns > kMaxChunks) ns = kMaxChunks;
   const int per = (b.n_cap + ns - 1) / ns;

@@ -91,6 +91,39 @@ def test_ties_from_duplicated_keys(dtype):
     run_case(w, mutate=dup)
 
 
+@pytest.mark.parametrize("n", [1500, 3000])
+def test_constant_logits(n):
+    """Every small key equal, so every logit of a row ties: the lowest indices
+    fill C, then M.  One sub-bin holds the whole row, which sends the select
+    to its general path (candidates in LDS up to 2048 keys, else the row)."""
+    w = custom(f"const-{n}", 115, 2, n, "bf16", SMALL, LARGE, ("pct", 10), ("pct", 25))
+
+    def flat(x):
+        k = x["s_k"]
+        x["s_k"] = k[:, :, :, :1].expand_as(k).contiguous()
+
+    run_case(w, mutate=flat)
+
+
+@pytest.mark.parametrize("n", [1500, 3000])
+def test_targets_far_below_the_max(n):
+    """Token 0's key points along its group's queries, 20x scaled: every other
+    logit is far more than 32 below the row max, so both targets sit in the
+    lowest, unrefined bin."""
+    w = custom(f"far-{n}", 116, 2, n, "bf16", SMALL, LARGE, ("pct", 10), ("pct", 25))
+
+    def spike(x):
+        q = x["s_q"].float()
+        B, l, hq, d = q.shape
+        hk = x["s_k"].shape[2]
+        qg = q.view(B, l, hk, hq // hk, d).mean(3)
+        k = x["s_k"].clone()
+        k[:, :, :, 0] = (20.0 * qg).to(k.dtype)
+        x["s_k"] = k
+
+    run_case(w, mutate=spike)
+
+
 @pytest.mark.parametrize("sd,ld", [(128, 64), (128, 128), (64, 64)])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_head_dims(sd, ld, dtype):
