@@ -252,10 +252,16 @@ struct Row {
       }
     } else {
       const int nk = chunks();
+      float4 nx[4];  // the next four chunks, in flight while these are used
+#pragma unroll
+      for (int j = 0; j < 4; ++j) nx[j] = j < nk ? fetch(j) : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
       for (int k0 = 0; k0 < nk; k0 += 4) {
         float4 v[4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) v[j] = k0 + j < nk ? fetch(k0 + j) : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        for (int j = 0; j < 4; ++j) v[j] = nx[j];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          if (k0 + 4 + j < nk) nx[j] = fetch(k0 + 4 + j);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           f(v[j].x, valid(k0 + j, 0));
@@ -563,44 +569,73 @@ void partition_kernel(PartArgs a) {
       carry_m += tot[k] >> 16;
     }
   } else {
+    // Long rows: one workgroup scan per NG chunks, the next NG in flight.
+    constexpr int NG = 3;
+    static_assert(NG <= kMaxNK, "scan slots");
     const int nk = row.chunks();
     uint32_t carry_eq = 0, carry_c = 0, carry_m = 0;
-    float4 nxt = row.chunk(0);
-    for (int k = 0; k < nk; ++k) {
-      const float4 cur = nxt;
-      if (k + 1 < nk) nxt = row.chunk(k + 1);  // in flight during this chunk's scans
-      const float sv[4] = {cur.x, cur.y, cur.z, cur.w};
-      const int par = 2 * (k & 1);
-      uint32_t u[4];
+    float4 nxt[NG];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) u[e] = logit_key(sv[e]);
-      uint32_t rank = 0;
+    for (int j = 0; j < NG; ++j) nxt[j] = j < nk ? row.chunk(j) : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    for (int k0 = 0, it = 0; k0 < nk; k0 += NG, ++it) {
+      float sv[NG][4];
+#pragma unroll
+      for (int j = 0; j < NG; ++j) {
+        sv[j][0] = nxt[j].x;
+        sv[j][1] = nxt[j].y;
+        sv[j][2] = nxt[j].z;
+        sv[j][3] = nxt[j].w;
+      }
+#pragma unroll
+      for (int j = 0; j < NG; ++j)
+        if (k0 + NG + j < nk) nxt[j] = row.chunk(k0 + NG + j);
+      const int par = 2 * (it & 1);
+      uint32_t rank[NG];  // keys are recomputed where used: fewer live registers
+#pragma unroll
+      for (int j = 0; j < NG; ++j) rank[j] = 0;
       if (split) {
-        uint32_t v = 0, ex, tot;
+        uint32_t v[NG], ex[NG], tot[NG];
+#pragma unroll
+        for (int j = 0; j < NG; ++j) {
+          v[j] = 0;
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            v[j] += (row.valid(k0 + j, e) && logit_key(sv[j][e]) == cp.t.T[0] ? 1u : 0u) +
+                    (row.valid(k0 + j, e) && logit_key(sv[j][e]) == cp.t.T[1] ? 0x10000u : 0u);
+        }
+        block_scan<NG>(sh, par, v, ex, tot);
+#pragma unroll
+        for (int j = 0; j < NG; ++j) {
+          rank[j] = carry_eq + ex[j];
+          carry_eq += tot[j];
+        }
+      }
+      bool inC[NG][4], inM[NG][4];
+      uint32_t v[NG], ex[NG], tot[NG];
+#pragma unroll
+      for (int j = 0; j < NG; ++j) {
+        uint32_t rC = rank[j] & 0xffffu, rP = rank[j] >> 16;
+        v[j] = 0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const bool ok = row.valid(k0 + j, e);
+          const uint32_t u = logit_key(sv[j][e]);
+          cp.classify(u, ok, rC, rP, inC[j][e], inM[j][e]);
+          rC += ok && u == cp.t.T[0] ? 1u : 0u;
+          rP += ok && u == cp.t.T[1] ? 1u : 0u;
+          v[j] += (inC[j][e] ? 1u : 0u) + (inM[j][e] ? 0x10000u : 0u);
+        }
+      }
+      block_scan<NG>(sh, par + 1, v, ex, tot);
+#pragma unroll
+      for (int j = 0; j < NG; ++j) {
+        uint32_t pc = carry_c + (ex[j] & 0xffffu), pm = carry_m + (ex[j] >> 16);
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-          v += (row.valid(k, e) && u[e] == cp.t.T[0] ? 1u : 0u) +
-               (row.valid(k, e) && u[e] == cp.t.T[1] ? 0x10000u : 0u);
-        block_scan<1>(sh, par, &v, &ex, &tot);
-        rank = carry_eq + ex;
-        carry_eq += tot;
+          cp.emit(sv[j][e], (k0 + j) * kChunk + 4 * tid + e, inC[j][e], inM[j][e], pc, pm);
+        carry_c += tot[j] & 0xffffu;
+        carry_m += tot[j] >> 16;
       }
-      bool inC[4], inM[4];
-      uint32_t rC = rank & 0xffffu, rP = rank >> 16, v = 0, ex, tot;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const bool ok = row.valid(k, e);
-        cp.classify(u[e], ok, rC, rP, inC[e], inM[e]);
-        rC += ok && u[e] == cp.t.T[0] ? 1u : 0u;
-        rP += ok && u[e] == cp.t.T[1] ? 1u : 0u;
-        v += (inC[e] ? 1u : 0u) + (inM[e] ? 0x10000u : 0u);
-      }
-      block_scan<1>(sh, par + 1, &v, &ex, &tot);
-      uint32_t pc = carry_c + (ex & 0xffffu), pm = carry_m + (ex >> 16);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) cp.emit(sv[e], k * kChunk + 4 * tid + e, inC[e], inM[e], pc, pm);
-      carry_c += tot & 0xffffu;
-      carry_m += tot >> 16;
     }
   }
   finish_row(a, sh, r, cp.sc, cp.sm);
