@@ -8,9 +8,9 @@
 // workgroup serves the whole group over a range of tokens and reads each
 // row of the union once:
 //   * per window of kWin tokens, the group's 2g sorted index lists (C and M
-//     of each head) are scanned from per-list cursors into an LDS membership
-//     word per token (bit h: critical for head h, bit 8+h: marginal), which
-//     is compacted into the ascending list of union rows;
+//     of each head) are scanned from per-list cursors into 16 LDS membership
+//     bits per token (bit h: critical for head h, bit 8+h: marginal), which
+//     are compacted into the ascending list of union rows;
 //   * each wave streams blocks of 32 union rows.  QK runs on MFMA
 //     (v_mfma_f32_16x16x32_bf16) with the K rows loaded straight from HBM as
 //     the A operand (M = 16 rows, K = 32 dims) and the group's queries as B
@@ -41,8 +41,8 @@ constexpr int kGT = 256;                 // threads per workgroup
 constexpr int kGW = kGT / kWave;         // waves
 constexpr int kD = 128;                  // head dim
 constexpr int kRowB = kD * 2;            // bytes per bf16 K/V row
-constexpr int kWin = 2048;               // tokens per membership window
-constexpr int kPosBits = 11;             // log2(kWin)
+constexpr int kWin = 4096;               // tokens per membership window
+constexpr int kPosBits = 12;             // log2(kWin)
 constexpr int kBR = 32;                  // union rows per wave block
 constexpr int kVTS = kBR * 2 + 16;       // V^T row stride in LDS (bytes)
 // V^T byte offset of (dim, 8-row group): every 8 dims shift by 16 bytes more,
@@ -84,13 +84,12 @@ struct WaveTiles {
 };
 
 struct GroupShared {
-  uint32_t mem[kWin];           // membership bits per window position
+  uint32_t mem[kWin / 2];       // membership bits of window positions 2i (low half), 2i+1
   uint32_t uni[kWin];           // union rows: (bits << kPosBits) | position
   WaveTiles w[kGW];
   int cur[2 * kMaxG];           // list cursors (first entry not yet consumed)
   int mstart[kMaxG];            // M-list cursor at the window start
   int wcnt[kGW][kMaxG];         // marginal entries per head in each wave's rows
-  int wsum[kGW];
   int64_t hrow[kMaxG];          // small-model row (b, j) of each head
   float ac[kMaxG], am[kMaxG];
 };
@@ -262,6 +261,7 @@ __global__ __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2))) void h
   // P slots no head writes stay zero; slots 8..15 (marginal) never rescale
   for (int i = lane; i < 16 * kPS; i += kWave) (&wt.p[0][0])[i] = 0.0f;
   if (lane < 16) wt.alpha[lane] = 1.0f;
+  for (int i = tid; i < kWin / 2; i += kGT) sh.mem[i] = 0u;  // each window's compaction clears it again
   __syncthreads();
 
   ListRef lists[kLPW];
@@ -301,8 +301,6 @@ __global__ __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2))) void h
 
   for (int ws = t_begin; ws < t_end; ws += kWin) {
     const int we = min(ws + kWin, t_end);
-    for (int i = tid; i < kWin; i += kGT) sh.mem[i] = 0u;
-    __syncthreads();  // also: every wave is done with the previous window's union rows
 
     // ---- membership: scan each owned list from its cursor up to we -------
     {
@@ -335,7 +333,10 @@ __global__ __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2))) void h
 #pragma unroll
           for (int k = 0; k < 4; ++k) {
             const bool in = e[i][k] < we;
-            if (in && e[i][k] >= ws) atomicOr(&sh.mem[e[i][k] - ws], lists[i].bit);
+            if (in && e[i][k] >= ws) {
+              const int p = e[i][k] - ws;
+              atomicOr(&sh.mem[p >> 1], lists[i].bit << (16 * (p & 1)));
+            }
             cnt += __popcll(__ballot(in));
           }
           c[i] += cnt;
@@ -353,38 +354,63 @@ __global__ __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2))) void h
     // Thread t takes pc consecutive positions, so wave w's rows are those
     // of positions [w * 64 * pc, (w + 1) * 64 * pc): it streams exactly the
     // rows its own threads compact, and counts their marginal bits here.
-    constexpr int PT = kWin / kGT;  // most positions per thread
+    // Thread t takes positions t*pc .. +pc-1: the membership words from
+    // word t*pc/2 on, shifted by half a word when t*pc is odd, so that
+    // mw[k] holds positions 2k and 2k+1 of the thread.
+    constexpr int PW = kWin / kGT / 2;  // most membership words per thread
     const int pc = (we - ws + kGT - 1) / kGT;
-    uint32_t mv[PT];
+    const int w0 = (tid * pc) >> 1, odd = (tid * pc) & 1;
+    // (loops over words and positions stop at the window's pc: wave-uniform)
+    uint32_t mw[PW];
+    if ((pc & 1) == 0) {  // every thread starts on a word boundary
+#pragma unroll
+      for (int k = 0; k < PW; ++k) mw[k] = 2 * k < pc ? sh.mem[w0 + k] : 0u;
+    } else {
+      uint32_t nx = 0u;
+#pragma unroll
+      for (int k = PW; k >= 0; --k) {
+        uint32_t x = 0u;
+        if (2 * k <= pc && 2 * k < pc + odd && w0 + k < kWin / 2) x = sh.mem[w0 + k];
+        if (k < PW) {
+          mw[k] = odd ? __builtin_amdgcn_alignbit(nx, x, 16) : x;
+          if (2 * k + 1 >= pc) mw[k] &= 2 * k < pc ? 0xffffu : 0u;  // past the thread's last position
+        }
+        nx = x;
+      }
+    }
     int cnt = 0;
 #pragma unroll
-    for (int k = 0; k < PT; ++k) {
-      mv[k] = k < pc ? sh.mem[tid * pc + k] : 0u;
-      cnt += mv[k] != 0u;
-    }
+    for (int k = 0; k < PW; ++k) cnt += ((mw[k] & 0xffffu) != 0u) + ((mw[k] >> 16) != 0u);
     int inc = cnt;
 #pragma unroll
     for (int o = 1; o < kWave; o <<= 1) {
       const int y = __shfl_up(inc, o, kWave);
       if (lane >= o) inc += y;
     }
-    if (lane == kWave - 1) sh.wsum[wave] = inc;
+    // each wave's union rows go to its own range of uni, from wave*64*pc on
+    const int r0 = wave * kWave * pc;
+    const int r1 = r0 + __builtin_amdgcn_readlane(inc, kWave - 1);
     for (int h = 0; h < g; ++h) {
       int c = 0;
 #pragma unroll
-      for (int k = 0; k < PT; ++k) c += __popcll(__ballot((mv[k] >> (8 + h)) & 1u));
+      for (int k = 0; k < PW; ++k) {
+        if (2 * k >= pc) break;
+        c += __popcll(__ballot((mw[k] >> (8 + h)) & 1u)) + __popcll(__ballot((mw[k] >> (24 + h)) & 1u));
+      }
       if (lane == 0) sh.wcnt[wave][h] = c;
     }
-    __syncthreads();
-    int r0 = 0;
+    __syncthreads();  // every thread has read its words (a word may be shared by two): clear them
 #pragma unroll
-    for (int w = 0; w < kGW; ++w) r0 += w < wave ? sh.wsum[w] : 0;
-    const int r1 = r0 + sh.wsum[wave];
+    for (int k = 0; k <= PW; ++k)
+      if (2 * k <= pc && 2 * k < pc + odd) sh.mem[w0 + k] = 0u;
     {
       int o = r0 + inc - cnt;
 #pragma unroll
-      for (int k = 0; k < PT; ++k)
-        if (mv[k]) sh.uni[o++] = (mv[k] << kPosBits) | (uint32_t)(tid * pc + k);
+      for (int k = 0; k < 2 * PW; ++k) {
+        if (k >= pc) break;
+        const uint32_t m = (mw[k >> 1] >> (16 * (k & 1))) & 0xffffu;
+        if (m) sh.uni[o++] = (m << kPosBits) | (uint32_t)(tid * pc + k);
+      }
     }
     // element index in marg_prob of the next marginal entry of each head
     // (wave-uniform: kept in SGPRs)
