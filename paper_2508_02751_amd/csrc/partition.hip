@@ -37,6 +37,18 @@ namespace {
 // PT: threads per row (a template parameter: 256 when many rows share the
 // GPU, 512 or 1024 when a few rows must finish fast)
 constexpr int kBins = 2048;
+// With 512 or more threads per row, histograms keep 16 bytes of padding
+// after every 32 bins: find_digit's lanes each read 32 consecutive bins, and
+// the 144-byte stride between lanes puts the 16 lanes of an access on
+// distinct banks (a 128-byte stride piles them 8 deep on the same ones).
+// Narrow rows are bound by their per-logit passes instead, where the padded
+// index costs two instructions per logit.
+template <int PT>
+struct Hist {
+  static constexpr bool pad = PT >= 512;
+  static constexpr int size = pad ? kBins + kBins / 8 : kBins;
+  static __device__ __forceinline__ int idx(int b) { return pad ? b + (b >> 5) * 4 : b; }
+};
 constexpr int kCap = 2048;       // candidate keys per target kept in LDS
 constexpr int kMaxNK = 5;        // chunks of a register-cached row
 template <int PT>
@@ -93,7 +105,7 @@ __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v) {
 // One wave: find the bin of hist[0..NB) (scanned from the top) holding the
 // rr-th element (1-based); returns the bin and the count strictly above it.
 // Each lane owns NB/64 consecutive bins (lane 0 the highest) in registers.
-template <int NB>
+template <int NB, int PT>
 __device__ __forceinline__ void find_digit(const uint32_t *hist, uint32_t rr, int &digit,
                                            uint32_t &above) {
   constexpr int PER = NB / kWave;
@@ -102,7 +114,7 @@ __device__ __forceinline__ void find_digit(const uint32_t *hist, uint32_t rr, in
   uint32_t hv[PER];
 #pragma unroll
   for (int k = 0; k < PER; k += 4) {
-    const uint4 v = *reinterpret_cast<const uint4 *>(hist + lo + k);
+    const uint4 v = *reinterpret_cast<const uint4 *>(hist + Hist<PT>::idx(lo) + k);  // inside one 32-bin group
     hv[k] = v.x;
     hv[k + 1] = v.y;
     hv[k + 2] = v.z;
@@ -132,7 +144,7 @@ __device__ __forceinline__ void find_digit(const uint32_t *hist, uint32_t rr, in
 
 template <int PT>
 struct alignas(16) PartShared {
-  uint32_t hist[2][kBins];
+  uint32_t hist[2][Hist<PT>::size];  // bin b at Hist<PT>::idx(b)
   uint32_t cand[2][kCap];
   uint32_t sel[2][4];  // radix: prefix, mask, remaining rank, count of T
   uint32_t res[2][4];  // counting: key, ties taken, ties in all
@@ -285,11 +297,11 @@ template <int PT, typename Row>
 __device__ __forceinline__ Targets select_targets(PartShared<PT> &sh, const RowCtx &r, const Row &row) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const float M = r.M;
-  for (int x = tid; x < kBins; x += PT) sh.hist[0][x] = 0;
+  for (int x = tid; x < Hist<PT>::size; x += PT) sh.hist[0][x] = 0;
   if (tid < 2) sh.ncand[tid] = 0;
   __syncthreads();
   row.each([&](float s, bool valid) {
-    if (valid) atomicAdd(&sh.hist[0][logit_bin(s, M)], 1u);
+    if (valid) atomicAdd(&sh.hist[0][Hist<PT>::idx(logit_bin(s, M))], 1u);
   });
   __syncthreads();
   // every wave finds both targets' bins itself: no broadcast needed
@@ -299,9 +311,9 @@ __device__ __forceinline__ Targets select_targets(PartShared<PT> &sh, const RowC
 #pragma unroll
   for (int x = 0; x < 2; ++x) {
     uint32_t above;
-    find_digit<kBins>(sh.hist[0], rr[x], bin[x], above);
+    find_digit<kBins, PT>(sh.hist[0], rr[x], bin[x], above);
     rr[x] -= above;
-    cnt[x] = sh.hist[0][bin[x]];
+    cnt[x] = sh.hist[0][Hist<PT>::idx(bin[x])];
   }
   // 0: rank by counting, 1: radix over LDS candidates, 2: radix over the row
   int mode[2];
@@ -359,39 +371,39 @@ __device__ __forceinline__ Targets select_targets(PartShared<PT> &sh, const RowC
       const int shf = pass == 0 ? 21 : (pass == 1 ? 10 : 0), nb = pass < 2 ? 2048 : 1024;
       const uint32_t dmask = (uint32_t)nb - 1u;
       __syncthreads();  // previous selection visible; hist free
-      for (int x = tid; x < 2 * kBins; x += PT) (&sh.hist[0][0])[x] = 0;
+      for (int x = tid; x < 2 * Hist<PT>::size; x += PT) (&sh.hist[0][0])[x] = 0;
       __syncthreads();
       const uint32_t p0 = sh.sel[0][0], m0 = sh.sel[0][1], p1 = sh.sel[1][0], m1 = sh.sel[1][1];
       if (mode[0] == 1)
         for (int k = tid; k < (int)cnt[0]; k += PT) {
           const uint32_t u = sh.cand[0][k];
-          if ((u & m0) == p0) atomicAdd(&sh.hist[0][(u >> shf) & dmask], 1u);
+          if ((u & m0) == p0) atomicAdd(&sh.hist[0][Hist<PT>::idx((u >> shf) & dmask)], 1u);
         }
       if (mode[1] == 1)
         for (int k = tid; k < (int)cnt[1]; k += PT) {
           const uint32_t u = sh.cand[1][k];
-          if ((u & m1) == p1) atomicAdd(&sh.hist[1][(u >> shf) & dmask], 1u);
+          if ((u & m1) == p1) atomicAdd(&sh.hist[1][Hist<PT>::idx((u >> shf) & dmask)], 1u);
         }
       if (mode[0] == 2 || mode[1] == 2)
         row.each([&](float s, bool valid) {
           const int bn = valid ? logit_bin(s, M) : -1;
           const uint32_t u = logit_key(s);
-          if (mode[0] == 2 && bn == bin[0] && (u & m0) == p0) atomicAdd(&sh.hist[0][(u >> shf) & dmask], 1u);
-          if (mode[1] == 2 && bn == bin[1] && (u & m1) == p1) atomicAdd(&sh.hist[1][(u >> shf) & dmask], 1u);
+          if (mode[0] == 2 && bn == bin[0] && (u & m0) == p0) atomicAdd(&sh.hist[0][Hist<PT>::idx((u >> shf) & dmask)], 1u);
+          if (mode[1] == 2 && bn == bin[1] && (u & m1) == p1) atomicAdd(&sh.hist[1][Hist<PT>::idx((u >> shf) & dmask)], 1u);
         });
       __syncthreads();
       if (wave < 2 && mode[wave] != 0) {
         int digit;
         uint32_t above;
         if (pass < 2)
-          find_digit<2048>(sh.hist[wave], sh.sel[wave][2], digit, above);
+          find_digit<2048, PT>(sh.hist[wave], sh.sel[wave][2], digit, above);
         else
-          find_digit<1024>(sh.hist[wave], sh.sel[wave][2], digit, above);
+          find_digit<1024, PT>(sh.hist[wave], sh.sel[wave][2], digit, above);
         if (lane == 0) {
           sh.sel[wave][0] |= (uint32_t)digit << shf;
           sh.sel[wave][1] |= dmask << shf;
           sh.sel[wave][2] -= above;
-          sh.sel[wave][3] = sh.hist[wave][digit];  // after the last pass: count of T
+          sh.sel[wave][3] = sh.hist[wave][Hist<PT>::idx(digit)];  // after the last pass: count of T
         }
       }
     }
