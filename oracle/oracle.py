@@ -45,7 +45,7 @@ _I = C.POINTER(C.c_int32)
 class StepIn(C.Structure):
     _fields_ = [
         ("batch", C.c_int32), ("n_cap", C.c_int32), ("kc_cap", C.c_int32), ("km_cap", C.c_int32),
-        ("seq_len", _I), ("k_crit", _I), ("k_marg", _I),
+        ("seq_len", _I), ("k_crit", _I), ("k_marg", _I), ("k_recent", _I),
         ("s_layers", C.c_int32), ("s_q_heads", C.c_int32), ("s_kv_heads", C.c_int32), ("s_dim", C.c_int32),
         ("s_scale", C.c_float),
         ("s_q", _F), ("s_k", _F), ("s_v", _F),
@@ -79,7 +79,7 @@ def lib():
         L.orc_key.argtypes = [C.c_float]
         L.orc_key.restype = C.c_uint32
         L.orc_small_head.argtypes = [C.c_int, C.c_int, C.c_float, _F, _F, _F, _F, _D, _D, _D]
-        L.orc_partition.argtypes = [C.c_int, C.c_int, C.c_int, _F, C.c_double, C.c_double,
+        L.orc_partition.argtypes = [C.c_int, C.c_int, C.c_int, C.c_int, _F, C.c_double, C.c_double,
                                     _I, C.c_int, _I, _D, C.c_int, _D, C.POINTER(C.c_int),
                                     C.POINTER(C.c_int)]
         L.orc_hybrid_head.argtypes = [C.c_int, C.c_float, _F, _F, _F, _I, _I, C.c_int, _I,
@@ -133,11 +133,13 @@ def small_head(q, K, V, scale):
     return logits, m.value, Z.value, O
 
 
-def partition(logits, k_crit, k_marg, m, Z, kc_cap=None, km_cap=None):
+def partition(logits, k_crit, k_marg, m, Z, kc_cap=None, km_cap=None, k_recent=0):
     """Stage 2 for one small head. Returns (crit, marg, marg_prob, mass) with -1 padding."""
     logits = _f32(logits)
     n = logits.size
-    nc_ = min(k_crit, n)
+    r_ = min(max(k_recent, 0), n)
+    ntop_ = min(k_crit, n - r_)
+    nc_ = ntop_ + r_
     nm_ = max(0, min(k_marg, n - nc_))
     kc_cap = nc_ if kc_cap is None else kc_cap
     km_cap = nm_ if km_cap is None else km_cap
@@ -146,7 +148,7 @@ def partition(logits, k_crit, k_marg, m, Z, kc_cap=None, km_cap=None):
     mp = np.empty(max(km_cap, 1), np.float64)
     mass = np.empty(2, np.float64)
     nc, nm = C.c_int(), C.c_int()
-    _check(lib().orc_partition(n, k_crit, k_marg, _p(logits, _F), m, Z, _p(crit, _I), kc_cap,
+    _check(lib().orc_partition(n, k_crit, k_marg, k_recent, _p(logits, _F), m, Z, _p(crit, _I), kc_cap,
                                _p(marg, _I), _p(mp, _D), km_cap, _p(mass, _D), C.byref(nc),
                                C.byref(nm)), "orc_partition")
     return crit[:kc_cap], marg[:km_cap], mp[:km_cap], mass
@@ -177,7 +179,8 @@ def hybrid_head(q, K, V, crit, marg, marg_prob, mass, scale, mode=NORM_REMAINING
 
 
 def step(*, seq_len, k_crit, k_marg, kc_cap, km_cap, head_map, mode,
-         s_q, s_k, s_v, s_scale, l_q, l_k, l_v, l_scale, k_slot=None, v_slot=None):
+         s_q, s_k, s_v, s_scale, l_q, l_k, l_v, l_scale, k_slot=None, v_slot=None,
+         k_recent=None):
     """A whole decode step over the library layout (see smallkv_oracle.h).
 
     Shapes: s_q [B,l,Hqs,ds], s_k/s_v [B,l,Hks,n_cap,ds], l_q [B,L,Hq,d],
@@ -185,6 +188,7 @@ def step(*, seq_len, k_crit, k_marg, kc_cap, km_cap, head_map, mode,
     """
     s_q, s_k, s_v, l_q, l_k, l_v = map(_f32, (s_q, s_k, s_v, l_q, l_k, l_v))
     seq_len, k_crit, k_marg, head_map = map(_i32, (seq_len, k_crit, k_marg, head_map))
+    kr = _i32(k_recent) if k_recent is not None else None
     B, l, hqs, ds = s_q.shape
     hks, ncap = s_k.shape[2], s_k.shape[3]
     _, L, hq, d = l_q.shape
@@ -203,6 +207,7 @@ def step(*, seq_len, k_crit, k_marg, kc_cap, km_cap, head_map, mode,
         large_out=np.empty((B, L, hq, d)),
     )
     si = StepIn(B, ncap, kc_cap, km_cap, _p(seq_len, _I), _p(k_crit, _I), _p(k_marg, _I),
+                _p(kr, _I) if kr is not None else None,
                 l, hqs, hks, ds, s_scale, _p(s_q, _F), _p(s_k, _F), _p(s_v, _F),
                 L, hq, hk, d, l_scale, nrows, _p(l_q, _F), _p(l_k, _F), _p(l_v, _F),
                 _p(ks, _I) if ks is not None else None,

@@ -92,35 +92,41 @@ static int orc_int_cmp(const void *a, const void *b) {
 /* Eq. 4 read as "keep the top-scored tokens" (the printed argmax would evict
  * the most important one, contradicting Eq. 6 and the pseudocode's topk);
  * Eq. 6: TopK gives the critical set, Top(P-K) the next P-K tokens of the
- * same order (the marginal set), everything else is evicted. */
-int orc_partition(int n, int k_crit, int k_marg, const float *logits, double m,
-                  double Z, int32_t *crit, int kc_cap, int32_t *marg,
+ * same order (the marginal set), everything else is evicted.
+ * Recent tokens (experimental setup: a fixed critical : recent : marginal
+ * split of the budget, 2 : 1 : 2): the last r = min(k_recent, n) tokens are
+ * kept whatever their score, like critical ones; only the n - r older
+ * tokens are ranked for the critical and marginal budgets. */
+int orc_partition(int n, int k_crit, int k_marg, int k_recent, const float *logits,
+                  double m, double Z, int32_t *crit, int kc_cap, int32_t *marg,
                   double *marg_prob, int km_cap, double *mass, int *n_crit,
                   int *n_marg) {
-  if (n < 1 || k_crit < 1 || k_marg < 0) return ORC_EINVAL;
-  int nc = k_crit < n ? k_crit : n;
-  int nm = k_marg < n - nc ? k_marg : n - nc;
+  if (n < 1 || k_crit < 1 || k_marg < 0 || k_recent < 0) return ORC_EINVAL;
+  const int r = k_recent < n ? k_recent : n;
+  const int older = n - r;
+  const int ntop = k_crit < older ? k_crit : older;
+  const int nm = k_marg < older - ntop ? k_marg : older - ntop;
+  const int nc = ntop + r;
   if (nc > kc_cap || nm > km_cap) return ORC_EINVAL;
 
-  orc_item *items = (orc_item *)malloc((size_t)n * sizeof *items);
+  for (int t = 0; t < n; ++t)
+    if (!isfinite(logits[t])) return ORC_ENONFINITE;
+  orc_item *items = (orc_item *)malloc((size_t)(older > 0 ? older : 1) * sizeof *items);
   if (!items) return ORC_EINVAL;
-  for (int t = 0; t < n; ++t) {
-    if (!isfinite(logits[t])) {
-      free(items);
-      return ORC_ENONFINITE;
-    }
+  for (int t = 0; t < older; ++t) {
     items[t].key = orc_key(logits[t]);
     items[t].idx = t;
   }
-  qsort(items, (size_t)n, sizeof *items, orc_rank_cmp);
+  qsort(items, (size_t)older, sizeof *items, orc_rank_cmp);
 
   for (int i = 0; i < kc_cap; ++i) crit[i] = -1;
   for (int i = 0; i < km_cap; ++i) {
     marg[i] = -1;
     marg_prob[i] = 0.0;
   }
-  for (int i = 0; i < nc; ++i) crit[i] = items[i].idx;
-  for (int i = 0; i < nm; ++i) marg[i] = items[nc + i].idx;
+  for (int i = 0; i < ntop; ++i) crit[i] = items[i].idx;
+  for (int i = 0; i < r; ++i) crit[ntop + i] = older + i;
+  for (int i = 0; i < nm; ++i) marg[i] = items[ntop + i].idx;
   free(items);
   qsort(crit, (size_t)nc, sizeof *crit, orc_int_cmp);
   qsort(marg, (size_t)nm, sizeof *marg, orc_int_cmp);
@@ -289,7 +295,7 @@ int orc_step(const orc_step_in *in, const orc_step_out *out) {
       if (rc != ORC_OK) break;
       out->row_max[row] = ms[j];
       out->row_sum[row] = zs[j];
-      rc = orc_partition(n, in->k_crit[b], in->k_marg[b],
+      rc = orc_partition(n, in->k_crit[b], in->k_marg[b], in->k_recent ? in->k_recent[b] : 0,
                          out->logits + row * ncap, ms[j], zs[j],
                          out->crit + row * in->kc_cap, in->kc_cap,
                          out->marg + row * in->km_cap,

@@ -67,15 +67,16 @@ int orc_small_head(int n, int d, float scale, const float *q, const float *K,
                    const float *V, float *logits, double *m, double *Z,
                    double *O);
 
-/* Stage 2 for one small head: tokens ordered by (logit descending, index
- * ascending); the first nc = min(k_crit, n) are critical, the next
- * nm = min(k_marg, n - nc) are marginal, the rest evicted.  Both lists are
- * emitted in ascending token order and padded with -1 up to kc_cap / km_cap.
- * marg_prob[i] = exp(s - m)/Z for marg[i] (0 in padding); mass[0] = S'_C,
- * mass[1] = S'_M.  Requires k_crit >= 1, k_marg >= 0, kc_cap >= nc,
- * km_cap >= nm. */
-int orc_partition(int n, int k_crit, int k_marg, const float *logits, double m,
-                  double Z, int32_t *crit, int kc_cap, int32_t *marg,
+/* Stage 2 for one small head.  The last r = min(k_recent, n) tokens are
+ * recent and always critical; the n - r older tokens are ordered by (logit
+ * descending, index ascending): the first ntop = min(k_crit, n - r) are
+ * critical too, the next nm = min(k_marg, n - r - ntop) marginal, the rest
+ * evicted (nc = ntop + r).  Both lists are emitted in ascending token order
+ * and padded with -1 up to kc_cap / km_cap.  marg_prob[i] = exp(s - m)/Z for
+ * marg[i] (0 in padding); mass[0] = S'_C, mass[1] = S'_M.  Requires
+ * k_crit >= 1, k_marg >= 0, k_recent >= 0, kc_cap >= nc, km_cap >= nm. */
+int orc_partition(int n, int k_crit, int k_marg, int k_recent, const float *logits,
+                  double m, double Z, int32_t *crit, int kc_cap, int32_t *marg,
                   double *marg_prob, int km_cap, double *mass, int *n_crit,
                   int *n_marg);
 
@@ -104,6 +105,7 @@ int orc_hybrid_head(int d, float scale, const float *q, const float *K,
 typedef struct {
   int32_t batch, n_cap, kc_cap, km_cap;
   const int32_t *seq_len, *k_crit, *k_marg;
+  const int32_t *k_recent; /* [B] recent tokens kept per sequence, or NULL: none */
   /* small model */
   int32_t s_layers, s_q_heads, s_kv_heads, s_dim;
   float s_scale;

@@ -233,6 +233,82 @@ def test_partition_class_order_invariant():
             assert a[logits[a] == t].max() < b[logits[b] == t].min()
 
 
+# ------------------------------------------------- stage 2, recent tokens --
+# Experimental setup: the budget is split 2 : 1 : 2 between critical, recent
+# and marginal tokens; recent tokens are kept whatever their score.
+
+@pytest.mark.parametrize("seed", range(40))
+def test_partition_recent_window_matches_bruteforce(seed):
+    """The last r tokens are critical; the older ones are ranked alone (O(N^2)
+    counting over the older prefix) for the critical and marginal budgets."""
+    rng = np.random.default_rng(500 + seed)
+    n = int(rng.integers(1, 33))
+    q, K, V = small_row(rng, n, 64, ties=bool(seed % 2))
+    if seed % 4 == 3:
+        q = np.round(q * 2) / 2
+        K = np.round(K * 2) / 2
+    logits, m, Z, _ = O.small_head(q, K, V, 0.125)
+    kc = int(rng.integers(1, n + 3))
+    km = int(rng.integers(0, n + 3))
+    kr = int(rng.integers(0, n + 3))
+    crit, marg, mp, mass = O.partition(logits, kc, km, m, Z, kc_cap=2 * n + 4, km_cap=n + 2,
+                                       k_recent=kr)
+    r = min(kr, n)
+    older = n - r
+    rank = rank_bruteforce(logits[:older])
+    ntop = min(kc, older)
+    nm = min(km, older - ntop)
+    want_c = sorted([t for t in range(older) if rank[t] < ntop] + list(range(older, n)))
+    want_m = sorted(t for t in range(older) if ntop <= rank[t] < ntop + nm)
+    nc = ntop + r
+    assert list(crit[:nc]) == want_c and all(crit[nc:] == -1)
+    assert list(marg[:nm]) == want_m and all(marg[nm:] == -1)
+    p = np.exp(logits.astype(np.float64) - m) / Z
+    np.testing.assert_allclose(mp[:nm], p[want_m], rtol=1e-13, atol=0)
+    np.testing.assert_allclose(mass, [p[want_c].sum(), p[want_m].sum()], rtol=1e-12, atol=1e-15)
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_partition_recent_top_is_max_sum_subset_of_older(seed):
+    """Exhaustive: C minus the recent tokens is the size-k subset of the older
+    tokens with the largest exact logit sum (lowest indices among equal sums)."""
+    rng = np.random.default_rng(600 + seed)
+    n = int(rng.integers(3, 11))
+    q, K, V = small_row(rng, n, 64, ties=True)
+    logits, m, Z, _ = O.small_head(q, K, V, 0.125)
+    exact = [Fraction(float(x)) for x in logits]
+    kr = int(rng.integers(1, n - 1))
+    older = n - kr
+    kc = int(rng.integers(1, older + 1))
+    km = int(rng.integers(0, older - kc + 1))
+    crit, marg, _, _ = O.partition(logits, kc, km, m, Z, kc_cap=kc + kr, k_recent=kr)
+
+    def best(k):
+        return min(itertools.combinations(range(older), k),
+                   key=lambda S: (-sum(exact[t] for t in S), S))
+
+    assert tuple(crit[:kc]) == best(kc) and tuple(crit[kc:]) == tuple(range(older, n))
+    assert tuple(sorted(list(crit[:kc]) + list(marg))) == best(kc + km)
+
+
+def test_partition_recent_window_special_cases():
+    rng = np.random.default_rng(42)
+    q, K, V = small_row(rng, 50, 64, ties=True)
+    logits, m, Z, _ = O.small_head(q, K, V, 0.125)
+    # no recent tokens: the plain partition
+    for a, b in zip(O.partition(logits, 7, 11, m, Z), O.partition(logits, 7, 11, m, Z, k_recent=0)):
+        np.testing.assert_array_equal(a, b)
+    # the whole sequence recent: everything critical, nothing marginal
+    crit, marg, mp, mass = O.partition(logits, 7, 11, m, Z, kc_cap=50, km_cap=11, k_recent=60)
+    assert list(crit) == list(range(50)) and all(marg == -1)
+    np.testing.assert_allclose(mass, [1.0, 0.0], rtol=1e-12, atol=0)
+    # the budgets do not fit in the caps: rejected
+    with pytest.raises(O.OracleError):
+        O.partition(logits, 7, 11, m, Z, kc_cap=7 + 4, km_cap=11, k_recent=5)
+    with pytest.raises(O.OracleError):
+        O.partition(logits, 7, 11, m, Z, kc_cap=20, km_cap=11, k_recent=-1)
+
+
 # ------------------------------------------------------------ stage 3 --
 
 def _hybrid_setup(seed, n, d=64):
@@ -366,10 +442,12 @@ def test_step_composes_the_three_stages():
     lv = rng.standard_normal((B, L, hk, ncap, d)).astype(np.float32)
     seq = np.array([40, 23], np.int32)
     hm = rng.integers(0, l * hqs, L * hq).astype(np.int32)
-    for kc, km in ((np.array([5, 3]), np.array([9, 30])), (np.array([40, 40]), np.array([0, 0]))):
+    for kc, km, kr in ((np.array([5, 3]), np.array([9, 30]), None),
+                       (np.array([5, 3]), np.array([9, 12]), np.array([4, 30])),
+                       (np.array([40, 40]), np.array([0, 0]), None)):
         r = O.step(seq_len=seq, k_crit=kc, k_marg=km, kc_cap=40, km_cap=30, head_map=hm,
                    mode=O.NORM_REMAINING, s_q=sq, s_k=sk, s_v=sv, s_scale=0.125,
-                   l_q=lq, l_k=lk, l_v=lv, l_scale=SCALE128)
+                   l_q=lq, l_k=lk, l_v=lv, l_scale=SCALE128, k_recent=kr)
         for b in range(B):
             n = seq[b]
             for j in range(l * hqs):
@@ -378,7 +456,8 @@ def test_step_composes_the_three_stages():
                 lg, m, Z, Os = O.small_head(sq[b, lay, h], sk[b, lay, g, :n], sv[b, lay, g, :n], 0.125)
                 np.testing.assert_array_equal(r["logits"][b, j, :n], lg)
                 np.testing.assert_array_equal(r["small_out"][b, lay, h], Os)
-                c, mg, mp, ms = O.partition(lg, int(kc[b]), int(km[b]), m, Z, kc_cap=40, km_cap=30)
+                c, mg, mp, ms = O.partition(lg, int(kc[b]), int(km[b]), m, Z, kc_cap=40, km_cap=30,
+                                            k_recent=0 if kr is None else int(kr[b]))
                 np.testing.assert_array_equal(r["crit"][b, j], c)
                 np.testing.assert_array_equal(r["marg"][b, j], mg)
                 np.testing.assert_array_equal(r["mass"][b, j], ms)
