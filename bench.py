@@ -209,6 +209,7 @@ def main():
         x = ps.inputs
         host = {k: h(x[k]) for k in ("seq_len", "k_crit", "k_marg", "head_map", "s_q", "s_k",
                                      "s_v", "l_q", "l_k", "l_v")}
+        host["k_recent"] = h(x["k_recent"]) if x.get("k_recent") is not None else None
         try:
             os.sched_setaffinity(0, {sorted(os.sched_getaffinity(0))[0]})
         except (AttributeError, OSError):
@@ -221,7 +222,8 @@ def main():
                    kc_cap=x["kc_cap"], km_cap=x["km_cap"], head_map=host["head_map"],
                    mode=O.NORM_REMAINING, s_q=host["s_q"], s_k=host["s_k"], s_v=host["s_v"],
                    s_scale=softmax_scale(w.small.head_dim), l_q=host["l_q"], l_k=host["l_k"],
-                   l_v=host["l_v"], l_scale=softmax_scale(w.large.head_dim))
+                   l_v=host["l_v"], l_scale=softmax_scale(w.large.head_dim),
+                   k_recent=host["k_recent"])
             spent += time.perf_counter() - c0
             reps += 1
         cpu = {"value": w.batch * reps / spent, "unit": "tokens/s", "cores": 1, "kind": "oracle",
@@ -246,6 +248,7 @@ def main():
             "large": shape_text(w.large), "small": shape_text(w.small),
             "kv_dtype": w.dtype, "batch": w.batch, "context": w.n_ctx,
             "critical": budget_text(w.crit), "marginal": budget_text(w.marg),
+            **({"recent": budget_text(w.recent)} if w.recent != ("abs", 0) else {}),
             "launch": "eager" if args.eager else "hip-graph",
             "rotated_input_copies": args.rotate,
         },

@@ -52,7 +52,7 @@
 extern "C" {
 #endif
 
-#define SMALLKV_ABI_VERSION 1
+#define SMALLKV_ABI_VERSION 2
 
 typedef enum { SMALLKV_F32 = 0, SMALLKV_BF16 = 1 } smallkv_dtype_t;
 
@@ -111,13 +111,20 @@ typedef struct {
                              precondition 1 <= N_b <= n_cap (clamped on device) */
   const int32_t *k_crit;  /* [B] critical budget K_b >= 1 */
   const int32_t *k_marg;  /* [B] marginal budget >= 0 */
+  const int32_t *k_recent; /* [B] recent tokens R_b >= 0, or NULL (none).  The
+                              experimental setup gives recent tokens a share of
+                              the budget (critical : recent : marginal =
+                              2 : 1 : 2): the last r_b tokens are critical
+                              whatever their score and are not ranked */
   int32_t kc_cap;         /* host: width of the critical index rows, >= 1 */
   int32_t km_cap;         /* host: width of the marginal index rows, >= 0 */
   /* Set sizes, computed on device per sequence:
-   *   |C| = min(max(K_b, 1), N_b, kc_cap)
-   *   |M| = min(max(k_marg_b, 0), N_b - |C|, km_cap)
-   * Within the preconditions (K_b <= kc_cap, the marginal count <= km_cap)
-   * the caps never bind. */
+   *   r     = min(max(R_b, 0), N_b, kc_cap)          (0 when k_recent is NULL)
+   *   top   = min(max(K_b, 1), N_b - r, kc_cap - r)  (top-ranked of the older tokens)
+   *   |C|   = r + top
+   *   |M|   = min(max(k_marg_b, 0), N_b - |C|, km_cap)
+   * Within the preconditions (K_b + R_b <= kc_cap, the marginal count <=
+   * km_cap) the caps never bind. */
 } smallkv_batch_t;
 
 /* Stage 1.  For every sequence b, small layer, small query head h (small head
@@ -132,9 +139,10 @@ int smallkv_small_attn(const smallkv_batch_t *batch, const smallkv_model_t *smal
                        float *logits, float *row_max, float *row_sum, void *ws,
                        size_t ws_bytes, void *stream);
 
-/* Stage 2.  For every row (b, j), j < n_small_heads: tokens t < N_b ordered by
- * (logit descending, index ascending); the first |C| are critical, the next
- * |M| marginal, the rest evicted.
+/* Stage 2.  For every row (b, j), j < n_small_heads: the last r tokens are
+ * critical; the older tokens t < N_b - r, ordered by (logit descending, index
+ * ascending), give the other |C| - r critical ones, then |M| marginal, the
+ * rest evicted (r = 0 without k_recent: every token is ranked).
  *   crit_idx  [B][n_small_heads][kc_cap] int32, ascending, padded with -1
  *   marg_idx  [B][n_small_heads][km_cap] int32, ascending, padded with -1
  *   marg_prob [B][n_small_heads][km_cap] fp32, p'_t = exp(logit_t - row_max)/row_sum

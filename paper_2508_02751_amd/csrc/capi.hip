@@ -56,14 +56,32 @@ int status_of(hipError_t e) { return e == hipSuccess ? SMALLKV_OK : SMALLKV_EDEV
 
 size_t max_sz(size_t x, size_t y) { return x > y ? x : y; }
 
+// Workspace of a whole step: stage 1's chunk records, then (reused) stage
+// 3's split records, and after both the partition's list offsets, which
+// stage 2 writes while it reads stage 1's records and stage 3 reads while it
+// writes its own (grouped stage 3 only).
+struct StepLayout {
+  size_t tab_offset, tab_bytes, total;
+};
+StepLayout step_layout(const smallkv_batch_t &b, const smallkv_model_t &small,
+                       const smallkv_model_t &large, int nsh) {
+  const SmallPlan p = plan_small(b, small);
+  const GroupPlan gp = plan_group(b, large, nsh);
+  StepLayout l{};
+  l.tab_offset = (max_sz(p.ws_bytes, gp.use ? gp.ws_bytes : 0) + 255) / 256 * 256;
+  l.tab_bytes = gp.use ? list_offsets_bytes(b, nsh) : 0;
+  l.total = gp.use ? l.tab_offset + l.tab_bytes : max_sz(p.ws_bytes, 0);
+  return l;
+}
+
 // Stage 3: the grouped kernel where it applies, the per-head kernel otherwise.
 hipError_t launch_stage3(const smallkv_batch_t &b, const smallkv_model_t &l, const int32_t *head_map,
                          int nsh, const int32_t *crit, const int32_t *marg, const float *marg_prob,
-                         const float *mass, int mode, void *ws, hipStream_t st) {
+                         const float *mass, int mode, void *ws, const int2 *tab, hipStream_t st) {
   const GroupPlan gp = plan_group(b, l, nsh);
   if (gp.use)
     return launch_hybrid_group(b, l, head_map, nsh, crit, marg, marg_prob, mass, mode, gp,
-                               static_cast<float *>(ws), st);
+                               static_cast<float *>(ws), tab, st);
   return launch_hybrid(b, l, head_map, nsh, crit, marg, marg_prob, mass, mode, st);
 }
 
@@ -96,9 +114,7 @@ int smallkv_workspace_size(const smallkv_step_t *step, size_t *bytes) {
   if (rc) return rc;
   const int nsh = step->small.n_layers * step->small.n_q_heads;
   if ((rc = check_large(&step->batch, &step->large, step->head_map, nsh))) return rc;
-  const SmallPlan p = plan_small(step->batch, step->small);
-  const GroupPlan gp = plan_group(step->batch, step->large, nsh);
-  *bytes = max_sz(p.ws_bytes, gp.use ? gp.ws_bytes : 0);
+  *bytes = step_layout(step->batch, step->small, step->large, nsh).total;
   return SMALLKV_OK;
 }
 
@@ -141,7 +157,8 @@ int smallkv_hybrid_attn(const smallkv_batch_t *batch, const smallkv_model_t *lar
   const GroupPlan gp = plan_group(*batch, *large, n_small_heads);
   if (gp.use && gp.ws_bytes && (!ws || ws_bytes < gp.ws_bytes)) return SMALLKV_EWORKSPACE;
   return status_of(launch_stage3(*batch, *large, head_map, n_small_heads, crit_idx, marg_idx,
-                                 marg_prob, mass, mode, ws, static_cast<hipStream_t>(stream)));
+                                 marg_prob, mass, mode, ws, nullptr,
+                                 static_cast<hipStream_t>(stream)));
 }
 
 int smallkv_step(const smallkv_step_t *s, void *ws, size_t ws_bytes, void *stream) {
@@ -154,19 +171,21 @@ int smallkv_step(const smallkv_step_t *s, void *ws, size_t ws_bytes, void *strea
   if (!s->logits || !s->row_max || !s->row_sum || !s->crit_idx || !s->mass) return SMALLKV_EINVAL;
   if (s->batch.km_cap > 0 && (!s->marg_idx || !s->marg_prob)) return SMALLKV_EINVAL;
   const SmallPlan p = plan_small(s->batch, s->small);
-  const GroupPlan gp = plan_group(s->batch, s->large, nsh);
-  const size_t need = max_sz(p.ws_bytes, gp.use ? gp.ws_bytes : 0);
-  if (need && (!ws || ws_bytes < need)) return SMALLKV_EWORKSPACE;
+  const StepLayout lay = step_layout(s->batch, s->small, s->large, nsh);
+  if (lay.total && (!ws || ws_bytes < lay.total)) return SMALLKV_EWORKSPACE;
   hipStream_t st = static_cast<hipStream_t>(stream);
+  int2 *tab = lay.tab_bytes ? reinterpret_cast<int2 *>(static_cast<char *>(ws) + lay.tab_offset)
+                            : nullptr;
   hipError_t e = launch_small_split(s->batch, s->small, s->logits, static_cast<float *>(ws), p, st);
   if (e != hipSuccess) return SMALLKV_EDEVICE;
   e = launch_merge_partition(s->batch, s->small, p, static_cast<const float *>(ws), s->logits,
                              s->row_max, s->row_sum, s->crit_idx, s->marg_idx, s->marg_prob,
-                             s->mass, st);
+                             s->mass, tab, st);
   if (e != hipSuccess) return SMALLKV_EDEVICE;
   // stage 1's records are consumed by now: stage 3 reuses the workspace
+  // below the list offsets
   e = launch_stage3(s->batch, s->large, s->head_map, nsh, s->crit_idx, s->marg_idx, s->marg_prob,
-                    s->mass, s->mode, ws, st);
+                    s->mass, s->mode, ws, tab, st);
   return status_of(e);
 }
 

@@ -76,16 +76,20 @@ __device__ __forceinline__ float wave_sum(float v) {
 
 __device__ __forceinline__ int clampi(int x, int lo, int hi) { return x < lo ? lo : (x > hi ? hi : x); }
 
-// Per-sequence set sizes, exactly as documented in smallkv.h.
+// Per-sequence set sizes, exactly as documented in smallkv.h: the last nr
+// tokens are recent (kept, not ranked); of the older n - nr tokens the top
+// ntop are critical and the next nm marginal; |C| = nc = nr + ntop.
 struct Sizes {
-  int n, nc, nm;
+  int n, nc, nm, nr, ntop;
 };
 __device__ __forceinline__ Sizes set_sizes(const int32_t *seq_len, const int32_t *k_crit,
-                                           const int32_t *k_marg, int b, int n_cap, int kc_cap,
-                                           int km_cap) {
+                                           const int32_t *k_marg, const int32_t *k_recent, int b,
+                                           int n_cap, int kc_cap, int km_cap) {
   Sizes s;
   s.n = clampi(seq_len[b], 1, n_cap);
-  s.nc = clampi(k_crit[b], 1, min(s.n, kc_cap));
+  s.nr = k_recent ? clampi(k_recent[b], 0, min(s.n, kc_cap)) : 0;
+  s.ntop = min(max(k_crit[b], 1), min(s.n - s.nr, kc_cap - s.nr));  // 0: nothing left to rank
+  s.nc = s.nr + s.ntop;
   s.nm = clampi(k_marg[b], 0, min(s.n - s.nc, km_cap));
   return s;
 }

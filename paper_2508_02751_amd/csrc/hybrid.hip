@@ -30,7 +30,7 @@ struct HybArgs {
   int n_cap, layers, hq, hkv, g, nsh, kc_cap, km_cap, mode, units;
   int64_t n_rows;
   float scale;
-  const int32_t *seq_len, *k_crit, *k_marg, *head_map;
+  const int32_t *seq_len, *k_crit, *k_marg, *k_recent, *head_map;
   const void *q, *k, *v;
   const int32_t *k_slot, *v_slot;
   const int32_t *crit, *marg;
@@ -104,7 +104,7 @@ __global__ __launch_bounds__(kHT) void hybrid_kernel(HybArgs a) {
   const int h = kvh * a.g + hh;
   const int j = clampi(a.head_map[layer * a.hq + h], 0, a.nsh - 1);
   const int64_t row = (int64_t)b * a.nsh + j;
-  const Sizes sz = set_sizes(a.seq_len, a.k_crit, a.k_marg, b, a.n_cap, a.kc_cap, a.km_cap);
+  const Sizes sz = set_sizes(a.seq_len, a.k_crit, a.k_marg, a.k_recent, b, a.n_cap, a.kc_cap, a.km_cap);
   const int nc = sz.nc, nm = sz.nm, ntot = sz.nc + sz.nm;
   const int32_t *crit = a.crit + row * a.kc_cap;
   const int32_t *marg = a.marg + row * a.km_cap;
@@ -252,6 +252,7 @@ hipError_t launch_hybrid(const smallkv_batch_t &b, const smallkv_model_t &m,
   a.seq_len = b.seq_len;
   a.k_crit = b.k_crit;
   a.k_marg = b.k_marg;
+  a.k_recent = b.k_recent;
   a.head_map = head_map;
   a.q = m.q;
   a.k = m.k;

@@ -68,13 +68,15 @@ struct GroupArgs {
   int mp_bytes;  // size of marg_prob in bytes (< 2^31)
   int64_t n_rows;
   float scale;
-  const int32_t *seq_len, *k_crit, *k_marg, *head_map;
+  const int32_t *seq_len, *k_crit, *k_marg, *k_recent, *head_map;
   const void *q, *k, *v;
   const int32_t *k_slot, *v_slot;
   const int32_t *crit, *marg;
   const float *marg_prob, *mass;
   float *rec;
   void *out;
+  const int2 *tab;  // the partition's list offsets ([rows][nblk]), or null
+  int nblk;
 };
 
 struct WaveTiles {
@@ -237,7 +239,7 @@ __global__ __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2))) void h
   const int u = (rest / a.n_split) * kXcd + x % kXcd, sp = rest % a.n_split;
   if (u >= a.units) return;
   const int kvh = u % a.hkv, bl = u / a.hkv, layer = bl % a.layers, b = bl / a.layers;
-  const Sizes sz = set_sizes(a.seq_len, a.k_crit, a.k_marg, b, a.n_cap, a.kc_cap, a.km_cap);
+  const Sizes sz = set_sizes(a.seq_len, a.k_crit, a.k_marg, a.k_recent, b, a.n_cap, a.kc_cap, a.km_cap);
   const int t_begin = sp * a.span;
   if (t_begin >= sz.n) return;
   const int t_end = min(t_begin + a.span, sz.n);
@@ -267,7 +269,19 @@ __global__ __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2))) void h
   ListRef lists[kLPW];
 #pragma unroll
   for (int i = 0; i < kLPW; ++i) lists[i] = list_ref(a, sh, wave + kGW * i, sz.nc, sz.nm);
-  {
+  if (a.tab) {
+    // the partition's offsets at the range start (a multiple of 256 tokens):
+    // entries of each list below t_begin
+    const int64_t blk = t_begin >> 8;
+    if (lane == 0)
+#pragma unroll
+      for (int i = 0; i < kLPW; ++i) {
+        const int L = wave + kGW * i;
+        if (!lists[i].on) continue;
+        const int2 v = a.tab[sh.hrow[L < g ? L : L - g] * a.nblk + blk];
+        sh.cur[L] = L < g ? v.x : v.y;
+      }
+  } else {
     int res[kLPW];
     lower_bounds(lists, t_begin, res);
     if (lane == 0)
@@ -699,7 +713,7 @@ GroupPlan plan_group(const smallkv_batch_t &b, const smallkv_model_t &m, int n_s
   int64_t s = 1;
   for (int64_t c = 2; c <= 16 && c <= max_s; ++c)
     if (cost(c) < cost(s)) s = c;
-  p.span = (int)((b.n_cap + s - 1) / s);
+  p.span = (int)(((b.n_cap + s - 1) / s + 255) / 256 * 256);  // range starts on list-offset blocks
   p.n_split = (int)((b.n_cap + p.span - 1) / p.span);
   p.ws_bytes = p.n_split > 1 ? (size_t)units * p.n_split * g * kRec * sizeof(float) : 0;
   return p;
@@ -708,7 +722,8 @@ GroupPlan plan_group(const smallkv_batch_t &b, const smallkv_model_t &m, int n_s
 hipError_t launch_hybrid_group(const smallkv_batch_t &b, const smallkv_model_t &m,
                                const int32_t *head_map, int n_small_heads, const int32_t *crit,
                                const int32_t *marg, const float *marg_prob, const float *mass,
-                               int mode, const GroupPlan &p, float *ws, hipStream_t st) {
+                               int mode, const GroupPlan &p, float *ws, const int2 *tab,
+                               hipStream_t st) {
   GroupArgs a;
   a.n_cap = b.n_cap;
   a.layers = m.n_layers;
@@ -728,6 +743,7 @@ hipError_t launch_hybrid_group(const smallkv_batch_t &b, const smallkv_model_t &
   a.seq_len = b.seq_len;
   a.k_crit = b.k_crit;
   a.k_marg = b.k_marg;
+  a.k_recent = b.k_recent;
   a.head_map = head_map;
   a.q = m.q;
   a.k = m.k;
@@ -739,6 +755,8 @@ hipError_t launch_hybrid_group(const smallkv_batch_t &b, const smallkv_model_t &
   a.marg_prob = marg_prob;
   a.mass = mass;
   a.rec = ws;
+  a.tab = tab;
+  a.nblk = list_blocks(b);
   a.out = m.out;
   const int groups = (a.units + kXcd - 1) / kXcd;
   hipLaunchKernelGGL(hybrid_group_kernel, dim3(groups * kXcd * a.n_split), dim3(kGT), 0, st, a);

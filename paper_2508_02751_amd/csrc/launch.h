@@ -29,12 +29,19 @@ hipError_t launch_small_attn(const smallkv_batch_t &b, const smallkv_model_t &m,
 hipError_t launch_small_split(const smallkv_batch_t &b, const smallkv_model_t &m, float *logits,
                               float *ws, const SmallPlan &p, hipStream_t st);
 
+// List offsets: per partition row and 256-token boundary t < N_b, the
+// (critical, marginal) entries with a token below t, [rows][list_blocks].
+inline int list_blocks(const smallkv_batch_t &b) { return (b.n_cap + 255) / 256; }
+inline size_t list_offsets_bytes(const smallkv_batch_t &b, int n_small_heads) {
+  return (size_t)b.batch * n_small_heads * list_blocks(b) * sizeof(int2);
+}
+
 // Stage 2 fused with stage 1's merge: writes row_max, row_sum and the small
-// model's output, then partitions.
+// model's output, then partitions; also the list offsets when tab is set.
 hipError_t launch_merge_partition(const smallkv_batch_t &b, const smallkv_model_t &m,
                                   const SmallPlan &p, const float *ws, const float *logits,
                                   float *row_max, float *row_sum, int32_t *crit, int32_t *marg,
-                                  float *marg_prob, float *mass, hipStream_t st);
+                                  float *marg_prob, float *mass, int2 *tab, hipStream_t st);
 
 hipError_t launch_partition(const smallkv_batch_t &b, int n_small_heads, const float *logits,
                             const float *row_max, const float *row_sum, int32_t *crit,
@@ -55,10 +62,13 @@ struct GroupPlan {
 
 GroupPlan plan_group(const smallkv_batch_t &b, const smallkv_model_t &m, int n_small_heads);
 
+// tab: the partition's list offsets, or null; with them the list cursors at
+// the start of each token range are read instead of searched.
 hipError_t launch_hybrid_group(const smallkv_batch_t &b, const smallkv_model_t &m,
                                const int32_t *head_map, int n_small_heads, const int32_t *crit,
                                const int32_t *marg, const float *marg_prob, const float *mass,
-                               int mode, const GroupPlan &p, float *ws, hipStream_t st);
+                               int mode, const GroupPlan &p, float *ws, const int2 *tab,
+                               hipStream_t st);
 
 hipError_t launch_hybrid(const smallkv_batch_t &b, const smallkv_model_t &m,
                          const int32_t *head_map, int n_small_heads, const int32_t *crit,

@@ -59,7 +59,7 @@ struct PC {
 
 struct PartArgs {
   int n_cap, nsh, kc_cap, km_cap;
-  const int32_t *seq_len, *k_crit, *k_marg;
+  const int32_t *seq_len, *k_crit, *k_marg, *k_recent;
   const float *logits;
   float *row_max, *row_sum;  // read (standalone) or written (fused)
   int32_t *crit, *marg;
@@ -68,6 +68,10 @@ struct PartArgs {
   const float *part;
   void *small_out;
   int layers, hq, hkv, g, chunk, n_split, d, gp, out_bf16;
+  // optional list offsets, [rows][nblk]: (critical, marginal) entries before
+  // each 256-token boundary of the row (written when not null)
+  int2 *tab;
+  int nblk;
 };
 
 __device__ __forceinline__ uint64_t lanemask_lt() {
@@ -156,6 +160,7 @@ struct alignas(16) PartShared {
 
 struct RowCtx {
   int row, n, nc, nm;
+  int ntop, older;  // top-ranked critical count; tokens ranked (the rest are recent)
   const float *lg;
   int32_t *crit, *marg;
   float *mp;
@@ -165,10 +170,13 @@ struct RowCtx {
 __device__ __forceinline__ void row_setup(const PartArgs &a, RowCtx &r) {
   r.row = blockIdx.x;
   const int b = r.row / a.nsh;
-  const Sizes sz = set_sizes(a.seq_len, a.k_crit, a.k_marg, b, a.n_cap, a.kc_cap, a.km_cap);
+  const Sizes sz = set_sizes(a.seq_len, a.k_crit, a.k_marg, a.k_recent, b, a.n_cap, a.kc_cap,
+                             a.km_cap);
   r.n = sz.n;
   r.nc = sz.nc;
   r.nm = sz.nm;
+  r.ntop = sz.ntop;
+  r.older = sz.n - sz.nr;
   r.lg = a.logits + (int64_t)r.row * a.n_cap;
   r.crit = a.crit + (int64_t)r.row * a.kc_cap;
   r.marg = a.marg + (int64_t)r.row * a.km_cap;
@@ -215,6 +223,7 @@ struct Row {
   float s[R > 0 ? R : 4];
   const float *lg;
   int n;
+  int nrank;     // tokens ranked: the first nrank (the rest, recent, are kept unranked)
   bool aligned;  // 16-byte aligned row: whole chunks load as one float4
 
   __device__ __forceinline__ float4 fetch(int k) const {
@@ -252,18 +261,22 @@ struct Row {
   __device__ __forceinline__ bool valid(int k, int e) const {
     return k * kChunk + 4 * (int)threadIdx.x + e < n;
   }
-  // f(value, valid) for every slot of every chunk, with the wave converged
+  __device__ __forceinline__ bool ranked(int k, int e) const {
+    return k * kChunk + 4 * (int)threadIdx.x + e < nrank;
+  }
+  // f(value, ranked) for every slot of every chunk holding ranked tokens,
+  // with the wave converged
   template <typename F>
   __device__ __forceinline__ void each(F f) const {
     if constexpr (R > 0) {
 #pragma unroll
       for (int k = 0; k < R / 4; ++k) {
-        if (k * kChunk >= n) break;
+        if (k * kChunk >= nrank) break;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) f(s[4 * k + e], valid(k, e));
+        for (int e = 0; e < 4; ++e) f(s[4 * k + e], ranked(k, e));
       }
     } else {
-      const int nk = chunks();
+      const int nk = (nrank + kChunk - 1) / kChunk;
       float4 nx[4];  // the next four chunks, in flight while these are used
 #pragma unroll
       for (int j = 0; j < 4; ++j) nx[j] = j < nk ? fetch(j) : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
@@ -276,10 +289,10 @@ struct Row {
           if (k0 + 4 + j < nk) nx[j] = fetch(k0 + 4 + j);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          f(v[j].x, valid(k0 + j, 0));
-          f(v[j].y, valid(k0 + j, 1));
-          f(v[j].z, valid(k0 + j, 2));
-          f(v[j].w, valid(k0 + j, 3));
+          f(v[j].x, ranked(k0 + j, 0));
+          f(v[j].y, ranked(k0 + j, 1));
+          f(v[j].z, ranked(k0 + j, 2));
+          f(v[j].w, ranked(k0 + j, 3));
         }
       }
     }
@@ -296,6 +309,10 @@ struct Targets {
 template <int PT, typename Row>
 __device__ __forceinline__ Targets select_targets(PartShared<PT> &sh, const RowCtx &r, const Row &row) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // The targets' ranks count ranked (older) tokens only.  Rank 0 -- no
+  // ranked token in the set -- is resolved as rank 1 and then replaced by a
+  // key above every logit's.
+  if (r.ntop + r.nm == 0) return Targets{{~0u, ~0u}, {0u, 0u}, {0u, 0u}};
   const float M = r.M;
   for (int x = tid; x < Hist<PT>::size; x += PT) sh.hist[0][x] = 0;
   if (tid < 2) sh.ncand[tid] = 0;
@@ -305,7 +322,7 @@ __device__ __forceinline__ Targets select_targets(PartShared<PT> &sh, const RowC
   });
   __syncthreads();
   // every wave finds both targets' bins itself: no broadcast needed
-  uint32_t rr[2] = {(uint32_t)r.nc, (uint32_t)(r.nc + r.nm)};
+  uint32_t rr[2] = {(uint32_t)max(r.ntop, 1), (uint32_t)(r.ntop + r.nm)};
   int bin[2];
   uint32_t cnt[2];
 #pragma unroll
@@ -417,6 +434,11 @@ __device__ __forceinline__ Targets select_targets(PartShared<PT> &sh, const RowC
     t.need[x] = c ? sh.res[x][1] : sh.sel[x][2];
     t.eq[x] = c ? sh.res[x][2] : sh.sel[x][3];
   }
+  if (r.ntop == 0) {
+    t.T[0] = ~0u;
+    t.need[0] = 0u;
+    t.eq[0] = 0u;
+  }
   return t;
 }
 
@@ -483,11 +505,12 @@ struct Compactor {
   float Zinv;
   float sc = 0.0f, sm = 0.0f;
 
-  // rC / rP: the value's rank (0-based, token order) among the row's ties at T
-  __device__ __forceinline__ void classify(uint32_t u, bool valid, uint32_t rC, uint32_t rP,
-                                           bool &inC, bool &inM) const {
-    inC = valid && (u > t.T[0] || (u == t.T[0] && rC < t.need[0]));
-    const bool inP = valid && (u > t.T[1] || (u == t.T[1] && rP < t.need[1]));
+  // rC / rP: the value's rank (0-based, token order) among the row's ties at
+  // T; recent tokens are critical whatever their key
+  __device__ __forceinline__ void classify(uint32_t u, bool ranked, bool recent, uint32_t rC,
+                                           uint32_t rP, bool &inC, bool &inM) const {
+    inC = recent || (ranked && (u > t.T[0] || (u == t.T[0] && rC < t.need[0])));
+    const bool inP = ranked && (u > t.T[1] || (u == t.T[1] && rP < t.need[1]));
     inM = inP && !inC;
   }
   __device__ __forceinline__ void emit(float s, int tok, bool inC, bool inM, uint32_t &pc,
@@ -506,6 +529,15 @@ struct Compactor {
   }
 };
 
+// The list offsets at a 256-token boundary: the thread whose first token
+// starts the block (lane 0 of its wave: 64 threads x 4 tokens) records the
+// list positions it is about to write.
+__device__ __forceinline__ void offsets(const PartArgs &a, const RowCtx &r, int tok0, uint32_t pc,
+                                        uint32_t pm) {
+  if (a.tab && (threadIdx.x & 63) == 0 && tok0 < r.n)
+    a.tab[(int64_t)r.row * a.nblk + (tok0 >> 8)] = make_int2((int)pc, (int)pm);
+}
+
 // ---------------------------------------------------------------- kernel --
 
 template <bool kMerge, int R, int PT>
@@ -519,6 +551,7 @@ void partition_kernel(PartArgs a) {
   Row<R, PT> row;
   row.lg = r.lg;
   row.n = r.n;
+  row.nrank = r.older;
   row.aligned = (reinterpret_cast<uintptr_t>(r.lg) & 15) == 0;
   row.load();  // in flight while the row's statistics arrive
   row_stats<kMerge>(a, sh, r);
@@ -539,7 +572,7 @@ void partition_kernel(PartArgs a) {
         v[k] = 0;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const bool ok = row.valid(k, e);
+          const bool ok = row.ranked(k, e);
           const uint32_t u = logit_key(row.s[4 * k + e]);
           v[k] += (ok && u == cp.t.T[0] ? 1u : 0u) + (ok && u == cp.t.T[1] ? 0x10000u : 0u);
         }
@@ -561,9 +594,9 @@ void partition_kernel(PartArgs a) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int i = 4 * k + e;
-        const bool ok = row.valid(k, e);
+        const bool ok = row.ranked(k, e);
         const uint32_t u = logit_key(row.s[i]);
-        cp.classify(u, ok, rC, rP, inC[i], inM[i]);
+        cp.classify(u, ok, row.valid(k, e) && !ok, rC, rP, inC[i], inM[i]);
         rC += ok && u == cp.t.T[0] ? 1u : 0u;
         rP += ok && u == cp.t.T[1] ? 1u : 0u;
         v[k] += (inC[i] ? 1u : 0u) + (inM[i] ? 0x10000u : 0u);
@@ -574,6 +607,7 @@ void partition_kernel(PartArgs a) {
 #pragma unroll
     for (int k = 0; k < NK; ++k) {
       uint32_t pc = carry_c + (ex[k] & 0xffffu), pm = carry_m + (ex[k] >> 16);
+      offsets(a, r, k * kChunk + 4 * tid, pc, pm);
 #pragma unroll
       for (int e = 0; e < 4; ++e)
         cp.emit(row.s[4 * k + e], k * kChunk + 4 * tid + e, inC[4 * k + e], inM[4 * k + e], pc, pm);
@@ -612,8 +646,8 @@ void partition_kernel(PartArgs a) {
           v[j] = 0;
 #pragma unroll
           for (int e = 0; e < 4; ++e)
-            v[j] += (row.valid(k0 + j, e) && logit_key(sv[j][e]) == cp.t.T[0] ? 1u : 0u) +
-                    (row.valid(k0 + j, e) && logit_key(sv[j][e]) == cp.t.T[1] ? 0x10000u : 0u);
+            v[j] += (row.ranked(k0 + j, e) && logit_key(sv[j][e]) == cp.t.T[0] ? 1u : 0u) +
+                    (row.ranked(k0 + j, e) && logit_key(sv[j][e]) == cp.t.T[1] ? 0x10000u : 0u);
         }
         block_scan<NG>(sh, par, v, ex, tot);
 #pragma unroll
@@ -630,9 +664,9 @@ void partition_kernel(PartArgs a) {
         v[j] = 0;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const bool ok = row.valid(k0 + j, e);
+          const bool ok = row.ranked(k0 + j, e);
           const uint32_t u = logit_key(sv[j][e]);
-          cp.classify(u, ok, rC, rP, inC[j][e], inM[j][e]);
+          cp.classify(u, ok, row.valid(k0 + j, e) && !ok, rC, rP, inC[j][e], inM[j][e]);
           rC += ok && u == cp.t.T[0] ? 1u : 0u;
           rP += ok && u == cp.t.T[1] ? 1u : 0u;
           v[j] += (inC[j][e] ? 1u : 0u) + (inM[j][e] ? 0x10000u : 0u);
@@ -642,6 +676,7 @@ void partition_kernel(PartArgs a) {
 #pragma unroll
       for (int j = 0; j < NG; ++j) {
         uint32_t pc = carry_c + (ex[j] & 0xffffu), pm = carry_m + (ex[j] >> 16);
+        offsets(a, r, (k0 + j) * kChunk + 4 * tid, pc, pm);
 #pragma unroll
         for (int e = 0; e < 4; ++e)
           cp.emit(sv[j][e], (k0 + j) * kChunk + 4 * tid + e, inC[j][e], inM[j][e], pc, pm);
@@ -664,6 +699,7 @@ PartArgs base_args(const smallkv_batch_t &b, int n_small_heads, const float *log
   a.seq_len = b.seq_len;
   a.k_crit = b.k_crit;
   a.k_marg = b.k_marg;
+  a.k_recent = b.k_recent;
   a.logits = logits;
   a.row_max = row_max;
   a.row_sum = row_sum;
@@ -714,7 +750,7 @@ hipError_t launch_partition(const smallkv_batch_t &b, int n_small_heads, const f
 hipError_t launch_merge_partition(const smallkv_batch_t &b, const smallkv_model_t &m,
                                   const SmallPlan &p, const float *ws, const float *logits,
                                   float *row_max, float *row_sum, int32_t *crit, int32_t *marg,
-                                  float *marg_prob, float *mass, hipStream_t st) {
+                                  float *marg_prob, float *mass, int2 *tab, hipStream_t st) {
   const int nsh = m.n_layers * m.n_q_heads;
   PartArgs a = base_args(b, nsh, logits, row_max, row_sum, crit, marg, marg_prob, mass);
   a.part = ws;
@@ -728,6 +764,8 @@ hipError_t launch_merge_partition(const smallkv_batch_t &b, const smallkv_model_
   a.d = m.head_dim;
   a.gp = p.gp;
   a.out_bf16 = m.dtype == SMALLKV_BF16;
+  a.tab = tab;
+  a.nblk = list_blocks(b);
   return launch_rows<true>(a, b.batch * nsh, st);
 }
 

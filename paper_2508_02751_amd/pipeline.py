@@ -35,7 +35,7 @@ class PreparedStep:
         S.smallkv_step(self.desc, self.buf.ws, stream)
 
     def with_query(self, s_q: torch.Tensor, l_q: torch.Tensor, seq_len=None, k_crit=None,
-                   k_marg=None):
+                   k_marg=None, k_recent=None):
         """Point the descriptor at new queries/lengths (same shapes; for multi-step runs)."""
         self.small.q.copy_(s_q)
         self.large.q.copy_(l_q)
@@ -43,6 +43,8 @@ class PreparedStep:
             self.batch.seq_len.copy_(seq_len)
             self.batch.k_crit.copy_(k_crit)
             self.batch.k_marg.copy_(k_marg)
+        if k_recent is not None:
+            self.batch.k_recent.copy_(k_recent)
 
 
 def prepare_step(x: dict, mode: int = S.NORM_REMAINING,
@@ -55,8 +57,10 @@ def prepare_step(x: dict, mode: int = S.NORM_REMAINING,
     l_k = x["l_k"] if l_k is None else l_k
     l_v = x["l_v"] if l_v is None else l_v
     n_cap = s_k.shape[3]
+    kr = x.get("k_recent")
     batch = S.BatchSpec(x["seq_len"].contiguous(), x["k_crit"].contiguous(),
-                        x["k_marg"].contiguous(), n_cap, int(x["kc_cap"]), int(x["km_cap"]))
+                        x["k_marg"].contiguous(), n_cap, int(x["kc_cap"]), int(x["km_cap"]),
+                        kr.contiguous() if kr is not None else None)
     small = S.ModelSpec(s_q.contiguous(), s_k, s_v, torch.empty_like(s_q),
                         softmax_scale(s_q.shape[-1]))
     large = S.ModelSpec(l_q.contiguous(), l_k, l_v, torch.empty_like(l_q),

@@ -29,7 +29,7 @@ OK, EINVAL, EUNSUPPORTED, EWORKSPACE, EDEVICE = 0, -1, -2, -3, -4
 class Batch(C.Structure):
     _fields_ = [("batch", C.c_int32), ("n_cap", C.c_int32),
                 ("seq_len", C.c_void_p), ("k_crit", C.c_void_p), ("k_marg", C.c_void_p),
-                ("kc_cap", C.c_int32), ("km_cap", C.c_int32)]
+                ("k_recent", C.c_void_p), ("kc_cap", C.c_int32), ("km_cap", C.c_int32)]
 
 
 class Model(C.Structure):
@@ -113,20 +113,26 @@ def _stream(stream) -> Optional[int]:
 
 @dataclasses.dataclass
 class BatchSpec:
-    """Sequences and budgets: seq_len/k_crit/k_marg are int32 device tensors [B]."""
+    """Sequences and budgets: seq_len/k_crit/k_marg (and the optional recent
+    budget k_recent) are int32 device tensors [B]."""
     seq_len: torch.Tensor
     k_crit: torch.Tensor
     k_marg: torch.Tensor
     n_cap: int
     kc_cap: int
     km_cap: int
+    k_recent: Optional[torch.Tensor] = None
 
     def c(self) -> Batch:
-        for t in (self.seq_len, self.k_crit, self.k_marg):
+        ts = [self.seq_len, self.k_crit, self.k_marg]
+        if self.k_recent is not None:
+            ts.append(self.k_recent)
+        for t in ts:
             if t.dtype != torch.int32:
-                raise ValueError("seq_len, k_crit and k_marg must be int32")
+                raise ValueError("seq_len, k_crit, k_marg and k_recent must be int32")
         return Batch(self.seq_len.numel(), self.n_cap, _ptr(self.seq_len), _ptr(self.k_crit),
-                     _ptr(self.k_marg), self.kc_cap, self.km_cap)
+                     _ptr(self.k_marg), _ptr(self.k_recent) if self.k_recent is not None else None,
+                     self.kc_cap, self.km_cap)
 
 
 @dataclasses.dataclass

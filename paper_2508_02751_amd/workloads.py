@@ -19,7 +19,9 @@ synthetic padded prompts):
   * the large-to-small head map f(layer, head) is iid uniform over the small
     model's l*Hq_s heads;
   * budgets: a fixed count per sequence, or floor(N_b * pct / 100) of the
-    sequence's current length N_b.
+    sequence's current length N_b; workloads with recent tokens split the
+    budget critical : recent : marginal = 2 : 1 : 2, as in the paper's
+    experimental setup (its 20% example: 10%, 5%, 10%).
 
 Seeds: base 1000 + workload id; each named tensor has its own generator
 seeded from (base, tag) through crc32, so any tensor can be regenerated alone.
@@ -56,6 +58,7 @@ class Workload:
     large: ModelShape
     crit: tuple                   # ("abs", k) or ("pct", p)
     marg: tuple
+    recent: tuple = ("abs", 0)    # recent tokens kept whatever their score
     sinks: int = 4
     sink_gain: float = 8.0
     heavy_frac: float = 0.0       # fraction of positions that are heavy hitters
@@ -95,6 +98,8 @@ WORKLOADS = {
                 QWEN2_0_5B, QWEN2_7B, ("pct", 20), ("pct", 30), ragged_min=1024, steps=256),
     5: Workload(5, "qwen2-72b+0.5b-n65536-b2-bf16-compact", 2, 65536, "bf16",
                 QWEN2_0_5B, QWEN2_72B, ("pct", 2), ("pct", 8), compact_large=True),
+    6: Workload(6, "qwen2-7b+0.5b-n8192-b1-bf16-c10r5m10", 1, 8192, "bf16",
+                QWEN2_0_5B, QWEN2_7B, ("pct", 10), ("pct", 10), recent=("pct", 5)),
 }
 
 LATENT = 64
@@ -163,10 +168,18 @@ def budgets(w: Workload, step: int = 0):
     return n, kc, km
 
 
+def recent_budget(w: Workload, step: int = 0):
+    """Recent tokens per sequence [B] int32, or None for workloads without them."""
+    if w.recent == ("abs", 0):
+        return None
+    return torch.tensor([w.budget(w.recent, int(x)) for x in seq_lens(w, step)], dtype=torch.int32)
+
+
 def caps(w: Workload):
     """Widths of the index buffers: the largest budget any step can ask for."""
     n_max = w.n_cap
-    return max(1, w.budget(w.crit, n_max)), max(1, w.budget(w.marg, n_max))
+    return (max(1, w.budget(w.crit, n_max) + w.budget(w.recent, n_max)),
+            max(1, w.budget(w.marg, n_max)))
 
 
 def head_map(w: Workload, device) -> torch.Tensor:
@@ -248,6 +261,9 @@ def make_step_inputs(w: Workload, device, step: int = 0, *, z=None, large=True):
         out["l_k"], out["l_v"] = l_k, l_v
     n, kc, km = budgets(w, step)
     out["seq_len"], out["k_crit"], out["k_marg"] = n.to(device), kc.to(device), km.to(device)
+    kr = recent_budget(w, step)
+    if kr is not None:
+        out["k_recent"] = kr.to(device)
     out["head_map"] = head_map(w, device)
     out["kc_cap"], out["km_cap"] = caps(w)
     return out

@@ -40,7 +40,8 @@ def oracle_step(x: dict, mode: int, k_slot=None, v_slot=None, l_k=None, l_v=None
         s_scale=softmax_scale(x["s_q"].shape[-1]), l_q=host(x["l_q"]), l_k=host(l_k),
         l_v=host(l_v), l_scale=softmax_scale(x["l_q"].shape[-1]),
         k_slot=None if k_slot is None else host(k_slot),
-        v_slot=None if v_slot is None else host(v_slot))
+        v_slot=None if v_slot is None else host(v_slot),
+        k_recent=host(x["k_recent"]) if x.get("k_recent") is not None else None)
 
 
 def head_err(got: np.ndarray, ref: np.ndarray) -> float:
@@ -96,8 +97,9 @@ def oracle_small_row(x, b: int, j: int):
     lg, m, Z, out = O.small_head(host(s_q[b, layer, h]), host(s_k[b, layer, g, :n]),
                                  host(s_v[b, layer, g, :n]), softmax_scale(ds))
     kc, km = int(x["k_crit"][b]), int(x["k_marg"][b])
+    kr = int(x["k_recent"][b]) if x.get("k_recent") is not None else 0
     crit, marg, mp, mass = O.partition(lg, kc, km, m, Z, kc_cap=int(x["kc_cap"]),
-                                       km_cap=int(x["km_cap"]))
+                                       km_cap=int(x["km_cap"]), k_recent=kr)
     return dict(logits=lg, m=m, Z=Z, out=out, crit=crit, marg=marg, marg_prob=mp, mass=mass)
 
 

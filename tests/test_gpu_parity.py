@@ -124,6 +124,47 @@ def test_targets_far_below_the_max(n):
     run_case(w, mutate=spike)
 
 
+# ------------------------------------------------------ recent tokens --
+# The experimental setup's 2 : 1 : 2 split of the budget between critical,
+# recent and marginal tokens: the last r tokens are critical unranked.
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_recent_window_ragged(dtype):
+    """Ragged lengths from 1; sequences shorter than the recent budget keep
+    every token critical and rank none."""
+    w = custom(f"recent-{dtype}", 117, 5, 700, dtype, SMALL, LARGE, ("abs", 40), ("abs", 60),
+               ragged_min=1, recent=("abs", 20))
+    run_case(w)
+
+
+def test_recent_window_qwen2_7b_full_step():
+    """The Qwen2-7B + 0.5B step with the paper's 20% example budget: 10%
+    critical, 5% recent, 10% marginal."""
+    run_case(W.WORKLOADS[6])
+
+
+def test_recent_window_with_ties():
+    w = custom("recent-ties", 120, 2, 1500, "bf16", SMALL, LARGE, ("pct", 10), ("pct", 25),
+               recent=("pct", 5))
+
+    def dup(x):
+        k = x["s_k"]
+        src = torch.arange(k.shape[3], device=k.device)
+        src = torch.where(src % 3 == 0, (src * 7 + 1) % k.shape[3], src)
+        x["s_k"] = k[:, :, :, src].contiguous()
+
+    run_case(w, mutate=dup)
+
+
+def test_recent_window_long_rows_and_many_rows():
+    """Rows re-read from memory per pass, and rows of 256 threads (1024 rows)."""
+    run_case(custom("recent-long", 118, 1, 20000, "bf16", W.ModelShape(1, 4, 1, 64),
+                    W.ModelShape(1, 8, 2, 128), ("pct", 5), ("pct", 15), recent=("pct", 3)))
+    run_case(custom("recent-many", 119, 16, 1500, "bf16", W.ModelShape(4, 16, 4, 64),
+                    W.ModelShape(2, 8, 2, 128), ("pct", 10), ("pct", 20), ragged_min=200,
+                    recent=("abs", 64)))
+
+
 @pytest.mark.parametrize("sd,ld", [(128, 64), (128, 128), (64, 64)])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_head_dims(sd, ld, dtype):
