@@ -69,8 +69,9 @@ StepLayout step_layout(const smallkv_batch_t &b, const smallkv_model_t &small,
   const GroupPlan gp = plan_group(b, large, nsh);
   StepLayout l{};
   l.tab_offset = (max_sz(p.ws_bytes, gp.use ? gp.ws_bytes : 0) + 255) / 256 * 256;
-  l.tab_bytes = gp.use ? list_offsets_bytes(b, nsh) : 0;
-  l.total = gp.use ? l.tab_offset + l.tab_bytes : max_sz(p.ws_bytes, 0);
+  // (with one token range per kv head every cursor starts at 0: no offsets)
+  l.tab_bytes = gp.use && gp.n_split > 1 ? list_offsets_bytes(b, nsh) : 0;
+  l.total = l.tab_bytes ? l.tab_offset + l.tab_bytes : max_sz(p.ws_bytes, gp.use ? gp.ws_bytes : 0);
   return l;
 }
 

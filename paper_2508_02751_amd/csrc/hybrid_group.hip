@@ -279,7 +279,8 @@ __global__ __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2))) void h
         const int L = wave + kGW * i;
         if (!lists[i].on) continue;
         const int2 v = a.tab[sh.hrow[L < g ? L : L - g] * a.nblk + blk];
-        sh.cur[L] = L < g ? v.x : v.y;
+        // clamped: no table content can move a cursor outside its list
+        sh.cur[L] = clampi(L < g ? v.x : v.y, 0, lists[i].len);
       }
   } else {
     int res[kLPW];

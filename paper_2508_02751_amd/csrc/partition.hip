@@ -217,7 +217,9 @@ __device__ __forceinline__ void row_stats(const PartArgs &a, PartShared<PT> &sh,
 // 4 consecutive tokens per thread (token of value e = k*kChunk + 4*tid + e).
 // R > 0: the row sits in R registers per thread, read from memory once.
 // R == 0: every pass reads it from memory, four chunks in flight at a time.
-template <int R, int PT>
+// kRecent: the row may end in recent tokens (kept unranked); without them
+// every token is ranked and the kernel carries no test for it.
+template <int R, int PT, bool kRecent>
 struct Row {
   static constexpr int kChunk = PC<PT>::chunk;
   float s[R > 0 ? R : 4];
@@ -262,6 +264,7 @@ struct Row {
     return k * kChunk + 4 * (int)threadIdx.x + e < n;
   }
   __device__ __forceinline__ bool ranked(int k, int e) const {
+    if constexpr (!kRecent) return valid(k, e);
     return k * kChunk + 4 * (int)threadIdx.x + e < nrank;
   }
   // f(value, ranked) for every slot of every chunk holding ranked tokens,
@@ -271,12 +274,12 @@ struct Row {
     if constexpr (R > 0) {
 #pragma unroll
       for (int k = 0; k < R / 4; ++k) {
-        if (k * kChunk >= nrank) break;
+        if (k * kChunk >= (kRecent ? nrank : n)) break;
 #pragma unroll
         for (int e = 0; e < 4; ++e) f(s[4 * k + e], ranked(k, e));
       }
     } else {
-      const int nk = (nrank + kChunk - 1) / kChunk;
+      const int nk = ((kRecent ? nrank : n) + kChunk - 1) / kChunk;
       float4 nx[4];  // the next four chunks, in flight while these are used
 #pragma unroll
       for (int j = 0; j < 4; ++j) nx[j] = j < nk ? fetch(j) : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
@@ -540,7 +543,7 @@ __device__ __forceinline__ void offsets(const PartArgs &a, const RowCtx &r, int 
 
 // ---------------------------------------------------------------- kernel --
 
-template <bool kMerge, int R, int PT>
+template <bool kMerge, int R, int PT, bool kRecent>
 __global__ __launch_bounds__(PT) __attribute__((amdgpu_waves_per_eu(4)))
 void partition_kernel(PartArgs a) {
   constexpr int kChunk = PC<PT>::chunk;
@@ -548,7 +551,7 @@ void partition_kernel(PartArgs a) {
   RowCtx r;
   row_setup(a, r);
   const int tid = threadIdx.x;
-  Row<R, PT> row;
+  Row<R, PT, kRecent> row;
   row.lg = r.lg;
   row.n = r.n;
   row.nrank = r.older;
@@ -596,7 +599,7 @@ void partition_kernel(PartArgs a) {
         const int i = 4 * k + e;
         const bool ok = row.ranked(k, e);
         const uint32_t u = logit_key(row.s[i]);
-        cp.classify(u, ok, row.valid(k, e) && !ok, rC, rP, inC[i], inM[i]);
+        cp.classify(u, ok, kRecent && row.valid(k, e) && !ok, rC, rP, inC[i], inM[i]);
         rC += ok && u == cp.t.T[0] ? 1u : 0u;
         rP += ok && u == cp.t.T[1] ? 1u : 0u;
         v[k] += (inC[i] ? 1u : 0u) + (inM[i] ? 0x10000u : 0u);
@@ -607,7 +610,7 @@ void partition_kernel(PartArgs a) {
 #pragma unroll
     for (int k = 0; k < NK; ++k) {
       uint32_t pc = carry_c + (ex[k] & 0xffffu), pm = carry_m + (ex[k] >> 16);
-      offsets(a, r, k * kChunk + 4 * tid, pc, pm);
+      if constexpr (kMerge) offsets(a, r, k * kChunk + 4 * tid, pc, pm);
 #pragma unroll
       for (int e = 0; e < 4; ++e)
         cp.emit(row.s[4 * k + e], k * kChunk + 4 * tid + e, inC[4 * k + e], inM[4 * k + e], pc, pm);
@@ -666,7 +669,7 @@ void partition_kernel(PartArgs a) {
         for (int e = 0; e < 4; ++e) {
           const bool ok = row.ranked(k0 + j, e);
           const uint32_t u = logit_key(sv[j][e]);
-          cp.classify(u, ok, row.valid(k0 + j, e) && !ok, rC, rP, inC[j][e], inM[j][e]);
+          cp.classify(u, ok, kRecent && row.valid(k0 + j, e) && !ok, rC, rP, inC[j][e], inM[j][e]);
           rC += ok && u == cp.t.T[0] ? 1u : 0u;
           rP += ok && u == cp.t.T[1] ? 1u : 0u;
           v[j] += (inC[j][e] ? 1u : 0u) + (inM[j][e] ? 0x10000u : 0u);
@@ -676,7 +679,7 @@ void partition_kernel(PartArgs a) {
 #pragma unroll
       for (int j = 0; j < NG; ++j) {
         uint32_t pc = carry_c + (ex[j] & 0xffffu), pm = carry_m + (ex[j] >> 16);
-        offsets(a, r, (k0 + j) * kChunk + 4 * tid, pc, pm);
+        if constexpr (kMerge) offsets(a, r, (k0 + j) * kChunk + 4 * tid, pc, pm);
 #pragma unroll
         for (int e = 0; e < 4; ++e)
           cp.emit(sv[j][e], (k0 + j) * kChunk + 4 * tid + e, inC[j][e], inM[j][e], pc, pm);
@@ -710,20 +713,20 @@ PartArgs base_args(const smallkv_batch_t &b, int n_small_heads, const float *log
   return a;
 }
 
-template <bool kMerge, int PT>
+template <bool kMerge, int PT, bool kRecent>
 hipError_t launch_pt(const PartArgs &a, int rows, hipStream_t st) {
   const dim3 grid(rows), block(PT);
   const int n = a.n_cap;
   if (n <= 4 * PT)
-    hipLaunchKernelGGL((partition_kernel<kMerge, 4, PT>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((partition_kernel<kMerge, 4, PT, kRecent>), grid, block, 0, st, a);
   else if (n <= 8 * PT)
-    hipLaunchKernelGGL((partition_kernel<kMerge, 8, PT>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((partition_kernel<kMerge, 8, PT, kRecent>), grid, block, 0, st, a);
   else if (n <= 16 * PT)
-    hipLaunchKernelGGL((partition_kernel<kMerge, 16, PT>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((partition_kernel<kMerge, 16, PT, kRecent>), grid, block, 0, st, a);
   else if (PT == 256 && n <= 20 * PT)  // narrow rows: one more register chunk
-    hipLaunchKernelGGL((partition_kernel<kMerge, PT == 256 ? 20 : 16, PT>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((partition_kernel<kMerge, PT == 256 ? 20 : 16, PT, kRecent>), grid, block, 0, st, a);
   else
-    hipLaunchKernelGGL((partition_kernel<kMerge, 0, PT>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((partition_kernel<kMerge, 0, PT, kRecent>), grid, block, 0, st, a);
   return hipGetLastError();
 }
 
@@ -733,8 +736,12 @@ constexpr int kManyRows = 4 * 256;
 
 template <bool kMerge>
 hipError_t launch_rows(const PartArgs &a, int rows, hipStream_t st) {
-  if (rows >= kManyRows) return launch_pt<kMerge, 256>(a, rows, st);
-  return launch_pt<kMerge, 512>(a, rows, st);
+  if (a.k_recent) {
+    if (rows >= kManyRows) return launch_pt<kMerge, 256, true>(a, rows, st);
+    return launch_pt<kMerge, 512, true>(a, rows, st);
+  }
+  if (rows >= kManyRows) return launch_pt<kMerge, 256, false>(a, rows, st);
+  return launch_pt<kMerge, 512, false>(a, rows, st);
 }
 
 }  // namespace
