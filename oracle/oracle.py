@@ -19,6 +19,7 @@ import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(HERE, "smallkv_oracle.c")
+SRCS = [SRC, os.path.join(HERE, "match_oracle.c")]
 LIB = os.path.join(HERE, "libsmallkv_oracle.so")
 
 NORM_REMAINING, NORM_NONE, NORM_SLM_CRIT, NORM_RETAINED, NORM_MARG_FILL = range(5)
@@ -31,7 +32,7 @@ def build(force: bool = True) -> str:
         tmp = LIB + ".tmp"
         subprocess.check_call([
             "gcc", "-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math",
-            "-Wall", "-Wextra", "-fPIC", "-shared", SRC, "-o", tmp, "-lm"])
+            "-Wall", "-Wextra", "-fPIC", "-shared", *SRCS, "-o", tmp, "-lm"])
         os.replace(tmp, LIB)
     return LIB
 
@@ -40,6 +41,7 @@ _lib = None
 _F = C.POINTER(C.c_float)
 _D = C.POINTER(C.c_double)
 _I = C.POINTER(C.c_int32)
+_U8 = C.POINTER(C.c_uint8)
 
 
 class StepIn(C.Structure):
@@ -59,6 +61,16 @@ class StepIn(C.Structure):
     ]
 
 
+class Window(C.Structure):
+    _fields_ = [("layers", C.c_int32), ("q_heads", C.c_int32), ("kv_heads", C.c_int32),
+                ("dim", C.c_int32), ("scale", C.c_float), ("q", _F), ("k", _F)]
+
+
+class MatchIn(C.Structure):
+    _fields_ = [("batch", C.c_int32), ("w_cap", C.c_int32), ("win_len", _I), ("top_k", _I),
+                ("large", Window), ("small", Window)]
+
+
 class StepOut(C.Structure):
     _fields_ = [
         ("logits", _F),
@@ -71,7 +83,9 @@ class StepOut(C.Structure):
 def lib():
     global _lib
     if _lib is None:
-        if not os.path.exists(LIB) or os.path.getmtime(LIB) < os.path.getmtime(SRC):
+        hdr = os.path.join(HERE, "smallkv_oracle.h")
+        if not os.path.exists(LIB) or os.path.getmtime(LIB) < max(
+                os.path.getmtime(f) for f in SRCS + [hdr]):
             build()
         L = C.CDLL(LIB)
         L.orc_logit.argtypes = [C.c_int, C.c_float, _F, _F]
@@ -85,7 +99,17 @@ def lib():
         L.orc_hybrid_head.argtypes = [C.c_int, C.c_float, _F, _F, _F, _I, _I, C.c_int, _I,
                                       C.c_int, _I, _D, _D, C.c_int, _D]
         L.orc_step.argtypes = [C.POINTER(StepIn), C.POINTER(StepOut)]
-        for f in (L.orc_small_head, L.orc_partition, L.orc_hybrid_head, L.orc_step):
+        L.orc_exp.argtypes = [C.c_float]
+        L.orc_exp.restype = C.c_float
+        L.orc_exp_n.argtypes = [C.c_int, _F, _F]
+        L.orc_exp_n.restype = None
+        L.orc_match_scores.argtypes = [C.c_int, C.c_int, C.c_float, _F, _F, _F]
+        L.orc_topk.argtypes = [C.c_int, C.c_int, _F, _U8]
+        L.orc_jaccard.argtypes = [C.c_int, _U8, _U8, C.POINTER(C.c_int), C.POINTER(C.c_int)]
+        L.orc_jaccard.restype = None
+        L.orc_match.argtypes = [C.POINTER(MatchIn), _I, _F, _U8]
+        for f in (L.orc_small_head, L.orc_partition, L.orc_hybrid_head, L.orc_step,
+                  L.orc_match_scores, L.orc_topk, L.orc_match):
             f.restype = C.c_int
         _lib = L
     return _lib
@@ -221,3 +245,62 @@ def step(*, seq_len, k_crit, k_marg, kc_cap, km_cap, head_map, mode,
     out["marg"] = out["marg"][..., :km_cap]
     out["marg_prob"] = out["marg_prob"][..., :km_cap]
     return out
+
+
+# ------------------------------------------------------- prefill matching --
+
+def exp32(x):
+    """orc_exp elementwise over a float32 array."""
+    x = _f32(x)
+    y = np.empty_like(x)
+    lib().orc_exp_n(x.size, _p(x, _F), _p(y, _F))
+    return y
+
+
+def match_scores(Q, K, scale):
+    """Eq. 1 column sums F [w] (float32) of one head's causal prefill attention."""
+    Q, K = _f32(Q), _f32(K)
+    w, d = Q.shape
+    F = np.empty(w, np.float32)
+    _check(lib().orc_match_scores(w, d, C.c_float(scale), _p(Q, _F), _p(K, _F), _p(F, _F)),
+           "orc_match_scores")
+    return F
+
+
+def topk_set(F, k):
+    """TopK of Eq. 2 as a bool array (ties to the lower index)."""
+    F = _f32(F)
+    t = np.empty(F.size, np.uint8)
+    _check(lib().orc_topk(F.size, int(k), _p(F, _F), _p(t, _U8)), "orc_topk")
+    return t.astype(bool)
+
+
+def jaccard(a, b):
+    """Eq. 2 as the integer pair (|A n B|, |A u B|)."""
+    a = np.ascontiguousarray(a, np.uint8)
+    b = np.ascontiguousarray(b, np.uint8)
+    n, d = C.c_int(), C.c_int()
+    lib().orc_jaccard(a.size, _p(a, _U8), _p(b, _U8), C.byref(n), C.byref(d))
+    return n.value, d.value
+
+
+def match(*, win_len, top_k, l_q, l_k, l_scale, s_q, s_k, s_scale):
+    """Eq. 3 per sequence.  l_q [B,L,Hq,w_cap,d], l_k [B,L,Hk,w_cap,d] and the
+    small model's likewise.  Returns (head_map [B,L*Hq] int32, scores
+    [B,L*Hq+l*Hqs,w_cap] float32, top [B,L*Hq+l*Hqs,w_cap] bool); entries at
+    or beyond a sequence's window are 0."""
+    l_q, l_k, s_q, s_k = map(_f32, (l_q, l_k, s_q, s_k))
+    win_len, top_k = _i32(win_len), _i32(top_k)
+    B, L, hq, w_cap, d = l_q.shape
+    hk = l_k.shape[2]
+    _, l, hqs, _, ds = s_q.shape
+    hks = s_k.shape[2]
+    H = L * hq + l * hqs
+    hm = np.empty((B, L * hq), np.int32)
+    scores = np.zeros((B, H, w_cap), np.float32)
+    top = np.zeros((B, H, w_cap), np.uint8)
+    mi = MatchIn(B, w_cap, _p(win_len, _I), _p(top_k, _I),
+                 Window(L, hq, hk, d, l_scale, _p(l_q, _F), _p(l_k, _F)),
+                 Window(l, hqs, hks, ds, s_scale, _p(s_q, _F), _p(s_k, _F)))
+    _check(lib().orc_match(C.byref(mi), _p(hm, _I), _p(scores, _F), _p(top, _U8)), "orc_match")
+    return hm, scores, top.astype(bool)

@@ -9,11 +9,14 @@
  * HIP library under paper_2508_02751_amd/csrc.
  *
  * Precision: the ranking key (a small-model logit) is an fp32 value with one
- * defined evaluation order (see orc_logit); everything else is fp64.
+ * defined evaluation order (see orc_logit); everything else in the decode
+ * step is fp64.  The prefill matching (match_oracle.c) is fp32 throughout,
+ * in one defined order, because its fp32 sums decide integer outcomes.
  *
  * Paper passages followed:
  *   - Method section, "Similarity Matching": attention rows A = softmax(QK^T/sqrt(d_h)),
- *     accumulative score F (Eq. 1) and the head map f(i) (Eq. 3);
+ *     accumulative score F (Eq. 1), the Jaccard similarity of TopK sets
+ *     (Eq. 2) and the head map f(i) (Eq. 3);
  *   - "Saliency Shift Compensation": eviction keeps the top-scored tokens (Eq. 4)
  *     and selection is made from the small model's full cache;
  *   - "Marginal Information Compensation": the compensated row A* (Eq. 6), with
@@ -128,6 +131,44 @@ typedef struct {
 } orc_step_out;
 
 int orc_step(const orc_step_in *in, const orc_step_out *out);
+
+/* ---- prefill similarity matching (Eqs. 1-3), match_oracle.c ---- */
+
+/* exp(x) for x <= 0 by Cody-Waite reduction and a degree-7 Taylor polynomial
+ * (all steps in match_oracle.c); 0 below -80. */
+float orc_exp(float x);
+void orc_exp_n(int n, const float *x, float *y);
+
+/* Eq. 1 over a w-token window with the causal prefill mask: F_v = sum over
+ * rows u >= v of softmax_u(logits)[v].  Q, K: [w][d]; F: [w]. */
+int orc_match_scores(int w, int d, float scale, const float *Q, const float *K, float *F);
+
+/* TopK of Eq. 2 with ties to the lower index: in_top[v] in {0, 1}. */
+int orc_topk(int w, int k, const float *F, uint8_t *in_top);
+
+/* Eq. 2 as the integer pair |A n B|, |A u B|. */
+void orc_jaccard(int w, const uint8_t *a, const uint8_t *b, int *num, int *den);
+
+/* One model's prefill operands over the matching window (fp32 host arrays):
+ *   q [B][layers][q_heads][w_cap][dim], k [B][layers][kv_heads][w_cap][dim]. */
+typedef struct {
+  int32_t layers, q_heads, kv_heads, dim;
+  float scale;
+  const float *q, *k;
+} orc_window;
+
+typedef struct {
+  int32_t batch, w_cap;
+  const int32_t *win_len; /* [B] window tokens, clamped to [1, w_cap] */
+  const int32_t *top_k;   /* [B] K of Eq. 2, clamped to [1, window] */
+  orc_window large, small;
+} orc_match_in;
+
+/* Eq. 3 for every sequence: head_map [B][L*Hq] = argmax over the l*Hq_s small
+ * heads (lowest on ties).  Optional outputs (NULL to skip), rows of
+ * [B][L*Hq + l*Hq_s][w_cap], large heads first, entries >= window untouched:
+ * scores = F of Eq. 1, top = the TopK sets (0/1 bytes). */
+int orc_match(const orc_match_in *in, int32_t *head_map, float *scores, uint8_t *top);
 
 #ifdef __cplusplus
 }
