@@ -15,6 +15,10 @@ the host never starves the GPU) gives per-stage kernel durations for the
 roofline.  The CPU baseline is the oracle on one host core over whole steps.
 
 Prints one JSON line.
+
+`--match` benchmarks the prefill similarity matching instead (Eqs. 1-3: the
+step before decoding that computes the head map): the Qwen2-7B + Qwen2-0.5B
+shapes over a 200-token window, one JSON line of its own.
 """
 from __future__ import annotations
 
@@ -29,6 +33,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, 8 TB/s
+FP32_VECTOR_PEAK_TFLOPS = 157.3  # MI355X fp32 vector (packed FMA counted as 4 flops)
 
 
 def parse():
@@ -42,6 +47,10 @@ def parse():
     p.add_argument("--eager", action="store_true", help="launch without HIP graphs")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time budget")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--match", action="store_true",
+                   help="benchmark the prefill head matching instead of the decode step")
+    p.add_argument("--match-batch", type=int, default=1)
+    p.add_argument("--match-window", type=int, default=200)
     p.add_argument("--copy-probe-mib", type=int, default=0,
                    help="first run a plain device copy of this many MiB (counter calibration)")
     return p.parse_args()
@@ -104,6 +113,8 @@ def main():
               "(see the sharding section of DESIGN.md), so --gpus must be 1", file=sys.stderr)
         sys.exit(2)
 
+    if args.match:
+        return bench_match(args)
     import torch
     from paper_2508_02751_amd import smallkv as S
     from paper_2508_02751_amd import workloads as W
@@ -272,6 +283,110 @@ def main():
             / max(1, sb.large_k_union + sb.large_v_union),
             "index_metadata_bytes": sb.index_meta,
         },
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def bench_match(args):
+    """The prefill similarity matching on the Qwen2-7B + Qwen2-0.5B shapes."""
+    import dataclasses
+
+    import torch
+    from paper_2508_02751_amd import workloads as W
+    from paper_2508_02751_amd.pipeline import prepare_match, softmax_scale
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = dataclasses.replace(W.WORKLOADS[2], batch=args.match_batch)
+    win = args.match_window
+    print(f"[bench] generating the {win}-token matching window", file=sys.stderr, flush=True)
+    x = W.match_inputs(w, win, dev)
+    mc = prepare_match(x, scores=False, top_bits=False)
+    stream = torch.cuda.current_stream()
+    for _ in range(max(args.warmup, 1)):
+        mc.run()
+    torch.cuda.synchronize()
+    g = None
+    if not args.eager:
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            mc.run()
+        g.replay()
+        torch.cuda.synchronize()
+    K = args.steps
+    t0 = time.perf_counter()
+    for _ in range(K):
+        g.replay() if g is not None else mc.run()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / K
+    # the matching call's kernels, timed with HIP events on their stream
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(K)]
+    torch.cuda._sleep(50_000_000)
+    for e0, e1 in ev:
+        e0.record(stream)
+        mc.run(stream)
+        e1.record(stream)
+    torch.cuda.synchronize()
+    call_ms = sum(a.elapsed_time(b) for a, b in ev) / K
+    # algorithmic flops: one d-long FMA chain (2 flops per term) per causal logit
+    heads = [(w.large.layers * w.large.q_heads, w.large.head_dim),
+             (w.small.layers * w.small.q_heads, w.small.head_dim)]
+    flops = w.batch * sum(n * d * win * (win + 1) for n, d in heads)
+    achieved = flops / (call_ms * 1e-3) / 1e12
+    cpu = None
+    if not args.no_cpu_baseline:
+        sys.path.insert(0, os.path.join(ROOT, "oracle"))
+        import oracle as O
+
+        def h(t):
+            return t.detach().float().cpu().numpy() if t.dtype == torch.bfloat16 else t.cpu().numpy()
+
+        hx = {k: h(v) for k, v in x.items()}
+        try:
+            os.sched_setaffinity(0, {sorted(os.sched_getaffinity(0))[0]})
+        except (AttributeError, OSError):
+            pass
+        print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
+        c0 = time.perf_counter()
+        O.match(win_len=hx["win_len"], top_k=hx["top_k"], l_q=hx["l_q"], l_k=hx["l_k"],
+                l_scale=softmax_scale(w.large.head_dim), s_q=hx["s_q"], s_k=hx["s_k"],
+                s_scale=softmax_scale(w.small.head_dim))
+        spent = time.perf_counter() - c0
+        cpu = {"value": w.batch / spent, "unit": "sequences/s", "cores": 1, "kind": "oracle",
+               "sample": f"one whole matching of the same {w.batch} window(s), single-threaded "
+                         f"C oracle pinned to one core ({spent:.1f} s)"}
+    out = {
+        "metric": "SmallKV prefill head matching (Eqs. 1-3) sequences/s at 1 MI355X",
+        "value": w.batch * 1e3 / ms,
+        "unit": "sequences/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": f"qwen2-7b+0.5b-prefill-window{win}-b{w.batch}-bf16",
+            "large": shape_text(w.large), "small": shape_text(w.small),
+            "input_dtype": "bf16", "batch": w.batch, "window": win,
+            "top_k": int(x["top_k"][0]), "launch": "eager" if args.eager else "hip-graph",
+        },
+        "roofline": {
+            "kernel": "match_logits+match_scores+match_map",
+            "bound": "alu",
+            "achieved": achieved,
+            "peak": FP32_VECTOR_PEAK_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": achieved / FP32_VECTOR_PEAK_TFLOPS,
+            "traffic": None,
+        },
+        "call_ms": call_ms,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

@@ -52,7 +52,7 @@
 extern "C" {
 #endif
 
-#define SMALLKV_ABI_VERSION 2
+#define SMALLKV_ABI_VERSION 3
 
 typedef enum { SMALLKV_F32 = 0, SMALLKV_BF16 = 1 } smallkv_dtype_t;
 
@@ -188,6 +188,71 @@ int smallkv_step(const smallkv_step_t *step, void *ws, size_t ws_bytes, void *st
 /* Bytes of workspace that smallkv_step needs for `step`; the single-stage
  * calls need no more than this for the same shapes.  Host only. */
 int smallkv_workspace_size(const smallkv_step_t *step, size_t *bytes);
+
+/* ---------------------------------------------------------------------------
+ * Prefill similarity matching (Method section, "Similarity Matching",
+ * Eqs. 1-3; Algorithm 1, prefill branch): computes the head map f that the
+ * decode step takes as head_map.
+ *
+ * For each sequence b, over a window of its first w_b prompt tokens, and for
+ * every head of both models (large heads i = layer*n_q_heads + h first, then
+ * small heads at L*Hq + j):
+ *   A      = the causal prefill attention of the window: row u is the softmax
+ *            over tokens v <= u of the logits s[u][v]
+ *   F_v    = sum over rows u of A[u][v]                               (Eq. 1)
+ *   TopK   = the k_b tokens of largest F (equal F: lower token first)
+ *   S(i,j) = |TopK_i n TopK'_j| / |TopK_i u TopK'_j|                  (Eq. 2)
+ *   head_map[b][i] = argmax over every small head j of S(i, j),
+ *                    the lowest j on ties                             (Eq. 3)
+ * The TopK sets and the argmax are integer decisions taken on fp32 values,
+ * so every value has one defined evaluation and the result is exact and
+ * deterministic:
+ *   s[u][v] = the fp32 logit of the conventions above (FMA chain, then scale)
+ *   m_u     = max over v <= u of s[u][v]
+ *   e[u][v] = exp32(s[u][v] - m_u), fp32 subtraction, with exp32(x) for
+ *             x <= 0 defined as: k = rne(x * 0x1.715476p+0), r = fma(-k,
+ *             0x1.62e4p-1, x), r = fma(-k, 0x1.7f7d1cp-20, r), then Horner's
+ *             rule p = fma(p, r, c) from p = 0x1.a01a02p-13 through
+ *             c = 0x1.6c16c2p-10, 0x1.111112p-7, 0x1.555556p-5,
+ *             0x1.555556p-3, 0.5, 1, 1 (the Taylor coefficients 1/n!), result
+ *             p * 2^k; exp32(x) = 0 for x < -80.  Within 1 ulp of exp.
+ *   Z_u     = ((e[u][0] + e[u][1]) + ...) + e[u][u]            (fp32 adds)
+ *   F_v     = ((p[v][v] + p[v+1][v]) + ...) + p[w-1][v],  p[u][v] = e[u][v] / Z_u
+ *             (correctly rounded fp32 division and adds)
+ *   S(i,j) compared as exact integer fractions.
+ * The paper matches on 100 to 200 prompt tokens, delaying the matching of a
+ * shorter prompt and truncating a longer one ("Method Details"); choosing
+ * w_b is the caller's (the window is the prompt's first w_b tokens). */
+
+/* One model's operands over the window.  q and k must be 16-byte aligned. */
+typedef struct {
+  int32_t n_layers, n_q_heads, n_kv_heads; /* as in smallkv_model_t */
+  int32_t head_dim;   /* 64 or 128 */
+  int32_t dtype;      /* smallkv_dtype_t of q and k */
+  float scale;        /* softmax scale, normally 1/sqrt(head_dim) */
+  const void *q;      /* [B][n_layers][n_q_heads][w_cap][head_dim] */
+  const void *k;      /* [B][n_layers][n_kv_heads][w_cap][head_dim] */
+} smallkv_window_t;
+
+typedef struct {
+  int32_t batch;            /* B, 1..65535 */
+  int32_t w_cap;            /* window capacity, 1..256 (host) */
+  const int32_t *win_len;   /* [B] window tokens w_b, clamped to [1, w_cap] on device */
+  const int32_t *top_k;     /* [B] K of Eq. 2, clamped to [1, w_b] on device */
+  smallkv_window_t large, small;
+  int32_t *head_map;        /* out [B][large.n_layers*large.n_q_heads]: small head ids */
+  float *scores;            /* optional out (NULL: skipped) [B][H][w_cap] F of Eq. 1,
+                               H = L*Hq + l*Hq_s; entries v >= w_b not written */
+  uint64_t *top_bits;       /* optional out [B][H][(w_cap+63)/64]: bit v%64 of word v/64
+                               set iff token v is in the head's TopK set */
+} smallkv_match_t;
+
+/* Bytes of workspace smallkv_match needs: two fp32 [B][H][w_cap][w_cap]
+ * logit matrices plus the TopK bitsets.  Host only. */
+int smallkv_match_workspace_size(const smallkv_match_t *match, size_t *bytes);
+
+/* Enqueues the matching on `stream` (four kernel launches). */
+int smallkv_match(const smallkv_match_t *match, void *ws, size_t ws_bytes, void *stream);
 
 /* A static string for a status code. */
 const char *smallkv_status_string(int status);

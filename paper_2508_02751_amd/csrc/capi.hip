@@ -86,6 +86,32 @@ hipError_t launch_stage3(const smallkv_batch_t &b, const smallkv_model_t &l, con
   return launch_hybrid(b, l, head_map, nsh, crit, marg, marg_prob, mass, mode, st);
 }
 
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+int check_window(const smallkv_window_t &m) {
+  if (!m.q || !m.k || m.n_layers < 1 || m.n_q_heads < 1 || m.n_kv_heads < 1) return SMALLKV_EINVAL;
+  if (m.n_q_heads % m.n_kv_heads) return SMALLKV_EINVAL;
+  if (m.dtype != SMALLKV_F32 && m.dtype != SMALLKV_BF16) return SMALLKV_EINVAL;
+  if (!(m.scale == m.scale)) return SMALLKV_EINVAL;
+  if (!aligned16(m.q) || !aligned16(m.k)) return SMALLKV_EINVAL;
+  if (m.head_dim != 64 && m.head_dim != 128) return SMALLKV_EUNSUPPORTED;
+  if ((int64_t)m.n_layers * m.n_q_heads > 65535) return SMALLKV_EUNSUPPORTED;
+  return SMALLKV_OK;
+}
+
+int check_match(const smallkv_match_t *m) {
+  if (!m || !m->win_len || !m->top_k || !m->head_map) return SMALLKV_EINVAL;
+  if (m->batch < 1 || m->w_cap < 1) return SMALLKV_EINVAL;
+  if (m->batch > 65535 || m->w_cap > 256) return SMALLKV_EUNSUPPORTED;
+  int rc = check_window(m->large);
+  if (rc) return rc;
+  if ((rc = check_window(m->small))) return rc;
+  const int64_t H = (int64_t)m->large.n_layers * m->large.n_q_heads +
+                    (int64_t)m->small.n_layers * m->small.n_q_heads;
+  if (H > 65535) return SMALLKV_EUNSUPPORTED;
+  return SMALLKV_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -160,6 +186,21 @@ int smallkv_hybrid_attn(const smallkv_batch_t *batch, const smallkv_model_t *lar
   return status_of(launch_stage3(*batch, *large, head_map, n_small_heads, crit_idx, marg_idx,
                                  marg_prob, mass, mode, ws, nullptr,
                                  static_cast<hipStream_t>(stream)));
+}
+
+int smallkv_match_workspace_size(const smallkv_match_t *m, size_t *bytes) {
+  if (!bytes) return SMALLKV_EINVAL;
+  const int rc = check_match(m);
+  if (rc) return rc;
+  *bytes = match_layout(*m).total;
+  return SMALLKV_OK;
+}
+
+int smallkv_match(const smallkv_match_t *m, void *ws, size_t ws_bytes, void *stream) {
+  const int rc = check_match(m);
+  if (rc) return rc;
+  if (!ws || ws_bytes < match_layout(*m).total) return SMALLKV_EWORKSPACE;
+  return status_of(launch_match(*m, ws, static_cast<hipStream_t>(stream)));
 }
 
 int smallkv_step(const smallkv_step_t *s, void *ws, size_t ws_bytes, void *stream) {

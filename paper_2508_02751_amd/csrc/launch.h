@@ -70,6 +70,18 @@ hipError_t launch_hybrid_group(const smallkv_batch_t &b, const smallkv_model_t &
                                int mode, const GroupPlan &p, float *ws, const int2 *tab,
                                hipStream_t st);
 
+// Workspace of the prefill matching: the logit matrix S of every head
+// ([B][H][w_cap][ld] fp32, ld = w_cap rounded up to 4), the row maxima per
+// 64-token tile column ([B][H][w_cap][nt] fp32), each row's (max, sum)
+// ([B][H][w_cap] float2), then the TopK bitsets ([B][H][nw] words of 64
+// tokens).
+struct MatchLayout {
+  int nw, nt, ld;
+  size_t pmax_offset, mz_offset, bits_offset, total;
+};
+MatchLayout match_layout(const smallkv_match_t &m);
+hipError_t launch_match(const smallkv_match_t &m, void *ws, hipStream_t st);
+
 hipError_t launch_hybrid(const smallkv_batch_t &b, const smallkv_model_t &m,
                          const int32_t *head_map, int n_small_heads, const int32_t *crit,
                          const int32_t *marg, const float *marg_prob, const float *mass,

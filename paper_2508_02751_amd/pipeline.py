@@ -16,6 +16,25 @@ import torch
 from . import smallkv as S
 
 
+MATCH_MIN, MATCH_MAX = 100, 200  # prompt tokens the matching uses ("Method Details")
+
+
+def match_window(prompt_len: int) -> Optional[int]:
+    """Window of the prefill matching for a prompt: None (delay the matching
+    until the context reaches MATCH_MIN tokens) below MATCH_MIN, else the
+    first min(prompt_len, MATCH_MAX) tokens (a longer prompt is truncated)."""
+    if prompt_len < MATCH_MIN:
+        return None
+    return min(prompt_len, MATCH_MAX)
+
+
+def prepare_match(x: dict, scores: bool = True, top_bits: bool = True) -> S.MatchCall:
+    """smallkv_match over the window operands produced by workloads.match_inputs."""
+    return S.prepare_match(x["win_len"], x["top_k"], x["l_q"], x["l_k"],
+                           softmax_scale(x["l_q"].shape[-1]), x["s_q"], x["s_k"],
+                           softmax_scale(x["s_q"].shape[-1]), scores, top_bits)
+
+
 def softmax_scale(head_dim: int) -> float:
     return float(torch.tensor(1.0 / math.sqrt(head_dim), dtype=torch.float32))
 

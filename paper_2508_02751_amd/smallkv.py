@@ -7,7 +7,8 @@ is no fallback: if the library is not built, or a call fails, this module
 raises.
 
 Entry points mirror the C names: smallkv_small_attn, smallkv_partition,
-smallkv_hybrid_attn, smallkv_step, smallkv_workspace_size.
+smallkv_hybrid_attn, smallkv_step, smallkv_workspace_size, and the prefill
+matching smallkv_match, smallkv_match_workspace_size.
 """
 from __future__ import annotations
 
@@ -48,8 +49,21 @@ class Step(C.Structure):
                 ("marg_prob", C.c_void_p), ("mass", C.c_void_p)]
 
 
+class Window(C.Structure):
+    _fields_ = [("n_layers", C.c_int32), ("n_q_heads", C.c_int32), ("n_kv_heads", C.c_int32),
+                ("head_dim", C.c_int32), ("dtype", C.c_int32), ("scale", C.c_float),
+                ("q", C.c_void_p), ("k", C.c_void_p)]
+
+
+class Match(C.Structure):
+    _fields_ = [("batch", C.c_int32), ("w_cap", C.c_int32), ("win_len", C.c_void_p),
+                ("top_k", C.c_void_p), ("large", Window), ("small", Window),
+                ("head_map", C.c_void_p), ("scores", C.c_void_p), ("top_bits", C.c_void_p)]
+
+
 EXPORTS = ("smallkv_small_attn", "smallkv_partition", "smallkv_hybrid_attn", "smallkv_step",
-           "smallkv_workspace_size", "smallkv_status_string", "smallkv_abi_version")
+           "smallkv_workspace_size", "smallkv_match", "smallkv_match_workspace_size",
+           "smallkv_status_string", "smallkv_abi_version")
 
 _lib = None
 
@@ -72,11 +86,14 @@ def lib():
                                           C.c_void_p, C.c_size_t, C.c_void_p]
         L.smallkv_step.argtypes = [P(Step), C.c_void_p, C.c_size_t, C.c_void_p]
         L.smallkv_workspace_size.argtypes = [P(Step), P(C.c_size_t)]
+        L.smallkv_match.argtypes = [P(Match), C.c_void_p, C.c_size_t, C.c_void_p]
+        L.smallkv_match_workspace_size.argtypes = [P(Match), P(C.c_size_t)]
         L.smallkv_status_string.argtypes = [C.c_int]
         L.smallkv_status_string.restype = C.c_char_p
         L.smallkv_abi_version.argtypes = []
         for f in ("smallkv_small_attn", "smallkv_partition", "smallkv_hybrid_attn",
-                  "smallkv_step", "smallkv_workspace_size", "smallkv_abi_version"):
+                  "smallkv_step", "smallkv_workspace_size", "smallkv_abi_version",
+                  "smallkv_match", "smallkv_match_workspace_size"):
             getattr(L, f).restype = C.c_int
         _lib = L
     return _lib
@@ -254,3 +271,53 @@ def alloc_step_buffers(batch: BatchSpec, s_q: torch.Tensor, l_q: torch.Tensor,
         large_out=torch.empty_like(l_q),
         ws=torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev) if ws_bytes else None,
     )
+
+
+# ------------------------------------------------------- prefill matching --
+
+def window_spec(q: torch.Tensor, k: torch.Tensor, scale: float) -> Window:
+    """One model's window operands: q [B][layers][Hq][w_cap][d], k [B][layers][Hkv][w_cap][d]."""
+    if q.dim() != 5 or k.dim() != 5 or q.dtype != k.dtype:
+        raise ValueError("window q/k must be 5-d tensors of one dtype")
+    _, layers, hq, _, d = q.shape
+    return Window(layers, hq, k.shape[2], d, _dtype_code(q), scale, _ptr(q), _ptr(k))
+
+
+@dataclasses.dataclass
+class MatchCall:
+    """A prepared smallkv_match descriptor and the tensors it points at."""
+    desc: Match
+    head_map: torch.Tensor          # [B][L*Hq] int32
+    scores: Optional[torch.Tensor]  # [B][H][w_cap] fp32
+    top_bits: Optional[torch.Tensor]  # [B][H][nw] int64 (bit patterns of uint64 words)
+    ws: torch.Tensor
+    keep: tuple
+
+    def run(self, stream=None):
+        smallkv_match(self.desc, self.ws, stream)
+
+
+def prepare_match(win_len: torch.Tensor, top_k: torch.Tensor, l_q, l_k, l_scale, s_q, s_k,
+                  s_scale, scores=True, top_bits=True) -> MatchCall:
+    """Descriptor, outputs and workspace for smallkv_match over the given windows."""
+    for t in (win_len, top_k):
+        if t.dtype != torch.int32:
+            raise ValueError("win_len and top_k must be int32")
+    B, L, hq, w_cap, _ = l_q.shape
+    H = L * hq + s_q.shape[1] * s_q.shape[2]
+    dev = l_q.device
+    hm = torch.empty((B, L * hq), dtype=torch.int32, device=dev)
+    sc = torch.zeros((B, H, w_cap), dtype=torch.float32, device=dev) if scores else None
+    nw = (w_cap + 63) // 64
+    tb = torch.zeros((B, H, nw), dtype=torch.int64, device=dev) if top_bits else None
+    d = Match(B, w_cap, _ptr(win_len), _ptr(top_k), window_spec(l_q, l_k, l_scale),
+              window_spec(s_q, s_k, s_scale), _ptr(hm), _ptr(sc), _ptr(tb))
+    n = C.c_size_t()
+    _check("smallkv_match_workspace_size", lib().smallkv_match_workspace_size(C.byref(d), C.byref(n)))
+    ws = torch.empty(max(n.value, 1), dtype=torch.uint8, device=dev)
+    return MatchCall(d, hm, sc, tb, ws, (win_len, top_k, l_q, l_k, s_q, s_k))
+
+
+def smallkv_match(desc: Match, ws, stream=None):
+    w, wb = _ws(ws)
+    _check("smallkv_match", lib().smallkv_match(C.byref(desc), w, wb, _stream(stream)))

@@ -23,6 +23,13 @@ synthetic padded prompts):
     budget critical : recent : marginal = 2 : 1 : 2, as in the paper's
     experimental setup (its 20% example: 10%, 5%, 10%).
 
+Prefill matching window (match_inputs): the first w_cap prompt tokens of
+the same latents; keys as above with the cache's projections W_g and their
+own noise; query head h of kv head g projects with W_g + 0.5 E_h (E_h iid
+N(0,1), so that heads of one group differ) plus 0.1 noise, over sqrt(d);
+TopK budget 10% of the window (at least 1), the critical share of the
+step workloads.
+
 Seeds: base 1000 + workload id; each named tensor has its own generator
 seeded from (base, tag) through crc32, so any tensor can be regenerated alone.
 """
@@ -266,4 +273,45 @@ def make_step_inputs(w: Workload, device, step: int = 0, *, z=None, large=True):
         out["k_recent"] = kr.to(device)
     out["head_map"] = head_map(w, device)
     out["kc_cap"], out["km_cap"] = caps(w)
+    return out
+
+
+def match_inputs(w: Workload, w_cap: int, device, win_len=None, top_pct: int = 10):
+    """Prefill operands of both models over the first w_cap prompt tokens.
+
+    Returns l_q [B][L][Hq][w_cap][d], l_k [B][L][Hk][w_cap][d], s_q, s_k (same
+    for the small model), win_len [B] int32 (w_cap when not given) and top_k
+    [B] int32 = max(1, win_len * top_pct // 100).
+    """
+    z = latents(w, device)[:, :w_cap]
+    heavy = heavy_positions(w, device)
+    base = 1000 + w.wid
+    gain = torch.ones((w.batch, w_cap), device=device)
+    gain[:, : w.sinks] = w.sink_gain
+    if heavy is not None:
+        gain = torch.where(heavy[:, :w_cap], torch.full_like(gain, w.heavy_gain), gain)
+    out = {}
+    for which, m, pre in (("large", w.large, "l"), ("small", w.small, "s")):
+        d = m.head_dim
+        qs, ks = [], []
+        for layer in range(m.layers):
+            W = _randn((m.kv_heads, LATENT, d), base, f"{which}/W/{layer}", device)
+            k = torch.einsum("bnz,hzd->bhnd", z, W)
+            k += 0.1 * _randn(k.shape, base, f"prefill/{which}/keps/{layer}", device)
+            k /= d ** 0.5
+            k *= gain[:, None, :, None]
+            E = _randn((m.q_heads, LATENT, d), base, f"prefill/{which}/E/{layer}", device)
+            Wq = W.repeat_interleave(m.group, dim=0) + 0.5 * E
+            q = torch.einsum("bnz,hzd->bhnd", z, Wq)
+            q += 0.1 * _randn(q.shape, base, f"prefill/{which}/qeps/{layer}", device)
+            q /= d ** 0.5
+            qs.append(q.to(w.torch_dtype))
+            ks.append(k.to(w.torch_dtype))
+        out[f"{pre}_q"] = torch.stack(qs, 1).contiguous()
+        out[f"{pre}_k"] = torch.stack(ks, 1).contiguous()
+    if win_len is None:
+        win_len = [w_cap] * w.batch
+    win = torch.tensor(win_len, dtype=torch.int32)
+    out["win_len"] = win.to(device)
+    out["top_k"] = torch.clamp(win * top_pct // 100, min=1).to(torch.int32).to(device)
     return out

@@ -33,7 +33,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_abi_version_and_status_strings():
     L = S.lib()
-    assert L.smallkv_abi_version() == 2
+    assert L.smallkv_abi_version() == 3
     assert L.smallkv_status_string(0) == b"ok"
     assert L.smallkv_status_string(-3) == b"workspace too small"
     assert L.smallkv_status_string(123) == b"unknown status"
@@ -42,7 +42,8 @@ def test_abi_version_and_status_strings():
 def _fake_step(**over):
     """A descriptor with plausible (never dereferenced) pointers."""
     p = 0x1000
-    b = S.Batch(1, 512, p, p, p, 64, 128)
+    b = S.Batch(batch=1, n_cap=512, seq_len=p, k_crit=p, k_marg=p, k_recent=None, kc_cap=64,
+                km_cap=128)
     sm = S.Model(1, 14, 2, 64, S.BF16, 0.125, p, p, p, 512, None, None, p)
     lg = S.Model(1, 28, 4, 128, S.BF16, 0.088, p, p, p, 512, None, None, p)
     st = S.Step(b, sm, lg, p, 0, p, p, p, p, p, p, p)
@@ -93,9 +94,58 @@ def test_step_needs_workspace():
 
 
 def test_partition_and_hybrid_reject_nulls():
-    b = S.Batch(1, 512, 0x1000, 0x1000, 0x1000, 64, 128)
+    b = S.Batch(batch=1, n_cap=512, seq_len=0x1000, k_crit=0x1000, k_marg=0x1000, k_recent=None,
+                kc_cap=64, km_cap=128)
     L = S.lib()
     assert L.smallkv_partition(C.byref(b), 14, None, 1, 1, 1, 1, 1, 1, None, 0, None) == S.EINVAL
     lg = S.Model(1, 28, 4, 128, S.BF16, 0.088, 1, 1, 1, 512, None, None, 1)
     assert L.smallkv_hybrid_attn(C.byref(b), C.byref(lg), None, 14, 1, 1, 1, 1, 0, None, 0,
                                  None) == S.EINVAL
+
+
+def _fake_match(**over):
+    """A matching descriptor with plausible (never dereferenced) 16-byte aligned pointers."""
+    p = 0x1000
+    lg = S.Window(28, 28, 4, 128, S.BF16, 0.088, p, p)
+    sm = S.Window(24, 14, 2, 64, S.BF16, 0.125, p, p)
+    m = S.Match(1, 200, p, p, lg, sm, p, None, None)
+    for k, v in over.items():
+        obj, field = k.split("__")
+        setattr({"m": m, "l": m.large, "s": m.small}[obj], field, v)
+    return m
+
+
+def test_header_declares_the_matching_calls():
+    names = declared_functions()
+    assert "smallkv_match" in names and "smallkv_match_workspace_size" in names
+
+
+@pytest.mark.parametrize("over,status", [
+    ({"m__w_cap": 0}, S.EINVAL),
+    ({"m__w_cap": 257}, S.EUNSUPPORTED),
+    ({"m__batch": 0}, S.EINVAL),
+    ({"m__win_len": None}, S.EINVAL),
+    ({"m__top_k": None}, S.EINVAL),
+    ({"m__head_map": None}, S.EINVAL),
+    ({"l__head_dim": 96}, S.EUNSUPPORTED),
+    ({"s__n_kv_heads": 3}, S.EINVAL),
+    ({"s__dtype": 5}, S.EINVAL),
+    ({"l__q": 0x1004}, S.EINVAL),               # not 16-byte aligned
+    ({"s__k": None}, S.EINVAL),
+    ({"l__n_layers": 3000}, S.EUNSUPPORTED),    # more heads than one grid dimension
+])
+def test_match_rejects_before_launch(over, status):
+    m = _fake_match(**over)
+    n = C.c_size_t()
+    assert S.lib().smallkv_match_workspace_size(C.byref(m), C.byref(n)) == status
+    assert S.lib().smallkv_match(C.byref(m), C.c_void_p(0x1000), 1 << 40, None) == status
+
+
+def test_match_workspace_size_and_check():
+    m = _fake_match()
+    n = C.c_size_t()
+    assert S.lib().smallkv_match_workspace_size(C.byref(m), C.byref(n)) == 0
+    H = 28 * 28 + 24 * 14
+    assert n.value >= 2 * H * 200 * 200 * 4 + H * 4 * 8
+    assert S.lib().smallkv_match(C.byref(m), None, 0, None) == S.EWORKSPACE
+    assert S.lib().smallkv_match(C.byref(m), C.c_void_p(0x1000), n.value - 1, None) == S.EWORKSPACE

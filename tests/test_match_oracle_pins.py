@@ -209,3 +209,13 @@ def test_budget_and_window_clamps():
     hm2, s2, t2 = O.match(win_len=[24], top_k=[1], **x)
     assert np.array_equal(hm1, hm2) and np.array_equal(s1, s2) and np.array_equal(t1, t2)
     assert t1[0].sum(1).tolist() == [1] * t1.shape[1]
+
+
+# ------------------------------------------------------ window policy --
+
+def test_match_window_policy():
+    from paper_2508_02751_amd.pipeline import MATCH_MAX, MATCH_MIN, match_window
+    assert (MATCH_MIN, MATCH_MAX) == (100, 200)  # "Method Details": 100 to 200 tokens
+    assert match_window(99) is None              # too short: matching is delayed
+    assert match_window(100) == 100 and match_window(173) == 173
+    assert match_window(200) == 200 and match_window(8192) == 200  # truncated
