@@ -378,7 +378,7 @@ def bench_match(args):
             "top_k": int(x["top_k"][0]), "launch": "eager" if args.eager else "hip-graph",
         },
         "roofline": {
-            "kernel": "match_logits+match_scores+match_map",
+            "kernel": "match_logits+match_rowsum+match_scores+match_map",
             "bound": "alu",
             "achieved": achieved,
             "peak": FP32_VECTOR_PEAK_TFLOPS,

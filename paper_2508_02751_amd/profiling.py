@@ -36,6 +36,10 @@ KERNEL_SOURCES = {
     "hybrid_kernel": "hybrid.hip",
     "hybrid_group_kernel": "hybrid_group.hip",
     "hybrid_group_merge": "hybrid_group.hip",
+    "match_logits": "match.hip",
+    "match_rowsum": "match.hip",
+    "match_scores": "match.hip",
+    "match_map": "match.hip",
 }
 
 
