@@ -17,7 +17,8 @@ synthetic padded prompts):
     models; optionally a seeded set of "heavy hitter" positions gets keys x4;
   * values V ~ N(0, 1); everything is rounded to the storage dtype (RNE);
   * the large-to-small head map f(layer, head) is iid uniform over the small
-    model's l*Hq_s heads;
+    model's l*Hq_s heads (with an early-stopped small model, over the heads
+    of the layers it runs);
   * budgets: a fixed count per sequence, or floor(N_b * pct / 100) of the
     sequence's current length N_b; workloads with recent tokens split the
     budget critical : recent : marginal = 2 : 1 : 2, as in the paper's
@@ -107,6 +108,11 @@ WORKLOADS = {
                 QWEN2_0_5B, QWEN2_72B, ("pct", 2), ("pct", 8), compact_large=True),
     6: Workload(6, "qwen2-7b+0.5b-n8192-b1-bf16-c10r5m10", 1, 8192, "bf16",
                 QWEN2_0_5B, QWEN2_7B, ("pct", 10), ("pct", 10), recent=("pct", 5)),
+    # the small model stopped after its first 20 of 24 layers (the stop with
+    # no accuracy loss in the paper's early-stop table): only those layers
+    # run, so only their KV exists and the head map ranges over their heads
+    7: Workload(7, "qwen2-7b+0.5b@20of24-n8192-b1-bf16", 1, 8192, "bf16",
+                dataclasses.replace(QWEN2_0_5B, layers=20), QWEN2_7B, ("pct", 10), ("pct", 20)),
 }
 
 LATENT = 64

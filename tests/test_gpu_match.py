@@ -39,6 +39,7 @@ def oracle_match(x):
 
 
 def check_match(x, what):
+    """Run both sides; return the oracle's head map after asserting the GPU's equals it."""
     _, _, prepare_match, _ = lib_modules()
     log(f"[match] {what}: GPU")
     mc = prepare_match(x)
@@ -136,3 +137,24 @@ def test_repeat_calls_are_identical():
     torch.cuda.synchronize()
     assert torch.equal(first[0], mc.head_map) and torch.equal(first[1], mc.scores)
     assert torch.equal(first[2], mc.top_bits)
+
+
+def test_matched_map_drives_an_early_stopped_step():
+    """Prefill matching over the small model's first 20 layers, then the
+    decode step with that map: the GPU map equals the oracle's, and the step
+    run with the oracle's map matches the oracle's step."""
+    import parity as P
+    from paper_2508_02751_amd.pipeline import prepare_step
+
+    _, W, _, _ = lib_modules()
+    w = W.WORKLOADS[7]
+    win = W.match_inputs(w, 200, DEV)
+    hm = check_match(win, "early-stopped small model, window 200")
+    assert hm.max() < w.small.layers * w.small.q_heads
+    x = W.make_step_inputs(w, DEV)
+    x["head_map"] = torch.from_numpy(hm[0].copy()).to(DEV)  # the oracle's map (equal to the GPU's)
+    ps = prepare_step(x)
+    ps.run()
+    torch.cuda.synchronize()
+    ref = P.oracle_step(x, P.O.NORM_REMAINING)
+    P.compare_step(ps.buf, ref, x, torch.bfloat16, "matched map, early stop")

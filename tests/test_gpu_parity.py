@@ -143,6 +143,15 @@ def test_recent_window_qwen2_7b_full_step():
     run_case(W.WORKLOADS[6])
 
 
+def test_early_stopped_small_model_full_step():
+    """The Qwen2-7B step with the small model stopped after 20 of its 24
+    layers: stages 1-2 run over 20 layers and the head map ranges over their
+    280 heads."""
+    w = W.WORKLOADS[7]
+    assert w.small.layers == 20 and int(W.head_map(w, "cpu").max()) < 20 * 14
+    run_case(w)
+
+
 def test_recent_window_with_ties():
     w = custom("recent-ties", 120, 2, 1500, "bf16", SMALL, LARGE, ("pct", 10), ("pct", 25),
                recent=("pct", 5))
