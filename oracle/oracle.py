@@ -51,6 +51,7 @@ class StepIn(C.Structure):
         ("s_layers", C.c_int32), ("s_q_heads", C.c_int32), ("s_kv_heads", C.c_int32), ("s_dim", C.c_int32),
         ("s_scale", C.c_float),
         ("s_q", _F), ("s_k", _F), ("s_v", _F),
+        ("s_rows", C.c_int64), ("s_held", _I), ("s_row_pos", _I),
         ("l_layers", C.c_int32), ("l_q_heads", C.c_int32), ("l_kv_heads", C.c_int32), ("l_dim", C.c_int32),
         ("l_scale", C.c_float),
         ("l_rows", C.c_int64),
@@ -204,24 +205,29 @@ def hybrid_head(q, K, V, crit, marg, marg_prob, mass, scale, mode=NORM_REMAINING
 
 def step(*, seq_len, k_crit, k_marg, kc_cap, km_cap, head_map, mode,
          s_q, s_k, s_v, s_scale, l_q, l_k, l_v, l_scale, k_slot=None, v_slot=None,
-         k_recent=None):
+         k_recent=None, s_held=None, s_row_pos=None, n_cap=None):
     """A whole decode step over the library layout (see smallkv_oracle.h).
 
-    Shapes: s_q [B,l,Hqs,ds], s_k/s_v [B,l,Hks,n_cap,ds], l_q [B,L,Hq,d],
-    l_k/l_v [B,L,Hk,n_rows,d], slots [B,L,Hk,n_cap] or None.
+    Shapes: s_q [B,l,Hqs,ds], s_k/s_v [B,l,Hks,n_cap,ds] (with the small
+    model's own eviction: [B,l,Hks,s_rows,ds] plus s_held [B] and s_row_pos
+    [B,l,Hks,s_rows], and n_cap given), l_q [B,L,Hq,d], l_k/l_v
+    [B,L,Hk,n_rows,d], slots [B,L,Hk,n_cap] or None.
     """
     s_q, s_k, s_v, l_q, l_k, l_v = map(_f32, (s_q, s_k, s_v, l_q, l_k, l_v))
     seq_len, k_crit, k_marg, head_map = map(_i32, (seq_len, k_crit, k_marg, head_map))
     kr = _i32(k_recent) if k_recent is not None else None
     B, l, hqs, ds = s_q.shape
-    hks, ncap = s_k.shape[2], s_k.shape[3]
+    hks, s_rows = s_k.shape[2], s_k.shape[3]
+    held = _i32(s_held) if s_held is not None else None
+    rpos = _i32(s_row_pos) if s_row_pos is not None else None
+    ncap = s_rows if held is None else int(n_cap)
     _, L, hq, d = l_q.shape
     hk, nrows = l_k.shape[2], l_k.shape[3]
     ks = _i32(k_slot) if k_slot is not None else None
     vs = _i32(v_slot) if v_slot is not None else None
     nsh = l * hqs
     out = dict(
-        logits=np.zeros((B, nsh, ncap), np.float32),
+        logits=np.zeros((B, nsh, s_rows), np.float32),
         row_max=np.empty((B, nsh)), row_sum=np.empty((B, nsh)),
         small_out=np.empty((B, l, hqs, ds)),
         crit=np.empty((B, nsh, max(kc_cap, 1)), np.int32),
@@ -233,6 +239,8 @@ def step(*, seq_len, k_crit, k_marg, kc_cap, km_cap, head_map, mode,
     si = StepIn(B, ncap, kc_cap, km_cap, _p(seq_len, _I), _p(k_crit, _I), _p(k_marg, _I),
                 _p(kr, _I) if kr is not None else None,
                 l, hqs, hks, ds, s_scale, _p(s_q, _F), _p(s_k, _F), _p(s_v, _F),
+                s_rows, _p(held, _I) if held is not None else None,
+                _p(rpos, _I) if rpos is not None else None,
                 L, hq, hk, d, l_scale, nrows, _p(l_q, _F), _p(l_k, _F), _p(l_v, _F),
                 _p(ks, _I) if ks is not None else None,
                 _p(vs, _I) if vs is not None else None,

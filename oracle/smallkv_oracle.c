@@ -283,24 +283,43 @@ int orc_step(const orc_step_in *in, const orc_step_out *out) {
       rc = ORC_EINVAL;
       break;
     }
+    /* The small model's cache: every token (row t = token t), or after its
+     * own eviction the held rows r < held[b] of token positions row_pos[r]
+     * (the small model's KV compression, "Implementation Optimization" (2)).
+     * Stages 1-2 run over the rows; the lists name token positions. */
+    const int64_t srows = in->s_held ? in->s_rows : ncap;
+    const int ns = in->s_held ? in->s_held[b] : n;
+    if (ns < 1 || ns > n || ns > srows) {
+      rc = ORC_EINVAL;
+      break;
+    }
     /* stage 1 and stage 2 for every small head j = layer*Hq_s + head */
     for (int j = 0; j < nsh && rc == ORC_OK; ++j) {
       const int layer = j / hqs, h = j % hqs, g = h / gs;
       const size_t row = (size_t)b * nsh + j;
       const float *q = in->s_q + row * ds;
-      const size_t kv = (((size_t)b * l + layer) * hks + g) * (size_t)ncap * ds;
-      rc = orc_small_head(n, ds, in->s_scale, q, in->s_k + kv, in->s_v + kv,
-                          out->logits + row * ncap, &ms[j], &zs[j],
+      const size_t unit = ((size_t)b * l + layer) * hks + g;
+      const size_t kv = unit * (size_t)srows * ds;
+      rc = orc_small_head(ns, ds, in->s_scale, q, in->s_k + kv, in->s_v + kv,
+                          out->logits + row * srows, &ms[j], &zs[j],
                           out->small_out + row * ds);
       if (rc != ORC_OK) break;
       out->row_max[row] = ms[j];
       out->row_sum[row] = zs[j];
-      rc = orc_partition(n, in->k_crit[b], in->k_marg[b], in->k_recent ? in->k_recent[b] : 0,
-                         out->logits + row * ncap, ms[j], zs[j],
+      rc = orc_partition(ns, in->k_crit[b], in->k_marg[b], in->k_recent ? in->k_recent[b] : 0,
+                         out->logits + row * srows, ms[j], zs[j],
                          out->crit + row * in->kc_cap, in->kc_cap,
                          out->marg + row * in->km_cap,
                          out->marg_prob + row * in->km_cap, in->km_cap,
                          out->mass + row * 2, &nc[j], &nm[j]);
+      if (rc != ORC_OK || !in->s_held) continue;
+      const int32_t *pos = in->s_row_pos + unit * (size_t)srows;
+      for (int r = 0; r < ns; ++r)
+        if (pos[r] < 0 || pos[r] >= n || (r > 0 && pos[r] <= pos[r - 1])) rc = ORC_EINVAL;
+      for (int i = 0; i < nc[j] && rc == ORC_OK; ++i)
+        out->crit[row * in->kc_cap + i] = pos[out->crit[row * in->kc_cap + i]];
+      for (int i = 0; i < nm[j] && rc == ORC_OK; ++i)
+        out->marg[row * in->km_cap + i] = pos[out->marg[row * in->km_cap + i]];
     }
     /* stage 3 for every large head (layer, h) through j = f(layer, h) */
     for (int li = 0; li < L && rc == ORC_OK; ++li) {

@@ -101,7 +101,8 @@ int orc_hybrid_head(int d, float scale, const float *q, const float *K,
  *   large q  [B][L][Hq][d]             large K,V [B][L][Hkv][n_rows][d]
  *   k_slot, v_slot [B][L][Hkv][n_cap] or NULL
  *   head_map [L*Hq] -> small head id j = layer*Hq_s + head
- * Outputs: logits [B][l*Hq_s][n_cap] (entries t >= seq_len untouched),
+ * Outputs: logits [B][l*Hq_s][n_cap] (entries t >= seq_len untouched; with
+ *   s_held, [B][l*Hq_s][s_rows] indexed by held row),
  *   row_max, row_sum [B][l*Hq_s], small_out [B][l][Hq_s][d_s],
  *   crit [B][l*Hq_s][kc_cap], marg/marg_prob [B][l*Hq_s][km_cap],
  *   mass [B][l*Hq_s][2], large_out [B][L][Hq][d]. */
@@ -113,6 +114,12 @@ typedef struct {
   int32_t s_layers, s_q_heads, s_kv_heads, s_dim;
   float s_scale;
   const float *s_q, *s_k, *s_v;
+  /* the small model's own KV eviction, optional: s_held [B] rows in use,
+   * s_row_pos [B][l][Hkv_s][s_rows] their token positions (strictly
+   * ascending, < seq_len); small K,V are then [B][l][Hkv_s][s_rows][d_s] and
+   * logits rows have stride s_rows.  s_held NULL: every token, stride n_cap */
+  int64_t s_rows;
+  const int32_t *s_held, *s_row_pos;
   /* large model */
   int32_t l_layers, l_q_heads, l_kv_heads, l_dim;
   float l_scale;

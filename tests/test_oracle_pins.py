@@ -471,3 +471,102 @@ def test_step_composes_the_three_stages():
                     if kc[0] == 40:
                         ref, _ = textbook_attention(lq[b, lay, h], lk[b, lay, g, :n], lv[b, lay, g, :n], SCALE128)
                         np.testing.assert_allclose(r["large_out"][b, lay, h], ref, rtol=1e-10, atol=1e-12)
+
+
+# ---------------------------------------- small model's own KV eviction --
+
+def _evicted_small_store(rng, sk, sv, held, ncap_rows):
+    """Each (sequence, layer, kv head) keeps `held[b]` ascending positions
+    (tokens 0 and the last one always among them); returns the compact store
+    and its row -> position map."""
+    B, l, hks, ncap, ds = sk.shape
+    pos = np.full((B, l, hks, ncap_rows), -1, np.int32)
+    ck = np.zeros((B, l, hks, ncap_rows, ds), np.float32)
+    cv = np.zeros_like(ck)
+    for b in range(B):
+        for la in range(l):
+            for g in range(hks):
+                n = held[b][1]
+                keep = np.sort(np.concatenate([[0, n - 1], rng.choice(np.arange(1, n - 1), held[b][0] - 2,
+                                                                     replace=False)]))
+                pos[b, la, g, :keep.size] = keep
+                ck[b, la, g, :keep.size] = sk[b, la, g, keep]
+                cv[b, la, g, :keep.size] = sv[b, la, g, keep]
+    return ck, cv, pos
+
+
+def test_step_with_all_rows_held_is_the_plain_step():
+    rng = np.random.default_rng(21)
+    B, ncap, l, hqs, hks, ds, L, hq, hk, d = 2, 48, 2, 4, 2, 64, 2, 4, 2, 128
+    f = lambda *s: rng.standard_normal(s).astype(np.float32)
+    sq, sk, sv = f(B, l, hqs, ds), f(B, l, hks, ncap, ds), f(B, l, hks, ncap, ds)
+    lq, lk, lv = f(B, L, hq, d), f(B, L, hk, ncap, d), f(B, L, hk, ncap, d)
+    seq = np.array([48, 30], np.int32)
+    kc, km = np.array([6, 4], np.int32), np.array([10, 7], np.int32)
+    hm = rng.integers(0, l * hqs, L * hq).astype(np.int32)
+    common = dict(seq_len=seq, k_crit=kc, k_marg=km, kc_cap=8, km_cap=12, head_map=hm,
+                  mode=O.NORM_REMAINING, s_q=sq, s_v=None, s_scale=0.125, l_q=lq, l_k=lk, l_v=lv,
+                  l_scale=SCALE128)
+    plain = O.step(**{**common, "s_k": sk, "s_v": sv})
+    pos = np.broadcast_to(np.arange(ncap, dtype=np.int32), (B, l, hks, ncap)).copy()
+    held = O.step(**{**common, "s_k": sk, "s_v": sv}, s_held=seq, s_row_pos=pos, n_cap=ncap)
+    for k in ("crit", "marg", "marg_prob", "mass", "small_out", "large_out", "row_max", "row_sum"):
+        np.testing.assert_array_equal(plain[k], held[k], err_msg=k)
+
+
+@pytest.mark.parametrize("recent", [False, True])
+def test_step_with_evicted_small_cache_brute_force(recent):
+    """The lists are the top of the held tokens only, ranked by the small
+    model's logit over its held rows (fp64 numpy), named by position; a token
+    the small model dropped is never critical or marginal."""
+    rng = np.random.default_rng(22 + recent)
+    B, ncap, l, hqs, hks, ds, L, hq, hk, d = 2, 64, 2, 4, 2, 64, 1, 4, 2, 128
+    f = lambda *s: rng.standard_normal(s).astype(np.float32)
+    sq, sk, sv = f(B, l, hqs, ds), f(B, l, hks, ncap, ds), f(B, l, hks, ncap, ds)
+    lq, lk, lv = f(B, L, hq, d), f(B, L, hk, ncap, d), f(B, L, hk, ncap, d)
+    seq = np.array([64, 41], np.int32)
+    held = np.array([26, 17], np.int32)  # about 40% of each sequence
+    ck, cv, pos = _evicted_small_store(rng, sk, sv, [(26, 64), (17, 41)], 32)
+    kc, km = np.array([5, 3], np.int32), np.array([8, 6], np.int32)
+    kr = np.array([3, 2], np.int32) if recent else None
+    hm = rng.integers(0, l * hqs, L * hq).astype(np.int32)
+    r = O.step(seq_len=seq, k_crit=kc, k_marg=km, kc_cap=8, km_cap=8, head_map=hm,
+               mode=O.NORM_REMAINING, s_q=sq, s_k=ck, s_v=cv, s_scale=0.125, l_q=lq, l_k=lk,
+               l_v=lv, l_scale=SCALE128, k_recent=kr, s_held=held, s_row_pos=pos, n_cap=ncap)
+    for b in range(B):
+        nh = int(held[b])
+        rr = 0 if kr is None else int(kr[b])
+        for j in range(l * hqs):
+            la, h = divmod(j, hqs)
+            g = h // (hqs // hks)
+            p = pos[b, la, g, :nh]
+            s = (ck[b, la, g, :nh].astype(np.float64) @ sq[b, la, h].astype(np.float64)) * 0.125
+            older = nh - rr
+            order = sorted(range(older), key=lambda t: (-s[t], t))
+            ntop = min(int(kc[b]), older)
+            crit = sorted(set(p[order[:ntop]].tolist()) | set(p[older:].tolist()))
+            marg = sorted(p[order[ntop:ntop + min(int(km[b]), older - ntop)]].tolist())
+            got_c = r["crit"][b, j][r["crit"][b, j] >= 0].tolist()
+            got_m = r["marg"][b, j][r["marg"][b, j] >= 0].tolist()
+            assert got_c == crit and got_m == marg
+            assert set(got_c + got_m) <= set(p.tolist())
+            # the small model's softmax runs over its held rows only
+            e = np.exp(s - s.max())
+            np.testing.assert_allclose(r["row_sum"][b, j], e.sum(), rtol=1e-5)  # fp32 logits
+
+
+def test_step_rejects_a_bad_position_map():
+    rng = np.random.default_rng(23)
+    B, ncap, l, hqs, hks, ds, L, hq, hk, d = 1, 32, 1, 2, 1, 64, 1, 2, 1, 128
+    f = lambda *s: rng.standard_normal(s).astype(np.float32)
+    args = dict(seq_len=np.array([32], np.int32), k_crit=np.array([3], np.int32),
+                k_marg=np.array([4], np.int32), kc_cap=4, km_cap=4,
+                head_map=np.zeros(2, np.int32), mode=O.NORM_REMAINING, s_q=f(1, 1, 2, 64),
+                s_k=f(1, 1, 1, 16, 64), s_v=f(1, 1, 1, 16, 64), s_scale=0.125,
+                l_q=f(1, 1, 2, 128), l_k=f(1, 1, 1, 32, 128), l_v=f(1, 1, 1, 32, 128),
+                l_scale=SCALE128, s_held=np.array([10], np.int32), n_cap=32)
+    good = np.arange(0, 32, 2, dtype=np.int32).reshape(1, 1, 1, 16)
+    O.step(**args, s_row_pos=good)
+    for bad in (good[..., ::-1].copy(), good + 20):  # descending; beyond the sequence
+        with pytest.raises(O.OracleError):
+            O.step(**args, s_row_pos=bad)
