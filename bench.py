@@ -185,7 +185,7 @@ def main():
         S.smallkv_small_attn(ps.batch, ps.small, b.logits, b.row_max, b.row_sum, b.ws, stream)
         e[1].record(stream)
         S.smallkv_partition(ps.batch, nsh, b.logits, b.row_max, b.row_sum, b.crit_idx,
-                            b.marg_idx, b.marg_prob, b.mass, None, stream)
+                            b.marg_idx, b.marg_prob, b.mass, None, stream, small=ps.small)
         e[2].record(stream)
         S.smallkv_hybrid_attn(ps.batch, ps.large, ps.head_map, nsh, b.crit_idx, b.marg_idx,
                               b.marg_prob, b.mass, ps.mode, b.ws, stream)
@@ -221,6 +221,8 @@ def main():
         host = {k: h(x[k]) for k in ("seq_len", "k_crit", "k_marg", "head_map", "s_q", "s_k",
                                      "s_v", "l_q", "l_k", "l_v")}
         host["k_recent"] = h(x["k_recent"]) if x.get("k_recent") is not None else None
+        held = {} if x.get("s_held") is None else dict(
+            s_held=h(x["s_held"]), s_row_pos=h(x["s_row_pos"]), n_cap=x["n_cap"])
         try:
             os.sched_setaffinity(0, {sorted(os.sched_getaffinity(0))[0]})
         except (AttributeError, OSError):
@@ -234,7 +236,7 @@ def main():
                    mode=O.NORM_REMAINING, s_q=host["s_q"], s_k=host["s_k"], s_v=host["s_v"],
                    s_scale=softmax_scale(w.small.head_dim), l_q=host["l_q"], l_k=host["l_k"],
                    l_v=host["l_v"], l_scale=softmax_scale(w.large.head_dim),
-                   k_recent=host["k_recent"])
+                   k_recent=host["k_recent"], **held)
             spent += time.perf_counter() - c0
             reps += 1
         cpu = {"value": w.batch * reps / spent, "unit": "tokens/s", "cores": 1, "kind": "oracle",
@@ -260,6 +262,7 @@ def main():
             "kv_dtype": w.dtype, "batch": w.batch, "context": w.n_ctx,
             "critical": budget_text(w.crit), "marginal": budget_text(w.marg),
             **({"recent": budget_text(w.recent)} if w.recent != ("abs", 0) else {}),
+            **({"small_cache_kept": f"{w.slm_keep}%"} if w.slm_keep else {}),
             "launch": "eager" if args.eager else "hip-graph",
             "rotated_input_copies": args.rotate,
         },

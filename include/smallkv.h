@@ -52,7 +52,7 @@
 extern "C" {
 #endif
 
-#define SMALLKV_ABI_VERSION 3
+#define SMALLKV_ABI_VERSION 4
 
 typedef enum { SMALLKV_F32 = 0, SMALLKV_BF16 = 1 } smallkv_dtype_t;
 
@@ -101,6 +101,19 @@ typedef struct {
                             token -> row of k (-1: not held); NULL means row = token */
   const int32_t *v_slot; /* same for v */
   void *out;          /* [B][n_layers][n_q_heads][head_dim] attention output */
+  /* Small model only, optional, both or neither: the small model's own KV
+   * eviction (its cache compressed, "Implementation Optimization" (2)).
+   * held[b]: rows of its cache in use, clamped to [1, n_rows] (precondition
+   * held[b] <= N_b); row_pos [B][n_layers][n_kv_heads][n_rows]: the token
+   * position each row holds, strictly ascending over the first held[b] rows
+   * and below N_b.  k and v then hold n_rows <= n_cap rows per kv head.
+   * Stages 1-2 run over the held rows: logits rows have stride n_rows and
+   * entry r is row r's logit; the partition ranks rows (recent tokens are the
+   * last rows) and names tokens by row_pos (clamped to [0, N_b - 1]); a
+   * token the small model does not hold is never critical or marginal.
+   * NULL: the small cache holds every token (row t = token t). */
+  const int32_t *held;
+  const int32_t *row_pos;
 } smallkv_model_t;
 
 /* The batch of sequences and their budgets. */
@@ -134,7 +147,9 @@ typedef struct {
  *   row_max[b][j]   = max_t logits,  row_sum[b][j] = sum_t exp(logit - row_max)
  *   small->out      = sum_t (exp(logit - row_max) / row_sum) * V_t
  * logits: [B][n_layers*n_q_heads][n_cap] fp32; row_max, row_sum: [B][n_layers*n_q_heads]
- * fp32.  small->k_slot and v_slot must be NULL and small->n_rows == n_cap. */
+ * fp32.  small->k_slot and v_slot must be NULL; small->n_rows == n_cap, or
+ * with small->held the held rows r < held[b] are attended and logits rows
+ * have stride n_rows. */
 int smallkv_small_attn(const smallkv_batch_t *batch, const smallkv_model_t *small,
                        float *logits, float *row_max, float *row_sum, void *ws,
                        size_t ws_bytes, void *stream);
@@ -143,14 +158,18 @@ int smallkv_small_attn(const smallkv_batch_t *batch, const smallkv_model_t *smal
  * critical; the older tokens t < N_b - r, ordered by (logit descending, index
  * ascending), give the other |C| - r critical ones, then |M| marginal, the
  * rest evicted (r = 0 without k_recent: every token is ranked).
+ * `small` is optional (NULL: the rows are tokens 0..N_b-1); with the small
+ * model's own eviction (small->held) the rows are its held rows, ranked the
+ * same way and named by small->row_pos, as in smallkv_step; n_small_heads
+ * must then be small->n_layers * small->n_q_heads.
  *   crit_idx  [B][n_small_heads][kc_cap] int32, ascending, padded with -1
  *   marg_idx  [B][n_small_heads][km_cap] int32, ascending, padded with -1
  *   marg_prob [B][n_small_heads][km_cap] fp32, p'_t = exp(logit_t - row_max)/row_sum
  *             for marg_idx's token (0 in padding)
  *   mass      [B][n_small_heads][2] fp32, {S'_C, S'_M}: the sum of p' over each set
  * Inputs are stage 1's logits, row_max and row_sum.  Deterministic. */
-int smallkv_partition(const smallkv_batch_t *batch, int32_t n_small_heads,
-                      const float *logits, const float *row_max,
+int smallkv_partition(const smallkv_batch_t *batch, const smallkv_model_t *small,
+                      int32_t n_small_heads, const float *logits, const float *row_max,
                       const float *row_sum, int32_t *crit_idx,
                       int32_t *marg_idx, float *marg_prob, float *mass, void *ws,
                       size_t ws_bytes, void *stream);

@@ -70,12 +70,13 @@ def step_bytes(x: dict, crit_idx: torch.Tensor, marg_idx: torch.Tensor, km_cap: 
     _, L, hq, d = l_q.shape
     hk = x["l_k"].shape[2] if "l_k" in x else hq
     g = hq // hk
-    n_cap = s_k.shape[3]
+    n_cap = x["n_cap"] if "n_cap" in x else s_k.shape[3]
     seq = x["seq_len"].to(torch.int64)
-    tot_tok = int(seq.sum())
-    small_kv = 2 * l * hks * ds * esz * tot_tok
+    # the small model reads (and scores) only the rows it holds
+    s_tok = int(x["s_held"].to(torch.int64).sum()) if x.get("s_held") is not None else int(seq.sum())
+    small_kv = 2 * l * hks * ds * esz * s_tok
     small_qo = 2 * B * l * hqs * ds * esz
-    logits = 4 * l * hqs * tot_tok
+    logits = 4 * l * hqs * s_tok
     part_out = B * l * hqs * (crit_idx.shape[-1] * 4 + km_cap * 8 + 8)
     large_qo = 2 * B * L * hq * d * esz
     dev = crit_idx.device

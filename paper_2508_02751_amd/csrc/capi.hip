@@ -28,7 +28,10 @@ bool dim_supported(const smallkv_model_t *m) { return m->head_dim == 64 || m->he
 
 int check_small(const smallkv_batch_t *b, const smallkv_model_t *s) {
   if (!batch_ok(b) || !model_ok(s)) return SMALLKV_EINVAL;
-  if (s->k_slot || s->v_slot || s->n_rows != b->n_cap) return SMALLKV_EINVAL;
+  if (s->k_slot || s->v_slot) return SMALLKV_EINVAL;
+  if (!s->held != !s->row_pos) return SMALLKV_EINVAL;  // both or neither
+  if (s->held ? (s->n_rows < 1 || s->n_rows > b->n_cap) : s->n_rows != b->n_cap)
+    return SMALLKV_EINVAL;
   if (!dim_supported(s)) return SMALLKV_EUNSUPPORTED;
   if (s->n_q_heads / s->n_kv_heads > 16) return SMALLKV_EUNSUPPORTED;
   if ((int64_t)b->batch * s->n_layers * s->n_q_heads > INT32_MAX / 2) return SMALLKV_EUNSUPPORTED;
@@ -39,6 +42,7 @@ int check_large(const smallkv_batch_t *b, const smallkv_model_t *l, const int32_
                 int n_small_heads) {
   if (!batch_ok(b) || !model_ok(l) || !head_map || n_small_heads < 1) return SMALLKV_EINVAL;
   if (!l->k_slot != !l->v_slot) return SMALLKV_EINVAL;  // both maps or neither
+  if (l->held || l->row_pos) return SMALLKV_EINVAL;      // small model only
   if (!l->k_slot && l->n_rows != b->n_cap) return SMALLKV_EINVAL;
   if (l->n_rows > INT32_MAX) return SMALLKV_EUNSUPPORTED;
   if (!dim_supported(l)) return SMALLKV_EUNSUPPORTED;
@@ -56,6 +60,17 @@ int status_of(hipError_t e) { return e == hipSuccess ? SMALLKV_OK : SMALLKV_EDEV
 
 size_t max_sz(size_t x, size_t y) { return x > y ? x : y; }
 
+// The batch as stages 1-2 see it: with the small model's own eviction they
+// run over its held rows (lengths held[b], n_rows rows per kv head).
+smallkv_batch_t small_view(const smallkv_batch_t &b, const smallkv_model_t &s) {
+  smallkv_batch_t v = b;
+  if (s.held) {
+    v.seq_len = s.held;
+    v.n_cap = (int32_t)s.n_rows;
+  }
+  return v;
+}
+
 // Workspace of a whole step: stage 1's chunk records, then (reused) stage
 // 3's split records, and after both the partition's list offsets, which
 // stage 2 writes while it reads stage 1's records and stage 3 reads while it
@@ -65,12 +80,13 @@ struct StepLayout {
 };
 StepLayout step_layout(const smallkv_batch_t &b, const smallkv_model_t &small,
                        const smallkv_model_t &large, int nsh) {
-  const SmallPlan p = plan_small(b, small);
+  const SmallPlan p = plan_small(small_view(b, small), small);
   const GroupPlan gp = plan_group(b, large, nsh);
   StepLayout l{};
   l.tab_offset = (max_sz(p.ws_bytes, gp.use ? gp.ws_bytes : 0) + 255) / 256 * 256;
-  // (with one token range per kv head every cursor starts at 0: no offsets)
-  l.tab_bytes = gp.use && gp.n_split > 1 ? list_offsets_bytes(b, nsh) : 0;
+  // (with one token range per kv head every cursor starts at 0: no offsets;
+  // the partition writes them in row order, so not with held rows either)
+  l.tab_bytes = gp.use && gp.n_split > 1 && !small.held ? list_offsets_bytes(b, nsh) : 0;
   l.total = l.tab_bytes ? l.tab_offset + l.tab_bytes : max_sz(p.ws_bytes, gp.use ? gp.ws_bytes : 0);
   return l;
 }
@@ -150,25 +166,33 @@ int smallkv_small_attn(const smallkv_batch_t *batch, const smallkv_model_t *smal
   int rc = check_small(batch, small);
   if (rc) return rc;
   if (!logits || !row_max || !row_sum) return SMALLKV_EINVAL;
-  const SmallPlan p = plan_small(*batch, *small);
+  const smallkv_batch_t sb = small_view(*batch, *small);
+  const SmallPlan p = plan_small(sb, *small);
   if (p.ws_bytes && (!ws || ws_bytes < p.ws_bytes)) return SMALLKV_EWORKSPACE;
-  return status_of(launch_small_attn(*batch, *small, logits, row_max, row_sum,
+  return status_of(launch_small_attn(sb, *small, logits, row_max, row_sum,
                                      static_cast<float *>(ws), p,
                                      static_cast<hipStream_t>(stream)));
 }
 
-int smallkv_partition(const smallkv_batch_t *batch, int32_t n_small_heads, const float *logits,
-                      const float *row_max, const float *row_sum, int32_t *crit_idx,
-                      int32_t *marg_idx, float *marg_prob, float *mass, void *ws, size_t ws_bytes,
-                      void *stream) {
+int smallkv_partition(const smallkv_batch_t *batch, const smallkv_model_t *small,
+                      int32_t n_small_heads, const float *logits, const float *row_max,
+                      const float *row_sum, int32_t *crit_idx, int32_t *marg_idx,
+                      float *marg_prob, float *mass, void *ws, size_t ws_bytes, void *stream) {
   (void)ws;
   (void)ws_bytes;
   if (!batch_ok(batch) || n_small_heads < 1) return SMALLKV_EINVAL;
   if (!logits || !row_max || !row_sum || !crit_idx || !mass) return SMALLKV_EINVAL;
   if (batch->km_cap > 0 && (!marg_idx || !marg_prob)) return SMALLKV_EINVAL;
   if ((int64_t)batch->batch * n_small_heads > INT32_MAX / 2) return SMALLKV_EUNSUPPORTED;
-  return status_of(launch_partition(*batch, n_small_heads, logits, row_max, row_sum, crit_idx,
-                                    marg_idx, marg_prob, mass,
+  const bool held = small && small->held;
+  if (held) {
+    const int rc = check_small(batch, small);
+    if (rc) return rc;
+    if (n_small_heads != small->n_layers * small->n_q_heads) return SMALLKV_EINVAL;
+  }
+  return status_of(launch_partition(held ? small_view(*batch, *small) : *batch, n_small_heads,
+                                    logits, row_max, row_sum, crit_idx, marg_idx, marg_prob, mass,
+                                    held ? small : nullptr, batch->seq_len, batch->n_cap,
                                     static_cast<hipStream_t>(stream)));
 }
 
@@ -212,17 +236,18 @@ int smallkv_step(const smallkv_step_t *s, void *ws, size_t ws_bytes, void *strea
   if ((rc = check_mode(s->mode))) return rc;
   if (!s->logits || !s->row_max || !s->row_sum || !s->crit_idx || !s->mass) return SMALLKV_EINVAL;
   if (s->batch.km_cap > 0 && (!s->marg_idx || !s->marg_prob)) return SMALLKV_EINVAL;
-  const SmallPlan p = plan_small(s->batch, s->small);
+  const smallkv_batch_t sb = small_view(s->batch, s->small);
+  const SmallPlan p = plan_small(sb, s->small);
   const StepLayout lay = step_layout(s->batch, s->small, s->large, nsh);
   if (lay.total && (!ws || ws_bytes < lay.total)) return SMALLKV_EWORKSPACE;
   hipStream_t st = static_cast<hipStream_t>(stream);
   int2 *tab = lay.tab_bytes ? reinterpret_cast<int2 *>(static_cast<char *>(ws) + lay.tab_offset)
                             : nullptr;
-  hipError_t e = launch_small_split(s->batch, s->small, s->logits, static_cast<float *>(ws), p, st);
+  hipError_t e = launch_small_split(sb, s->small, s->logits, static_cast<float *>(ws), p, st);
   if (e != hipSuccess) return SMALLKV_EDEVICE;
-  e = launch_merge_partition(s->batch, s->small, p, static_cast<const float *>(ws), s->logits,
+  e = launch_merge_partition(sb, s->small, p, static_cast<const float *>(ws), s->logits,
                              s->row_max, s->row_sum, s->crit_idx, s->marg_idx, s->marg_prob,
-                             s->mass, tab, st);
+                             s->mass, tab, s->batch.seq_len, s->batch.n_cap, st);
   if (e != hipSuccess) return SMALLKV_EDEVICE;
   // stage 1's records are consumed by now: stage 3 reuses the workspace
   // below the list offsets

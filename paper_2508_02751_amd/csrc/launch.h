@@ -38,14 +38,22 @@ inline size_t list_offsets_bytes(const smallkv_batch_t &b, int n_small_heads) {
 
 // Stage 2 fused with stage 1's merge: writes row_max, row_sum and the small
 // model's output, then partitions; also the list offsets when tab is set.
+// `b` is the batch as stages 1-2 see it (with the small model's own
+// eviction: held rows); with m.row_pos the lists name row_pos[row], clamped
+// below tok_len[b] (the sequences' token counts, capacity tok_cap).
 hipError_t launch_merge_partition(const smallkv_batch_t &b, const smallkv_model_t &m,
                                   const SmallPlan &p, const float *ws, const float *logits,
                                   float *row_max, float *row_sum, int32_t *crit, int32_t *marg,
-                                  float *marg_prob, float *mass, int2 *tab, hipStream_t st);
+                                  float *marg_prob, float *mass, int2 *tab,
+                                  const int32_t *tok_len, int tok_cap, hipStream_t st);
 
+// Stage 2 alone; `held` (or null): the small model whose held rows the
+// rows are (b is then the batch as stages 1-2 see it), named by its row_pos.
 hipError_t launch_partition(const smallkv_batch_t &b, int n_small_heads, const float *logits,
                             const float *row_max, const float *row_sum, int32_t *crit,
-                            int32_t *marg, float *marg_prob, float *mass, hipStream_t st);
+                            int32_t *marg, float *marg_prob, float *mass,
+                            const smallkv_model_t *held, const int32_t *tok_len, int tok_cap,
+                            hipStream_t st);
 
 // Largest kc_cap the per-head hybrid kernel keeps in LDS.
 constexpr int kHybridMaxCrit = 12288;

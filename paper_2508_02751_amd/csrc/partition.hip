@@ -72,6 +72,11 @@ struct PartArgs {
   // each 256-token boundary of the row (written when not null)
   int2 *tab;
   int nblk;
+  // optional (fused only): the small model's held rows -> token positions,
+  // [B][layers][hkv][n_cap] (n_cap = rows per kv head here), clamped below
+  // tok_len[b]
+  const int32_t *row_pos, *tok_len;
+  int tok_cap;
 };
 
 __device__ __forceinline__ uint64_t lanemask_lt() {
@@ -165,6 +170,8 @@ struct RowCtx {
   int32_t *crit, *marg;
   float *mp;
   float M, Z;
+  const int32_t *pos;  // row -> token position (null: row = token)
+  int last;            // largest position a list may name
 };
 
 __device__ __forceinline__ void row_setup(const PartArgs &a, RowCtx &r) {
@@ -181,6 +188,14 @@ __device__ __forceinline__ void row_setup(const PartArgs &a, RowCtx &r) {
   r.crit = a.crit + (int64_t)r.row * a.kc_cap;
   r.marg = a.marg + (int64_t)r.row * a.km_cap;
   r.mp = a.marg_prob + (int64_t)r.row * a.km_cap;
+  r.pos = nullptr;
+  r.last = 0;
+  if (a.row_pos) {
+    const int j = r.row % a.nsh, layer = j / a.hq, h = j % a.hq;
+    const int64_t unit = ((int64_t)b * a.layers + layer) * a.hkv + h / a.g;
+    r.pos = a.row_pos + unit * a.n_cap;
+    r.last = clampi(a.tok_len[b], 1, a.tok_cap) - 1;
+  }
 }
 
 // Row max and sum: combined from stage 1's chunk records (fused; also writes
@@ -521,6 +536,8 @@ struct Compactor {
     const float p = (inC || inM) ? __expf(s - r.M) * Zinv : 0.0f;
     sc += inC ? p : 0.0f;
     sm += inM ? p : 0.0f;
+    // the small model's held rows name their token positions
+    if (r.pos && (inC || inM)) tok = clampi(r.pos[tok], 0, r.last);
     // the guards only matter if the select were wrong: never write past a row
     if (inC && pc < (uint32_t)r.nc) r.crit[pc] = tok;
     if (inM && pm < (uint32_t)r.nm) {
@@ -748,16 +765,28 @@ hipError_t launch_rows(const PartArgs &a, int rows, hipStream_t st) {
 
 hipError_t launch_partition(const smallkv_batch_t &b, int n_small_heads, const float *logits,
                             const float *row_max, const float *row_sum, int32_t *crit,
-                            int32_t *marg, float *marg_prob, float *mass, hipStream_t st) {
-  const PartArgs a = base_args(b, n_small_heads, logits, const_cast<float *>(row_max),
-                               const_cast<float *>(row_sum), crit, marg, marg_prob, mass);
+                            int32_t *marg, float *marg_prob, float *mass,
+                            const smallkv_model_t *held, const int32_t *tok_len, int tok_cap,
+                            hipStream_t st) {
+  PartArgs a = base_args(b, n_small_heads, logits, const_cast<float *>(row_max),
+                         const_cast<float *>(row_sum), crit, marg, marg_prob, mass);
+  if (held) {
+    a.layers = held->n_layers;
+    a.hq = held->n_q_heads;
+    a.hkv = held->n_kv_heads;
+    a.g = held->n_q_heads / held->n_kv_heads;
+    a.row_pos = held->row_pos;
+    a.tok_len = tok_len;
+    a.tok_cap = tok_cap;
+  }
   return launch_rows<false>(a, b.batch * n_small_heads, st);
 }
 
 hipError_t launch_merge_partition(const smallkv_batch_t &b, const smallkv_model_t &m,
                                   const SmallPlan &p, const float *ws, const float *logits,
                                   float *row_max, float *row_sum, int32_t *crit, int32_t *marg,
-                                  float *marg_prob, float *mass, int2 *tab, hipStream_t st) {
+                                  float *marg_prob, float *mass, int2 *tab,
+                                  const int32_t *tok_len, int tok_cap, hipStream_t st) {
   const int nsh = m.n_layers * m.n_q_heads;
   PartArgs a = base_args(b, nsh, logits, row_max, row_sum, crit, marg, marg_prob, mass);
   a.part = ws;
@@ -773,6 +802,9 @@ hipError_t launch_merge_partition(const smallkv_batch_t &b, const smallkv_model_
   a.out_bf16 = m.dtype == SMALLKV_BF16;
   a.tab = tab;
   a.nblk = list_blocks(b);
+  a.row_pos = m.row_pos;
+  a.tok_len = tok_len;
+  a.tok_cap = tok_cap;
   return launch_rows<true>(a, b.batch * nsh, st);
 }
 

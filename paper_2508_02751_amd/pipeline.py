@@ -75,13 +75,14 @@ def prepare_step(x: dict, mode: int = S.NORM_REMAINING,
     l_q = x["l_q"]
     l_k = x["l_k"] if l_k is None else l_k
     l_v = x["l_v"] if l_v is None else l_v
-    n_cap = s_k.shape[3]
+    n_cap = x["n_cap"] if "n_cap" in x else s_k.shape[3]
     kr = x.get("k_recent")
     batch = S.BatchSpec(x["seq_len"].contiguous(), x["k_crit"].contiguous(),
                         x["k_marg"].contiguous(), n_cap, int(x["kc_cap"]), int(x["km_cap"]),
                         kr.contiguous() if kr is not None else None)
     small = S.ModelSpec(s_q.contiguous(), s_k, s_v, torch.empty_like(s_q),
-                        softmax_scale(s_q.shape[-1]))
+                        softmax_scale(s_q.shape[-1]), held=x.get("s_held"),
+                        row_pos=x.get("s_row_pos"))
     large = S.ModelSpec(l_q.contiguous(), l_k, l_v, torch.empty_like(l_q),
                         softmax_scale(l_q.shape[-1]), k_slot, v_slot)
     hm = x["head_map"].contiguous()

@@ -38,7 +38,7 @@ class Model(C.Structure):
                 ("head_dim", C.c_int32), ("dtype", C.c_int32), ("scale", C.c_float),
                 ("q", C.c_void_p), ("k", C.c_void_p), ("v", C.c_void_p),
                 ("n_rows", C.c_int64), ("k_slot", C.c_void_p), ("v_slot", C.c_void_p),
-                ("out", C.c_void_p)]
+                ("out", C.c_void_p), ("held", C.c_void_p), ("row_pos", C.c_void_p)]
 
 
 class Step(C.Structure):
@@ -78,9 +78,9 @@ def lib():
         P = C.POINTER
         L.smallkv_small_attn.argtypes = [P(Batch), P(Model), C.c_void_p, C.c_void_p, C.c_void_p,
                                          C.c_void_p, C.c_size_t, C.c_void_p]
-        L.smallkv_partition.argtypes = [P(Batch), C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p,
+        L.smallkv_partition.argtypes = [P(Batch), P(Model), C.c_int32, C.c_void_p, C.c_void_p,
                                         C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
-                                        C.c_void_p, C.c_size_t, C.c_void_p]
+                                        C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]
         L.smallkv_hybrid_attn.argtypes = [P(Batch), P(Model), C.c_void_p, C.c_int32, C.c_void_p,
                                           C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32,
                                           C.c_void_p, C.c_size_t, C.c_void_p]
@@ -154,7 +154,9 @@ class BatchSpec:
 
 @dataclasses.dataclass
 class ModelSpec:
-    """One model's operands: q [B][L][Hq][d], k/v [B][L][Hkv][n_rows][d], out like q."""
+    """One model's operands: q [B][L][Hq][d], k/v [B][L][Hkv][n_rows][d], out like q.
+    Small model only: held [B] and row_pos [B][L][Hkv][n_rows] (int32) when its
+    own cache is compressed."""
     q: torch.Tensor
     k: torch.Tensor
     v: torch.Tensor
@@ -162,6 +164,8 @@ class ModelSpec:
     scale: float
     k_slot: Optional[torch.Tensor] = None
     v_slot: Optional[torch.Tensor] = None
+    held: Optional[torch.Tensor] = None
+    row_pos: Optional[torch.Tensor] = None
 
     def c(self) -> Model:
         B, L, hq, d = self.q.shape
@@ -170,11 +174,12 @@ class ModelSpec:
             raise ValueError("k/v or out shape mismatch")
         if not (self.q.dtype == self.k.dtype == self.v.dtype == self.out.dtype):
             raise ValueError("q, k, v and out must share a dtype")
-        for t in (self.k_slot, self.v_slot):
+        for t in (self.k_slot, self.v_slot, self.held, self.row_pos):
             if t is not None and t.dtype != torch.int32:
-                raise ValueError("slot maps must be int32")
+                raise ValueError("slot and position maps must be int32")
         return Model(L, hq, hkv, d, _dtype_code(self.q), self.scale, _ptr(self.q), _ptr(self.k),
-                     _ptr(self.v), rows, _ptr(self.k_slot), _ptr(self.v_slot), _ptr(self.out))
+                     _ptr(self.v), rows, _ptr(self.k_slot), _ptr(self.v_slot), _ptr(self.out),
+                     _ptr(self.held), _ptr(self.row_pos))
 
 
 def _check(fn, rc):
@@ -208,12 +213,17 @@ def smallkv_small_attn(batch: BatchSpec, small: ModelSpec, logits, row_max, row_
 
 
 def smallkv_partition(batch: BatchSpec, n_small_heads: int, logits, row_max, row_sum,
-                      crit_idx, marg_idx, marg_prob, mass, ws=None, stream=None):
+                      crit_idx, marg_idx, marg_prob, mass, ws=None, stream=None,
+                      small: Optional[ModelSpec] = None):
+    """Stage 2; `small` is needed only when the small model's own cache is
+    compressed (its held rows and their positions)."""
     b = batch.c()
+    m = small.c() if small is not None else None
     w, wb = _ws(ws)
     _check("smallkv_partition", lib().smallkv_partition(
-        C.byref(b), n_small_heads, _ptr(logits), _ptr(row_max), _ptr(row_sum), _ptr(crit_idx),
-        _ptr(marg_idx), _ptr(marg_prob), _ptr(mass), w, wb, _stream(stream)))
+        C.byref(b), C.byref(m) if m is not None else None, n_small_heads, _ptr(logits),
+        _ptr(row_max), _ptr(row_sum), _ptr(crit_idx), _ptr(marg_idx), _ptr(marg_prob),
+        _ptr(mass), w, wb, _stream(stream)))
 
 
 def smallkv_hybrid_attn(batch: BatchSpec, large: ModelSpec, head_map, n_small_heads: int,

@@ -24,6 +24,12 @@ synthetic padded prompts):
     budget critical : recent : marginal = 2 : 1 : 2, as in the paper's
     experimental setup (its 20% example: 10%, 5%, 10%).
 
+Small model's own KV eviction (slm_keep = p): each (sequence, small layer,
+kv head) holds floor(N_b * p / 100) of its tokens: the sinks, the most
+recent 10% of the sequence, and a seeded uniform sample of the rest, in
+ascending position; its K/V rows are gathered into a compact store and
+row_pos maps rows to positions.
+
 Prefill matching window (match_inputs): the first w_cap prompt tokens of
 the same latents; keys as above with the cache's projections W_g and their
 own noise; query head h of kv head g projects with W_g + 0.5 E_h (E_h iid
@@ -74,6 +80,7 @@ class Workload:
     ragged_min: int = 0           # >0: prompt length per sequence ~ U[ragged_min, n_ctx]
     steps: int = 1                # consecutive decode steps (drifting latent)
     compact_large: bool = False   # large KV held only for retained tokens
+    slm_keep: int = 0             # >0: the small model's own cache keeps this % of tokens
 
     @property
     def n_cap(self) -> int:
@@ -113,6 +120,10 @@ WORKLOADS = {
     # run, so only their KV exists and the head map ranges over their heads
     7: Workload(7, "qwen2-7b+0.5b@20of24-n8192-b1-bf16", 1, 8192, "bf16",
                 dataclasses.replace(QWEN2_0_5B, layers=20), QWEN2_7B, ("pct", 10), ("pct", 20)),
+    # the small model's own cache compressed to 40% of the tokens (the
+    # paper's best small-model budget with the large model at 20%)
+    8: Workload(8, "qwen2-7b+0.5b-slm40-n8192-b1-bf16", 1, 8192, "bf16",
+                QWEN2_0_5B, QWEN2_7B, ("pct", 10), ("pct", 20), slm_keep=40),
 }
 
 LATENT = 64
@@ -274,6 +285,8 @@ def make_step_inputs(w: Workload, device, step: int = 0, *, z=None, large=True):
         out["l_k"], out["l_v"] = l_k, l_v
     n, kc, km = budgets(w, step)
     out["seq_len"], out["k_crit"], out["k_marg"] = n.to(device), kc.to(device), km.to(device)
+    if w.slm_keep:
+        evict_small_cache(w, out, n, device)
     kr = recent_budget(w, step)
     if kr is not None:
         out["k_recent"] = kr.to(device)
@@ -321,3 +334,33 @@ def match_inputs(w: Workload, w_cap: int, device, win_len=None, top_pct: int = 1
     out["win_len"] = win.to(device)
     out["top_k"] = torch.clamp(win * top_pct // 100, min=1).to(torch.int32).to(device)
     return out
+
+
+def evict_small_cache(w: Workload, x: dict, n: torch.Tensor, device):
+    """Replace x's small K/V by a compact store of the rows the small model
+    keeps (see the module recipe); adds s_held [B], s_row_pos
+    [B][l][Hkv][n_rows] and n_cap."""
+    base = 1000 + w.wid
+    B, l, hk = w.batch, w.small.layers, w.small.kv_heads
+    held = [max(w.sinks + 2, int(n[b]) * w.slm_keep // 100) for b in range(B)]
+    rows = max(held)
+    pos = torch.full((B, l, hk, rows), -1, dtype=torch.int32)
+    for b in range(B):
+        nb = int(n[b])
+        recent = max(1, nb // 10)
+        fixed = torch.cat([torch.arange(w.sinks), torch.arange(nb - recent, nb)])
+        middle = torch.arange(w.sinks, nb - recent)
+        extra = held[b] - fixed.numel()
+        g = _gen(base, f"slm_keep/{b}", "cpu")
+        for la in range(l):
+            for h in range(hk):
+                pick = middle[torch.randperm(middle.numel(), generator=g)[:extra]]
+                keep = torch.sort(torch.cat([fixed, pick])).values
+                pos[b, la, h, : keep.numel()] = keep.to(torch.int32)
+    pos = pos.to(device)
+    idx = pos.clamp(min=0).to(torch.int64)[..., None].expand(-1, -1, -1, -1, w.small.head_dim)
+    x["s_k"] = torch.gather(x["s_k"], 3, idx).contiguous()
+    x["s_v"] = torch.gather(x["s_v"], 3, idx).contiguous()
+    x["s_held"] = torch.tensor(held, dtype=torch.int32, device=device)
+    x["s_row_pos"] = pos.contiguous()
+    x["n_cap"] = w.n_cap

@@ -41,7 +41,10 @@ def oracle_step(x: dict, mode: int, k_slot=None, v_slot=None, l_k=None, l_v=None
         l_v=host(l_v), l_scale=softmax_scale(x["l_q"].shape[-1]),
         k_slot=None if k_slot is None else host(k_slot),
         v_slot=None if v_slot is None else host(v_slot),
-        k_recent=host(x["k_recent"]) if x.get("k_recent") is not None else None)
+        k_recent=host(x["k_recent"]) if x.get("k_recent") is not None else None,
+        s_held=host(x["s_held"]) if x.get("s_held") is not None else None,
+        s_row_pos=host(x["s_row_pos"]) if x.get("s_row_pos") is not None else None,
+        n_cap=x.get("n_cap"))
 
 
 def head_err(got: np.ndarray, ref: np.ndarray) -> float:
@@ -57,6 +60,12 @@ def compare_step(buf, ref: dict, x: dict, dtype, what: str = "", check_logits=Tr
     seq = host(x["seq_len"]).astype(np.int64)
     B = seq.size
     lg = host(buf.logits)
+    if x.get("s_held") is not None:
+        # stages 1-2 ran over the small model's held rows: logits rows have
+        # stride n_rows and entry r is held row r
+        seq = host(x["s_held"]).astype(np.int64)
+        rows = ref["logits"].shape[-1]
+        lg = lg.reshape(-1)[: B * lg.shape[1] * rows].reshape(B, lg.shape[1], rows)
     if check_logits:
         for b in range(B):
             n = seq[b]

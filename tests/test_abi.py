@@ -33,7 +33,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_abi_version_and_status_strings():
     L = S.lib()
-    assert L.smallkv_abi_version() == 3
+    assert L.smallkv_abi_version() == 4
     assert L.smallkv_status_string(0) == b"ok"
     assert L.smallkv_status_string(-3) == b"workspace too small"
     assert L.smallkv_status_string(123) == b"unknown status"
@@ -64,6 +64,10 @@ def _fake_step(**over):
     ({"s__n_rows": 100}, S.EINVAL),
     ({"s__k_slot": 0x1000}, S.EINVAL),
     ({"s__n_q_heads": 34, "s__n_kv_heads": 2}, S.EUNSUPPORTED),
+    ({"s__held": 0x1000}, S.EINVAL),                      # held rows without positions
+    ({"s__row_pos": 0x1000}, S.EINVAL),                   # positions without held rows
+    ({"s__held": 0x1000, "s__row_pos": 0x1000, "s__n_rows": 600}, S.EINVAL),  # > n_cap
+    ({"l__held": 0x1000, "l__row_pos": 0x1000}, S.EINVAL),  # small model only
 ])
 def test_workspace_size_rejects_bad_small_model(over, status):
     n = C.c_size_t()
@@ -97,7 +101,8 @@ def test_partition_and_hybrid_reject_nulls():
     b = S.Batch(batch=1, n_cap=512, seq_len=0x1000, k_crit=0x1000, k_marg=0x1000, k_recent=None,
                 kc_cap=64, km_cap=128)
     L = S.lib()
-    assert L.smallkv_partition(C.byref(b), 14, None, 1, 1, 1, 1, 1, 1, None, 0, None) == S.EINVAL
+    assert L.smallkv_partition(C.byref(b), None, 14, None, 1, 1, 1, 1, 1, 1, None, 0,
+                               None) == S.EINVAL
     lg = S.Model(1, 28, 4, 128, S.BF16, 0.088, 1, 1, 1, 512, None, None, 1)
     assert L.smallkv_hybrid_attn(C.byref(b), C.byref(lg), None, 14, 1, 1, 1, 1, 0, None, 0,
                                  None) == S.EINVAL
@@ -149,3 +154,23 @@ def test_match_workspace_size_and_check():
     assert n.value >= H * 200 * 200 * 4 + H * 200 * 8 + H * 4 * 8  # S, row (max, sum), bitsets
     assert S.lib().smallkv_match(C.byref(m), None, 0, None) == S.EWORKSPACE
     assert S.lib().smallkv_match(C.byref(m), C.c_void_p(0x1000), n.value - 1, None) == S.EWORKSPACE
+
+
+def test_small_model_held_rows_accepted():
+    st = _fake_step(s__held=0x1000, s__row_pos=0x1000, s__n_rows=200)
+    n = C.c_size_t()
+    assert S.lib().smallkv_workspace_size(C.byref(st), C.byref(n)) == 0 and n.value > 0
+
+
+def test_partition_with_held_rows_checks_the_small_model():
+    b = S.Batch(batch=1, n_cap=512, seq_len=0x1000, k_crit=0x1000, k_marg=0x1000, k_recent=None,
+                kc_cap=64, km_cap=128)
+    sm = S.Model(1, 14, 2, 64, S.BF16, 0.125, 0x1000, 0x1000, 0x1000, 200, None, None, 0x1000,
+                 0x1000, 0x1000)
+    L = S.lib()
+    # 13 heads for a 14-head small model
+    assert L.smallkv_partition(C.byref(b), C.byref(sm), 13, 1, 1, 1, 1, 1, 1, 1, None, 0,
+                               None) == S.EINVAL
+    sm.row_pos = None  # held rows without positions
+    assert L.smallkv_partition(C.byref(b), C.byref(sm), 14, 1, 1, 1, 1, 1, 1, 1, None, 0,
+                               None) == S.EINVAL

@@ -152,6 +152,27 @@ def test_early_stopped_small_model_full_step():
     run_case(w)
 
 
+def test_evicted_small_cache_full_step():
+    """The Qwen2-7B step with the small model's own cache compressed to 40%
+    of the tokens: stages 1-2 run over the held rows, the lists name their
+    positions and never a token the small model dropped."""
+    ps, x, ref = run_case(W.WORKLOADS[8])
+    pos = host(x["s_row_pos"])
+    crit = host(ps.buf.crit_idx)
+    held_any = set(pos[pos >= 0].tolist())
+    assert set(crit[crit >= 0].tolist()) <= held_any
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_evicted_small_cache_ragged_with_recent(dtype):
+    """Ragged lengths, recent tokens and several kv heads with different
+    held sets; the grouped and the per-head stage 3 both read positions."""
+    w = custom("slm-evict", 121, 3, 3000, dtype, W.ModelShape(2, 8, 2, 64),
+               W.ModelShape(2, 8, 2, 128), ("pct", 8), ("pct", 12), ragged_min=700,
+               recent=("pct", 3), slm_keep=45)
+    run_case(w)
+
+
 def test_recent_window_with_ties():
     w = custom("recent-ties", 120, 2, 1500, "bf16", SMALL, LARGE, ("pct", 10), ("pct", 25),
                recent=("pct", 5))
@@ -244,9 +265,10 @@ def test_deterministic_repeat():
 
 # --------------------------------------------------- single-stage entries --
 
-def test_single_stage_calls_match_step():
+@pytest.mark.parametrize("slm_keep", [0, 45])
+def test_single_stage_calls_match_step(slm_keep):
     w = custom("stages", 109, 3, 2000, "bf16", SMALL, LARGE, ("pct", 10), ("pct", 20),
-               ragged_min=500)
+               ragged_min=500, slm_keep=slm_keep)
     x = W.make_step_inputs(w, DEV)
     ps = prepare_step(x)
     ps.run()
@@ -254,19 +276,26 @@ def test_single_stage_calls_match_step():
     nsh = SMALL.layers * SMALL.q_heads
     lg, rm, rs = torch.empty_like(b.logits), torch.empty_like(b.row_max), torch.empty_like(b.row_sum)
     small = S.ModelSpec(ps.small.q, ps.small.k, ps.small.v, torch.empty_like(ps.small.out),
-                        ps.small.scale)
+                        ps.small.scale, held=ps.small.held, row_pos=ps.small.row_pos)
     S.smallkv_small_attn(ps.batch, small, lg, rm, rs, b.ws)
     ci, mi = torch.empty_like(b.crit_idx), torch.empty_like(b.marg_idx)
     mp, ms = torch.empty_like(b.marg_prob), torch.empty_like(b.mass)
-    S.smallkv_partition(ps.batch, nsh, lg, rm, rs, ci, mi, mp, ms)
+    S.smallkv_partition(ps.batch, nsh, lg, rm, rs, ci, mi, mp, ms, small=small)
     large = S.ModelSpec(ps.large.q, ps.large.k, ps.large.v, torch.empty_like(ps.large.out),
                         ps.large.scale)
     S.smallkv_hybrid_attn(ps.batch, large, ps.head_map, nsh, ci, mi, mp, ms, ws=b.ws)
     torch.cuda.synchronize()
-    seq = host(x["seq_len"])
-    for bi in range(3):
-        n = int(seq[bi])
-        assert torch.equal(lg[bi, :, :n], b.logits[bi, :, :n])
+    if slm_keep:  # logits rows over the held rows (stride n_rows)
+        held, rows = host(x["s_held"]), x["s_k"].shape[3]
+        a_ = lg.view(-1)[: 3 * nsh * rows].view(3, nsh, rows)
+        b_ = b.logits.view(-1)[: 3 * nsh * rows].view(3, nsh, rows)
+        for bi in range(3):
+            assert torch.equal(a_[bi, :, : int(held[bi])], b_[bi, :, : int(held[bi])])
+    else:
+        seq = host(x["seq_len"])
+        for bi in range(3):
+            n = int(seq[bi])
+            assert torch.equal(lg[bi, :, :n], b.logits[bi, :, :n])
     for got, want in ((rm, b.row_max), (rs, b.row_sum), (ci, b.crit_idx), (mi, b.marg_idx),
                       (mp, b.marg_prob), (ms, b.mass), (small.out, b.small_out),
                       (large.out, b.large_out)):
