@@ -23,6 +23,7 @@ SRCS = [SRC, os.path.join(HERE, "match_oracle.c")]
 LIB = os.path.join(HERE, "libsmallkv_oracle.so")
 
 NORM_REMAINING, NORM_NONE, NORM_SLM_CRIT, NORM_RETAINED, NORM_MARG_FILL = range(5)
+SELECT_HEAD, SELECT_GROUP = 0, 1
 MODES = (NORM_REMAINING, NORM_NONE, NORM_SLM_CRIT, NORM_RETAINED, NORM_MARG_FILL)
 
 
@@ -59,6 +60,7 @@ class StepIn(C.Structure):
         ("k_slot", _I), ("v_slot", _I),
         ("head_map", _I),
         ("mode", C.c_int32),
+        ("select", C.c_int32),
     ]
 
 
@@ -109,6 +111,8 @@ def lib():
         L.orc_jaccard.argtypes = [C.c_int, _U8, _U8, C.POINTER(C.c_int), C.POINTER(C.c_int)]
         L.orc_jaccard.restype = None
         L.orc_match.argtypes = [C.POINTER(MatchIn), _I, _F, _U8]
+        L.orc_zq.argtypes = [C.c_int, _F, C.c_float]
+        L.orc_zq.restype = C.c_float
         for f in (L.orc_small_head, L.orc_partition, L.orc_hybrid_head, L.orc_step,
                   L.orc_match_scores, L.orc_topk, L.orc_match):
             f.restype = C.c_int
@@ -205,7 +209,7 @@ def hybrid_head(q, K, V, crit, marg, marg_prob, mass, scale, mode=NORM_REMAINING
 
 def step(*, seq_len, k_crit, k_marg, kc_cap, km_cap, head_map, mode,
          s_q, s_k, s_v, s_scale, l_q, l_k, l_v, l_scale, k_slot=None, v_slot=None,
-         k_recent=None, s_held=None, s_row_pos=None, n_cap=None):
+         k_recent=None, s_held=None, s_row_pos=None, n_cap=None, select=SELECT_HEAD):
     """A whole decode step over the library layout (see smallkv_oracle.h).
 
     Shapes: s_q [B,l,Hqs,ds], s_k/s_v [B,l,Hks,n_cap,ds] (with the small
@@ -226,14 +230,16 @@ def step(*, seq_len, k_crit, k_marg, kc_cap, km_cap, head_map, mode,
     ks = _i32(k_slot) if k_slot is not None else None
     vs = _i32(v_slot) if v_slot is not None else None
     nsh = l * hqs
+    # group selection: lists per (large layer, kv head), weights per large head
+    lrows, prows = (L * hk, L * hq) if select == SELECT_GROUP else (nsh, nsh)
     out = dict(
         logits=np.zeros((B, nsh, s_rows), np.float32),
         row_max=np.empty((B, nsh)), row_sum=np.empty((B, nsh)),
         small_out=np.empty((B, l, hqs, ds)),
-        crit=np.empty((B, nsh, max(kc_cap, 1)), np.int32),
-        marg=np.empty((B, nsh, max(km_cap, 1)), np.int32),
-        marg_prob=np.empty((B, nsh, max(km_cap, 1))),
-        mass=np.empty((B, nsh, 2)),
+        crit=np.empty((B, lrows, max(kc_cap, 1)), np.int32),
+        marg=np.empty((B, lrows, max(km_cap, 1)), np.int32),
+        marg_prob=np.empty((B, prows, max(km_cap, 1))),
+        mass=np.empty((B, prows, 2)),
         large_out=np.empty((B, L, hq, d)),
     )
     si = StepIn(B, ncap, kc_cap, km_cap, _p(seq_len, _I), _p(k_crit, _I), _p(k_marg, _I),
@@ -244,7 +250,7 @@ def step(*, seq_len, k_crit, k_marg, kc_cap, km_cap, head_map, mode,
                 L, hq, hk, d, l_scale, nrows, _p(l_q, _F), _p(l_k, _F), _p(l_v, _F),
                 _p(ks, _I) if ks is not None else None,
                 _p(vs, _I) if vs is not None else None,
-                _p(head_map, _I), int(mode))
+                _p(head_map, _I), int(mode), int(select))
     so = StepOut(_p(out["logits"], _F), _p(out["row_max"], _D), _p(out["row_sum"], _D),
                  _p(out["small_out"], _D), _p(out["crit"], _I), _p(out["marg"], _I),
                  _p(out["marg_prob"], _D), _p(out["mass"], _D), _p(out["large_out"], _D))
@@ -312,3 +318,9 @@ def match(*, win_len, top_k, l_q, l_k, l_scale, s_q, s_k, s_scale):
                  Window(l, hqs, hks, ds, s_scale, _p(s_q, _F), _p(s_k, _F)))
     _check(lib().orc_match(C.byref(mi), _p(hm, _I), _p(scores, _F), _p(top, _U8)), "orc_match")
     return hm, scores, top.astype(bool)
+
+
+def zq(logits, m) -> np.float32:
+    """The group key's normaliser of one small head (orc_zq)."""
+    lg = _f32(logits)
+    return np.float32(lib().orc_zq(lg.size, _p(lg, _F), C.c_float(m)))

@@ -254,6 +254,102 @@ int orc_hybrid_head(int d, float scale, const float *q, const float *K,
 /* Algorithm 1, decode branch, restricted to attention: the small model's
  * attention over all its layers, the selection for every small head, then
  * every large layer's compensated attention through the head map. */
+/* ---------------------------------------------------- group selection -- */
+
+/* The implementation pseudocode selects the large model's cache with the
+ * top of the mapped small-model attention summed (`.sum.topk`); the cache is
+ * stored per kv head, so the query heads sharing one are summed.  The sum is
+ * an fp32 value that decides integers: it is evaluated in one defined way,
+ * with orc_exp and a normaliser that is an exact fixed-point sum. */
+float orc_zq(int n, const float *logits, float m) {
+  uint64_t z = 0;
+  for (int t = 0; t < n; ++t) {
+    const float e = orc_exp(logits[t] - m);
+    z += (uint64_t)ldexp((double)e, 40); /* exact scaling, then truncation */
+  }
+  return ldexpf((float)z, -40);
+}
+
+void orc_group_key(int n, int g, const float *const *logits, const float *m, const float *zq,
+                   float *F) {
+  for (int t = 0; t < n; ++t) {
+    float f = 0.0f;
+    for (int h = 0; h < g; ++h) f = f + orc_exp(logits[h][t] - m[h]) / zq[h];
+    F[t] = f;
+  }
+}
+
+/* Group mode of orc_step for sequence b, after stage 1 of every small head:
+ * one selection per (large layer, kv head) from orc_group_key, the weights of
+ * each large head from its own small head, then stage 3. */
+static int group_step(const orc_step_in *in, const orc_step_out *out, int b, int n, int ns,
+                      int64_t srows, const double *ms, const double *zs) {
+  const int l = in->s_layers, hqs = in->s_q_heads;
+  const int L = in->l_layers, hq = in->l_q_heads, hk = in->l_kv_heads, d = in->l_dim;
+  const int nsh = l * hqs, gl = hq / hk;
+  if (in->s_held) return ORC_EINVAL; /* group keys need every token scored */
+  (void)srows;
+  float *F = (float *)malloc(sizeof(float) * (size_t)n);
+  float *zq = (float *)malloc(sizeof(float) * (size_t)nsh);
+  float *mf = (float *)malloc(sizeof(float) * (size_t)gl);
+  float *zg = (float *)malloc(sizeof(float) * (size_t)gl);
+  const float **rows = (const float **)malloc(sizeof(float *) * (size_t)gl);
+  double *scratch = (double *)malloc(sizeof(double) * (size_t)(in->km_cap > 0 ? in->km_cap : 1));
+  int rc = (F && zq && mf && zg && rows && scratch) ? ORC_OK : ORC_EINVAL;
+  for (int j = 0; j < nsh && rc == ORC_OK; ++j)
+    zq[j] = orc_zq(n, out->logits + ((size_t)b * nsh + j) * (size_t)in->n_cap, (float)ms[j]);
+  for (int li = 0; li < L && rc == ORC_OK; ++li)
+    for (int g = 0; g < hk && rc == ORC_OK; ++g) {
+      for (int h = 0; h < gl; ++h) {
+        const int j = in->head_map[li * hq + g * gl + h];
+        if (j < 0 || j >= nsh) {
+          rc = ORC_EINVAL;
+          break;
+        }
+        rows[h] = out->logits + ((size_t)b * nsh + j) * (size_t)in->n_cap;
+        mf[h] = (float)ms[j];
+        zg[h] = zq[j];
+      }
+      if (rc) break;
+      orc_group_key(n, gl, rows, mf, zg, F);
+      const size_t grow = ((size_t)b * L + li) * hk + g;
+      int32_t *crit = out->crit + grow * in->kc_cap, *marg = out->marg + grow * in->km_cap;
+      double mass_g[2];
+      int nc, nm;
+      /* the lists only: the p' this computes from F are not used */
+      rc = orc_partition(n, in->k_crit[b], in->k_marg[b], in->k_recent ? in->k_recent[b] : 0, F,
+                         0.0, 1.0, crit, in->kc_cap, marg, scratch, in->km_cap, mass_g, &nc, &nm);
+      if (rc) break;
+      for (int h = 0; h < gl && rc == ORC_OK; ++h) {
+        const int hh = g * gl + h, j = in->head_map[li * hq + hh];
+        const float *lg = out->logits + ((size_t)b * nsh + j) * (size_t)in->n_cap;
+        const size_t prow = ((size_t)b * L + li) * hq + hh;
+        double *mp = out->marg_prob + prow * in->km_cap, *mass = out->mass + prow * 2;
+        mass[0] = mass[1] = 0.0;
+        for (int i = 0; i < nc; ++i) mass[0] += exp((double)lg[crit[i]] - ms[j]) / zs[j];
+        for (int i = 0; i < in->km_cap; ++i) {
+          mp[i] = i < nm ? exp((double)lg[marg[i]] - ms[j]) / zs[j] : 0.0;
+          mass[1] += mp[i];
+        }
+        const size_t unit = ((size_t)b * L + li) * hk + g;
+        const size_t kv = unit * (size_t)in->l_rows * d;
+        const int32_t *ks = in->k_slot ? in->k_slot + unit * in->n_cap : NULL;
+        const int32_t *vs = in->v_slot ? in->v_slot + unit * in->n_cap : NULL;
+        rc = orc_hybrid_head(d, in->l_scale, in->l_q + prow * d, in->l_k + kv, in->l_v + kv, ks,
+                             vs, nc, crit, nm, marg, mp, mass, in->mode,
+                             out->large_out + prow * d);
+      }
+    }
+  (void)ns;
+  free(F);
+  free(zq);
+  free(mf);
+  free(zg);
+  free(rows);
+  free(scratch);
+  return rc;
+}
+
 int orc_step(const orc_step_in *in, const orc_step_out *out) {
   const int B = in->batch, ncap = in->n_cap;
   const int l = in->s_layers, hqs = in->s_q_heads, hks = in->s_kv_heads,
@@ -306,6 +402,7 @@ int orc_step(const orc_step_in *in, const orc_step_out *out) {
       if (rc != ORC_OK) break;
       out->row_max[row] = ms[j];
       out->row_sum[row] = zs[j];
+      if (in->select == ORC_SELECT_GROUP) continue; /* selected per group below */
       rc = orc_partition(ns, in->k_crit[b], in->k_marg[b], in->k_recent ? in->k_recent[b] : 0,
                          out->logits + row * srows, ms[j], zs[j],
                          out->crit + row * in->kc_cap, in->kc_cap,
@@ -320,6 +417,10 @@ int orc_step(const orc_step_in *in, const orc_step_out *out) {
         out->crit[row * in->kc_cap + i] = pos[out->crit[row * in->kc_cap + i]];
       for (int i = 0; i < nm[j] && rc == ORC_OK; ++i)
         out->marg[row * in->km_cap + i] = pos[out->marg[row * in->km_cap + i]];
+    }
+    if (rc == ORC_OK && in->select == ORC_SELECT_GROUP) {
+      rc = group_step(in, out, b, n, ns, srows, ms, zs);
+      continue;
     }
     /* stage 3 for every large head (layer, h) through j = f(layer, h) */
     for (int li = 0; li < L && rc == ORC_OK; ++li) {

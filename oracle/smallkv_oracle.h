@@ -128,7 +128,26 @@ typedef struct {
   const int32_t *k_slot, *v_slot;
   const int32_t *head_map;
   int32_t mode;
+  /* selection granularity: ORC_SELECT_HEAD (each large head takes the sets of
+   * its small head f(i)) or ORC_SELECT_GROUP (the query heads of one large
+   * kv head share one selection, ranked by the sum of their small heads'
+   * probabilities: orc_group_key).  Group mode writes crit/marg per group,
+   * [B][L*Hkv][cap], and marg_prob/mass per large head, [B][L*Hq][...]. */
+  int32_t select;
 } orc_step_in;
+
+enum { ORC_SELECT_HEAD = 0, ORC_SELECT_GROUP = 1 };
+
+/* The normaliser of one small head for the group key: Zq = the exact integer
+ * sum over t < n of floor(orc_exp(logits[t] - m) * 2^40); returns the fp32
+ * value nearest Zq, times 2^-40 (m: the row's maximum logit). */
+float orc_zq(int n, const float *logits, float m);
+
+/* Group key of token t: ((p_0 + p_1) + ...) + p_{g-1} in fp32 over the group's
+ * query heads in ascending order, p_h = orc_exp(logit_h[t] - m_h) / Zq_h
+ * (fp32 division).  logits[h] points at head h's row; writes F[0..n). */
+void orc_group_key(int n, int g, const float *const *logits, const float *m, const float *zq,
+                   float *F);
 
 typedef struct {
   float *logits;

@@ -570,3 +570,121 @@ def test_step_rejects_a_bad_position_map():
     for bad in (good[..., ::-1].copy(), good + 20):  # descending; beyond the sequence
         with pytest.raises(O.OracleError):
             O.step(**args, s_row_pos=bad)
+
+
+# ------------------------------------------------- group selection (GQA) --
+
+def test_zq_closed_form_and_error_bound():
+    # equal logits: every term is exactly 2^40, so Zq = n exactly
+    for n in (1, 7, 4096, 65536):
+        assert O.zq(np.full(n, 0.37, np.float32), 0.37) == np.float32(n)
+    rng = np.random.default_rng(31)
+    for n, sc in ((100, 1.0), (8192, 3.0), (65536, 0.5)):
+        s = (rng.standard_normal(n) * sc).astype(np.float32)
+        s[:4] += 8 * sc  # sink-like
+        m = np.float32(s.max())
+        z = float(O.zq(s, m))
+        ref = float(np.exp(s.astype(np.float64) - float(m)).sum())
+        # truncation (< 2^-40 per term), exp (1 ulp) and the final rounding
+        assert abs(z - ref) <= n * 2.0 ** -40 + 3e-7 * ref, (n, z, ref)
+
+
+def _group_case(rng, B=1, n=96, l=2, hqs=4, hks=2, ds=16, L=2, hq=8, hk=2, d=128, separated=True,
+                head_map=None):
+    f = lambda *s: rng.standard_normal(s).astype(np.float32)
+    sq, sk, sv = f(B, l, hqs, ds), f(B, l, hks, n, ds), f(B, l, hks, n, ds)
+    if separated:
+        # logits of every small head are distinct and at least 0.02 apart:
+        # q = e_0, k_t[0] = a permutation of an arithmetic sequence
+        sq[:] = 0.0
+        sq[..., 0] = np.sqrt(ds)
+        for b in range(B):
+            for la in range(l):
+                for g in range(hks):
+                    sk[b, la, g, :, 0] = rng.permutation(np.arange(n) * 0.02 - 1.0)
+                    sk[b, la, g, :, 1:] = 0.0
+    lq, lk, lv = f(B, L, hq, d), f(B, L, hk, n, d), f(B, L, hk, n, d)
+    hm = rng.integers(0, l * hqs, L * hq).astype(np.int32) if head_map is None else head_map
+    return dict(seq_len=np.full(B, n, np.int32), s_q=sq, s_k=sk, s_v=sv, s_scale=1 / np.sqrt(ds),
+                l_q=lq, l_k=lk, l_v=lv, l_scale=SCALE128, head_map=hm)
+
+
+def _run(x, kc, km, select, kr=None, mode=O.NORM_REMAINING):
+    B = x["seq_len"].size
+    return O.step(**x, k_crit=np.full(B, kc, np.int32), k_marg=np.full(B, km, np.int32),
+                  kc_cap=kc + (kr or 0), km_cap=km, mode=mode, select=select,
+                  k_recent=None if kr is None else np.full(B, kr, np.int32))
+
+
+def test_group_selection_of_one_head_groups_is_per_head_selection():
+    rng = np.random.default_rng(32)
+    x = _group_case(rng, L=2, hq=4, hk=4)  # every kv head serves one query head
+    for kr in (None, 5):
+        head = _run(x, 9, 14, O.SELECT_HEAD, kr)
+        grp = _run(x, 9, 14, O.SELECT_GROUP, kr)
+        hm = x["head_map"]
+        for i in range(8):
+            j = hm[i]
+            np.testing.assert_array_equal(grp["crit"][0, i], head["crit"][0, j])
+            np.testing.assert_array_equal(grp["marg"][0, i], head["marg"][0, j])
+            np.testing.assert_allclose(grp["marg_prob"][0, i], head["marg_prob"][0, j], rtol=1e-12)
+            np.testing.assert_allclose(grp["mass"][0, i], head["mass"][0, j], rtol=1e-12)
+        np.testing.assert_allclose(grp["large_out"], head["large_out"], rtol=1e-12, atol=1e-15)
+
+
+def test_group_whose_heads_share_a_small_head_selects_like_it():
+    rng = np.random.default_rng(33)
+    hm = np.repeat(rng.integers(0, 8, 4), 4).astype(np.int32)  # 4 groups of 4 query heads
+    x = _group_case(rng, L=2, hq=8, hk=2, head_map=hm)
+    head = _run(x, 7, 11, O.SELECT_HEAD)
+    grp = _run(x, 7, 11, O.SELECT_GROUP)
+    for gi in range(4):
+        j = hm[4 * gi]
+        np.testing.assert_array_equal(grp["crit"][0, gi], head["crit"][0, j])
+        np.testing.assert_array_equal(grp["marg"][0, gi], head["marg"][0, j])
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_group_selection_is_the_top_of_the_exact_sum(seed):
+    """The group's C and M are a top-|C| and next-|M| of the fp64 sum of the
+    heads' probabilities, up to fp32 rounding; weights are each head's own."""
+    rng = np.random.default_rng(40 + seed)
+    x = _group_case(rng, n=150, separated=False)
+    kc, km = 12, 20
+    r = _run(x, kc, km, O.SELECT_GROUP)
+    L, hq, hk = 2, 8, 2
+    gq = hq // hk
+    logits = r["logits"][0].astype(np.float64)
+    p = np.exp(logits - logits.max(1, keepdims=True))
+    p /= p.sum(1, keepdims=True)
+    for li in range(L):
+        for g in range(hk):
+            js = x["head_map"][li * hq + g * gq: li * hq + (g + 1) * gq]
+            F = p[js].sum(0)
+            c = r["crit"][0, li * hk + g]
+            m = r["marg"][0, li * hk + g]
+            assert c.size == kc and m.size == km and not set(c) & set(m)
+            rest = np.setdiff1d(np.arange(150), np.concatenate([c, m]))
+            tol = 1e-5 * F.max()
+            assert F[c].min() >= F[np.concatenate([m, rest])].max() - tol
+            assert F[m].min() >= F[rest].max() - tol
+            for h in range(gq):
+                i = li * hq + g * gq + h
+                np.testing.assert_allclose(r["marg_prob"][0, i], p[js[h], m], rtol=1e-12)
+                np.testing.assert_allclose(r["mass"][0, i], [p[js[h], c].sum(), p[js[h], m].sum()],
+                                           rtol=1e-12)
+
+
+def test_group_selection_with_everything_critical_is_full_attention():
+    rng = np.random.default_rng(34)
+    x = _group_case(rng, n=60, separated=False)
+    r = _run(x, 60, 0, O.SELECT_GROUP)
+    lq, lk, lv = x["l_q"], x["l_k"], x["l_v"]
+    for li in range(2):
+        for h in range(8):
+            g = h // 4
+            s = (lk[0, li, g].astype(np.float64) @ lq[0, li, h].astype(np.float64)) * SCALE128
+            w = np.exp(s - s.max())
+            w /= w.sum()
+            np.testing.assert_allclose(r["large_out"][0, li, h], w @ lv[0, li, g].astype(np.float64),
+                                       rtol=1e-9, atol=1e-12)
