@@ -175,6 +175,7 @@ def main():
 
     # ---- per-stage kernel durations with HIP events -------------------------
     nsh = w.small.layers * w.small.q_heads
+    group = w.select == 1
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
     torch.cuda._sleep(50_000_000)  # keep the GPU busy while the host enqueues
     for i in range(K):
@@ -184,11 +185,17 @@ def main():
         e[0].record(stream)
         S.smallkv_small_attn(ps.batch, ps.small, b.logits, b.row_max, b.row_sum, b.ws, stream)
         e[1].record(stream)
-        S.smallkv_partition(ps.batch, nsh, b.logits, b.row_max, b.row_sum, b.crit_idx,
-                            b.marg_idx, b.marg_prob, b.mass, None, stream, small=ps.small)
+        if group:
+            S.smallkv_group_select(ps.batch, ps.small, ps.large, ps.head_map, b.logits, b.row_max,
+                                   b.row_sum, b.crit_idx, b.marg_idx, b.marg_prob, b.mass, b.ws,
+                                   stream)
+        else:
+            S.smallkv_partition(ps.batch, nsh, b.logits, b.row_max, b.row_sum, b.crit_idx,
+                                b.marg_idx, b.marg_prob, b.mass, None, stream, small=ps.small)
         e[2].record(stream)
         S.smallkv_hybrid_attn(ps.batch, ps.large, ps.head_map, nsh, b.crit_idx, b.marg_idx,
-                              b.marg_prob, b.mass, ps.mode, b.ws, stream)
+                              b.marg_prob, b.mass, ps.mode, b.ws, stream,
+                              select=S.SELECT_GROUP if group else S.SELECT_HEAD)
         e[3].record(stream)
     torch.cuda.synchronize()
     stage_ms = [sum(ev[i][s].elapsed_time(ev[i][s + 1]) for i in range(K)) / K for s in range(3)]
@@ -200,8 +207,9 @@ def main():
     # kernels each single-stage call launches for this workload (bf16, large
     # head_dim 128, 7 query heads per kv head, 112 kv-head units: stage 3 is
     # the grouped kernel over token splits plus their merge)
-    stage_kernels = [["small_attn_mfma", "small_attn_merge"], ["partition_kernel"],
-                     stage3_kernels(w)]
+    stage_kernels = [["small_attn_mfma", "small_attn_merge"],
+                     ["group_zq", "group_scores", "partition_kernel", "group_weights"] if group
+                     else ["partition_kernel"], stage3_kernels(w)]
     dom = max(range(3), key=lambda s: stage_ms[s])
     achieved = stage_bytes[dom] / (stage_ms[dom] * 1e-3) / 1e9
     traffic = load_traffic(stage_kernels[dom], w.name)
@@ -223,6 +231,8 @@ def main():
         host["k_recent"] = h(x["k_recent"]) if x.get("k_recent") is not None else None
         held = {} if x.get("s_held") is None else dict(
             s_held=h(x["s_held"]), s_row_pos=h(x["s_row_pos"]), n_cap=x["n_cap"])
+        if group:
+            held["select"] = O.SELECT_GROUP
         try:
             os.sched_setaffinity(0, {sorted(os.sched_getaffinity(0))[0]})
         except (AttributeError, OSError):
@@ -263,6 +273,7 @@ def main():
             "critical": budget_text(w.crit), "marginal": budget_text(w.marg),
             **({"recent": budget_text(w.recent)} if w.recent != ("abs", 0) else {}),
             **({"small_cache_kept": f"{w.slm_keep}%"} if w.slm_keep else {}),
+            **({"selection": "one per large kv head (summed)"} if group else {}),
             "launch": "eager" if args.eager else "hip-graph",
             "rotated_input_copies": args.rotate,
         },

@@ -52,7 +52,7 @@
 extern "C" {
 #endif
 
-#define SMALLKV_ABI_VERSION 4
+#define SMALLKV_ABI_VERSION 5
 
 typedef enum { SMALLKV_F32 = 0, SMALLKV_BF16 = 1 } smallkv_dtype_t;
 
@@ -181,17 +181,59 @@ int smallkv_partition(const smallkv_batch_t *batch, const smallkv_model_t *small
  *   O_c = sum_C softmax_C(s)_t V_g[row(t)],  O_m = sum_M marg_prob_t V_g[row(t)]
  *   large->out = alpha_C * O_c + alpha_M * O_m   (alphas from `mode` and mass[b][j])
  * head_map: [n_layers * n_q_heads] int32 (device).  Rows come from
- * large->k_slot / v_slot when given. */
+ * large->k_slot / v_slot when given.  select = SMALLKV_SELECT_GROUP: the
+ * lists are those of the large head's (layer, kv head) and marg_prob / mass
+ * its own (the layouts of smallkv_group_select). */
 int smallkv_hybrid_attn(const smallkv_batch_t *batch, const smallkv_model_t *large,
                         const int32_t *head_map, int32_t n_small_heads,
                         const int32_t *crit_idx, const int32_t *marg_idx,
                         const float *marg_prob, const float *mass, int32_t mode,
-                        void *ws, size_t ws_bytes, void *stream);
+                        int32_t select, void *ws, size_t ws_bytes, void *stream);
+
+/* Stage 2 of SMALLKV_SELECT_GROUP (see smallkv_select_t): from stage 1's
+ * logits, row_max and row_sum, the lists of every (sequence, large layer, kv
+ * head), crit_idx [B][L*Hkv][kc_cap] and marg_idx [B][L*Hkv][km_cap], and the
+ * weights of every large query head, marg_prob [B][L*Hq][km_cap] (its own
+ * small head's p' on the group's marginal list) and mass [B][L*Hq][2].  Only
+ * the shapes of `large` are read.  ws: smallkv_group_select_workspace_size. */
+int smallkv_group_select(const smallkv_batch_t *batch, const smallkv_model_t *small,
+                         const smallkv_model_t *large, const int32_t *head_map,
+                         const float *logits, const float *row_max, const float *row_sum,
+                         int32_t *crit_idx, int32_t *marg_idx, float *marg_prob, float *mass,
+                         void *ws, size_t ws_bytes, void *stream);
+int smallkv_group_select_workspace_size(const smallkv_batch_t *batch,
+                                        const smallkv_model_t *small,
+                                        const smallkv_model_t *large, size_t *bytes);
+
+/* Who shares a selection (smallkv_step_t.select). */
+typedef enum {
+  SMALLKV_SELECT_HEAD = 0,  /* default: each large head i takes the sets of its
+                               small head f(i) (the partition of stage 2) */
+  SMALLKV_SELECT_GROUP = 1  /* the query heads of one large kv head share one
+                               critical and one marginal set (the cache is
+                               stored per kv head), ranked by
+                               F(t) = sum over the group's heads h of
+                               p_f(h)(t) -- the implementation pseudocode's
+                               `.sum.topk` (Appendix D).  F decides integers and
+                               is evaluated one way: e = exp32(logit - row_max)
+                               (exp32 as for smallkv_match), Zq = the exact
+                               integer sum over the row of floor(e * 2^40),
+                               Z = fp32(Zq) * 2^-40, F = ((e_0/Z_0 + e_1/Z_1) +
+                               ...) in fp32 over the group's heads in ascending
+                               order; ranked like the partition (F descending,
+                               index ascending; recent tokens first).  Each
+                               head keeps its own p' = exp(logit - row_max) /
+                               row_sum on the shared marginal set. */
+} smallkv_select_t;
 
 /* A whole decode step: stage 1 over every small layer, stage 2 over every
  * small head, stage 3 over every large layer, enqueued back to back on one
  * stream.  The intermediate buffers are the caller's, laid out as above,
- * with n_small_heads = small.n_layers * small.n_q_heads. */
+ * with n_small_heads = small.n_layers * small.n_q_heads.  With
+ * SMALLKV_SELECT_GROUP: crit_idx and marg_idx are [B][L*Hkv][cap] (one row
+ * per large layer and kv head), marg_prob [B][L*Hq][km_cap] and mass
+ * [B][L*Hq][2] (one row per large query head); the small model's cache must
+ * hold every token (small.held NULL) and L's query heads per kv head <= 16. */
 typedef struct {
   smallkv_batch_t batch;
   smallkv_model_t small, large;
@@ -200,6 +242,7 @@ typedef struct {
   float *logits, *row_max, *row_sum;
   int32_t *crit_idx, *marg_idx;
   float *marg_prob, *mass;
+  int32_t select;          /* smallkv_select_t */
 } smallkv_step_t;
 
 int smallkv_step(const smallkv_step_t *step, void *ws, size_t ws_bytes, void *stream);

@@ -83,11 +83,14 @@ def step_bytes(x: dict, crit_idx: torch.Tensor, marg_idx: torch.Tensor, km_cap: 
     hm = x["head_map"].to(torch.int64).to(dev).view(L, hk, g)
     rowb = d * esz
     k_union = v_union = k_per = v_per = meta = 0
+    group = x.get("select", 0) == 1  # lists per (large layer, kv head): the union is the list
     for b in range(B):
-        c = crit_idx[b].to(torch.int64)          # [nsh][kc]
+        c = crit_idx[b].to(torch.int64)          # [nsh][kc] (group selection: [L*hk][kc])
         m = marg_idx[b, :, :km_cap].to(torch.int64) if km_cap else None
         for li in range(L):
             js = hm[li]                          # [hk][g]
+            if group:
+                js = (li * hk + torch.arange(hk, device=dev))[:, None].expand(hk, g)
             cs = c[js.reshape(-1)].view(hk, -1)  # [hk][g*kc]
             bm = torch.zeros((hk, n_cap + 1), dtype=torch.bool, device=dev)
             bm.scatter_(1, torch.where(cs >= 0, cs, n_cap), True)

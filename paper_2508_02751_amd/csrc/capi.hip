@@ -75,14 +75,21 @@ smallkv_batch_t small_view(const smallkv_batch_t &b, const smallkv_model_t &s) {
 // 3's split records, and after both the partition's list offsets, which
 // stage 2 writes while it reads stage 1's records and stage 3 reads while it
 // writes its own (grouped stage 3 only).
+// With group selection the group intermediates also start at offset 0:
+// they are written after stage 1's merge and read before stage 3.
 struct StepLayout {
   size_t tab_offset, tab_bytes, total;
 };
 StepLayout step_layout(const smallkv_batch_t &b, const smallkv_model_t &small,
-                       const smallkv_model_t &large, int nsh) {
+                       const smallkv_model_t &large, int nsh, int select) {
   const SmallPlan p = plan_small(small_view(b, small), small);
   const GroupPlan gp = plan_group(b, large, nsh);
   StepLayout l{};
+  if (select == SMALLKV_SELECT_GROUP) {
+    l.total = max_sz(max_sz(p.ws_bytes, gp.use ? gp.ws_bytes : 0),
+                     group_layout(b, small, large, 0).end);
+    return l;
+  }
   l.tab_offset = (max_sz(p.ws_bytes, gp.use ? gp.ws_bytes : 0) + 255) / 256 * 256;
   // (with one token range per kv head every cursor starts at 0: no offsets;
   // the partition writes them in row order, so not with held rows either)
@@ -94,12 +101,13 @@ StepLayout step_layout(const smallkv_batch_t &b, const smallkv_model_t &small,
 // Stage 3: the grouped kernel where it applies, the per-head kernel otherwise.
 hipError_t launch_stage3(const smallkv_batch_t &b, const smallkv_model_t &l, const int32_t *head_map,
                          int nsh, const int32_t *crit, const int32_t *marg, const float *marg_prob,
-                         const float *mass, int mode, void *ws, const int2 *tab, hipStream_t st) {
+                         const float *mass, int mode, void *ws, const int2 *tab, bool group_sel,
+                         hipStream_t st) {
   const GroupPlan gp = plan_group(b, l, nsh);
   if (gp.use)
     return launch_hybrid_group(b, l, head_map, nsh, crit, marg, marg_prob, mass, mode, gp,
-                               static_cast<float *>(ws), tab, st);
-  return launch_hybrid(b, l, head_map, nsh, crit, marg, marg_prob, mass, mode, st);
+                               static_cast<float *>(ws), tab, group_sel, st);
+  return launch_hybrid(b, l, head_map, nsh, crit, marg, marg_prob, mass, mode, group_sel, st);
 }
 
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
@@ -157,7 +165,9 @@ int smallkv_workspace_size(const smallkv_step_t *step, size_t *bytes) {
   if (rc) return rc;
   const int nsh = step->small.n_layers * step->small.n_q_heads;
   if ((rc = check_large(&step->batch, &step->large, step->head_map, nsh))) return rc;
-  *bytes = step_layout(step->batch, step->small, step->large, nsh).total;
+  if (step->select != SMALLKV_SELECT_HEAD && step->select != SMALLKV_SELECT_GROUP)
+    return SMALLKV_EINVAL;
+  *bytes = step_layout(step->batch, step->small, step->large, nsh, step->select).total;
   return SMALLKV_OK;
 }
 
@@ -199,17 +209,49 @@ int smallkv_partition(const smallkv_batch_t *batch, const smallkv_model_t *small
 int smallkv_hybrid_attn(const smallkv_batch_t *batch, const smallkv_model_t *large,
                         const int32_t *head_map, int32_t n_small_heads, const int32_t *crit_idx,
                         const int32_t *marg_idx, const float *marg_prob, const float *mass,
-                        int32_t mode, void *ws, size_t ws_bytes, void *stream) {
+                        int32_t mode, int32_t select, void *ws, size_t ws_bytes, void *stream) {
   int rc = check_large(batch, large, head_map, n_small_heads);
   if (rc) return rc;
   if ((rc = check_mode(mode))) return rc;
+  if (select != SMALLKV_SELECT_HEAD && select != SMALLKV_SELECT_GROUP) return SMALLKV_EINVAL;
   if (!crit_idx || !mass) return SMALLKV_EINVAL;
   if (batch->km_cap > 0 && (!marg_idx || !marg_prob)) return SMALLKV_EINVAL;
   const GroupPlan gp = plan_group(*batch, *large, n_small_heads);
   if (gp.use && gp.ws_bytes && (!ws || ws_bytes < gp.ws_bytes)) return SMALLKV_EWORKSPACE;
   return status_of(launch_stage3(*batch, *large, head_map, n_small_heads, crit_idx, marg_idx,
                                  marg_prob, mass, mode, ws, nullptr,
+                                 select == SMALLKV_SELECT_GROUP,
                                  static_cast<hipStream_t>(stream)));
+}
+
+int smallkv_group_select_workspace_size(const smallkv_batch_t *batch,
+                                        const smallkv_model_t *small,
+                                        const smallkv_model_t *large, size_t *bytes) {
+  if (!bytes || !large) return SMALLKV_EINVAL;
+  int rc = check_small(batch, small);
+  if (rc) return rc;
+  if (!model_ok(large)) return SMALLKV_EINVAL;
+  *bytes = group_layout(*batch, *small, *large, 0).end;
+  return SMALLKV_OK;
+}
+
+int smallkv_group_select(const smallkv_batch_t *batch, const smallkv_model_t *small,
+                         const smallkv_model_t *large, const int32_t *head_map,
+                         const float *logits, const float *row_max, const float *row_sum,
+                         int32_t *crit_idx, int32_t *marg_idx, float *marg_prob, float *mass,
+                         void *ws, size_t ws_bytes, void *stream) {
+  int rc = check_small(batch, small);
+  if (rc) return rc;
+  const int nsh = small->n_layers * small->n_q_heads;
+  if ((rc = check_large(batch, large, head_map, nsh))) return rc;
+  if (small->held || large->n_q_heads / large->n_kv_heads > 16) return SMALLKV_EUNSUPPORTED;
+  if (!logits || !row_max || !row_sum || !crit_idx || !mass) return SMALLKV_EINVAL;
+  if (batch->km_cap > 0 && (!marg_idx || !marg_prob)) return SMALLKV_EINVAL;
+  const GroupLayout lay = group_layout(*batch, *small, *large, 0);
+  if (!ws || ws_bytes < lay.end) return SMALLKV_EWORKSPACE;
+  return status_of(launch_group_select(*batch, *small, *large, head_map, logits, row_max, row_sum,
+                                       crit_idx, marg_idx, marg_prob, mass, ws, lay,
+                                       static_cast<hipStream_t>(stream)));
 }
 
 int smallkv_match_workspace_size(const smallkv_match_t *m, size_t *bytes) {
@@ -236,11 +278,27 @@ int smallkv_step(const smallkv_step_t *s, void *ws, size_t ws_bytes, void *strea
   if ((rc = check_mode(s->mode))) return rc;
   if (!s->logits || !s->row_max || !s->row_sum || !s->crit_idx || !s->mass) return SMALLKV_EINVAL;
   if (s->batch.km_cap > 0 && (!s->marg_idx || !s->marg_prob)) return SMALLKV_EINVAL;
+  const bool group = s->select == SMALLKV_SELECT_GROUP;
+  if (!group && s->select != SMALLKV_SELECT_HEAD) return SMALLKV_EINVAL;
+  if (group && (s->small.held || s->large.n_q_heads / s->large.n_kv_heads > 16))
+    return SMALLKV_EUNSUPPORTED;
   const smallkv_batch_t sb = small_view(s->batch, s->small);
   const SmallPlan p = plan_small(sb, s->small);
-  const StepLayout lay = step_layout(s->batch, s->small, s->large, nsh);
+  const StepLayout lay = step_layout(s->batch, s->small, s->large, nsh, s->select);
   if (lay.total && (!ws || ws_bytes < lay.total)) return SMALLKV_EWORKSPACE;
   hipStream_t st = static_cast<hipStream_t>(stream);
+  if (group) {
+    // stage 1 with its own merge, the group selection, stage 3 on its sets
+    hipError_t e = launch_small_attn(sb, s->small, s->logits, s->row_max, s->row_sum,
+                                     static_cast<float *>(ws), p, st);
+    if (e != hipSuccess) return SMALLKV_EDEVICE;
+    e = launch_group_select(s->batch, s->small, s->large, s->head_map, s->logits, s->row_max,
+                            s->row_sum, s->crit_idx, s->marg_idx, s->marg_prob, s->mass, ws,
+                            group_layout(s->batch, s->small, s->large, 0), st);
+    if (e != hipSuccess) return SMALLKV_EDEVICE;
+    return status_of(launch_stage3(s->batch, s->large, s->head_map, nsh, s->crit_idx, s->marg_idx,
+                                   s->marg_prob, s->mass, s->mode, ws, nullptr, true, st));
+  }
   int2 *tab = lay.tab_bytes ? reinterpret_cast<int2 *>(static_cast<char *>(ws) + lay.tab_offset)
                             : nullptr;
   hipError_t e = launch_small_split(sb, s->small, s->logits, static_cast<float *>(ws), p, st);
@@ -252,7 +310,7 @@ int smallkv_step(const smallkv_step_t *s, void *ws, size_t ws_bytes, void *strea
   // stage 1's records are consumed by now: stage 3 reuses the workspace
   // below the list offsets
   e = launch_stage3(s->batch, s->large, s->head_map, nsh, s->crit_idx, s->marg_idx, s->marg_prob,
-                    s->mass, s->mode, ws, tab, st);
+                    s->mass, s->mode, ws, tab, false, st);
   return status_of(e);
 }
 

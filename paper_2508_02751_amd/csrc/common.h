@@ -94,6 +94,27 @@ __device__ __forceinline__ Sizes set_sizes(const int32_t *seq_len, const int32_t
   return s;
 }
 
+// exp(x), x <= 0: k = rne(x * fl(1/ln 2)); r = x - k*ln2 in two FMAs with ln2
+// split into a 16-bit head and a tail; e^r from the Taylor polynomial of
+// degree 7 by Horner's rule (coefficients 1/n! rounded to fp32); the result
+// scaled by 2^k exactly.  0 below -80, so no result is subnormal.
+__device__ __forceinline__ float cw_exp(float x) {
+#pragma clang fp contract(off)
+  if (!(x >= -80.0f)) return 0.0f;
+  const float k = __builtin_rintf(__fmul_rn(x, 0x1.715476p+0f));
+  float r = __builtin_fmaf(-k, 0x1.62e4p-1f, x);
+  r = __builtin_fmaf(-k, 0x1.7f7d1cp-20f, r);
+  float p = 0x1.a01a02p-13f;
+  p = __builtin_fmaf(p, r, 0x1.6c16c2p-10f);
+  p = __builtin_fmaf(p, r, 0x1.111112p-7f);
+  p = __builtin_fmaf(p, r, 0x1.555556p-5f);
+  p = __builtin_fmaf(p, r, 0x1.555556p-3f);
+  p = __builtin_fmaf(p, r, 0.5f);
+  p = __builtin_fmaf(p, r, 1.0f);
+  p = __builtin_fmaf(p, r, 1.0f);
+  return ldexpf(p, (int)k);
+}
+
 // Order-preserving uint32 key of an fp32 logit; -0 and +0 share a key.
 __device__ __forceinline__ uint32_t logit_key(float s) {
   uint32_t u = __float_as_uint(s == 0.0f ? 0.0f : s);

@@ -36,6 +36,7 @@ struct HybArgs {
   const int32_t *crit, *marg;
   const float *marg_prob, *mass;
   void *out;
+  int group_sel;  // lists per (b, layer, kv head), marg_prob/mass per query head
 };
 
 __device__ __forceinline__ void alphas(int mode, float sc, float sm, float &ac, float &am) {
@@ -103,14 +104,16 @@ __global__ __launch_bounds__(kHT) void hybrid_kernel(HybArgs a) {
   const int kvh = u % a.hkv, bl = u / a.hkv, layer = bl % a.layers, b = bl / a.layers;
   const int h = kvh * a.g + hh;
   const int j = clampi(a.head_map[layer * a.hq + h], 0, a.nsh - 1);
-  const int64_t row = (int64_t)b * a.nsh + j;
+  const int64_t qrow = ((int64_t)b * a.layers + layer) * a.hq + h;
+  // lists of the small head f(i), or of the group; weights of f(i), or of the head
+  const int64_t lrow = a.group_sel ? (int64_t)u : (int64_t)b * a.nsh + j;
+  const int64_t row = a.group_sel ? qrow : lrow;
   const Sizes sz = set_sizes(a.seq_len, a.k_crit, a.k_marg, a.k_recent, b, a.n_cap, a.kc_cap, a.km_cap);
   const int nc = sz.nc, nm = sz.nm, ntot = sz.nc + sz.nm;
-  const int32_t *crit = a.crit + row * a.kc_cap;
-  const int32_t *marg = a.marg + row * a.km_cap;
+  const int32_t *crit = a.crit + lrow * a.kc_cap;
+  const int32_t *marg = a.marg + lrow * a.km_cap;
   const float *mp = a.marg_prob + row * a.km_cap;
 
-  const int64_t qrow = ((int64_t)b * a.layers + layer) * a.hq + h;
   float qv[EPL];
   elem<T>::unpack(*reinterpret_cast<const uint4 *>(reinterpret_cast<const unsigned char *>(a.q) +
                                                    (qrow * D + sub * EPL) * (int64_t)sizeof(T)),
@@ -235,8 +238,9 @@ __global__ __launch_bounds__(kHT) void hybrid_kernel(HybArgs a) {
 hipError_t launch_hybrid(const smallkv_batch_t &b, const smallkv_model_t &m,
                          const int32_t *head_map, int n_small_heads, const int32_t *crit,
                          const int32_t *marg, const float *marg_prob, const float *mass,
-                         int mode, hipStream_t st) {
+                         int mode, bool group_sel, hipStream_t st) {
   HybArgs a;
+  a.group_sel = group_sel ? 1 : 0;
   a.n_cap = b.n_cap;
   a.layers = m.n_layers;
   a.hq = m.n_q_heads;

@@ -27,6 +27,8 @@
 // they all scan stay in that XCD's L2.
 #include <limits.h>
 
+#include <algorithm>
+
 #include "common.h"
 #include "launch.h"
 
@@ -77,6 +79,7 @@ struct GroupArgs {
   void *out;
   const int2 *tab;  // the partition's list offsets ([rows][nblk]), or null
   int nblk;
+  int group_sel;    // lists per (b, layer, kv head), marg_prob/mass per query head
 };
 
 struct WaveTiles {
@@ -92,7 +95,8 @@ struct GroupShared {
   int cur[2 * kMaxG];           // list cursors (first entry not yet consumed)
   int mstart[kMaxG];            // M-list cursor at the window start
   int wcnt[kGW][kMaxG];         // marginal entries per head in each wave's rows
-  int64_t hrow[kMaxG];          // small-model row (b, j) of each head
+  int64_t hrow[kMaxG];          // row of each head's lists: small head (b, j), or its group
+  int64_t prow[kMaxG];          // row of each head's marg_prob and mass
   float ac[kMaxG], am[kMaxG];
 };
 
@@ -250,13 +254,17 @@ __global__ __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2))) void h
   if (tid < g) {
     const int j = clampi(a.head_map[layer * a.hq + kvh * g + tid], 0, a.nsh - 1);
     const int64_t row = (int64_t)b * a.nsh + j;
-    sh.hrow[tid] = row;
+    const int64_t qrow = ((int64_t)b * a.layers + layer) * a.hq + (int64_t)kvh * g + tid;
+    sh.hrow[tid] = a.group_sel ? (int64_t)u : row;
+    const int64_t prow = a.group_sel ? qrow : row;
+    sh.prow[tid] = prow;
     float ac, am;
-    alphas(a.mode, a.mass[2 * row], a.mass[2 * row + 1], ac, am);
+    alphas(a.mode, a.mass[2 * prow], a.mass[2 * prow + 1], ac, am);
     sh.ac[tid] = ac;
     sh.am[tid] = am;
   } else if (tid < kMaxG) {
     sh.hrow[tid] = 0;
+    sh.prow[tid] = 0;
     sh.ac[tid] = 0.0f;
     sh.am[tid] = 0.0f;
   }
@@ -434,7 +442,7 @@ __global__ __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2))) void h
     for (int h = 0; h < kMaxG; ++h) {
       int p = 0;
       if (h < g) {
-        p = (int)(sh.hrow[h] * a.km_cap) + sh.mstart[h];
+        p = (int)(sh.prow[h] * a.km_cap) + sh.mstart[h];
         for (int w = 0; w < wave; ++w) p += sh.wcnt[w][h];
       }
       mpos[h] = __builtin_amdgcn_readfirstlane(p);
@@ -675,7 +683,7 @@ __global__ __launch_bounds__(kD) void hybrid_group_merge(GroupArgs a) {
   const int g = a.g;
   const int64_t qrow = ((int64_t)b * a.layers + layer) * a.hq + (int64_t)kvh * g + h;
   const int j = clampi(a.head_map[layer * a.hq + kvh * g + h], 0, a.nsh - 1);
-  const int64_t row = (int64_t)b * a.nsh + j;
+  const int64_t row = a.group_sel ? qrow : (int64_t)b * a.nsh + j;
   float ac, am;
   alphas(a.mode, a.mass[2 * row], a.mass[2 * row + 1], ac, am);
   const float *rec0 = a.rec + ((int64_t)u * a.n_split * g + h) * kRec;
@@ -701,7 +709,8 @@ GroupPlan plan_group(const smallkv_batch_t &b, const smallkv_model_t &m, int n_s
   const int g = m.n_q_heads / m.n_kv_heads;
   p.use = m.dtype == SMALLKV_BF16 && m.head_dim == kD && g <= kMaxG &&
           m.n_rows * kRowB <= kMaxBuf &&
-          (int64_t)b.batch * n_small_heads * b.km_cap * (int64_t)sizeof(float) <= kMaxBuf;
+          (int64_t)b.batch * std::max<int64_t>(n_small_heads, (int64_t)m.n_layers * m.n_q_heads) *
+                  b.km_cap * (int64_t)sizeof(float) <= kMaxBuf;  // marg_prob of either selection
   if (!p.use) return p;
   const int64_t units = (int64_t)b.batch * m.n_layers * m.n_kv_heads;
   // splits per kv head: the fewest token-equivalents on the critical path,
@@ -724,7 +733,7 @@ hipError_t launch_hybrid_group(const smallkv_batch_t &b, const smallkv_model_t &
                                const int32_t *head_map, int n_small_heads, const int32_t *crit,
                                const int32_t *marg, const float *marg_prob, const float *mass,
                                int mode, const GroupPlan &p, float *ws, const int2 *tab,
-                               hipStream_t st) {
+                               bool group_sel, hipStream_t st) {
   GroupArgs a;
   a.n_cap = b.n_cap;
   a.layers = m.n_layers;
@@ -738,7 +747,8 @@ hipError_t launch_hybrid_group(const smallkv_batch_t &b, const smallkv_model_t &
   a.units = b.batch * m.n_layers * m.n_kv_heads;
   a.n_split = p.n_split;
   a.span = p.span;
-  a.mp_bytes = (int)((int64_t)b.batch * n_small_heads * b.km_cap * (int64_t)sizeof(float));
+  const int64_t prows = group_sel ? (int64_t)m.n_layers * m.n_q_heads : n_small_heads;
+  a.mp_bytes = (int)((int64_t)b.batch * prows * b.km_cap * (int64_t)sizeof(float));
   a.n_rows = m.n_rows;
   a.scale = m.scale;
   a.seq_len = b.seq_len;
@@ -755,6 +765,7 @@ hipError_t launch_hybrid_group(const smallkv_batch_t &b, const smallkv_model_t &
   a.marg = marg;
   a.marg_prob = marg_prob;
   a.mass = mass;
+  a.group_sel = group_sel ? 1 : 0;
   a.rec = ws;
   a.tab = tab;
   a.nblk = list_blocks(b);

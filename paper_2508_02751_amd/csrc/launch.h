@@ -71,12 +71,33 @@ struct GroupPlan {
 GroupPlan plan_group(const smallkv_batch_t &b, const smallkv_model_t &m, int n_small_heads);
 
 // tab: the partition's list offsets, or null; with them the list cursors at
-// the start of each token range are read instead of searched.
+// the start of each token range are read instead of searched.  group_sel:
+// the lists are per (sequence, layer, kv head) and marg_prob / mass per
+// large query head (group selection); otherwise all are per small head f(i).
 hipError_t launch_hybrid_group(const smallkv_batch_t &b, const smallkv_model_t &m,
                                const int32_t *head_map, int n_small_heads, const int32_t *crit,
                                const int32_t *marg, const float *marg_prob, const float *mass,
                                int mode, const GroupPlan &p, float *ws, const int2 *tab,
-                               hipStream_t st);
+                               bool group_sel, hipStream_t st);
+
+// Group selection (the query heads of a kv head share one selection):
+// workspace offsets of its intermediates, placed from `offset` on.
+struct GroupLayout {
+  size_t zq, keys, key_max, part_mp, part_mass, end;
+};
+GroupLayout group_layout(const smallkv_batch_t &b, const smallkv_model_t &small,
+                         const smallkv_model_t &large, size_t offset);
+// From stage 1's logits and statistics: group lists crit/marg
+// [B][L*Hkv][cap] and per-large-head marg_prob/mass [B][L*Hq][...].
+hipError_t launch_group_select(const smallkv_batch_t &b, const smallkv_model_t &small,
+                               const smallkv_model_t &large, const int32_t *head_map,
+                               const float *logits, const float *row_max, const float *row_sum,
+                               int32_t *crit, int32_t *marg, float *marg_prob, float *mass,
+                               void *ws, const GroupLayout &lay, hipStream_t st);
+// The partition over group keys (rows [B][group_rows][n_cap], row maxima).
+hipError_t launch_group_partition(const smallkv_batch_t &b, int group_rows, const float *keys,
+                                  const float *key_max, int32_t *crit, int32_t *marg,
+                                  float *marg_prob, float *mass, hipStream_t st);
 
 // Workspace of the prefill matching: the logit matrix S of every head
 // ([B][H][w_cap][ld] fp32, ld = w_cap rounded up to 4), the row maxima per
@@ -93,6 +114,6 @@ hipError_t launch_match(const smallkv_match_t &m, void *ws, hipStream_t st);
 hipError_t launch_hybrid(const smallkv_batch_t &b, const smallkv_model_t &m,
                          const int32_t *head_map, int n_small_heads, const int32_t *crit,
                          const int32_t *marg, const float *marg_prob, const float *mass,
-                         int mode, hipStream_t st);
+                         int mode, bool group_sel, hipStream_t st);
 
 }  // namespace smallkv

@@ -36,26 +36,6 @@ namespace {
 constexpr int kTile = 64;     // tokens per side of a logit tile
 constexpr int kMatchThreads = 256;
 
-// exp(x), x <= 0: k = rne(x * fl(1/ln 2)); r = x - k*ln2 in two FMAs with ln2
-// split into a 16-bit head and a tail; e^r from the Taylor polynomial of
-// degree 7 by Horner's rule (coefficients 1/n! rounded to fp32); the result
-// scaled by 2^k exactly.  0 below -80, so no result is subnormal.
-__device__ __forceinline__ float cw_exp(float x) {
-  if (!(x >= -80.0f)) return 0.0f;
-  const float k = __builtin_rintf(__fmul_rn(x, 0x1.715476p+0f));
-  float r = __builtin_fmaf(-k, 0x1.62e4p-1f, x);
-  r = __builtin_fmaf(-k, 0x1.7f7d1cp-20f, r);
-  float p = 0x1.a01a02p-13f;
-  p = __builtin_fmaf(p, r, 0x1.6c16c2p-10f);
-  p = __builtin_fmaf(p, r, 0x1.111112p-7f);
-  p = __builtin_fmaf(p, r, 0x1.555556p-5f);
-  p = __builtin_fmaf(p, r, 0x1.555556p-3f);
-  p = __builtin_fmaf(p, r, 0.5f);
-  p = __builtin_fmaf(p, r, 1.0f);
-  p = __builtin_fmaf(p, r, 1.0f);
-  return ldexpf(p, (int)k);
-}
-
 struct LogitArgs {
   const void *q, *k;  // [B][layers][hq][w_cap][D], [B][layers][hkv][w_cap][D]
   int layers, hq, hkv, w_cap, ld, nt;  // ld: row pitch of S

@@ -234,9 +234,22 @@ __device__ __forceinline__ void row_stats(const PartArgs &a, PartShared<PT> &sh,
 // R == 0: every pass reads it from memory, four chunks in flight at a time.
 // kRecent: the row may end in recent tokens (kept unranked); without them
 // every token is ranked and the kernel carries no test for it.
-template <int R, int PT, bool kRecent>
+// Bin of a non-negative key that is a probability (or a sum of them) rather
+// than a logit: its bit pattern read as exponent + mantissa fraction, a
+// monotone stand-in for log2 with 64 bins per binade.  Exact (integer below
+// 2^24, power-of-2 scaling).
+__device__ __forceinline__ float plog2(float x) {
+  return (float)(__float_as_uint(x) >> 8) * (1.0f / 32768.0f);
+}
+
+template <int R, int PT, bool kRecent, bool kProb = false>
 struct Row {
   static constexpr int kChunk = PC<PT>::chunk;
+  // histogram bin of a key below the row's largest key M
+  __device__ static __forceinline__ int bin(float s, float M) {
+    if constexpr (kProb) return logit_bin(plog2(s), plog2(M));
+    return logit_bin(s, M);
+  }
   float s[R > 0 ? R : 4];
   const float *lg;
   int n;
@@ -336,7 +349,7 @@ __device__ __forceinline__ Targets select_targets(PartShared<PT> &sh, const RowC
   if (tid < 2) sh.ncand[tid] = 0;
   __syncthreads();
   row.each([&](float s, bool valid) {
-    if (valid) atomicAdd(&sh.hist[0][Hist<PT>::idx(logit_bin(s, M))], 1u);
+    if (valid) atomicAdd(&sh.hist[0][Hist<PT>::idx(Row::bin(s, M))], 1u);
   });
   __syncthreads();
   // every wave finds both targets' bins itself: no broadcast needed
@@ -357,7 +370,7 @@ __device__ __forceinline__ Targets select_targets(PartShared<PT> &sh, const RowC
   if (mode[0] < 2 || mode[1] < 2) {
     const uint64_t lt = lanemask_lt();
     row.each([&](float s, bool valid) {
-      const int bn = valid ? logit_bin(s, M) : -1;
+      const int bn = valid ? Row::bin(s, M) : -1;
       const uint32_t u = logit_key(s);
 #pragma unroll
       for (int x = 0; x < 2; ++x) {
@@ -421,7 +434,7 @@ __device__ __forceinline__ Targets select_targets(PartShared<PT> &sh, const RowC
         }
       if (mode[0] == 2 || mode[1] == 2)
         row.each([&](float s, bool valid) {
-          const int bn = valid ? logit_bin(s, M) : -1;
+          const int bn = valid ? Row::bin(s, M) : -1;
           const uint32_t u = logit_key(s);
           if (mode[0] == 2 && bn == bin[0] && (u & m0) == p0) atomicAdd(&sh.hist[0][Hist<PT>::idx((u >> shf) & dmask)], 1u);
           if (mode[1] == 2 && bn == bin[1] && (u & m1) == p1) atomicAdd(&sh.hist[1][Hist<PT>::idx((u >> shf) & dmask)], 1u);
@@ -560,7 +573,7 @@ __device__ __forceinline__ void offsets(const PartArgs &a, const RowCtx &r, int 
 
 // ---------------------------------------------------------------- kernel --
 
-template <bool kMerge, int R, int PT, bool kRecent>
+template <bool kMerge, int R, int PT, bool kRecent, bool kProb = false>
 __global__ __launch_bounds__(PT) __attribute__((amdgpu_waves_per_eu(4)))
 void partition_kernel(PartArgs a) {
   constexpr int kChunk = PC<PT>::chunk;
@@ -568,7 +581,7 @@ void partition_kernel(PartArgs a) {
   RowCtx r;
   row_setup(a, r);
   const int tid = threadIdx.x;
-  Row<R, PT, kRecent> row;
+  Row<R, PT, kRecent, kProb> row;
   row.lg = r.lg;
   row.n = r.n;
   row.nrank = r.older;
@@ -730,20 +743,21 @@ PartArgs base_args(const smallkv_batch_t &b, int n_small_heads, const float *log
   return a;
 }
 
-template <bool kMerge, int PT, bool kRecent>
+template <bool kMerge, int PT, bool kRecent, bool kProb>
 hipError_t launch_pt(const PartArgs &a, int rows, hipStream_t st) {
   const dim3 grid(rows), block(PT);
   const int n = a.n_cap;
   if (n <= 4 * PT)
-    hipLaunchKernelGGL((partition_kernel<kMerge, 4, PT, kRecent>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((partition_kernel<kMerge, 4, PT, kRecent, kProb>), grid, block, 0, st, a);
   else if (n <= 8 * PT)
-    hipLaunchKernelGGL((partition_kernel<kMerge, 8, PT, kRecent>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((partition_kernel<kMerge, 8, PT, kRecent, kProb>), grid, block, 0, st, a);
   else if (n <= 16 * PT)
-    hipLaunchKernelGGL((partition_kernel<kMerge, 16, PT, kRecent>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((partition_kernel<kMerge, 16, PT, kRecent, kProb>), grid, block, 0, st, a);
   else if (PT == 256 && n <= 20 * PT)  // narrow rows: one more register chunk
-    hipLaunchKernelGGL((partition_kernel<kMerge, PT == 256 ? 20 : 16, PT, kRecent>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((partition_kernel<kMerge, PT == 256 ? 20 : 16, PT, kRecent, kProb>), grid,
+                       block, 0, st, a);
   else
-    hipLaunchKernelGGL((partition_kernel<kMerge, 0, PT, kRecent>), grid, block, 0, st, a);
+    hipLaunchKernelGGL((partition_kernel<kMerge, 0, PT, kRecent, kProb>), grid, block, 0, st, a);
   return hipGetLastError();
 }
 
@@ -751,14 +765,14 @@ hipError_t launch_pt(const PartArgs &a, int rows, hipStream_t st) {
 // resident at once; few rows: 512 threads, so that each finishes sooner.
 constexpr int kManyRows = 4 * 256;
 
-template <bool kMerge>
+template <bool kMerge, bool kProb = false>
 hipError_t launch_rows(const PartArgs &a, int rows, hipStream_t st) {
   if (a.k_recent) {
-    if (rows >= kManyRows) return launch_pt<kMerge, 256, true>(a, rows, st);
-    return launch_pt<kMerge, 512, true>(a, rows, st);
+    if (rows >= kManyRows) return launch_pt<kMerge, 256, true, kProb>(a, rows, st);
+    return launch_pt<kMerge, 512, true, kProb>(a, rows, st);
   }
-  if (rows >= kManyRows) return launch_pt<kMerge, 256, false>(a, rows, st);
-  return launch_pt<kMerge, 512, false>(a, rows, st);
+  if (rows >= kManyRows) return launch_pt<kMerge, 256, false, kProb>(a, rows, st);
+  return launch_pt<kMerge, 512, false, kProb>(a, rows, st);
 }
 
 }  // namespace
@@ -806,6 +820,20 @@ hipError_t launch_merge_partition(const smallkv_batch_t &b, const smallkv_model_
   a.tok_len = tok_len;
   a.tok_cap = tok_cap;
   return launch_rows<true>(a, b.batch * nsh, st);
+}
+
+}  // namespace smallkv
+
+namespace smallkv {
+
+hipError_t launch_group_partition(const smallkv_batch_t &b, int group_rows, const float *keys,
+                                  const float *key_max, int32_t *crit, int32_t *marg,
+                                  float *marg_prob, float *mass, hipStream_t st) {
+  // keys are sums of probabilities: the row's largest key stands in for both
+  // the row max and the normaliser (the p' this writes are not used)
+  const PartArgs a = base_args(b, group_rows, keys, const_cast<float *>(key_max),
+                               const_cast<float *>(key_max), crit, marg, marg_prob, mass);
+  return launch_rows<false, true>(a, b.batch * group_rows, st);
 }
 
 }  // namespace smallkv

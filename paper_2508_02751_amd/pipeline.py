@@ -70,7 +70,11 @@ def prepare_step(x: dict, mode: int = S.NORM_REMAINING,
                  k_slot: Optional[torch.Tensor] = None,
                  v_slot: Optional[torch.Tensor] = None,
                  l_k: Optional[torch.Tensor] = None,
-                 l_v: Optional[torch.Tensor] = None) -> PreparedStep:
+                 l_v: Optional[torch.Tensor] = None,
+                 select: Optional[int] = None) -> PreparedStep:
+    """`select` defaults to x["select"] when present, else per-head selection."""
+    if select is None:
+        select = x.get("select", S.SELECT_HEAD)
     s_q, s_k, s_v = x["s_q"], x["s_k"], x["s_v"]
     l_q = x["l_q"]
     l_k = x["l_k"] if l_k is None else l_k
@@ -86,10 +90,10 @@ def prepare_step(x: dict, mode: int = S.NORM_REMAINING,
     large = S.ModelSpec(l_q.contiguous(), l_k, l_v, torch.empty_like(l_q),
                         softmax_scale(l_q.shape[-1]), k_slot, v_slot)
     hm = x["head_map"].contiguous()
-    ws_bytes = S.smallkv_workspace_size(batch, small, large, hm)
-    buf = S.alloc_step_buffers(batch, s_q, l_q, ws_bytes)
+    ws_bytes = S.smallkv_workspace_size(batch, small, large, hm, select)
+    buf = S.alloc_step_buffers(batch, s_q, l_q, ws_bytes, select, l_k.shape[2])
     buf.small_out = small.out
     buf.large_out = large.out
     desc = S.make_step(batch, small, large, hm, mode, buf.logits, buf.row_max, buf.row_sum,
-                       buf.crit_idx, buf.marg_idx, buf.marg_prob, buf.mass)
+                       buf.crit_idx, buf.marg_idx, buf.marg_prob, buf.mass, select)
     return PreparedStep(batch, small, large, hm, mode, buf, desc, x)

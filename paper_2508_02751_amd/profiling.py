@@ -40,6 +40,9 @@ KERNEL_SOURCES = {
     "match_rowsum": "match.hip",
     "match_scores": "match.hip",
     "match_map": "match.hip",
+    "group_zq": "group_select.hip",
+    "group_scores": "group_select.hip",
+    "group_weights": "group_select.hip",
 }
 
 

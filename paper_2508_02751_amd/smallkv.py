@@ -24,6 +24,7 @@ LIB_PATH = os.path.join(_HERE, "libsmallkv.so")
 
 F32, BF16 = 0, 1
 NORM_REMAINING, NORM_NONE, NORM_SLM_CRIT, NORM_RETAINED, NORM_MARG_FILL = range(5)
+SELECT_HEAD, SELECT_GROUP = 0, 1
 OK, EINVAL, EUNSUPPORTED, EWORKSPACE, EDEVICE = 0, -1, -2, -3, -4
 
 
@@ -46,7 +47,7 @@ class Step(C.Structure):
                 ("head_map", C.c_void_p), ("mode", C.c_int32),
                 ("logits", C.c_void_p), ("row_max", C.c_void_p), ("row_sum", C.c_void_p),
                 ("crit_idx", C.c_void_p), ("marg_idx", C.c_void_p),
-                ("marg_prob", C.c_void_p), ("mass", C.c_void_p)]
+                ("marg_prob", C.c_void_p), ("mass", C.c_void_p), ("select", C.c_int32)]
 
 
 class Window(C.Structure):
@@ -63,6 +64,7 @@ class Match(C.Structure):
 
 EXPORTS = ("smallkv_small_attn", "smallkv_partition", "smallkv_hybrid_attn", "smallkv_step",
            "smallkv_workspace_size", "smallkv_match", "smallkv_match_workspace_size",
+           "smallkv_group_select", "smallkv_group_select_workspace_size",
            "smallkv_status_string", "smallkv_abi_version")
 
 _lib = None
@@ -83,7 +85,13 @@ def lib():
                                         C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]
         L.smallkv_hybrid_attn.argtypes = [P(Batch), P(Model), C.c_void_p, C.c_int32, C.c_void_p,
                                           C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32,
-                                          C.c_void_p, C.c_size_t, C.c_void_p]
+                                          C.c_int32, C.c_void_p, C.c_size_t, C.c_void_p]
+        L.smallkv_group_select.argtypes = [P(Batch), P(Model), P(Model), C.c_void_p, C.c_void_p,
+                                           C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
+                                           C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t,
+                                           C.c_void_p]
+        L.smallkv_group_select_workspace_size.argtypes = [P(Batch), P(Model), P(Model),
+                                                          P(C.c_size_t)]
         L.smallkv_step.argtypes = [P(Step), C.c_void_p, C.c_size_t, C.c_void_p]
         L.smallkv_workspace_size.argtypes = [P(Step), P(C.c_size_t)]
         L.smallkv_match.argtypes = [P(Match), C.c_void_p, C.c_size_t, C.c_void_p]
@@ -93,7 +101,8 @@ def lib():
         L.smallkv_abi_version.argtypes = []
         for f in ("smallkv_small_attn", "smallkv_partition", "smallkv_hybrid_attn",
                   "smallkv_step", "smallkv_workspace_size", "smallkv_abi_version",
-                  "smallkv_match", "smallkv_match_workspace_size"):
+                  "smallkv_match", "smallkv_match_workspace_size", "smallkv_group_select",
+                  "smallkv_group_select_workspace_size"):
             getattr(L, f).restype = C.c_int
         _lib = L
     return _lib
@@ -192,8 +201,9 @@ def _ws(ws: Optional[torch.Tensor]):
 
 
 def smallkv_workspace_size(batch: BatchSpec, small: ModelSpec, large: ModelSpec,
-                           head_map) -> int:
+                           head_map, select: int = SELECT_HEAD) -> int:
     st = Step()
+    st.select = int(select)
     st.batch = batch.c()
     st.small = small.c()
     st.large = large.c()
@@ -228,20 +238,32 @@ def smallkv_partition(batch: BatchSpec, n_small_heads: int, logits, row_max, row
 
 def smallkv_hybrid_attn(batch: BatchSpec, large: ModelSpec, head_map, n_small_heads: int,
                         crit_idx, marg_idx, marg_prob, mass, mode=NORM_REMAINING, ws=None,
-                        stream=None):
+                        stream=None, select: int = SELECT_HEAD):
     b, m = batch.c(), large.c()
     w, wb = _ws(ws)
     _check("smallkv_hybrid_attn", lib().smallkv_hybrid_attn(
         C.byref(b), C.byref(m), _ptr(head_map), n_small_heads, _ptr(crit_idx), _ptr(marg_idx),
-        _ptr(marg_prob), _ptr(mass), int(mode), w, wb, _stream(stream)))
+        _ptr(marg_prob), _ptr(mass), int(mode), int(select), w, wb, _stream(stream)))
+
+
+def smallkv_group_select(batch: BatchSpec, small: ModelSpec, large: ModelSpec, head_map, logits,
+                         row_max, row_sum, crit_idx, marg_idx, marg_prob, mass, ws, stream=None):
+    """Stage 2 of group selection (lists per large kv head, weights per large head)."""
+    b, sm, lg = batch.c(), small.c(), large.c()
+    w, wb = _ws(ws)
+    _check("smallkv_group_select", lib().smallkv_group_select(
+        C.byref(b), C.byref(sm), C.byref(lg), _ptr(head_map), _ptr(logits), _ptr(row_max),
+        _ptr(row_sum), _ptr(crit_idx), _ptr(marg_idx), _ptr(marg_prob), _ptr(mass), w, wb,
+        _stream(stream)))
 
 
 def make_step(batch: BatchSpec, small: ModelSpec, large: ModelSpec, head_map, mode, logits,
-              row_max, row_sum, crit_idx, marg_idx, marg_prob, mass) -> Step:
+              row_max, row_sum, crit_idx, marg_idx, marg_prob, mass,
+              select: int = SELECT_HEAD) -> Step:
     """Build the C step descriptor once (it holds raw pointers: keep the tensors alive)."""
     return Step(batch.c(), small.c(), large.c(), _ptr(head_map), int(mode), _ptr(logits),
                 _ptr(row_max), _ptr(row_sum), _ptr(crit_idx), _ptr(marg_idx), _ptr(marg_prob),
-                _ptr(mass))
+                _ptr(mass), int(select))
 
 
 def smallkv_step(step: Step, ws=None, stream=None):
@@ -265,18 +287,22 @@ class StepBuffers:
 
 
 def alloc_step_buffers(batch: BatchSpec, s_q: torch.Tensor, l_q: torch.Tensor,
-                       ws_bytes: int) -> StepBuffers:
+                       ws_bytes: int, select: int = SELECT_HEAD,
+                       l_kv_heads: Optional[int] = None) -> StepBuffers:
+    """Group selection: lists per (large layer, kv head), weights per large head."""
     B, l, hqs, _ = s_q.shape
     nsh = l * hqs
+    _, L, hq, _ = l_q.shape
+    lrows, prows = (L * l_kv_heads, L * hq) if select == SELECT_GROUP else (nsh, nsh)
     dev = s_q.device
     return StepBuffers(
         logits=torch.empty((B, nsh, batch.n_cap), dtype=torch.float32, device=dev),
         row_max=torch.empty((B, nsh), dtype=torch.float32, device=dev),
         row_sum=torch.empty((B, nsh), dtype=torch.float32, device=dev),
-        crit_idx=torch.empty((B, nsh, batch.kc_cap), dtype=torch.int32, device=dev),
-        marg_idx=torch.empty((B, nsh, max(batch.km_cap, 1)), dtype=torch.int32, device=dev),
-        marg_prob=torch.empty((B, nsh, max(batch.km_cap, 1)), dtype=torch.float32, device=dev),
-        mass=torch.empty((B, nsh, 2), dtype=torch.float32, device=dev),
+        crit_idx=torch.empty((B, lrows, batch.kc_cap), dtype=torch.int32, device=dev),
+        marg_idx=torch.empty((B, lrows, max(batch.km_cap, 1)), dtype=torch.int32, device=dev),
+        marg_prob=torch.empty((B, prows, max(batch.km_cap, 1)), dtype=torch.float32, device=dev),
+        mass=torch.empty((B, prows, 2), dtype=torch.float32, device=dev),
         small_out=torch.empty_like(s_q),
         large_out=torch.empty_like(l_q),
         ws=torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev) if ws_bytes else None,

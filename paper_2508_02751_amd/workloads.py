@@ -81,6 +81,7 @@ class Workload:
     steps: int = 1                # consecutive decode steps (drifting latent)
     compact_large: bool = False   # large KV held only for retained tokens
     slm_keep: int = 0             # >0: the small model's own cache keeps this % of tokens
+    select: int = 0               # 1: the query heads of a large kv head share one selection
 
     @property
     def n_cap(self) -> int:
@@ -124,6 +125,9 @@ WORKLOADS = {
     # paper's best small-model budget with the large model at 20%)
     8: Workload(8, "qwen2-7b+0.5b-slm40-n8192-b1-bf16", 1, 8192, "bf16",
                 QWEN2_0_5B, QWEN2_7B, ("pct", 10), ("pct", 20), slm_keep=40),
+    # the Qwen2 step with one selection per large kv head (summed selection)
+    9: Workload(9, "qwen2-7b+0.5b-n8192-b1-bf16-groupsel", 1, 8192, "bf16",
+                QWEN2_0_5B, QWEN2_7B, ("pct", 10), ("pct", 20), select=1),
 }
 
 LATENT = 64
@@ -287,6 +291,8 @@ def make_step_inputs(w: Workload, device, step: int = 0, *, z=None, large=True):
     out["seq_len"], out["k_crit"], out["k_marg"] = n.to(device), kc.to(device), km.to(device)
     if w.slm_keep:
         evict_small_cache(w, out, n, device)
+    if w.select:
+        out["select"] = w.select
     kr = recent_budget(w, step)
     if kr is not None:
         out["k_recent"] = kr.to(device)

@@ -44,7 +44,7 @@ def oracle_step(x: dict, mode: int, k_slot=None, v_slot=None, l_k=None, l_v=None
         k_recent=host(x["k_recent"]) if x.get("k_recent") is not None else None,
         s_held=host(x["s_held"]) if x.get("s_held") is not None else None,
         s_row_pos=host(x["s_row_pos"]) if x.get("s_row_pos") is not None else None,
-        n_cap=x.get("n_cap"))
+        n_cap=x.get("n_cap"), select=x.get("select", 0))
 
 
 def head_err(got: np.ndarray, ref: np.ndarray) -> float:

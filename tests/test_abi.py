@@ -33,7 +33,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_abi_version_and_status_strings():
     L = S.lib()
-    assert L.smallkv_abi_version() == 4
+    assert L.smallkv_abi_version() == 5
     assert L.smallkv_status_string(0) == b"ok"
     assert L.smallkv_status_string(-3) == b"workspace too small"
     assert L.smallkv_status_string(123) == b"unknown status"
@@ -46,7 +46,7 @@ def _fake_step(**over):
                 km_cap=128)
     sm = S.Model(1, 14, 2, 64, S.BF16, 0.125, p, p, p, 512, None, None, p)
     lg = S.Model(1, 28, 4, 128, S.BF16, 0.088, p, p, p, 512, None, None, p)
-    st = S.Step(b, sm, lg, p, 0, p, p, p, p, p, p, p)
+    st = S.Step(b, sm, lg, p, 0, p, p, p, p, p, p, p, S.SELECT_HEAD)
     for k, v in over.items():
         obj, field = k.split("__")
         setattr({"b": st.batch, "s": st.small, "l": st.large, "st": st}[obj], field, v)
@@ -68,6 +68,7 @@ def _fake_step(**over):
     ({"s__row_pos": 0x1000}, S.EINVAL),                   # positions without held rows
     ({"s__held": 0x1000, "s__row_pos": 0x1000, "s__n_rows": 600}, S.EINVAL),  # > n_cap
     ({"l__held": 0x1000, "l__row_pos": 0x1000}, S.EINVAL),  # small model only
+    ({"st__select": 2}, S.EINVAL),
 ])
 def test_workspace_size_rejects_bad_small_model(over, status):
     n = C.c_size_t()
@@ -104,7 +105,7 @@ def test_partition_and_hybrid_reject_nulls():
     assert L.smallkv_partition(C.byref(b), None, 14, None, 1, 1, 1, 1, 1, 1, None, 0,
                                None) == S.EINVAL
     lg = S.Model(1, 28, 4, 128, S.BF16, 0.088, 1, 1, 1, 512, None, None, 1)
-    assert L.smallkv_hybrid_attn(C.byref(b), C.byref(lg), None, 14, 1, 1, 1, 1, 0, None, 0,
+    assert L.smallkv_hybrid_attn(C.byref(b), C.byref(lg), None, 14, 1, 1, 1, 1, 0, 0, None, 0,
                                  None) == S.EINVAL
 
 
@@ -174,3 +175,14 @@ def test_partition_with_held_rows_checks_the_small_model():
     sm.row_pos = None  # held rows without positions
     assert L.smallkv_partition(C.byref(b), C.byref(sm), 14, 1, 1, 1, 1, 1, 1, 1, None, 0,
                                None) == S.EINVAL
+
+
+def test_group_selection_limits():
+    # a compressed small cache, or more than 16 query heads per kv head
+    for over in ({"s__held": 0x1000, "s__row_pos": 0x1000, "s__n_rows": 200},
+                 {"l__n_q_heads": 32, "l__n_kv_heads": 1}):
+        st = _fake_step(st__select=S.SELECT_GROUP, **over)
+        assert S.lib().smallkv_step(C.byref(st), C.c_void_p(0x1000), 1 << 40, None) == S.EUNSUPPORTED
+    st = _fake_step(st__select=S.SELECT_GROUP)
+    n = C.c_size_t()
+    assert S.lib().smallkv_workspace_size(C.byref(st), C.byref(n)) == 0 and n.value > 0

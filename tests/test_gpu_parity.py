@@ -353,3 +353,78 @@ def test_compact_store_with_slot_maps(dtype):
     ref = oracle_step(x, S.NORM_REMAINING, k_slot=ks, v_slot=vs, l_k=ck, l_v=cv)
     np.testing.assert_array_equal(ref["large_out"], ref_full["large_out"])
     compare_step(ps.buf, ref, x, w.torch_dtype, f"compact-{dtype}")
+
+
+# ------------------------------------------------------- group selection --
+
+def group_sel(x):
+    x["select"] = S.SELECT_GROUP
+
+
+@pytest.mark.parametrize("mode", O.MODES)
+def test_group_selection_tiny_f32_all_modes(mode):
+    """fp32: the per-head stage 3 reads the group's lists and each head's weights."""
+    run_case(W.WORKLOADS[1], mode, mutate=group_sel, what="group selection, tiny fp32")
+
+
+def test_group_selection_qwen2_7b_full_step():
+    """The query heads of each of the 112 large kv heads share one selection."""
+    ps, x, ref = run_case(W.WORKLOADS[2], mutate=group_sel, what="group selection, Qwen2-7B")
+    assert ps.buf.crit_idx.shape[1] == 28 * 4 and ps.buf.marg_prob.shape[1] == 28 * 28
+
+
+@pytest.mark.parametrize("g", [2, 8, 16])
+def test_group_selection_group_sizes(g):
+    """Groups of 2 and 8 query heads (grouped stage 3) and 16 (per-head stage 3)."""
+    w = custom(f"gsel{g}", 122, 2, 1100, "bf16", SMALL, W.ModelShape(2, 2 * g, 2, 128),
+               ("pct", 10), ("pct", 25), ragged_min=300)
+    run_case(w, mutate=group_sel)
+
+
+def test_group_selection_ragged_with_recent_tokens():
+    w = custom("gsel-recent", 123, 4, 2500, "bf16", W.ModelShape(3, 8, 2, 64),
+               W.ModelShape(2, 14, 2, 128), ("pct", 8), ("pct", 15), ragged_min=50,
+               recent=("pct", 4))
+    run_case(w, mutate=group_sel)
+
+
+def test_group_selection_repeats_bit_identically():
+    x = W.make_step_inputs(W.WORKLOADS[2], DEV)
+    group_sel(x)
+    ps = prepare_step(x)
+    ps.run()
+    torch.cuda.synchronize()
+    first = [t.clone() for t in (ps.buf.crit_idx, ps.buf.marg_idx, ps.buf.marg_prob, ps.buf.mass,
+                                 ps.buf.large_out)]
+    for _ in range(3):
+        ps.run()
+    torch.cuda.synchronize()
+    for a_, b_ in zip(first, (ps.buf.crit_idx, ps.buf.marg_idx, ps.buf.marg_prob, ps.buf.mass,
+                              ps.buf.large_out)):
+        assert torch.equal(a_.view(torch.uint8), b_.view(torch.uint8))
+
+
+def test_group_selection_single_stage_calls_match_step():
+    w = custom("gsel-stages", 124, 2, 1800, "bf16", SMALL, LARGE, ("pct", 10), ("pct", 20),
+               ragged_min=400, select=1)
+    x = W.make_step_inputs(w, DEV)
+    ps = prepare_step(x)
+    ps.run()
+    b = ps.buf
+    nsh = SMALL.layers * SMALL.q_heads
+    lg, rm, rs = torch.empty_like(b.logits), torch.empty_like(b.row_max), torch.empty_like(b.row_sum)
+    small = S.ModelSpec(ps.small.q, ps.small.k, ps.small.v, torch.empty_like(ps.small.out),
+                        ps.small.scale)
+    S.smallkv_small_attn(ps.batch, small, lg, rm, rs, b.ws)
+    ci, mi = torch.empty_like(b.crit_idx), torch.empty_like(b.marg_idx)
+    mp, ms = torch.empty_like(b.marg_prob), torch.empty_like(b.mass)
+    S.smallkv_group_select(ps.batch, small, ps.large, ps.head_map, lg, rm, rs, ci, mi, mp, ms, b.ws)
+    large = S.ModelSpec(ps.large.q, ps.large.k, ps.large.v, torch.empty_like(ps.large.out),
+                        ps.large.scale)
+    S.smallkv_hybrid_attn(ps.batch, large, ps.head_map, nsh, ci, mi, mp, ms, ws=b.ws,
+                          select=S.SELECT_GROUP)
+    torch.cuda.synchronize()
+    for got, want in ((rm, b.row_max), (rs, b.row_sum), (ci, b.crit_idx), (mi, b.marg_idx),
+                      (mp, b.marg_prob), (ms, b.mass), (small.out, b.small_out),
+                      (large.out, b.large_out)):
+        assert torch.equal(got, want)
