@@ -23,7 +23,7 @@ SRCS = [SRC, os.path.join(HERE, "match_oracle.c")]
 LIB = os.path.join(HERE, "libsmallkv_oracle.so")
 
 NORM_REMAINING, NORM_NONE, NORM_SLM_CRIT, NORM_RETAINED, NORM_MARG_FILL = range(5)
-SELECT_HEAD, SELECT_GROUP = 0, 1
+SELECT_HEAD, SELECT_GROUP, SELECT_ACCUM = 0, 1, 2
 MODES = (NORM_REMAINING, NORM_NONE, NORM_SLM_CRIT, NORM_RETAINED, NORM_MARG_FILL)
 
 
@@ -61,6 +61,7 @@ class StepIn(C.Structure):
         ("head_map", _I),
         ("mode", C.c_int32),
         ("select", C.c_int32),
+        ("acc", _F),
     ]
 
 
@@ -209,8 +210,12 @@ def hybrid_head(q, K, V, crit, marg, marg_prob, mass, scale, mode=NORM_REMAINING
 
 def step(*, seq_len, k_crit, k_marg, kc_cap, km_cap, head_map, mode,
          s_q, s_k, s_v, s_scale, l_q, l_k, l_v, l_scale, k_slot=None, v_slot=None,
-         k_recent=None, s_held=None, s_row_pos=None, n_cap=None, select=SELECT_HEAD):
+         k_recent=None, s_held=None, s_row_pos=None, n_cap=None, select=SELECT_HEAD,
+         acc=None):
     """A whole decode step over the library layout (see smallkv_oracle.h).
+
+    select=SELECT_ACCUM: `acc` is a float32 array [B, l*Hqs, n_cap] (C-contiguous)
+    updated in place: the running accumulated score of every small head.
 
     Shapes: s_q [B,l,Hqs,ds], s_k/s_v [B,l,Hks,n_cap,ds] (with the small
     model's own eviction: [B,l,Hks,s_rows,ds] plus s_held [B] and s_row_pos
@@ -218,6 +223,8 @@ def step(*, seq_len, k_crit, k_marg, kc_cap, km_cap, head_map, mode,
     [B,L,Hk,n_rows,d], slots [B,L,Hk,n_cap] or None.
     """
     s_q, s_k, s_v, l_q, l_k, l_v = map(_f32, (s_q, s_k, s_v, l_q, l_k, l_v))
+    if acc is not None and (acc.dtype != np.float32 or not acc.flags.c_contiguous):
+        raise ValueError("acc must be a C-contiguous float32 array (updated in place)")
     seq_len, k_crit, k_marg, head_map = map(_i32, (seq_len, k_crit, k_marg, head_map))
     kr = _i32(k_recent) if k_recent is not None else None
     B, l, hqs, ds = s_q.shape
@@ -250,7 +257,8 @@ def step(*, seq_len, k_crit, k_marg, kc_cap, km_cap, head_map, mode,
                 L, hq, hk, d, l_scale, nrows, _p(l_q, _F), _p(l_k, _F), _p(l_v, _F),
                 _p(ks, _I) if ks is not None else None,
                 _p(vs, _I) if vs is not None else None,
-                _p(head_map, _I), int(mode), int(select))
+                _p(head_map, _I), int(mode), int(select),
+                _p(acc, _F) if acc is not None else None)
     so = StepOut(_p(out["logits"], _F), _p(out["row_max"], _D), _p(out["row_sum"], _D),
                  _p(out["small_out"], _D), _p(out["crit"], _I), _p(out["marg"], _I),
                  _p(out["marg_prob"], _D), _p(out["mass"], _D), _p(out["large_out"], _D))

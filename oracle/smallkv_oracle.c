@@ -403,6 +403,33 @@ int orc_step(const orc_step_in *in, const orc_step_out *out) {
       out->row_max[row] = ms[j];
       out->row_sum[row] = zs[j];
       if (in->select == ORC_SELECT_GROUP) continue; /* selected per group below */
+      if (in->select == ORC_SELECT_ACCUM) {
+        /* H2O-style accumulated attention (the baseline the method builds on):
+         * this step's probabilities are added to the head's running score,
+         * which then ranks the tokens; the weights stay this step's p'. */
+        if (in->s_held || !in->acc) {
+          rc = ORC_EINVAL;
+          break;
+        }
+        const float *lg = out->logits + row * srows;
+        float *acc = in->acc + row * (size_t)ncap;
+        const float zq = orc_zq(ns, lg, (float)ms[j]);
+        for (int t = 0; t < ns; ++t) acc[t] = acc[t] + orc_exp(lg[t] - (float)ms[j]) / zq;
+        rc = orc_partition(ns, in->k_crit[b], in->k_marg[b], in->k_recent ? in->k_recent[b] : 0,
+                           acc, 0.0, 1.0, out->crit + row * in->kc_cap, in->kc_cap,
+                           out->marg + row * in->km_cap, out->marg_prob + row * in->km_cap,
+                           in->km_cap, out->mass + row * 2, &nc[j], &nm[j]);
+        if (rc) break;
+        double *mp = out->marg_prob + row * in->km_cap, *mass = out->mass + row * 2;
+        const int32_t *crit = out->crit + row * in->kc_cap, *marg = out->marg + row * in->km_cap;
+        mass[0] = mass[1] = 0.0;
+        for (int i = 0; i < nc[j]; ++i) mass[0] += exp((double)lg[crit[i]] - ms[j]) / zs[j];
+        for (int i = 0; i < in->km_cap; ++i) {
+          mp[i] = i < nm[j] ? exp((double)lg[marg[i]] - ms[j]) / zs[j] : 0.0;
+          mass[1] += mp[i];
+        }
+        continue;
+      }
       rc = orc_partition(ns, in->k_crit[b], in->k_marg[b], in->k_recent ? in->k_recent[b] : 0,
                          out->logits + row * srows, ms[j], zs[j],
                          out->crit + row * in->kc_cap, in->kc_cap,

@@ -134,9 +134,14 @@ typedef struct {
    * probabilities: orc_group_key).  Group mode writes crit/marg per group,
    * [B][L*Hkv][cap], and marg_prob/mass per large head, [B][L*Hq][...]. */
   int32_t select;
+  /* ORC_SELECT_ACCUM: per-head selection ranked by the accumulated score,
+   * acc [B][l*Hq_s][n_cap], updated in place before ranking:
+   * acc[t] = acc[t] + orc_exp(logit_t - m) / Zq (fp32, Zq as orc_zq) for
+   * t < seq_len; the caller zeroes it before the first step. */
+  float *acc;
 } orc_step_in;
 
-enum { ORC_SELECT_HEAD = 0, ORC_SELECT_GROUP = 1 };
+enum { ORC_SELECT_HEAD = 0, ORC_SELECT_GROUP = 1, ORC_SELECT_ACCUM = 2 };
 
 /* The normaliser of one small head for the group key: Zq = the exact integer
  * sum over t < n of floor(orc_exp(logits[t] - m) * 2^40); returns the fp32

@@ -688,3 +688,92 @@ def test_group_selection_with_everything_critical_is_full_attention():
             w /= w.sum()
             np.testing.assert_allclose(r["large_out"][0, li, h], w @ lv[0, li, g].astype(np.float64),
                                        rtol=1e-9, atol=1e-12)
+
+
+# ------------------------------------------- accumulated scores (H2O-style) --
+
+def _acc_run(x, kc, km, acc, kr=None):
+    B = x["seq_len"].size
+    return O.step(**x, k_crit=np.full(B, kc, np.int32), k_marg=np.full(B, km, np.int32),
+                  kc_cap=kc + (kr or 0), km_cap=km, mode=O.NORM_REMAINING,
+                  select=O.SELECT_ACCUM, acc=acc,
+                  k_recent=None if kr is None else np.full(B, kr, np.int32))
+
+
+def test_accumulated_first_step_is_per_head_selection():
+    rng = np.random.default_rng(51)
+    x = _group_case(rng, n=96)
+    nsh = 2 * 4
+    for kr in (None, 6):
+        acc = np.zeros((1, nsh, 96), np.float32)
+        r = _acc_run(x, 9, 14, acc, kr)
+        head = _run(x, 9, 14, O.SELECT_HEAD, kr)
+        for k in ("crit", "marg", "marg_prob", "mass", "large_out"):
+            np.testing.assert_allclose(r[k], head[k], rtol=1e-12, atol=1e-15, err_msg=k)
+        # the state holds this step's probabilities
+        lg = r["logits"][0].astype(np.float64)
+        p = np.exp(lg - lg.max(1, keepdims=True))
+        p /= p.sum(1, keepdims=True)
+        np.testing.assert_allclose(acc[0], p, rtol=1e-6, atol=1e-12)
+
+
+def test_accumulated_identical_steps_sum_up():
+    rng = np.random.default_rng(52)
+    x = _group_case(rng, n=64)
+    acc = np.zeros((1, 8, 64), np.float32)
+    for _ in range(5):
+        r = _acc_run(x, 5, 8, acc)
+    lg = r["logits"][0].astype(np.float64)
+    p = np.exp(lg - lg.max(1, keepdims=True))
+    p /= p.sum(1, keepdims=True)
+    np.testing.assert_allclose(acc[0], 5 * p, rtol=5e-6, atol=1e-12)
+    head = _run(x, 5, 8, O.SELECT_HEAD)
+    np.testing.assert_array_equal(r["crit"], head["crit"])
+
+
+def test_accumulated_keeps_an_earlier_heavy_hitter():
+    """Step 1 attends token 7 strongly; step 2 prefers token 20 slightly.  The
+    accumulated score keeps 7 critical (K = 1); the current step alone picks 20."""
+    n, ds = 32, 16
+    sk = np.zeros((1, 1, 1, n, ds), np.float32)
+    sk[0, 0, 0, :, 0] = np.linspace(-1, 1, n)
+    sk[0, 0, 0, 7, 1] = 4.0
+    sk[0, 0, 0, 20, 2] = 4.0
+    sv = np.ones_like(sk)
+    base = dict(seq_len=np.array([n], np.int32), s_k=sk, s_v=sv, s_scale=1.0,
+                l_q=np.ones((1, 1, 1, 128), np.float32), l_k=np.ones((1, 1, 1, n, 128), np.float32),
+                l_v=np.ones((1, 1, 1, n, 128), np.float32), l_scale=SCALE128,
+                head_map=np.zeros(1, np.int32))
+    q1 = np.zeros((1, 1, 1, ds), np.float32)
+    q1[..., 1] = 3.0                    # step 1: token 7 dominates
+    q2 = np.zeros((1, 1, 1, ds), np.float32)
+    q2[..., 1], q2[..., 2] = 1.0, 1.2   # step 2: token 20 slightly ahead of 7
+    acc = np.zeros((1, 1, n), np.float32)
+    _acc_run({**base, "s_q": q1}, 1, 0, acc)
+    r2 = _acc_run({**base, "s_q": q2}, 1, 0, acc)
+    head2 = _run({**base, "s_q": q2}, 1, 0, O.SELECT_HEAD)
+    assert r2["crit"][0, 0].tolist() == [7] and head2["crit"][0, 0].tolist() == [20]
+
+
+def test_accumulated_over_growing_steps_is_the_top_of_the_running_sum():
+    rng = np.random.default_rng(53)
+    ncap, l, hqs, hks, ds = 80, 1, 4, 2, 16
+    f = lambda *s: rng.standard_normal(s).astype(np.float32)
+    sk, sv = f(1, l, hks, ncap, ds), f(1, l, hks, ncap, ds)
+    lk, lv = f(1, 1, 2, ncap, 128), f(1, 1, 2, ncap, 128)
+    acc = np.zeros((1, l * hqs, ncap), np.float32)
+    run64 = np.zeros((l * hqs, ncap))
+    for step, n in enumerate((60, 61, 62, 63)):
+        x = dict(seq_len=np.array([n], np.int32), s_q=f(1, l, hqs, ds), s_k=sk, s_v=sv,
+                 s_scale=0.25, l_q=f(1, 1, 4, 128), l_k=lk, l_v=lv, l_scale=SCALE128,
+                 head_map=np.arange(4, dtype=np.int32))
+        r = _acc_run(x, 6, 9, acc)
+        lg = r["logits"][0][:, :n].astype(np.float64)
+        p = np.exp(lg - lg.max(1, keepdims=True))
+        run64[:, :n] += p / p.sum(1, keepdims=True)
+        for j in range(l * hqs):
+            c, m = r["crit"][0, j], r["marg"][0, j]
+            rest = np.setdiff1d(np.arange(n), np.concatenate([c, m]))
+            tol = 1e-5 * run64[j].max()
+            assert run64[j, c].min() >= run64[j, np.concatenate([m, rest])].max() - tol
+            assert run64[j, m].min() >= run64[j, rest].max() - tol
