@@ -189,6 +189,10 @@ def main():
             S.smallkv_group_select(ps.batch, ps.small, ps.large, ps.head_map, b.logits, b.row_max,
                                    b.row_sum, b.crit_idx, b.marg_idx, b.marg_prob, b.mass, b.ws,
                                    stream)
+        elif w.select == 2:
+            S.smallkv_accum_select(ps.batch, ps.small, b.logits, b.row_max, b.row_sum,
+                                   b.acc_score, b.crit_idx, b.marg_idx, b.marg_prob, b.mass, b.ws,
+                                   stream)
         else:
             S.smallkv_partition(ps.batch, nsh, b.logits, b.row_max, b.row_sum, b.crit_idx,
                                 b.marg_idx, b.marg_prob, b.mass, None, stream, small=ps.small)
@@ -209,7 +213,8 @@ def main():
     # the grouped kernel over token splits plus their merge)
     stage_kernels = [["small_attn_mfma", "small_attn_merge"],
                      ["group_zq", "group_scores", "partition_kernel", "group_weights"] if group
-                     else ["partition_kernel"], stage3_kernels(w)]
+                     else ["group_zq", "accum_scores", "partition_kernel", "group_weights"]
+                     if w.select == 2 else ["partition_kernel"], stage3_kernels(w)]
     dom = max(range(3), key=lambda s: stage_ms[s])
     achieved = stage_bytes[dom] / (stage_ms[dom] * 1e-3) / 1e9
     traffic = load_traffic(stage_kernels[dom], w.name)
@@ -219,6 +224,7 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         sys.path.insert(0, os.path.join(ROOT, "oracle"))
+        import numpy as np
         import oracle as O
         from paper_2508_02751_amd.pipeline import softmax_scale
 
@@ -233,6 +239,9 @@ def main():
             s_held=h(x["s_held"]), s_row_pos=h(x["s_row_pos"]), n_cap=x["n_cap"])
         if group:
             held["select"] = O.SELECT_GROUP
+        if w.select == 2:
+            held["select"] = O.SELECT_ACCUM
+            held["acc"] = np.zeros(tuple(ps.buf.acc_score.shape), np.float32)
         try:
             os.sched_setaffinity(0, {sorted(os.sched_getaffinity(0))[0]})
         except (AttributeError, OSError):
@@ -274,6 +283,7 @@ def main():
             **({"recent": budget_text(w.recent)} if w.recent != ("abs", 0) else {}),
             **({"small_cache_kept": f"{w.slm_keep}%"} if w.slm_keep else {}),
             **({"selection": "one per large kv head (summed)"} if group else {}),
+            **({"selection": "accumulated scores (running state)"} if w.select == 2 else {}),
             "launch": "eager" if args.eager else "hip-graph",
             "rotated_input_copies": args.rotate,
         },

@@ -52,7 +52,7 @@
 extern "C" {
 #endif
 
-#define SMALLKV_ABI_VERSION 5
+#define SMALLKV_ABI_VERSION 6
 
 typedef enum { SMALLKV_F32 = 0, SMALLKV_BF16 = 1 } smallkv_dtype_t;
 
@@ -205,11 +205,22 @@ int smallkv_group_select_workspace_size(const smallkv_batch_t *batch,
                                         const smallkv_model_t *small,
                                         const smallkv_model_t *large, size_t *bytes);
 
-/* Who shares a selection (smallkv_step_t.select). */
+/* Stage 2 of SMALLKV_SELECT_ACCUM (see smallkv_select_t): acc_score
+ * [B][n_small_heads][n_cap] (the running scores) += this step's
+ * probabilities, then the lists and weights in the per-head layout of
+ * smallkv_partition.  ws: smallkv_accum_select_workspace_size. */
+int smallkv_accum_select(const smallkv_batch_t *batch, const smallkv_model_t *small,
+                         const float *logits, const float *row_max, const float *row_sum,
+                         float *acc_score, int32_t *crit_idx, int32_t *marg_idx,
+                         float *marg_prob, float *mass, void *ws, size_t ws_bytes, void *stream);
+int smallkv_accum_select_workspace_size(const smallkv_batch_t *batch,
+                                        const smallkv_model_t *small, size_t *bytes);
+
+/* How tokens are selected (smallkv_step_t.select). */
 typedef enum {
   SMALLKV_SELECT_HEAD = 0,  /* default: each large head i takes the sets of its
                                small head f(i) (the partition of stage 2) */
-  SMALLKV_SELECT_GROUP = 1  /* the query heads of one large kv head share one
+  SMALLKV_SELECT_GROUP = 1, /* the query heads of one large kv head share one
                                critical and one marginal set (the cache is
                                stored per kv head), ranked by
                                F(t) = sum over the group's heads h of
@@ -224,6 +235,16 @@ typedef enum {
                                index ascending; recent tokens first).  Each
                                head keeps its own p' = exp(logit - row_max) /
                                row_sum on the shared marginal set. */
+  SMALLKV_SELECT_ACCUM = 2  /* per small head, ranked by an accumulated score
+                               (H2O's accumulated attention, the eviction the
+                               method builds on): the caller-owned state
+                               acc_score [B][n_small_heads][n_cap] (zeroed
+                               before the first step) becomes, for t < N_b,
+                               acc[t] = acc[t] + e(t)/Z in fp32 (e and Z as
+                               for SMALLKV_SELECT_GROUP), and the partition
+                               ranks acc (descending, index ascending; recent
+                               tokens first); marg_prob and mass are this
+                               step's p'.  Layouts as for the default. */
 } smallkv_select_t;
 
 /* A whole decode step: stage 1 over every small layer, stage 2 over every
@@ -233,7 +254,8 @@ typedef enum {
  * SMALLKV_SELECT_GROUP: crit_idx and marg_idx are [B][L*Hkv][cap] (one row
  * per large layer and kv head), marg_prob [B][L*Hq][km_cap] and mass
  * [B][L*Hq][2] (one row per large query head); the small model's cache must
- * hold every token (small.held NULL) and L's query heads per kv head <= 16. */
+ * hold every token (small.held NULL) and L's query heads per kv head <= 16.
+ * SMALLKV_SELECT_ACCUM also needs small.held NULL. */
 typedef struct {
   smallkv_batch_t batch;
   smallkv_model_t small, large;
@@ -243,6 +265,8 @@ typedef struct {
   int32_t *crit_idx, *marg_idx;
   float *marg_prob, *mass;
   int32_t select;          /* smallkv_select_t */
+  float *acc_score;        /* SMALLKV_SELECT_ACCUM only: [B][n_small_heads][n_cap]
+                              running scores, read and updated by every step */
 } smallkv_step_t;
 
 int smallkv_step(const smallkv_step_t *step, void *ws, size_t ws_bytes, void *stream);

@@ -85,9 +85,9 @@ StepLayout step_layout(const smallkv_batch_t &b, const smallkv_model_t &small,
   const SmallPlan p = plan_small(small_view(b, small), small);
   const GroupPlan gp = plan_group(b, large, nsh);
   StepLayout l{};
-  if (select == SMALLKV_SELECT_GROUP) {
+  if (select == SMALLKV_SELECT_GROUP || select == SMALLKV_SELECT_ACCUM) {
     l.total = max_sz(max_sz(p.ws_bytes, gp.use ? gp.ws_bytes : 0),
-                     group_layout(b, small, large, 0).end);
+                     group_layout(b, small, large, 0, select == SMALLKV_SELECT_ACCUM).end);
     return l;
   }
   l.tab_offset = (max_sz(p.ws_bytes, gp.use ? gp.ws_bytes : 0) + 255) / 256 * 256;
@@ -165,7 +165,7 @@ int smallkv_workspace_size(const smallkv_step_t *step, size_t *bytes) {
   if (rc) return rc;
   const int nsh = step->small.n_layers * step->small.n_q_heads;
   if ((rc = check_large(&step->batch, &step->large, step->head_map, nsh))) return rc;
-  if (step->select != SMALLKV_SELECT_HEAD && step->select != SMALLKV_SELECT_GROUP)
+  if (step->select < SMALLKV_SELECT_HEAD || step->select > SMALLKV_SELECT_ACCUM)
     return SMALLKV_EINVAL;
   *bytes = step_layout(step->batch, step->small, step->large, nsh, step->select).total;
   return SMALLKV_OK;
@@ -224,6 +224,31 @@ int smallkv_hybrid_attn(const smallkv_batch_t *batch, const smallkv_model_t *lar
                                  static_cast<hipStream_t>(stream)));
 }
 
+int smallkv_accum_select_workspace_size(const smallkv_batch_t *batch,
+                                        const smallkv_model_t *small, size_t *bytes) {
+  if (!bytes) return SMALLKV_EINVAL;
+  const int rc = check_small(batch, small);
+  if (rc) return rc;
+  *bytes = group_layout(*batch, *small, *small, 0, true).end;
+  return SMALLKV_OK;
+}
+
+int smallkv_accum_select(const smallkv_batch_t *batch, const smallkv_model_t *small,
+                         const float *logits, const float *row_max, const float *row_sum,
+                         float *acc_score, int32_t *crit_idx, int32_t *marg_idx,
+                         float *marg_prob, float *mass, void *ws, size_t ws_bytes, void *stream) {
+  const int rc = check_small(batch, small);
+  if (rc) return rc;
+  if (small->held) return SMALLKV_EUNSUPPORTED;
+  if (!logits || !row_max || !row_sum || !acc_score || !crit_idx || !mass) return SMALLKV_EINVAL;
+  if (batch->km_cap > 0 && (!marg_idx || !marg_prob)) return SMALLKV_EINVAL;
+  const GroupLayout lay = group_layout(*batch, *small, *small, 0, true);
+  if (!ws || ws_bytes < lay.end) return SMALLKV_EWORKSPACE;
+  return status_of(launch_accum_select(*batch, *small, logits, row_max, row_sum, acc_score,
+                                       crit_idx, marg_idx, marg_prob, mass, ws, lay,
+                                       static_cast<hipStream_t>(stream)));
+}
+
 int smallkv_group_select_workspace_size(const smallkv_batch_t *batch,
                                         const smallkv_model_t *small,
                                         const smallkv_model_t *large, size_t *bytes) {
@@ -279,14 +304,29 @@ int smallkv_step(const smallkv_step_t *s, void *ws, size_t ws_bytes, void *strea
   if (!s->logits || !s->row_max || !s->row_sum || !s->crit_idx || !s->mass) return SMALLKV_EINVAL;
   if (s->batch.km_cap > 0 && (!s->marg_idx || !s->marg_prob)) return SMALLKV_EINVAL;
   const bool group = s->select == SMALLKV_SELECT_GROUP;
-  if (!group && s->select != SMALLKV_SELECT_HEAD) return SMALLKV_EINVAL;
-  if (group && (s->small.held || s->large.n_q_heads / s->large.n_kv_heads > 16))
-    return SMALLKV_EUNSUPPORTED;
+  const bool accum = s->select == SMALLKV_SELECT_ACCUM;
+  if (!group && !accum && s->select != SMALLKV_SELECT_HEAD) return SMALLKV_EINVAL;
+  if (accum && !s->acc_score) return SMALLKV_EINVAL;
+  if ((group || accum) && s->small.held) return SMALLKV_EUNSUPPORTED;
+  if (group && s->large.n_q_heads / s->large.n_kv_heads > 16) return SMALLKV_EUNSUPPORTED;
   const smallkv_batch_t sb = small_view(s->batch, s->small);
   const SmallPlan p = plan_small(sb, s->small);
   const StepLayout lay = step_layout(s->batch, s->small, s->large, nsh, s->select);
   if (lay.total && (!ws || ws_bytes < lay.total)) return SMALLKV_EWORKSPACE;
   hipStream_t st = static_cast<hipStream_t>(stream);
+  if (accum) {
+    // stage 1 with its own merge, the accumulated scores and their
+    // partition, stage 3 as for per-head selection
+    hipError_t e = launch_small_attn(sb, s->small, s->logits, s->row_max, s->row_sum,
+                                     static_cast<float *>(ws), p, st);
+    if (e != hipSuccess) return SMALLKV_EDEVICE;
+    e = launch_accum_select(s->batch, s->small, s->logits, s->row_max, s->row_sum, s->acc_score,
+                            s->crit_idx, s->marg_idx, s->marg_prob, s->mass, ws,
+                            group_layout(s->batch, s->small, s->large, 0, true), st);
+    if (e != hipSuccess) return SMALLKV_EDEVICE;
+    return status_of(launch_stage3(s->batch, s->large, s->head_map, nsh, s->crit_idx, s->marg_idx,
+                                   s->marg_prob, s->mass, s->mode, ws, nullptr, false, st));
+  }
   if (group) {
     // stage 1 with its own merge, the group selection, stage 3 on its sets
     hipError_t e = launch_small_attn(sb, s->small, s->logits, s->row_max, s->row_sum,

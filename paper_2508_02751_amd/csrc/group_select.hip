@@ -38,6 +38,10 @@ struct GroupSelArgs {
   float *keys, *key_max;   // [B][L*hkv][n_cap], [B][L*hkv]
   const int32_t *crit, *marg;  // group lists [B][L*hkv][cap]
   float *marg_prob, *mass;     // per large head [B][L*hq][km_cap], [B][L*hq][2]
+  // accumulated-score selection: per small head, acc [B][nsh][n_cap] (the
+  // running score, updated in place); lists and weights per small head
+  int accum;
+  float *acc;
 };
 
 __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
@@ -145,14 +149,59 @@ __global__ __launch_bounds__(kGT) void group_scores(GroupSelArgs a) {
   }
 }
 
+// Accumulated scores: blockIdx.x a small head row, blockIdx.y a chunk of
+// kScoreTok tokens.  acc[t] += e(t) / Z in place; the row's largest score by
+// an atomic max on its bits.
+__global__ __launch_bounds__(kGT) void accum_scores(GroupSelArgs a) {
+  constexpr int kQ = kScoreTok / kGT;
+  __shared__ float wmax[kGT / kWave];
+  const int row = blockIdx.x, b = row / a.nsh;
+  const int n = clampi(a.seq_len[b], 1, a.n_cap);
+  const int t0 = blockIdx.y * kScoreTok;
+  if (t0 >= n) return;
+  const float m = a.row_max[row];
+  const float z = __fmul_rn(__ull2float_rn(a.zq_int[row]), 0x1p-40f);
+  const float *lg = a.logits + (int64_t)row * a.n_cap;
+  float *acc = a.acc + (int64_t)row * a.n_cap;
+  float fmx = 0.0f;
+#pragma unroll
+  for (int q = 0; q < kQ; ++q) {
+    const int t = t0 + q * kGT + threadIdx.x;
+    if (t < n) {
+      const float f = __fadd_rn(acc[t], __fdiv_rn(cw_exp(__fsub_rn(lg[t], m)), z));
+      acc[t] = f;
+      fmx = fmaxf(fmx, f);
+    }
+  }
+  fmx = wave_max(fmx);
+  if ((threadIdx.x & (kWave - 1)) == 0) wmax[threadIdx.x / kWave] = fmx;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float x = wmax[0];
+    for (int w = 1; w < kGT / kWave; ++w) x = fmaxf(x, wmax[w]);
+    atomicMax(reinterpret_cast<unsigned int *>(&a.key_max[row]), __float_as_uint(x));
+  }
+}
+
 __global__ __launch_bounds__(kGT) void group_weights(GroupSelArgs a) {
   __shared__ float red[2][kGT / kWave];
-  const int prow = blockIdx.x;  // (b, layer, query head)
-  const int perq = a.L * a.hq, b = prow / perq, layer = (prow % perq) / a.hq, h = prow % a.hq;
-  const int64_t grow = ((int64_t)b * a.L + layer) * a.hkv + h / a.gq;
+  // group selection: one workgroup per large query head (b, layer, h), lists
+  // of its group; accumulated scores: one per small head, its own lists
+  const int prow = blockIdx.x;
+  int b, j;
+  int64_t grow;
+  if (a.accum) {
+    b = prow / a.nsh;
+    j = prow % a.nsh;
+    grow = prow;
+  } else {
+    const int perq = a.L * a.hq, layer = (prow % perq) / a.hq, h = prow % a.hq;
+    b = prow / perq;
+    grow = ((int64_t)b * a.L + layer) * a.hkv + h / a.gq;
+    j = clampi(a.head_map[layer * a.hq + h], 0, a.nsh - 1);
+  }
   const Sizes sz = set_sizes(a.seq_len, a.k_crit, a.k_marg, a.k_recent, b, a.n_cap, a.kc_cap,
                              a.km_cap);
-  const int j = clampi(a.head_map[layer * a.hq + h], 0, a.nsh - 1);
   const int64_t row = (int64_t)b * a.nsh + j;
   const float m = a.row_max[row], zinv = 1.0f / a.row_sum[row];
   const float *lg = a.logits + row * a.n_cap;
@@ -210,14 +259,17 @@ GroupSelArgs group_args(const smallkv_batch_t &b, const smallkv_model_t &small,
 }  // namespace
 
 GroupLayout group_layout(const smallkv_batch_t &b, const smallkv_model_t &small,
-                         const smallkv_model_t &large, size_t offset) {
+                         const smallkv_model_t &large, size_t offset, bool accum) {
   auto r256 = [](size_t x) { return (x + 255) / 256 * 256; };
   const size_t nsh = (size_t)small.n_layers * small.n_q_heads;
-  const size_t grows = (size_t)b.batch * large.n_layers * large.n_kv_heads;
+  // rows ranked: groups, or small heads for accumulated scores (whose
+  // scores are the caller's state: no key buffer)
+  const size_t grows = accum ? (size_t)b.batch * nsh
+                             : (size_t)b.batch * large.n_layers * large.n_kv_heads;
   GroupLayout l{};
   l.zq = r256(offset);
   l.keys = l.zq + r256((size_t)b.batch * nsh * sizeof(uint64_t));
-  l.key_max = l.keys + r256(grows * b.n_cap * sizeof(float));
+  l.key_max = l.keys + (accum ? 0 : r256(grows * b.n_cap * sizeof(float)));
   l.part_mp = l.key_max + r256(grows * sizeof(float));
   l.part_mass = l.part_mp + r256(grows * (b.km_cap > 0 ? b.km_cap : 1) * sizeof(float));
   l.end = l.part_mass + r256(grows * 2 * sizeof(float));
@@ -256,6 +308,41 @@ hipError_t launch_group_select(const smallkv_batch_t &b, const smallkv_model_t &
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(group_weights, dim3(b.batch * large.n_layers * large.n_q_heads), dim3(kGT), 0,
                      st, a);
+  return hipGetLastError();
+}
+
+}  // namespace smallkv
+
+namespace smallkv {
+
+hipError_t launch_accum_select(const smallkv_batch_t &b, const smallkv_model_t &small,
+                               const float *logits, const float *row_max, const float *row_sum,
+                               float *acc, int32_t *crit, int32_t *marg, float *marg_prob,
+                               float *mass, void *ws, const GroupLayout &lay, hipStream_t st) {
+  char *w = static_cast<char *>(ws);
+  GroupSelArgs a = group_args(b, small, small, nullptr, logits, row_max, row_sum);
+  a.accum = 1;
+  a.acc = acc;
+  a.zq_int = reinterpret_cast<uint64_t *>(w + lay.zq);
+  a.key_max = reinterpret_cast<float *>(w + lay.key_max);
+  a.crit = crit;
+  a.marg = marg;
+  a.marg_prob = marg_prob;
+  a.mass = mass;
+  const int nsh = small.n_layers * small.n_q_heads, rows = b.batch * nsh;
+  hipLaunchKernelGGL(group_init, dim3((rows + kGT - 1) / kGT), dim3(kGT), 0, st, a, rows, rows);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(group_zq, dim3(rows, (b.n_cap + kZqTok - 1) / kZqTok), dim3(kGT), 0, st, a);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL(accum_scores, dim3(rows, (b.n_cap + kScoreTok - 1) / kScoreTok), dim3(kGT), 0,
+                     st, a);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  e = launch_group_partition(b, nsh, acc, a.key_max, crit, marg,
+                             reinterpret_cast<float *>(w + lay.part_mp),
+                             reinterpret_cast<float *>(w + lay.part_mass), st);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(group_weights, dim3(rows), dim3(kGT), 0, st, a);
   return hipGetLastError();
 }
 

@@ -86,7 +86,14 @@ struct GroupLayout {
   size_t zq, keys, key_max, part_mp, part_mass, end;
 };
 GroupLayout group_layout(const smallkv_batch_t &b, const smallkv_model_t &small,
-                         const smallkv_model_t &large, size_t offset);
+                         const smallkv_model_t &large, size_t offset, bool accum = false);
+// Accumulated-score selection (per small head): acc [B][nsh][n_cap] += this
+// step's probabilities, then the partition ranks acc; weights are this
+// step's p'.  Lists and weights in the per-head layout.
+hipError_t launch_accum_select(const smallkv_batch_t &b, const smallkv_model_t &small,
+                               const float *logits, const float *row_max, const float *row_sum,
+                               float *acc, int32_t *crit, int32_t *marg, float *marg_prob,
+                               float *mass, void *ws, const GroupLayout &lay, hipStream_t st);
 // From stage 1's logits and statistics: group lists crit/marg
 // [B][L*Hkv][cap] and per-large-head marg_prob/mass [B][L*Hq][...].
 hipError_t launch_group_select(const smallkv_batch_t &b, const smallkv_model_t &small,

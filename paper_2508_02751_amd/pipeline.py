@@ -94,6 +94,10 @@ def prepare_step(x: dict, mode: int = S.NORM_REMAINING,
     buf = S.alloc_step_buffers(batch, s_q, l_q, ws_bytes, select, l_k.shape[2])
     buf.small_out = small.out
     buf.large_out = large.out
+    # accumulated scores: the running state, zero before the first step
+    acc = (torch.zeros((batch.seq_len.numel(), buf.logits.shape[1], n_cap), dtype=torch.float32,
+                       device=s_q.device) if select == S.SELECT_ACCUM else None)
+    buf.acc_score = acc
     desc = S.make_step(batch, small, large, hm, mode, buf.logits, buf.row_max, buf.row_sum,
-                       buf.crit_idx, buf.marg_idx, buf.marg_prob, buf.mass, select)
+                       buf.crit_idx, buf.marg_idx, buf.marg_prob, buf.mass, select, acc)
     return PreparedStep(batch, small, large, hm, mode, buf, desc, x)

@@ -43,6 +43,8 @@ KERNEL_SOURCES = {
     "group_zq": "group_select.hip",
     "group_scores": "group_select.hip",
     "group_weights": "group_select.hip",
+    "group_init": "group_select.hip",
+    "accum_scores": "group_select.hip",
 }
 
 

@@ -24,7 +24,7 @@ LIB_PATH = os.path.join(_HERE, "libsmallkv.so")
 
 F32, BF16 = 0, 1
 NORM_REMAINING, NORM_NONE, NORM_SLM_CRIT, NORM_RETAINED, NORM_MARG_FILL = range(5)
-SELECT_HEAD, SELECT_GROUP = 0, 1
+SELECT_HEAD, SELECT_GROUP, SELECT_ACCUM = 0, 1, 2
 OK, EINVAL, EUNSUPPORTED, EWORKSPACE, EDEVICE = 0, -1, -2, -3, -4
 
 
@@ -47,7 +47,8 @@ class Step(C.Structure):
                 ("head_map", C.c_void_p), ("mode", C.c_int32),
                 ("logits", C.c_void_p), ("row_max", C.c_void_p), ("row_sum", C.c_void_p),
                 ("crit_idx", C.c_void_p), ("marg_idx", C.c_void_p),
-                ("marg_prob", C.c_void_p), ("mass", C.c_void_p), ("select", C.c_int32)]
+                ("marg_prob", C.c_void_p), ("mass", C.c_void_p), ("select", C.c_int32),
+                ("acc_score", C.c_void_p)]
 
 
 class Window(C.Structure):
@@ -65,6 +66,7 @@ class Match(C.Structure):
 EXPORTS = ("smallkv_small_attn", "smallkv_partition", "smallkv_hybrid_attn", "smallkv_step",
            "smallkv_workspace_size", "smallkv_match", "smallkv_match_workspace_size",
            "smallkv_group_select", "smallkv_group_select_workspace_size",
+           "smallkv_accum_select", "smallkv_accum_select_workspace_size",
            "smallkv_status_string", "smallkv_abi_version")
 
 _lib = None
@@ -92,6 +94,11 @@ def lib():
                                            C.c_void_p]
         L.smallkv_group_select_workspace_size.argtypes = [P(Batch), P(Model), P(Model),
                                                           P(C.c_size_t)]
+        L.smallkv_accum_select.argtypes = [P(Batch), P(Model), C.c_void_p, C.c_void_p,
+                                           C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
+                                           C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t,
+                                           C.c_void_p]
+        L.smallkv_accum_select_workspace_size.argtypes = [P(Batch), P(Model), P(C.c_size_t)]
         L.smallkv_step.argtypes = [P(Step), C.c_void_p, C.c_size_t, C.c_void_p]
         L.smallkv_workspace_size.argtypes = [P(Step), P(C.c_size_t)]
         L.smallkv_match.argtypes = [P(Match), C.c_void_p, C.c_size_t, C.c_void_p]
@@ -102,7 +109,8 @@ def lib():
         for f in ("smallkv_small_attn", "smallkv_partition", "smallkv_hybrid_attn",
                   "smallkv_step", "smallkv_workspace_size", "smallkv_abi_version",
                   "smallkv_match", "smallkv_match_workspace_size", "smallkv_group_select",
-                  "smallkv_group_select_workspace_size"):
+                  "smallkv_group_select_workspace_size", "smallkv_accum_select",
+                  "smallkv_accum_select_workspace_size"):
             getattr(L, f).restype = C.c_int
         _lib = L
     return _lib
@@ -259,11 +267,13 @@ def smallkv_group_select(batch: BatchSpec, small: ModelSpec, large: ModelSpec, h
 
 def make_step(batch: BatchSpec, small: ModelSpec, large: ModelSpec, head_map, mode, logits,
               row_max, row_sum, crit_idx, marg_idx, marg_prob, mass,
-              select: int = SELECT_HEAD) -> Step:
+              select: int = SELECT_HEAD, acc_score: Optional[torch.Tensor] = None) -> Step:
     """Build the C step descriptor once (it holds raw pointers: keep the tensors alive)."""
+    if acc_score is not None and acc_score.dtype != torch.float32:
+        raise ValueError("acc_score must be float32")
     return Step(batch.c(), small.c(), large.c(), _ptr(head_map), int(mode), _ptr(logits),
                 _ptr(row_max), _ptr(row_sum), _ptr(crit_idx), _ptr(marg_idx), _ptr(marg_prob),
-                _ptr(mass), int(select))
+                _ptr(mass), int(select), _ptr(acc_score))
 
 
 def smallkv_step(step: Step, ws=None, stream=None):
@@ -284,6 +294,7 @@ class StepBuffers:
     small_out: torch.Tensor
     large_out: torch.Tensor
     ws: Optional[torch.Tensor]
+    acc_score: Optional[torch.Tensor] = None  # accumulated-score selection state
 
 
 def alloc_step_buffers(batch: BatchSpec, s_q: torch.Tensor, l_q: torch.Tensor,
@@ -357,3 +368,13 @@ def prepare_match(win_len: torch.Tensor, top_k: torch.Tensor, l_q, l_k, l_scale,
 def smallkv_match(desc: Match, ws, stream=None):
     w, wb = _ws(ws)
     _check("smallkv_match", lib().smallkv_match(C.byref(desc), w, wb, _stream(stream)))
+
+
+def smallkv_accum_select(batch: BatchSpec, small: ModelSpec, logits, row_max, row_sum, acc_score,
+                         crit_idx, marg_idx, marg_prob, mass, ws, stream=None):
+    """Stage 2 of accumulated-score selection (acc_score updated in place)."""
+    b, sm = batch.c(), small.c()
+    w, wb = _ws(ws)
+    _check("smallkv_accum_select", lib().smallkv_accum_select(
+        C.byref(b), C.byref(sm), _ptr(logits), _ptr(row_max), _ptr(row_sum), _ptr(acc_score),
+        _ptr(crit_idx), _ptr(marg_idx), _ptr(marg_prob), _ptr(mass), w, wb, _stream(stream)))

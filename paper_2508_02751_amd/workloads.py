@@ -128,6 +128,9 @@ WORKLOADS = {
     # the Qwen2 step with one selection per large kv head (summed selection)
     9: Workload(9, "qwen2-7b+0.5b-n8192-b1-bf16-groupsel", 1, 8192, "bf16",
                 QWEN2_0_5B, QWEN2_7B, ("pct", 10), ("pct", 20), select=1),
+    # the Qwen2 step ranked by H2O-style accumulated scores (running state)
+    10: Workload(10, "qwen2-7b+0.5b-n8192-b1-bf16-accum", 1, 8192, "bf16",
+                 QWEN2_0_5B, QWEN2_7B, ("pct", 10), ("pct", 20), select=2),
 }
 
 LATENT = 64

@@ -33,7 +33,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_abi_version_and_status_strings():
     L = S.lib()
-    assert L.smallkv_abi_version() == 5
+    assert L.smallkv_abi_version() == 6
     assert L.smallkv_status_string(0) == b"ok"
     assert L.smallkv_status_string(-3) == b"workspace too small"
     assert L.smallkv_status_string(123) == b"unknown status"
@@ -46,7 +46,7 @@ def _fake_step(**over):
                 km_cap=128)
     sm = S.Model(1, 14, 2, 64, S.BF16, 0.125, p, p, p, 512, None, None, p)
     lg = S.Model(1, 28, 4, 128, S.BF16, 0.088, p, p, p, 512, None, None, p)
-    st = S.Step(b, sm, lg, p, 0, p, p, p, p, p, p, p, S.SELECT_HEAD)
+    st = S.Step(b, sm, lg, p, 0, p, p, p, p, p, p, p, S.SELECT_HEAD, None)
     for k, v in over.items():
         obj, field = k.split("__")
         setattr({"b": st.batch, "s": st.small, "l": st.large, "st": st}[obj], field, v)
@@ -68,7 +68,7 @@ def _fake_step(**over):
     ({"s__row_pos": 0x1000}, S.EINVAL),                   # positions without held rows
     ({"s__held": 0x1000, "s__row_pos": 0x1000, "s__n_rows": 600}, S.EINVAL),  # > n_cap
     ({"l__held": 0x1000, "l__row_pos": 0x1000}, S.EINVAL),  # small model only
-    ({"st__select": 2}, S.EINVAL),
+    ({"st__select": 3}, S.EINVAL),
 ])
 def test_workspace_size_rejects_bad_small_model(over, status):
     n = C.c_size_t()
@@ -84,6 +84,9 @@ def test_workspace_size_rejects_bad_small_model(over, status):
     ({"l__k_slot": 0x1000}, S.EINVAL),          # one slot map without the other
     ({"l__n_rows": 100}, S.EINVAL),             # compact rows need slot maps
     ({"b__kc_cap": 20000, "l__dtype": S.F32}, S.EUNSUPPORTED),  # per-head kernel's LDS
+    ({"st__select": 2}, S.EINVAL),               # accumulated scores without their state
+    ({"st__select": 2, "st__acc_score": 0x1000, "s__held": 0x1000, "s__row_pos": 0x1000,
+      "s__n_rows": 200}, S.EUNSUPPORTED),        # ... or over a compressed small cache
 ])
 def test_step_rejects_before_launch(over, status):
     st = _fake_step(**over)

@@ -428,3 +428,66 @@ def test_group_selection_single_stage_calls_match_step():
                       (mp, b.marg_prob), (ms, b.mass), (small.out, b.small_out),
                       (large.out, b.large_out)):
         assert torch.equal(got, want)
+
+
+# --------------------------------------------- accumulated scores (H2O-style) --
+
+@pytest.mark.parametrize("dtype,recent", [("f32", None), ("bf16", ("pct", 3))])
+def test_accumulated_scores_over_drifting_steps(dtype, recent):
+    """Four consecutive steps of a drifting ragged batch: the running scores
+    stay bit-identical to the oracle's, and so do the lists they select."""
+    kw = {"recent": recent} if recent else {}
+    w = custom("accum", 125, 3, 1400, dtype, W.ModelShape(2, 8, 2, 64), W.ModelShape(2, 8, 2, 128),
+               ("pct", 8), ("pct", 15), ragged_min=600, steps=4, **kw)
+    ps, acc_ref = None, None
+    for step in range(4):
+        x = W.make_step_inputs(w, DEV, step)
+        x["select"] = S.SELECT_ACCUM
+        if ps is None:
+            ps = prepare_step(x)
+            acc_ref = np.zeros(tuple(ps.buf.acc_score.shape), np.float32)
+        else:
+            ps.with_query(x["s_q"], x["l_q"], x["seq_len"], x["k_crit"], x["k_marg"],
+                          x.get("k_recent"))
+        log(f"[parity] accumulated scores, step {step}")
+        ps.run()
+        torch.cuda.synchronize()
+        ref = O.step(seq_len=host(x["seq_len"]), k_crit=host(x["k_crit"]), k_marg=host(x["k_marg"]),
+                     kc_cap=int(x["kc_cap"]), km_cap=int(x["km_cap"]), head_map=host(x["head_map"]),
+                     mode=O.NORM_REMAINING, s_q=host(x["s_q"]), s_k=host(x["s_k"]), s_v=host(x["s_v"]),
+                     s_scale=0.125, l_q=host(x["l_q"]), l_k=host(x["l_k"]), l_v=host(x["l_v"]),
+                     l_scale=1 / np.sqrt(128.0),
+                     k_recent=host(x["k_recent"]) if x.get("k_recent") is not None else None,
+                     select=O.SELECT_ACCUM, acc=acc_ref)
+        compare_step(ps.buf, ref, x, w.torch_dtype, f"accumulated step {step}")
+        seq = host(x["seq_len"])
+        got = host(ps.buf.acc_score)
+        for b in range(seq.size):
+            n = int(seq[b])
+            assert np.array_equal(got[b, :, :n].view(np.uint32), acc_ref[b, :, :n].view(np.uint32)), \
+                f"running scores differ at step {step}, sequence {b}"
+
+
+def test_accumulated_single_stage_calls_match_step():
+    w = custom("accum-stages", 126, 2, 1500, "bf16", SMALL, LARGE, ("pct", 10), ("pct", 20),
+               ragged_min=400, select=2)
+    x = W.make_step_inputs(w, DEV)
+    ps = prepare_step(x)
+    ps.run()
+    b = ps.buf
+    nsh = SMALL.layers * SMALL.q_heads
+    lg, rm, rs = torch.empty_like(b.logits), torch.empty_like(b.row_max), torch.empty_like(b.row_sum)
+    small = S.ModelSpec(ps.small.q, ps.small.k, ps.small.v, torch.empty_like(ps.small.out),
+                        ps.small.scale)
+    S.smallkv_small_attn(ps.batch, small, lg, rm, rs, b.ws)
+    acc = torch.zeros_like(b.acc_score)
+    ci, mi = torch.empty_like(b.crit_idx), torch.empty_like(b.marg_idx)
+    mp, ms = torch.empty_like(b.marg_prob), torch.empty_like(b.mass)
+    S.smallkv_accum_select(ps.batch, small, lg, rm, rs, acc, ci, mi, mp, ms, b.ws)
+    large = S.ModelSpec(ps.large.q, ps.large.k, ps.large.v, torch.empty_like(ps.large.out),
+                        ps.large.scale)
+    S.smallkv_hybrid_attn(ps.batch, large, ps.head_map, nsh, ci, mi, mp, ms, ws=b.ws)
+    torch.cuda.synchronize()
+    for got, want in ((acc, b.acc_score), (ci, b.crit_idx), (mi, b.marg_idx), (mp, b.marg_prob),
+                      (ms, b.mass), (large.out, b.large_out)):
+        assert torch.equal(got, want)
