@@ -75,6 +75,15 @@ class MatchIn(C.Structure):
                 ("large", Window), ("small", Window)]
 
 
+class StoreIn(C.Structure):
+    _fields_ = [("batch", C.c_int32), ("n_cap", C.c_int32), ("layers", C.c_int32),
+                ("q_heads", C.c_int32), ("kv_heads", C.c_int32), ("dim", C.c_int32),
+                ("select", C.c_int32), ("n_small_heads", C.c_int32), ("kc_cap", C.c_int32),
+                ("km_cap", C.c_int32), ("rows", C.c_int64), ("seq_len", _I), ("head_map", _I),
+                ("crit", _I), ("marg", _I), ("full_k", _F), ("full_v", _F), ("old_k", _F),
+                ("old_v", _F), ("old_k_slot", _I), ("old_v_slot", _I)]
+
+
 class StepOut(C.Structure):
     _fields_ = [
         ("logits", _F),
@@ -112,6 +121,8 @@ def lib():
         L.orc_jaccard.argtypes = [C.c_int, _U8, _U8, C.POINTER(C.c_int), C.POINTER(C.c_int)]
         L.orc_jaccard.restype = None
         L.orc_match.argtypes = [C.POINTER(MatchIn), _I, _F, _U8]
+        L.orc_store_update.argtypes = [C.POINTER(StoreIn), _F, _F, _I, _I, _I]
+        L.orc_store_update.restype = C.c_int
         L.orc_zq.argtypes = [C.c_int, _F, C.c_float]
         L.orc_zq.restype = C.c_float
         for f in (L.orc_small_head, L.orc_partition, L.orc_hybrid_head, L.orc_step,
@@ -332,3 +343,30 @@ def zq(logits, m) -> np.float32:
     """The group key's normaliser of one small head (orc_zq)."""
     lg = _f32(logits)
     return np.float32(lib().orc_zq(lg.size, _p(lg, _F), C.c_float(m)))
+
+
+def store_update(*, seq_len, head_map, crit, marg, full_k, full_v, rows, n_small_heads,
+                 select=SELECT_HEAD, old_k=None, old_v=None, old_k_slot=None, old_v_slot=None):
+    """The compact store after a step (orc_store_update).  full_k/full_v
+    [B,L,Hk,n_cap,d]; crit/marg as the step wrote them.  Returns (k [B,L,Hk,rows,d],
+    v, k_slot [B,L,Hk,n_cap], v_slot, counts [B,L,Hk,2]); rows past a unit's
+    count and slot entries at or past its sequence length are left as -1 / 0."""
+    full_k, full_v = _f32(full_k), _f32(full_v)
+    seq_len, head_map, crit, marg = map(_i32, (seq_len, head_map, crit, marg))
+    B, L, hk, ncap, d = full_k.shape
+    hq = head_map.size // L
+    nk = np.zeros((B, L, hk, rows, d), np.float32)
+    nv = np.zeros_like(nk)
+    ks = np.full((B, L, hk, ncap), -1, np.int32)
+    vs = np.full_like(ks, -1)
+    cnt = np.zeros((B, L, hk, 2), np.int32)
+    ok, ov = (_f32(old_k), _f32(old_v)) if old_k is not None else (None, None)
+    oks, ovs = (_i32(old_k_slot), _i32(old_v_slot)) if old_k_slot is not None else (None, None)
+    si = StoreIn(B, ncap, L, hq, hk, d, int(select), int(n_small_heads), crit.shape[-1],
+                 marg.shape[-1], int(rows), _p(seq_len, _I), _p(head_map, _I), _p(crit, _I),
+                 _p(marg, _I), _p(full_k, _F), _p(full_v, _F),
+                 _p(ok, _F) if ok is not None else None, _p(ov, _F) if ov is not None else None,
+                 _p(oks, _I) if oks is not None else None, _p(ovs, _I) if ovs is not None else None)
+    _check(lib().orc_store_update(C.byref(si), _p(nk, _F), _p(nv, _F), _p(ks, _I), _p(vs, _I),
+                                  _p(cnt, _I)), "orc_store_update")
+    return nk, nv, ks, vs, cnt

@@ -480,3 +480,80 @@ int orc_step(const orc_step_in *in, const orc_step_out *out) {
   free(nm);
   return rc;
 }
+
+/* ----------------------------------------------------- store maintenance -- */
+
+/* Builds one kv head's store (see orc_store_update in the header). */
+static void store_unit(const orc_store_in *in, size_t unit, int n, const uint8_t *inset,
+                       const float *full, const float *old, const int32_t *old_slot,
+                       float *dst, int32_t *slot, int32_t *count) {
+  const int d = in->dim;
+  int r = 0;
+  for (int t = 0; t < n; ++t) {
+    if (!inset[t]) {
+      slot[t] = -1;
+      continue;
+    }
+    if (r < in->rows) {
+      const int os = old_slot ? old_slot[unit * in->n_cap + t] : -1;
+      const float *src = (os >= 0 && os < in->rows)
+                             ? old + (unit * (size_t)in->rows + (size_t)os) * d
+                             : full + (unit * (size_t)in->n_cap + (size_t)t) * d;
+      memcpy(dst + (unit * (size_t)in->rows + (size_t)r) * d, src, sizeof(float) * (size_t)d);
+      slot[t] = r;
+    } else {
+      slot[t] = -1;
+    }
+    ++r;
+  }
+  *count = r;
+}
+
+int orc_store_update(const orc_store_in *in, float *new_k, float *new_v, int32_t *k_slot,
+                     int32_t *v_slot, int32_t *counts) {
+  const int B = in->batch, L = in->layers, hq = in->q_heads, hk = in->kv_heads;
+  if (B < 1 || L < 1 || hk < 1 || hq % hk || in->n_cap < 1 || in->rows < 1) return ORC_EINVAL;
+  const int g = hq / hk;
+  uint8_t *inK = (uint8_t *)malloc((size_t)in->n_cap), *inV = (uint8_t *)malloc((size_t)in->n_cap);
+  if (!inK || !inV) {
+    free(inK);
+    free(inV);
+    return ORC_EINVAL;
+  }
+  int rc = ORC_OK;
+  for (int b = 0; b < B && rc == ORC_OK; ++b) {
+    const int n = in->seq_len[b];
+    if (n < 1 || n > in->n_cap) {
+      rc = ORC_EINVAL;
+      break;
+    }
+    for (int li = 0; li < L; ++li)
+      for (int kv = 0; kv < hk; ++kv) {
+        memset(inK, 0, (size_t)n);
+        memset(inV, 0, (size_t)n);
+        for (int h = 0; h < g; ++h) {
+          /* the lists this query head reads */
+          size_t row;
+          if (in->select == 1) {
+            row = ((size_t)b * L + li) * hk + kv;
+          } else {
+            const int j = in->head_map[li * hq + kv * g + h];
+            row = (size_t)b * in->n_small_heads + j;
+          }
+          const int32_t *c = in->crit + row * in->kc_cap, *m = in->marg + row * in->km_cap;
+          for (int i = 0; i < in->kc_cap; ++i)
+            if (c[i] >= 0 && c[i] < n) inK[c[i]] = inV[c[i]] = 1;
+          for (int i = 0; i < in->km_cap; ++i)
+            if (m[i] >= 0 && m[i] < n) inV[m[i]] = 1;
+        }
+        const size_t unit = ((size_t)b * L + li) * hk + kv;
+        store_unit(in, unit, n, inK, in->full_k, in->old_k, in->old_k_slot, new_k,
+                   k_slot + unit * in->n_cap, &counts[2 * unit]);
+        store_unit(in, unit, n, inV, in->full_v, in->old_v, in->old_v_slot, new_v,
+                   v_slot + unit * in->n_cap, &counts[2 * unit + 1]);
+      }
+  }
+  free(inK);
+  free(inV);
+  return rc;
+}

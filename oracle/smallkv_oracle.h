@@ -201,6 +201,35 @@ typedef struct {
  * scores = F of Eq. 1, top = the TopK sets (0/1 bytes). */
 int orc_match(const orc_match_in *in, int32_t *head_map, float *scores, uint8_t *top);
 
+/* ---- retained-store maintenance, smallkv_oracle.c ---- */
+
+/* The large model's compact store after a step's selection (Algorithm 1:
+ * the critical tokens' K and V and the marginal tokens' V are kept; the
+ * paper migrates them between host and device memory in parallel with the
+ * large model's forward).  For every (sequence b, large layer, kv head):
+ *   U_K = the union of the critical lists of the query heads it serves,
+ *   U_V = U_K united with their marginal lists (token positions < N_b);
+ *   row r of the new K store holds the r-th token of U_K in ascending
+ *   order (V likewise), for r < rows; k_slot[t] = that row or -1 for t < N_b.
+ * A row is copied from the old store when the old slot map holds the token
+ * (old_k_slot[t] >= 0, row old_k_slot[t] of old_k), else from the full store
+ * (row t of full_k).  Per head the lists are those of its small head f(i)
+ * (select 0) or, with select 1, the group's own lists [B][L*Hkv][cap].
+ * counts [B][L][Hkv][2]: |U_K|, |U_V| (rows past `rows` are dropped).
+ * Arrays are host fp32 (bf16 widened exactly) or int32; old_* may be NULL. */
+typedef struct {
+  int32_t batch, n_cap, layers, q_heads, kv_heads, dim, select;
+  int32_t n_small_heads, kc_cap, km_cap;
+  int64_t rows;
+  const int32_t *seq_len, *head_map, *crit, *marg;
+  const float *full_k, *full_v;          /* [B][L][Hkv][n_cap][dim] */
+  const float *old_k, *old_v;            /* [B][L][Hkv][rows][dim] or NULL */
+  const int32_t *old_k_slot, *old_v_slot; /* [B][L][Hkv][n_cap] or NULL */
+} orc_store_in;
+
+int orc_store_update(const orc_store_in *in, float *new_k, float *new_v, int32_t *k_slot,
+                     int32_t *v_slot, int32_t *counts);
+
 #ifdef __cplusplus
 }
 #endif

@@ -777,3 +777,99 @@ def test_accumulated_over_growing_steps_is_the_top_of_the_running_sum():
             tol = 1e-5 * run64[j].max()
             assert run64[j, c].min() >= run64[j, np.concatenate([m, rest])].max() - tol
             assert run64[j, m].min() >= run64[j, rest].max() - tol
+
+
+# ----------------------------------------------------- store maintenance --
+
+def _store_case(rng, select=O.SELECT_HEAD, B=2, n=70, L=2, hq=8, hk=2):
+    x = _group_case(rng, B=B, n=n, L=L, hq=hq, hk=hk, separated=False)
+    r = _run(x, 6, 10, select)
+    return x, r
+
+
+@pytest.mark.parametrize("select", [O.SELECT_HEAD, O.SELECT_GROUP])
+def test_store_serves_stage3_like_the_full_cache(select):
+    rng = np.random.default_rng(61 + select)
+    x, r = _store_case(rng, select)
+    B, L, hq, hk = 2, 2, 8, 2
+    nk, nv, ks, vs, cnt = O.store_update(seq_len=x["seq_len"], head_map=x["head_map"],
+                                         crit=r["crit"], marg=r["marg"], full_k=x["l_k"],
+                                         full_v=x["l_v"], rows=70, n_small_heads=8, select=select)
+    for b in range(B):
+        for li in range(L):
+            for h in range(hq):
+                g = h // (hq // hk)
+                row = (li * hk + g) if select == O.SELECT_GROUP else x["head_map"][li * hq + h]
+                prow = li * hq + h if select == O.SELECT_GROUP else row
+                args = (x["l_q"][b, li, h], None, None, r["crit"][b, row], r["marg"][b, row],
+                        r["marg_prob"][b, prow], r["mass"][b, prow], SCALE128)
+                full = O.hybrid_head(x["l_q"][b, li, h], x["l_k"][b, li, g], x["l_v"][b, li, g],
+                                     *args[3:])
+                store = O.hybrid_head(x["l_q"][b, li, h], nk[b, li, g], nv[b, li, g], *args[3:],
+                                      k_slot=ks[b, li, g], v_slot=vs[b, li, g])
+                np.testing.assert_array_equal(store, full)
+
+
+def test_store_rows_are_the_ascending_unions():
+    rng = np.random.default_rng(63)
+    x, r = _store_case(rng)
+    nk, nv, ks, vs, cnt = O.store_update(seq_len=x["seq_len"], head_map=x["head_map"],
+                                         crit=r["crit"], marg=r["marg"], full_k=x["l_k"],
+                                         full_v=x["l_v"], rows=70, n_small_heads=8)
+    hq, hk = 8, 2
+    for b in range(2):
+        n = int(x["seq_len"][b])
+        for li in range(2):
+            for g in range(hk):
+                js = x["head_map"][li * hq + g * 4: li * hq + (g + 1) * 4]
+                UK = sorted(set().union(*[set(r["crit"][b, j][r["crit"][b, j] >= 0].tolist())
+                                          for j in js]))
+                UV = sorted(set(UK).union(*[set(r["marg"][b, j][r["marg"][b, j] >= 0].tolist())
+                                            for j in js]))
+                assert cnt[b, li, g].tolist() == [len(UK), len(UV)]
+                assert [int(np.flatnonzero(ks[b, li, g, :n] == i)[0]) for i in range(len(UK))] == UK
+                assert [int(np.flatnonzero(vs[b, li, g, :n] == i)[0]) for i in range(len(UV))] == UV
+                assert (ks[b, li, g, :n] >= 0).sum() == len(UK)
+                np.testing.assert_array_equal(nk[b, li, g, :len(UK)], x["l_k"][b, li, g, UK])
+                np.testing.assert_array_equal(nv[b, li, g, :len(UV)], x["l_v"][b, li, g, UV])
+
+
+def test_store_copies_held_rows_from_the_old_store():
+    rng = np.random.default_rng(64)
+    x, r = _store_case(rng)
+    common = dict(seq_len=x["seq_len"], head_map=x["head_map"], full_k=x["l_k"], full_v=x["l_v"],
+                  rows=70, n_small_heads=8)
+    ok, ov, oks, ovs, _ = O.store_update(**common, crit=r["crit"], marg=r["marg"])
+    ok, ov = ok + 1000.0, ov - 1000.0  # an old store distinguishable from the full one
+    x2 = dict(x)
+    x2["s_q"] = rng.standard_normal(x["s_q"].shape).astype(np.float32)
+    r2 = _run(x2, 6, 10, O.SELECT_HEAD)
+    nk, nv, ks, vs, cnt = O.store_update(**common, crit=r2["crit"], marg=r2["marg"], old_k=ok,
+                                         old_v=ov, old_k_slot=oks, old_v_slot=ovs)
+    for b in range(2):
+        n = int(x["seq_len"][b])
+        for li in range(2):
+            for g in range(2):
+                for t in range(n):
+                    if ks[b, li, g, t] >= 0:
+                        held = oks[b, li, g, t] >= 0
+                        want = ok[b, li, g, oks[b, li, g, t]] if held else x["l_k"][b, li, g, t]
+                        np.testing.assert_array_equal(nk[b, li, g, ks[b, li, g, t]], want)
+                    if vs[b, li, g, t] >= 0:
+                        held = ovs[b, li, g, t] >= 0
+                        want = ov[b, li, g, ovs[b, li, g, t]] if held else x["l_v"][b, li, g, t]
+                        np.testing.assert_array_equal(nv[b, li, g, vs[b, li, g, t]], want)
+
+
+def test_store_drops_rows_past_its_capacity():
+    rng = np.random.default_rng(65)
+    x, r = _store_case(rng)
+    nk, nv, ks, vs, cnt = O.store_update(seq_len=x["seq_len"], head_map=x["head_map"],
+                                         crit=r["crit"], marg=r["marg"], full_k=x["l_k"],
+                                         full_v=x["l_v"], rows=5, n_small_heads=8)
+    assert (cnt[..., 1] > 5).any()
+    assert ks.max() < 5 and vs.max() < 5
+    for b in range(2):
+        for li in range(2):
+            for g in range(2):
+                assert (vs[b, li, g] >= 0).sum() == min(5, cnt[b, li, g, 1])
