@@ -49,6 +49,8 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--match", action="store_true",
                    help="benchmark the prefill head matching instead of the decode step")
+    p.add_argument("--store", action="store_true",
+                   help="benchmark the retained-store maintenance after a step")
     p.add_argument("--match-batch", type=int, default=1)
     p.add_argument("--match-window", type=int, default=200)
     p.add_argument("--copy-probe-mib", type=int, default=0,
@@ -115,6 +117,8 @@ def main():
 
     if args.match:
         return bench_match(args)
+    if args.store:
+        return bench_store(args)
     import torch
     from paper_2508_02751_amd import smallkv as S
     from paper_2508_02751_amd import workloads as W
@@ -307,6 +311,124 @@ def main():
             / max(1, sb.large_k_union + sb.large_v_union),
             "index_metadata_bytes": sb.index_meta,
         },
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def bench_store(args):
+    """Retained-store maintenance after one step of the workload: a rebuild
+    from the full store in HBM (the roofline), and the update after a drifted
+    step, which reuses the rows the previous store holds and reads only the
+    others from the full store (the rows a host-resident full store would
+    have to send)."""
+    import torch
+    from paper_2508_02751_amd import smallkv as S
+    from paper_2508_02751_amd import workloads as W
+    from paper_2508_02751_amd.pipeline import prepare_step
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = W.WORKLOADS[args.workload]
+    print(f"[bench] generating {w.name}", file=sys.stderr, flush=True)
+    x = W.make_step_inputs(w, dev)
+    ps = prepare_step(x)
+    ps.run()
+    L = w.large
+    g = L.group
+    rows = min(w.n_cap, g * (int(x["kc_cap"]) + int(x["km_cap"])))
+    nsh = ps.buf.logits.shape[1]
+    K = args.steps
+    stream = torch.cuda.current_stream()
+
+    def timed(call):
+        for _ in range(max(args.warmup, 1)):
+            call.run()
+        torch.cuda.synchronize()
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(K)]
+        torch.cuda._sleep(50_000_000)
+        for e0, e1 in ev:
+            e0.record(stream)
+            call.run(stream)
+            e1.record(stream)
+        torch.cuda.synchronize()
+        return sum(a.elapsed_time(b) for a, b in ev) / K
+
+    def store(full_k, full_v, old=None):
+        return S.prepare_store(ps.batch, ps.head_map, nsh, ps.buf.crit_idx, ps.buf.marg_idx,
+                               full_k, full_v, rows, old=old)
+
+    hbm = store(x["l_k"], x["l_v"])
+    ms_hbm = timed(hbm)
+    cnt = hbm.counts.to(torch.int64)
+    row_b = L.head_dim * x["l_k"].element_size()
+    moved = int(cnt.sum()) * row_b                       # rows read once, written once
+    units = cnt.shape[0] * cnt.shape[1] * cnt.shape[2]
+    n_tok = int(x["seq_len"].to(torch.int64).sum()) // w.batch
+    maps = units * n_tok * 8                             # two slot maps written
+    lists = ps.buf.crit_idx.numel() * 4 + ps.buf.marg_idx.numel() * 4
+    alg = 2 * moved + maps + lists
+    achieved = alg / (ms_hbm * 1e-3) / 1e9
+    # the oracle's rebuild of the same store on one host core
+    cpu = None
+    if not args.no_cpu_baseline:
+        sys.path.insert(0, os.path.join(ROOT, "oracle"))
+        import oracle as O
+
+        def h(t):
+            return t.detach().float().cpu().numpy() if t.dtype == torch.bfloat16 else t.cpu().numpy()
+
+        args_h = dict(seq_len=h(x["seq_len"]), head_map=h(x["head_map"]),
+                      crit=h(ps.buf.crit_idx), marg=h(ps.buf.marg_idx), full_k=h(x["l_k"]),
+                      full_v=h(x["l_v"]), rows=rows, n_small_heads=nsh)
+        try:
+            os.sched_setaffinity(0, {sorted(os.sched_getaffinity(0))[0]})
+        except (AttributeError, OSError):
+            pass
+        c0 = time.perf_counter()
+        reps = 0
+        while reps < 1 or time.perf_counter() - c0 < 5.0:
+            O.store_update(**args_h)
+            reps += 1
+        spent = time.perf_counter() - c0
+        cpu = {"value": reps / spent, "unit": "updates/s", "cores": 1, "kind": "oracle",
+               "sample": f"{reps} whole store rebuild(s) of the same step, single-threaded C "
+                         f"oracle pinned to one core ({spent:.1f} s)"}
+    # a drifted step: rows the previous store holds are reused, the others read
+    old = store(x["l_k"], x["l_v"])
+    old.run()
+    s_q, l_q = W.step_queries(w, W.latents(w, dev), 1, dev)
+    ps.with_query(s_q, l_q)
+    ps.run()
+    inc = store(x["l_k"], x["l_v"], old=old)
+    ms_inc = timed(inc)
+    torch.cuda.synchronize()
+    ks_new, ks_old = inc.k_slot, old.k_slot
+    vs_new, vs_old = inc.v_slot, old.v_slot
+    fetched = int(((ks_new >= 0) & (ks_old < 0)).sum() + ((vs_new >= 0) & (vs_old < 0)).sum())
+    kept = int(((ks_new >= 0) & (ks_old >= 0)).sum() + ((vs_new >= 0) & (vs_old >= 0)).sum())
+    out = {
+        "metric": "SmallKV retained-store maintenance updates/s at 1 MI355X",
+        "value": 1e3 / ms_hbm,
+        "unit": "updates/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": ms_hbm,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": f"{w.name}-store", "rows_per_kv_head": rows,
+                   "union_rows": int(cnt.sum()), "kv_heads": units},
+        "roofline": {"kernel": "store_index+store_copy", "bound": "hbm", "achieved": achieved,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": None},
+        "after_a_drifted_step": {"ms": ms_inc, "rows_new": fetched, "rows_reused": kept,
+                                 "new_fraction": fetched / max(1, fetched + kept)},
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

@@ -52,7 +52,7 @@
 extern "C" {
 #endif
 
-#define SMALLKV_ABI_VERSION 6
+#define SMALLKV_ABI_VERSION 7
 
 typedef enum { SMALLKV_F32 = 0, SMALLKV_BF16 = 1 } smallkv_dtype_t;
 
@@ -274,6 +274,43 @@ int smallkv_step(const smallkv_step_t *step, void *ws, size_t ws_bytes, void *st
 /* Bytes of workspace that smallkv_step needs for `step`; the single-stage
  * calls need no more than this for the same shapes.  Host only. */
 int smallkv_workspace_size(const smallkv_step_t *step, size_t *bytes);
+
+/* ---------------------------------------------------------------------------
+ * Retained-store maintenance (Algorithm 1: the critical tokens keep K and V,
+ * the marginal tokens V; the paper migrates these rows between host and
+ * device memory in parallel with the large model's forward).  After a step's
+ * selection, for every (sequence b, large layer, kv head):
+ *   U_K = the union of the critical lists of the query heads it serves,
+ *   U_V = U_K united with their marginal lists (tokens < N_b);
+ *   new_k row r = the K row of U_K's r-th token in ascending order (new_v
+ *   likewise over U_V), for r < rows; k_slot[t] = t's row in new_k or -1,
+ *   v_slot[t] likewise, for t < N_b (entries t >= N_b are not written).
+ * Each row is copied from the old store when its old slot map holds the
+ * token (old_k row old_k_slot[t]), else from the full store (row t), so that
+ * only tokens new to a set are read from the full store, which may be
+ * device memory or host-pinned memory.  The result feeds smallkv_step /
+ * smallkv_hybrid_attn as large->k/v (n_rows = rows) with large->k_slot /
+ * v_slot.  Deterministic; a union longer than `rows` keeps its first rows
+ * and counts reports the full size. */
+typedef struct {
+  smallkv_batch_t batch;   /* the step's batch: seq_len, n_cap (<= 131072), kc_cap, km_cap */
+  int32_t n_layers, n_q_heads, n_kv_heads, head_dim, dtype;  /* the large model */
+  const int32_t *head_map; /* the step's head map (per-head lists) */
+  int32_t n_small_heads;
+  int32_t select;          /* the step's smallkv_select_t: lists per small head,
+                              or per (layer, kv head) for SMALLKV_SELECT_GROUP */
+  const int32_t *crit_idx, *marg_idx; /* the step's lists */
+  const void *full_k, *full_v;        /* [B][L][Hkv][n_cap][head_dim], 16-byte aligned */
+  int64_t rows;                       /* rows per kv head of the new and the old store */
+  const void *old_k, *old_v;          /* optional previous store [B][L][Hkv][rows][head_dim] */
+  const int32_t *old_k_slot, *old_v_slot; /* its slot maps [B][L][Hkv][n_cap] (all four or none) */
+  void *new_k, *new_v;                /* out, [B][L][Hkv][rows][head_dim]; not the old store */
+  int32_t *k_slot, *v_slot;           /* out, [B][L][Hkv][n_cap] */
+  int32_t *counts;                    /* optional out [B][L][Hkv][2]: |U_K|, |U_V| */
+} smallkv_store_t;
+
+int smallkv_store_workspace_size(const smallkv_store_t *store, size_t *bytes);
+int smallkv_store_update(const smallkv_store_t *store, void *ws, size_t ws_bytes, void *stream);
 
 /* ---------------------------------------------------------------------------
  * Prefill similarity matching (Method section, "Similarity Matching",

@@ -16,7 +16,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libsmallkv.so")
 BUILD = os.path.join(ROOT, "_build")
 SOURCES = ["small_attn.hip", "partition.hip", "hybrid.hip", "hybrid_group.hip", "match.hip",
-           "group_select.hip", "capi.hip"]
+           "group_select.hip", "store.hip", "capi.hip"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

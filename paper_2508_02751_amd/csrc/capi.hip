@@ -123,6 +123,28 @@ int check_window(const smallkv_window_t &m) {
   return SMALLKV_OK;
 }
 
+int check_store(const smallkv_store_t *s) {
+  if (!s || !batch_ok(&s->batch)) return SMALLKV_EINVAL;
+  if (s->n_layers < 1 || s->n_q_heads < 1 || s->n_kv_heads < 1 || s->n_q_heads % s->n_kv_heads)
+    return SMALLKV_EINVAL;
+  if (s->dtype != SMALLKV_F32 && s->dtype != SMALLKV_BF16) return SMALLKV_EINVAL;
+  if (s->select < SMALLKV_SELECT_HEAD || s->select > SMALLKV_SELECT_ACCUM) return SMALLKV_EINVAL;
+  if (!s->head_map || s->n_small_heads < 1 || !s->crit_idx || s->rows < 1) return SMALLKV_EINVAL;
+  if (s->batch.km_cap > 0 && !s->marg_idx) return SMALLKV_EINVAL;
+  if (!s->full_k || !s->full_v || !s->new_k || !s->new_v || !s->k_slot || !s->v_slot)
+    return SMALLKV_EINVAL;
+  const bool any_old = s->old_k || s->old_v || s->old_k_slot || s->old_v_slot;
+  const bool all_old = s->old_k && s->old_v && s->old_k_slot && s->old_v_slot;
+  if (any_old && !all_old) return SMALLKV_EINVAL;
+  if (all_old && (s->old_k == s->new_k || s->old_v == s->new_v)) return SMALLKV_EINVAL;
+  const void *ptrs[] = {s->full_k, s->full_v, s->new_k, s->new_v, s->old_k, s->old_v};
+  for (const void *p : ptrs)
+    if (p && !aligned16(p)) return SMALLKV_EINVAL;
+  if (s->head_dim != 64 && s->head_dim != 128) return SMALLKV_EUNSUPPORTED;
+  if (s->batch.n_cap > 131072 || s->rows > INT32_MAX / 2) return SMALLKV_EUNSUPPORTED;
+  return SMALLKV_OK;
+}
+
 int check_match(const smallkv_match_t *m) {
   if (!m || !m->win_len || !m->top_k || !m->head_map) return SMALLKV_EINVAL;
   if (m->batch < 1 || m->w_cap < 1) return SMALLKV_EINVAL;
@@ -277,6 +299,21 @@ int smallkv_group_select(const smallkv_batch_t *batch, const smallkv_model_t *sm
   return status_of(launch_group_select(*batch, *small, *large, head_map, logits, row_max, row_sum,
                                        crit_idx, marg_idx, marg_prob, mass, ws, lay,
                                        static_cast<hipStream_t>(stream)));
+}
+
+int smallkv_store_workspace_size(const smallkv_store_t *s, size_t *bytes) {
+  if (!bytes) return SMALLKV_EINVAL;
+  const int rc = check_store(s);
+  if (rc) return rc;
+  *bytes = store_workspace(*s);
+  return SMALLKV_OK;
+}
+
+int smallkv_store_update(const smallkv_store_t *s, void *ws, size_t ws_bytes, void *stream) {
+  const int rc = check_store(s);
+  if (rc) return rc;
+  if (!ws || ws_bytes < store_workspace(*s)) return SMALLKV_EWORKSPACE;
+  return status_of(launch_store_update(*s, ws, static_cast<hipStream_t>(stream)));
 }
 
 int smallkv_match_workspace_size(const smallkv_match_t *m, size_t *bytes) {

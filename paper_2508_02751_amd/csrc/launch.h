@@ -106,6 +106,11 @@ hipError_t launch_group_partition(const smallkv_batch_t &b, int group_rows, cons
                                   const float *key_max, int32_t *crit, int32_t *marg,
                                   float *marg_prob, float *mass, hipStream_t st);
 
+// Retained-store maintenance: workspace bytes (the unions' token lists and
+// sizes) and the two launches.
+size_t store_workspace(const smallkv_store_t &s);
+hipError_t launch_store_update(const smallkv_store_t &s, void *ws, hipStream_t st);
+
 // Workspace of the prefill matching: the logit matrix S of every head
 // ([B][H][w_cap][ld] fp32, ld = w_cap rounded up to 4), the row maxima per
 // 64-token tile column ([B][H][w_cap][nt] fp32), each row's (max, sum)

@@ -45,6 +45,8 @@ KERNEL_SOURCES = {
     "group_weights": "group_select.hip",
     "group_init": "group_select.hip",
     "accum_scores": "group_select.hip",
+    "store_index": "store.hip",
+    "store_copy": "store.hip",
 }
 
 

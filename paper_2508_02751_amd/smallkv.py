@@ -63,10 +63,22 @@ class Match(C.Structure):
                 ("head_map", C.c_void_p), ("scores", C.c_void_p), ("top_bits", C.c_void_p)]
 
 
+class Store(C.Structure):
+    _fields_ = [("batch", Batch), ("n_layers", C.c_int32), ("n_q_heads", C.c_int32),
+                ("n_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("dtype", C.c_int32),
+                ("head_map", C.c_void_p), ("n_small_heads", C.c_int32), ("select", C.c_int32),
+                ("crit_idx", C.c_void_p), ("marg_idx", C.c_void_p), ("full_k", C.c_void_p),
+                ("full_v", C.c_void_p), ("rows", C.c_int64), ("old_k", C.c_void_p),
+                ("old_v", C.c_void_p), ("old_k_slot", C.c_void_p), ("old_v_slot", C.c_void_p),
+                ("new_k", C.c_void_p), ("new_v", C.c_void_p), ("k_slot", C.c_void_p),
+                ("v_slot", C.c_void_p), ("counts", C.c_void_p)]
+
+
 EXPORTS = ("smallkv_small_attn", "smallkv_partition", "smallkv_hybrid_attn", "smallkv_step",
            "smallkv_workspace_size", "smallkv_match", "smallkv_match_workspace_size",
            "smallkv_group_select", "smallkv_group_select_workspace_size",
            "smallkv_accum_select", "smallkv_accum_select_workspace_size",
+           "smallkv_store_update", "smallkv_store_workspace_size",
            "smallkv_status_string", "smallkv_abi_version")
 
 _lib = None
@@ -99,6 +111,8 @@ def lib():
                                            C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t,
                                            C.c_void_p]
         L.smallkv_accum_select_workspace_size.argtypes = [P(Batch), P(Model), P(C.c_size_t)]
+        L.smallkv_store_update.argtypes = [P(Store), C.c_void_p, C.c_size_t, C.c_void_p]
+        L.smallkv_store_workspace_size.argtypes = [P(Store), P(C.c_size_t)]
         L.smallkv_step.argtypes = [P(Step), C.c_void_p, C.c_size_t, C.c_void_p]
         L.smallkv_workspace_size.argtypes = [P(Step), P(C.c_size_t)]
         L.smallkv_match.argtypes = [P(Match), C.c_void_p, C.c_size_t, C.c_void_p]
@@ -110,7 +124,8 @@ def lib():
                   "smallkv_step", "smallkv_workspace_size", "smallkv_abi_version",
                   "smallkv_match", "smallkv_match_workspace_size", "smallkv_group_select",
                   "smallkv_group_select_workspace_size", "smallkv_accum_select",
-                  "smallkv_accum_select_workspace_size"):
+                  "smallkv_accum_select_workspace_size", "smallkv_store_update",
+                  "smallkv_store_workspace_size"):
             getattr(L, f).restype = C.c_int
         _lib = L
     return _lib
@@ -378,3 +393,52 @@ def smallkv_accum_select(batch: BatchSpec, small: ModelSpec, logits, row_max, ro
     _check("smallkv_accum_select", lib().smallkv_accum_select(
         C.byref(b), C.byref(sm), _ptr(logits), _ptr(row_max), _ptr(row_sum), _ptr(acc_score),
         _ptr(crit_idx), _ptr(marg_idx), _ptr(marg_prob), _ptr(mass), w, wb, _stream(stream)))
+
+
+@dataclasses.dataclass
+class StoreCall:
+    """A prepared smallkv_store_update and the tensors it writes."""
+    desc: Store
+    new_k: torch.Tensor
+    new_v: torch.Tensor
+    k_slot: torch.Tensor
+    v_slot: torch.Tensor
+    counts: torch.Tensor
+    ws: torch.Tensor
+    keep: tuple
+
+    def run(self, stream=None):
+        smallkv_store_update(self.desc, self.ws, stream)
+
+
+def prepare_store(batch: BatchSpec, head_map, n_small_heads: int, crit_idx, marg_idx,
+                  full_k: torch.Tensor, full_v: torch.Tensor, rows: int, select: int = SELECT_HEAD,
+                  old: Optional["StoreCall"] = None) -> StoreCall:
+    """The new compact store (rows per kv head) built from a step's lists;
+    `old`: the previous store, whose rows are reused."""
+    B, L, hk, n_cap, d = full_k.shape
+    hq = head_map.numel() // L
+    dev = full_k.device
+    nk = torch.zeros((B, L, hk, rows, d), dtype=full_k.dtype, device=dev)
+    nv = torch.zeros_like(nk)
+    ks = torch.full((B, L, hk, n_cap), -1, dtype=torch.int32, device=dev)
+    vs = torch.full_like(ks, -1)
+    cnt = torch.zeros((B, L, hk, 2), dtype=torch.int32, device=dev)
+    o = old
+    desc = Store(batch.c(), L, hq, hk, d, _dtype_code(full_k), _ptr(head_map), n_small_heads,
+                 int(select), _ptr(crit_idx), _ptr(marg_idx), _ptr(full_k), _ptr(full_v), rows,
+                 _ptr(o.new_k) if o else None, _ptr(o.new_v) if o else None,
+                 _ptr(o.k_slot) if o else None, _ptr(o.v_slot) if o else None,
+                 _ptr(nk), _ptr(nv), _ptr(ks), _ptr(vs), _ptr(cnt))
+    n = C.c_size_t()
+    _check("smallkv_store_workspace_size", lib().smallkv_store_workspace_size(C.byref(desc),
+                                                                              C.byref(n)))
+    ws = torch.empty(max(n.value, 1), dtype=torch.uint8, device=dev)
+    return StoreCall(desc, nk, nv, ks, vs, cnt, ws, (batch, head_map, crit_idx, marg_idx, full_k,
+                                                     full_v, old))
+
+
+def smallkv_store_update(desc: Store, ws, stream=None):
+    w, wb = _ws(ws)
+    _check("smallkv_store_update", lib().smallkv_store_update(C.byref(desc), w, wb,
+                                                              _stream(stream)))

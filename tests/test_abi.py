@@ -33,7 +33,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_abi_version_and_status_strings():
     L = S.lib()
-    assert L.smallkv_abi_version() == 6
+    assert L.smallkv_abi_version() == 7
     assert L.smallkv_status_string(0) == b"ok"
     assert L.smallkv_status_string(-3) == b"workspace too small"
     assert L.smallkv_status_string(123) == b"unknown status"
