@@ -288,7 +288,9 @@ int smallkv_workspace_size(const smallkv_step_t *step, size_t *bytes);
  * Each row is copied from the old store when its old slot map holds the
  * token (old_k row old_k_slot[t]), else from the full store (row t), so that
  * only tokens new to a set are read from the full store, which may be
- * device memory or host-pinned memory.  The result feeds smallkv_step /
+ * device memory or pinned host memory (hipHostMalloc; the kernels read it
+ * over the host link at the device address the runtime maps it to);
+ * pageable host memory gives SMALLKV_EINVAL before anything is enqueued.  The result feeds smallkv_step /
  * smallkv_hybrid_attn as large->k/v (n_rows = rows) with large->k_slot /
  * v_slot.  Deterministic; a union longer than `rows` keeps its first rows
  * and counts reports the full size. */

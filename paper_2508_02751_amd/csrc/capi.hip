@@ -158,6 +158,31 @@ int check_match(const smallkv_match_t *m) {
   return SMALLKV_OK;
 }
 
+// The address the kernels read `p` at: device memory as it is; pinned host
+// memory (hipHostMalloc, mapped into the device's address space) at the
+// device address the runtime reports for it.  Pageable or unknown host
+// memory is rejected before anything is enqueued.
+int device_view(const void *p, const void **out) {
+  hipPointerAttribute_t at{};
+  if (hipPointerGetAttributes(&at, p) != hipSuccess) {
+    (void)hipGetLastError();
+    return SMALLKV_EINVAL;
+  }
+  if (at.type == hipMemoryTypeDevice || at.type == hipMemoryTypeManaged ||
+      at.type == hipMemoryTypeUnified) {
+    *out = p;
+    return SMALLKV_OK;
+  }
+  if (at.type == hipMemoryTypeHost && at.devicePointer && at.hostPointer) {
+    // both attributes name the same byte of the allocation, so the
+    // distance from either to `p` is the same
+    *out = static_cast<const char *>(at.devicePointer) +
+           (static_cast<const char *>(p) - static_cast<const char *>(at.hostPointer));
+    return aligned16(*out) ? SMALLKV_OK : SMALLKV_EINVAL;
+  }
+  return SMALLKV_EINVAL;
+}
+
 }  // namespace
 
 extern "C" {
@@ -313,7 +338,10 @@ int smallkv_store_update(const smallkv_store_t *s, void *ws, size_t ws_bytes, vo
   const int rc = check_store(s);
   if (rc) return rc;
   if (!ws || ws_bytes < store_workspace(*s)) return SMALLKV_EWORKSPACE;
-  return status_of(launch_store_update(*s, ws, static_cast<hipStream_t>(stream)));
+  smallkv_store_t d = *s;
+  if (device_view(s->full_k, &d.full_k) || device_view(s->full_v, &d.full_v))
+    return SMALLKV_EINVAL;
+  return status_of(launch_store_update(d, ws, static_cast<hipStream_t>(stream)));
 }
 
 int smallkv_match_workspace_size(const smallkv_match_t *m, size_t *bytes) {

@@ -415,10 +415,11 @@ def prepare_store(batch: BatchSpec, head_map, n_small_heads: int, crit_idx, marg
                   full_k: torch.Tensor, full_v: torch.Tensor, rows: int, select: int = SELECT_HEAD,
                   old: Optional["StoreCall"] = None) -> StoreCall:
     """The new compact store (rows per kv head) built from a step's lists;
-    `old`: the previous store, whose rows are reused."""
+    `old`: the previous store, whose rows are reused.  The full store may be
+    on the GPU or in pinned host memory; the new store is on the GPU."""
     B, L, hk, n_cap, d = full_k.shape
     hq = head_map.numel() // L
-    dev = full_k.device
+    dev = crit_idx.device
     nk = torch.zeros((B, L, hk, rows, d), dtype=full_k.dtype, device=dev)
     nv = torch.zeros_like(nk)
     ks = torch.full((B, L, hk, n_cap), -1, dtype=torch.int32, device=dev)

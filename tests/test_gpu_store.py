@@ -143,3 +143,87 @@ def test_stage3_through_the_built_store_matches_the_full_cache():
     err = head_err(host(large.out), host(b.large_out).astype(np.float64))
     log(f"[store] stage 3 through the store vs the full cache: {err:.3g}")
     assert err <= TOL[torch.bfloat16]
+
+
+def test_store_from_pinned_host_memory():
+    """The full store in pinned host memory: a rebuild and the update after a
+    drifted step read it over the host link and equal the oracle (and the
+    same calls over the full store in HBM)."""
+    S, W, prepare_step = modules()
+    w = workload("store-host", 137, steps=2)
+    x0 = W.make_step_inputs(w, DEV, 0)
+    ps = prepare_step(x0)
+    ps.run()
+    rows = capacity(x0, 4)
+    hk, hv = x0["l_k"].cpu().pin_memory(), x0["l_v"].cpu().pin_memory()
+    assert hk.is_pinned() and hv.is_pinned()
+    log("[store] full store in pinned host memory: rebuild")
+    old = S.prepare_store(ps.batch, ps.head_map, ps.buf.logits.shape[1], ps.buf.crit_idx,
+                          ps.buf.marg_idx, hk, hv, rows)
+    old.run()
+    torch.cuda.synchronize()
+    assert old.new_k.is_cuda
+    check_store(old, oracle_store(x0, ps, rows, 0), x0, "rebuild from host memory")
+    x1 = W.make_step_inputs(w, DEV, 1)
+    ps.with_query(x1["s_q"], x1["l_q"], x1["seq_len"], x1["k_crit"], x1["k_marg"])
+    ps.run()
+    log("[store] full store in pinned host memory: update after a drifted step")
+    inc = S.prepare_store(ps.batch, ps.head_map, ps.buf.logits.shape[1], ps.buf.crit_idx,
+                          ps.buf.marg_idx, hk, hv, rows, old=old)
+    inc.run()
+    dev_inc = S.prepare_store(ps.batch, ps.head_map, ps.buf.logits.shape[1], ps.buf.crit_idx,
+                              ps.buf.marg_idx, x1["l_k"], x1["l_v"], rows, old=old)
+    dev_inc.run()
+    torch.cuda.synchronize()
+    check_store(inc, oracle_store(x1, ps, rows, 0, old=old), x1, "update from host memory")
+    for a, b in ((inc.new_k, dev_inc.new_k), (inc.new_v, dev_inc.new_v),
+                 (inc.k_slot, dev_inc.k_slot), (inc.v_slot, dev_inc.v_slot)):
+        assert torch.equal(a, b)
+
+
+def test_store_rejects_pageable_host_memory():
+    S, W, prepare_step = modules()
+    w = workload("store-pageable", 138)
+    x = W.make_step_inputs(w, DEV)
+    ps = prepare_step(x)
+    ps.run()
+    torch.cuda.synchronize()
+    hk, hv = x["l_k"].cpu(), x["l_v"].cpu()
+    assert not hk.is_pinned()
+    sc = S.prepare_store(ps.batch, ps.head_map, ps.buf.logits.shape[1], ps.buf.crit_idx,
+                         ps.buf.marg_idx, hk, hv, capacity(x, 4))
+    with pytest.raises(S.SmallKVError) as e:
+        sc.run()
+    assert e.value.status == S.EINVAL
+    assert not sc.counts.any(), "nothing may run after the rejection"
+
+
+def test_steps_through_a_host_backed_store():
+    """Three drifting steps, each maintaining the store from the previous one
+    and the full store in pinned host memory, then running stage 3 through
+    it: every step equals stage 3 over the full cache."""
+    S, W, prepare_step = modules()
+    w = workload("store-steps-host", 139, steps=3)
+    x = W.make_step_inputs(w, DEV, 0)
+    ps = prepare_step(x)
+    rows = capacity(x, 4)
+    hk, hv = x["l_k"].cpu().pin_memory(), x["l_v"].cpu().pin_memory()
+    old = None
+    for t in range(3):
+        if t:
+            xt = W.make_step_inputs(w, DEV, t)
+            ps.with_query(xt["s_q"], xt["l_q"], xt["seq_len"], xt["k_crit"], xt["k_marg"])
+        ps.run()
+        sc = S.prepare_store(ps.batch, ps.head_map, ps.buf.logits.shape[1], ps.buf.crit_idx,
+                             ps.buf.marg_idx, hk, hv, rows, old=old)
+        sc.run()
+        large = S.ModelSpec(ps.large.q, sc.new_k, sc.new_v, torch.empty_like(ps.large.out),
+                            ps.large.scale, sc.k_slot, sc.v_slot)
+        b = ps.buf
+        S.smallkv_hybrid_attn(ps.batch, large, ps.head_map, b.logits.shape[1], b.crit_idx,
+                              b.marg_idx, b.marg_prob, b.mass, ws=b.ws)
+        torch.cuda.synchronize()
+        err = head_err(host(large.out), host(b.large_out).astype(np.float64))
+        log(f"[store] step {t}: stage 3 through the host-backed store vs the full cache: {err:.3g}")
+        assert err <= TOL[torch.bfloat16]
+        old = sc
