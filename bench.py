@@ -51,6 +51,8 @@ def parse():
                    help="benchmark the prefill head matching instead of the decode step")
     p.add_argument("--store", action="store_true",
                    help="benchmark the retained-store maintenance after a step")
+    p.add_argument("--store-hbm-only", action="store_true",
+                   help="with --store: only the timed rebuild from HBM (for counter runs)")
     p.add_argument("--match-batch", type=int, default=1)
     p.add_argument("--match-window", type=int, default=200)
     p.add_argument("--copy-probe-mib", type=int, default=0,
@@ -63,11 +65,11 @@ def source_hash(name: str) -> str:
     return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
 
 
-def load_traffic(kernels, workload: str):
+def load_traffic(kernels, workload: str, name: str = "traffic.json"):
     """HBM bytes of one stage call (the sum over its kernels) from the committed
     rocprofv3 --pmc summary, or None when the counters were taken on another
     workload, a kernel is missing, or its source changed since."""
-    path = os.path.join(ROOT, "profiles", "traffic.json")
+    path = os.path.join(ROOT, "profiles", name)
     if not os.path.exists(path):
         return None
     try:
@@ -84,6 +86,18 @@ def load_traffic(kernels, workload: str):
         return total
     except (KeyError, ValueError, TypeError):
         return None
+
+
+def copy_probe(args, dev):
+    """A plain device copy of known size, for the counter calibration."""
+    import torch
+    if args.copy_probe_mib:
+        src = torch.ones(args.copy_probe_mib << 18, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
 
 def shape_text(m) -> str:
@@ -129,13 +143,7 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     w = W.WORKLOADS[args.workload]
-    if args.copy_probe_mib:
-        src = torch.ones(args.copy_probe_mib << 18, dtype=torch.float32, device=dev)
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
+    copy_probe(args, dev)
     print(f"[bench] generating {w.name}", file=sys.stderr, flush=True)
     x0 = W.make_step_inputs(w, dev)
     copy_bytes = sum(v.numel() * v.element_size() for v in x0.values() if torch.is_tensor(v))
@@ -331,6 +339,7 @@ def bench_store(args):
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     w = W.WORKLOADS[args.workload]
+    copy_probe(args, dev)
     print(f"[bench] generating {w.name}", file=sys.stderr, flush=True)
     x = W.make_step_inputs(w, dev)
     ps = prepare_step(x)
@@ -371,6 +380,45 @@ def bench_store(args):
     lists = ps.buf.crit_idx.numel() * 4 + ps.buf.marg_idx.numel() * 4
     alg = 2 * moved + maps + lists
     achieved = alg / (ms_hbm * 1e-3) / 1e9
+    traffic = load_traffic(["store_index", "store_copy"], f"{w.name}-store", "traffic_store.json")
+    legs = None
+    if not args.store_hbm_only:
+        legs = store_legs(args, w, x, ps, store, timed, stream, moved, rows)
+    out = {
+        "metric": "SmallKV retained-store maintenance updates/s at 1 MI355X",
+        "value": 1e3 / ms_hbm,
+        "unit": "updates/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": ms_hbm,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": f"{w.name}-store", "rows_per_kv_head": rows,
+                   "union_rows": int(cnt.sum()), "kv_heads": units},
+        "roofline": {"kernel": "store_index+store_copy", "bound": "hbm", "achieved": achieved,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": traffic},
+    }
+    if legs:
+        out.update(legs)
+    print(json.dumps(out), flush=True)
+
+
+def store_legs(args, w, x, ps, store, timed, stream, moved, rows):
+    """The store bench's other legs: the oracle on the host, the update after
+    a drifted step, the full store in pinned host memory, and the update
+    overlapped with the next step."""
+    import torch
+    from paper_2508_02751_amd import smallkv as S
+    from paper_2508_02751_amd import workloads as W
+
+    dev = x["l_k"].device
+    K = args.steps
+    nsh = ps.buf.logits.shape[1]
     # the oracle's rebuild of the same store on one host core
     cpu = None
     if not args.no_cpu_baseline:
@@ -444,24 +492,7 @@ def bench_store(args):
     overlapped()
     ms_both = overlapped()
     torch.cuda.synchronize()
-    out = {
-        "metric": "SmallKV retained-store maintenance updates/s at 1 MI355X",
-        "value": 1e3 / ms_hbm,
-        "unit": "updates/s",
-        "n_gpus": 1,
-        "steps": K,
-        "warmup": args.warmup,
-        "ms_per_step": ms_hbm,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": w.dtype,
-        "data": "synthetic",
-        "config": {"workload": f"{w.name}-store", "rows_per_kv_head": rows,
-                   "union_rows": int(cnt.sum()), "kv_heads": units},
-        "roofline": {"kernel": "store_index+store_copy", "bound": "hbm", "achieved": achieved,
-                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": None},
+    return {
         "after_a_drifted_step": {"ms": ms_inc, "rows_new": fetched, "rows_reused": kept,
                                  "new_fraction": fetched / max(1, fetched + kept)},
         "full_store_in_pinned_host_memory": {
@@ -472,7 +503,6 @@ def bench_store(args):
                                               "both_ms": ms_both}},
         "cpu_baseline": cpu,
     }
-    print(json.dumps(out), flush=True)
 
 
 def bench_match(args):

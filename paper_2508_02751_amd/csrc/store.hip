@@ -10,19 +10,23 @@
 // in host memory.
 //
 //   store_index -- one workgroup per kv head: membership bits of both unions
-//                  in LDS (atomic ORs from the lists), ranks by a popcount
-//                  scan over the bitmap words, both slot maps for t < N_b,
-//                  the unions' token lists (workspace) and their sizes;
-//   store_copy  -- 16 lanes per row, 16 bytes each, four rows in flight,
-//                  eight workgroups per kv head and union: every row from the
-//                  old store or the full one.
+//                  in LDS (atomic ORs from the lists, eight list entries in
+//                  flight per thread), ranks by a popcount scan over the
+//                  bitmap words, both slot maps for t < N_b, the union sizes,
+//                  and per union row its source: a row of the old store, or
+//                  the token's row of the full store;
+//   store_copy  -- the rows as a flat array of 16-byte pieces (a wave reads
+//                  1 KB of consecutive rows), one piece per thread per pass,
+//                  128 workgroups per kv head and union; one load of the
+//                  row's source stands between a piece and its data.
 #include "common.h"
 #include "launch.h"
 
 namespace smallkv {
 namespace {
 
-constexpr int kST = 256;
+constexpr int kIT = 1024;  // store_index threads
+constexpr int kCT = 256;   // store_copy threads
 
 struct StoreArgs {
   int n_cap, layers, hq, hkv, g, nsh, kc_cap, km_cap, select, words;
@@ -33,7 +37,9 @@ struct StoreArgs {
   const int32_t *old_k_slot, *old_v_slot;
   unsigned char *new_k, *new_v;
   int32_t *k_slot, *v_slot, *counts;
-  int32_t *uk, *uv;  // [units][rows]: the unions' tokens in row order
+  // [units][rows] per union, in row order: the old store's row (>= 0) or
+  // -(t + 1) for token t's row of the full store
+  int32_t *src_k, *src_v;
 };
 
 // Exclusive scan of one value per thread over the workgroup.
@@ -49,7 +55,7 @@ __device__ __forceinline__ int block_exscan(int v, int *red, int &total) {
   __syncthreads();
   int base = 0;
   total = 0;
-  for (int w = 0; w < kST / kWave; ++w) {
+  for (int w = 0; w < kIT / kWave; ++w) {
     if (w < wave) base += red[w];
     total += red[w];
   }
@@ -57,43 +63,66 @@ __device__ __forceinline__ int block_exscan(int v, int *red, int &total) {
   return base + x - v;
 }
 
-__global__ __launch_bounds__(kST) void store_index(StoreArgs a) {
+// The source code of token t's row in a union: its row in the old store
+// when the old slot map holds it, else its row of the full store.
+__device__ __forceinline__ int32_t row_source(const int32_t *old_slot, int64_t sbase, int t,
+                                              int64_t rows) {
+  const int os = old_slot ? old_slot[sbase + t] : -1;
+  return (os >= 0 && os < rows) ? os : -(t + 1);
+}
+
+__global__ __launch_bounds__(kIT) void store_index(StoreArgs a) {
   extern __shared__ uint32_t smem[];  // bits K [words], bits V [words], word ranks K, V
   uint32_t *bk = smem, *bv = smem + a.words;
   int *rk = reinterpret_cast<int *>(smem + 2 * a.words), *rv = rk + a.words;
-  __shared__ int red[kST / kWave];
+  __shared__ int red[kIT / kWave];
   const int unit = blockIdx.x;
   const int kvh = unit % a.hkv, bl = unit / a.hkv, layer = bl % a.layers, b = bl / a.layers;
   const int n = clampi(a.seq_len[b], 1, a.n_cap);
   const int nw = (n + 31) / 32;
-  for (int w = threadIdx.x; w < nw; w += kST) bk[w] = bv[w] = 0u;
+  for (int w = threadIdx.x; w < nw; w += kIT) bk[w] = bv[w] = 0u;
   __syncthreads();
-  // membership from the lists of the group's query heads (-1 padding and
-  // anything outside [0, n) ignored)
-  for (int h = 0; h < a.g; ++h) {
-    int64_t row;
-    if (a.select) {
-      row = unit;
-    } else {
-      const int j = clampi(a.head_map[layer * a.hq + kvh * a.g + h], 0, a.nsh - 1);
-      row = (int64_t)b * a.nsh + j;
-    }
-    const int32_t *c = a.crit + row * a.kc_cap, *m = a.marg + row * a.km_cap;
-    for (int i = threadIdx.x; i < a.kc_cap; i += kST) {
-      const int t = c[i];
-      if (t >= 0 && t < n) {
-        atomicOr(&bk[t >> 5], 1u << (t & 31));
-        atomicOr(&bv[t >> 5], 1u << (t & 31));
+  // membership from the lists of the group's query heads (one shared set
+  // per kv head with group selection); -1 padding and anything outside
+  // [0, n) ignored.  Entry e of the flat walk: head e / per, then its
+  // critical list, then its marginal list.
+  const int heads = a.select ? 1 : a.g;
+  const int per = a.kc_cap + a.km_cap;
+  const int total = heads * per;
+  constexpr int kBatch = 8;
+  for (int e0 = threadIdx.x; e0 < total; e0 += kBatch * kIT) {
+    int tok[kBatch];
+    bool crit[kBatch];
+#pragma unroll
+    for (int k = 0; k < kBatch; ++k) {  // every load issued before any use
+      const int e = e0 + k * kIT;
+      tok[k] = -1;
+      crit[k] = false;
+      if (e < total) {
+        const int h = e / per, i = e - h * per;
+        int64_t row;
+        if (a.select) {
+          row = unit;
+        } else {
+          const int j = clampi(a.head_map[layer * a.hq + kvh * a.g + h], 0, a.nsh - 1);
+          row = (int64_t)b * a.nsh + j;
+        }
+        crit[k] = i < a.kc_cap;
+        tok[k] = crit[k] ? a.crit[row * a.kc_cap + i] : a.marg[row * a.km_cap + (i - a.kc_cap)];
       }
     }
-    for (int i = threadIdx.x; i < a.km_cap; i += kST) {
-      const int t = m[i];
-      if (t >= 0 && t < n) atomicOr(&bv[t >> 5], 1u << (t & 31));
+#pragma unroll
+    for (int k = 0; k < kBatch; ++k) {
+      const int t = tok[k];
+      if (t >= 0 && t < n) {
+        if (crit[k]) atomicOr(&bk[t >> 5], 1u << (t & 31));
+        atomicOr(&bv[t >> 5], 1u << (t & 31));
+      }
     }
   }
   __syncthreads();
   // word ranks: each thread scans a run of consecutive words
-  const int per = (nw + kST - 1) / kST, w0 = threadIdx.x * per, w1 = min(w0 + per, nw);
+  const int wper = (nw + kIT - 1) / kIT, w0 = threadIdx.x * wper, w1 = min(w0 + wper, nw);
   int ck = 0, cv = 0;
   for (int w = w0; w < w1; ++w) {
     ck += __popc(bk[w]);
@@ -109,9 +138,9 @@ __global__ __launch_bounds__(kST) void store_index(StoreArgs a) {
     ov += __popc(bv[w]);
   }
   __syncthreads();
-  // slot maps and the unions' token lists
+  // slot maps and the rows' sources
   const int64_t sbase = (int64_t)unit * a.n_cap, ubase = (int64_t)unit * a.rows;
-  for (int t = threadIdx.x; t < n; t += kST) {
+  for (int t = threadIdx.x; t < n; t += kIT) {
     const uint32_t below = (1u << (t & 31)) - 1u;
     const uint32_t wk = bk[t >> 5], wv = bv[t >> 5];
     int sk = -1, sv = -1;
@@ -119,14 +148,14 @@ __global__ __launch_bounds__(kST) void store_index(StoreArgs a) {
       const int r = rk[t >> 5] + __popc(wk & below);
       if (r < a.rows) {
         sk = r;
-        a.uk[ubase + r] = t;
+        a.src_k[ubase + r] = row_source(a.old_k ? a.old_k_slot : nullptr, sbase, t, a.rows);
       }
     }
     if (wv >> (t & 31) & 1u) {
       const int r = rv[t >> 5] + __popc(wv & below);
       if (r < a.rows) {
         sv = r;
-        a.uv[ubase + r] = t;
+        a.src_v[ubase + r] = row_source(a.old_v ? a.old_v_slot : nullptr, sbase, t, a.rows);
       }
     }
     a.k_slot[sbase + t] = sk;
@@ -139,47 +168,33 @@ __global__ __launch_bounds__(kST) void store_index(StoreArgs a) {
 }
 
 // blockIdx.x: kv head unit; blockIdx.y: one of kCopySplit interleaved
-// shares of its rows; blockIdx.z: K (0) or V (1).  Each group of 16 lanes
-// copies one row at a time in 16-byte pieces, four rows in flight; a row is
-// one of the union's, from the old store when its old slot map holds the
-// token, else from the full store.
-constexpr int kCopySplit = 8;
+// shares of the union's pieces; blockIdx.z: K (0) or V (1).  Piece q of the
+// flat array is piece q % pieces of row q / pieces.  One piece per thread
+// per pass: many workgroups each walking nearby rows keep the DRAM pages
+// they touch few (eight pieces in flight per thread, 128 rows apart, ran
+// the rebuild 60% slower).
+constexpr int kCopySplit = 128;
 
-__global__ __launch_bounds__(kST) void store_copy(StoreArgs a) {
-  constexpr int kGroups = kST / 16, kStride = kCopySplit * kGroups, kInFlight = 4;
+__global__ __launch_bounds__(kCT) void store_copy(StoreArgs a) {
+  constexpr int kStride = kCopySplit * kCT;
   const int unit = blockIdx.x, isv = blockIdx.z;
   const int lim = (int)min<int64_t>((int64_t)a.counts[2 * (int64_t)unit + isv], a.rows);
-  const int lane16 = threadIdx.x & 15;
-  const int first = blockIdx.y * kGroups + (threadIdx.x >> 4);
-  const int32_t *u = (isv ? a.uv : a.uk) + (int64_t)unit * a.rows;
-  const int32_t *old_slot = isv ? a.old_v_slot : a.old_k_slot;
-  const unsigned char *full = isv ? a.full_v : a.full_k;
+  // a power of two (8, 16 or 32); a union has at most n_cap <= 131072 rows,
+  // so piece indices fit 32 bits
+  const int pieces = a.row_bytes / 16, psh = __ffs(pieces) - 1;
+  const int items = lim * pieces;
+  const int32_t *src = (isv ? a.src_v : a.src_k) + (int64_t)unit * a.rows;
+  const unsigned char *full = (isv ? a.full_v : a.full_k) + (int64_t)unit * a.n_cap * a.row_bytes;
   const unsigned char *old = isv ? a.old_v : a.old_k;
-  unsigned char *dst = isv ? a.new_v : a.new_k;
-  const int pieces = a.row_bytes / 16;  // 4 .. 32
-  for (int p = lane16; p < pieces; p += 16)
-    for (int r0 = first; r0 < lim; r0 += kInFlight * kStride) {
-      uint4 v[kInFlight];
-#pragma unroll
-      for (int k = 0; k < kInFlight; ++k) {
-        const int r = r0 + k * kStride;
-        if (r < lim) {
-          const int t = clampi(u[r], 0, a.n_cap - 1);
-          const int os = old_slot ? old_slot[(int64_t)unit * a.n_cap + t] : -1;
-          const unsigned char *src =
-              (old && os >= 0 && os < a.rows)
-                  ? old + ((int64_t)unit * a.rows + os) * a.row_bytes
-                  : full + ((int64_t)unit * a.n_cap + t) * a.row_bytes;
-          v[k] = reinterpret_cast<const uint4 *>(src)[p];
-        }
-      }
-#pragma unroll
-      for (int k = 0; k < kInFlight; ++k) {
-        const int r = r0 + k * kStride;
-        if (r < lim)
-          reinterpret_cast<uint4 *>(dst + ((int64_t)unit * a.rows + r) * a.row_bytes)[p] = v[k];
-      }
-    }
+  if (old) old += (int64_t)unit * a.rows * a.row_bytes;
+  uint4 *dst = reinterpret_cast<uint4 *>((isv ? a.new_v : a.new_k) + (int64_t)unit * a.rows * a.row_bytes);
+  for (int q = blockIdx.y * kCT + threadIdx.x; q < items; q += kStride) {
+    const int c = src[q >> psh];
+    const unsigned char *row =
+        (c >= 0 && old) ? old + (int64_t)c * a.row_bytes
+                        : full + (int64_t)clampi(c >= 0 ? 0 : -c - 1, 0, a.n_cap - 1) * a.row_bytes;
+    dst[q] = reinterpret_cast<const uint4 *>(row)[q & (pieces - 1)];
+  }
 }
 
 }  // namespace
@@ -224,13 +239,13 @@ hipError_t launch_store_update(const smallkv_store_t &s, void *ws, hipStream_t s
   a.v_slot = s.v_slot;
   const int units = s.batch.batch * s.n_layers * s.n_kv_heads;
   int32_t *w = static_cast<int32_t *>(ws);
-  a.uk = w;
-  a.uv = w + (size_t)units * s.rows;
+  a.src_k = w;
+  a.src_v = w + (size_t)units * s.rows;
   a.counts = s.counts ? s.counts : w + 2 * (size_t)units * s.rows;
-  hipLaunchKernelGGL(store_index, dim3(units), dim3(kST), store_index_lds(s.batch.n_cap), st, a);
+  hipLaunchKernelGGL(store_index, dim3(units), dim3(kIT), store_index_lds(s.batch.n_cap), st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(store_copy, dim3(units, kCopySplit, 2), dim3(kST), 0, st, a);
+  hipLaunchKernelGGL(store_copy, dim3(units, kCopySplit, 2), dim3(kCT), 0, st, a);
   return hipGetLastError();
 }
 
