@@ -248,6 +248,22 @@ def test_long_rows_multi_chunk():
     run_case(w)
 
 
+def test_long_rows_reread_per_pass():
+    """Rows too long for registers, re-read from memory per pass: 256 threads
+    per row (1024 rows, ragged lengths up to 7000), and 512 threads per row
+    (few rows of 12 000 tokens) with every logit of a row tied, so that the
+    target bins overflow the candidate buffer and the radix passes run over
+    the row."""
+    run_case(custom("reread-many", 121, 8, 7000, "bf16", W.ModelShape(4, 32, 4, 64),
+                    W.ModelShape(2, 8, 2, 128), ("pct", 10), ("pct", 20), ragged_min=5200))
+
+    def flat(x):
+        x["s_q"].zero_()
+
+    run_case(custom("reread-ties", 122, 2, 12000, "bf16", W.ModelShape(1, 4, 1, 64),
+                    W.ModelShape(1, 8, 2, 128), ("pct", 10), ("pct", 20)), mutate=flat)
+
+
 def test_deterministic_repeat():
     w = W.WORKLOADS[1]
     x = W.make_step_inputs(w, DEV)
