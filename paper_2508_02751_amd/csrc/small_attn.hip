@@ -670,14 +670,16 @@ SmallPlan plan_small(const smallkv_batch_t &b, const smallkv_model_t &m) {
   const int max_split = (b.n_cap + p.tile - 1) / p.tile;
   // about two rounds of resident workgroups (three per CU): fewer, longer
   // chunks pipeline their tiles, more of them only add merge records; at
-  // least four tiles per chunk, so that the next tile's K loads overlap the
-  // current tile's arithmetic (a one-tile chunk loads, then computes); and
-  // at most 64 tiles, so that long rows give enough workgroups that the
-  // last round of them is a small part of the launch
+  // least four tiles per chunk when that still gives every CU a workgroup,
+  // so that the next tile's K loads overlap the current tile's arithmetic
+  // (a one-tile chunk loads, then computes); and at most 64 tiles, so that
+  // long rows give enough workgroups that the last round of them is a small
+  // part of the launch
   const int want = (int)((1536 + units - 1) / units);
-  const int most = max_split / 4 < 1 ? 1 : max_split / 4;
+  int ns = want < 1 ? 1 : (want > max_split ? max_split : want);
+  const int four = max_split / 4 < 1 ? 1 : max_split / 4;
+  if (units * four >= 256 && ns > four) ns = four;
   const int least = (max_split + 63) / 64;
-  int ns = want < 1 ? 1 : (want > most ? most : want);
   if (ns < least) ns = least;
   if (ns > kMaxChunks) ns = kMaxChunks;
   const int per = (b.n_cap + ns - 1) / ns;
