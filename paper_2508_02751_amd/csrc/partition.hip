@@ -652,7 +652,9 @@ void partition_kernel(PartArgs a) {
     constexpr int NG = 3;
     static_assert(NG <= kMaxNK, "scan slots");
     const int nk = row.chunks();
-    uint32_t carry_eq = 0, carry_c = 0, carry_m = 0;
+    // tie ranks before the group, one 32-bit count per threshold: a row may
+    // hold more than 65535 ties (only a group's own counts are packed)
+    uint32_t carry_eq_c = 0, carry_eq_p = 0, carry_c = 0, carry_m = 0;
     float4 nxt[NG];
 #pragma unroll
     for (int j = 0; j < NG; ++j) nxt[j] = j < nk ? row.chunk(j) : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
@@ -672,6 +674,7 @@ void partition_kernel(PartArgs a) {
       uint32_t rank[NG];  // keys are recomputed where used: fewer live registers
 #pragma unroll
       for (int j = 0; j < NG; ++j) rank[j] = 0;
+      uint32_t group_eq = 0;  // the group's ties of T[0] (low half) and T[1] (high half)
       if (split) {
         uint32_t v[NG], ex[NG], tot[NG];
 #pragma unroll
@@ -683,17 +686,19 @@ void partition_kernel(PartArgs a) {
                     (row.ranked(k0 + j, e) && logit_key(sv[j][e]) == cp.t.T[1] ? 0x10000u : 0u);
         }
         block_scan<NG>(sh, par, v, ex, tot);
+        uint32_t in_group = 0;  // ties of the group's earlier chunks (packed, < 2^16 each)
 #pragma unroll
         for (int j = 0; j < NG; ++j) {
-          rank[j] = carry_eq + ex[j];
-          carry_eq += tot[j];
+          rank[j] = in_group + ex[j];
+          in_group += tot[j];
         }
+        group_eq = in_group;
       }
       bool inC[NG][4], inM[NG][4];
       uint32_t v[NG], ex[NG], tot[NG];
 #pragma unroll
       for (int j = 0; j < NG; ++j) {
-        uint32_t rC = rank[j] & 0xffffu, rP = rank[j] >> 16;
+        uint32_t rC = carry_eq_c + (rank[j] & 0xffffu), rP = carry_eq_p + (rank[j] >> 16);
         v[j] = 0;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -716,6 +721,8 @@ void partition_kernel(PartArgs a) {
         carry_c += tot[j] & 0xffffu;
         carry_m += tot[j] >> 16;
       }
+      carry_eq_c += group_eq & 0xffffu;
+      carry_eq_p += group_eq >> 16;
     }
   }
   finish_row(a, sh, r, cp.sc, cp.sm);

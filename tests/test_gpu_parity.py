@@ -264,6 +264,17 @@ def test_long_rows_reread_per_pass():
                     W.ModelShape(1, 8, 2, 128), ("pct", 10), ("pct", 20)), mutate=flat)
 
 
+def test_more_than_65535_tied_logits():
+    """A 70 000-token row whose logits all tie (zero queries): every token's
+    rank among the ties is its index, past 2^16 for the last tokens, so the
+    tie ranks must not be kept in 16 bits anywhere."""
+    def flat(x):
+        x["s_q"].zero_()
+
+    run_case(custom("ties-70k", 123, 1, 70000, "bf16", W.ModelShape(1, 2, 1, 64),
+                    W.ModelShape(1, 4, 1, 128), ("pct", 10), ("pct", 20)), mutate=flat)
+
+
 def test_deterministic_repeat():
     w = W.WORKLOADS[1]
     x = W.make_step_inputs(w, DEV)
