@@ -52,18 +52,29 @@ constexpr int kPitch = kChunk + 4;    // LDS row pitch (floats)
 // Stage dims [c0, c0+kChunk) of 64 rows of one head's operand, from token r0,
 // into LDS as fp32; rows at or past the window are zero.  Every load of the
 // slice is issued before the first is used.
+// A 64-row x kChunk-dim slice in two steps: its 16-byte pieces into
+// registers (issued a chunk ahead of their use), then into LDS as fp32.
+template <typename T>
+struct Slice {
+  static constexpr int per = elem<T>::per16;
+  static constexpr int vpr = kChunk / per;       // 16-byte vectors per row slice
+  static constexpr int n = kTile * vpr / kWave;  // vectors per lane
+};
+
 template <typename T, int D>
-__device__ __forceinline__ void stage_chunk(float *dst, const T *src, int r0, int w, int c0) {
-  constexpr int per = elem<T>::per16;
-  constexpr int vpr = kChunk / per;          // 16-byte vectors per row slice
-  constexpr int n = kTile * vpr / kWave;     // vectors per lane
-  uint4 v[n];
+__device__ __forceinline__ void load_chunk(uint4 (&v)[Slice<T>::n], const T *src, int r0, int w, int c0) {
+  constexpr int per = Slice<T>::per, vpr = Slice<T>::vpr, n = Slice<T>::n;
 #pragma unroll
   for (int q = 0; q < n; ++q) {
     const int e = q * kWave + threadIdx.x, r = e / vpr, c = (e % vpr) * per;
     v[q] = r0 + r < w ? *reinterpret_cast<const uint4 *>(src + (int64_t)(r0 + r) * D + c0 + c)
                       : make_uint4(0u, 0u, 0u, 0u);
   }
+}
+
+template <typename T>
+__device__ __forceinline__ void store_chunk(float *dst, const uint4 (&v)[Slice<T>::n]) {
+  constexpr int per = Slice<T>::per, vpr = Slice<T>::vpr, n = Slice<T>::n;
 #pragma unroll
   for (int q = 0; q < n; ++q) {
     const int e = q * kWave + threadIdx.x, r = e / vpr, c = (e % vpr) * per;
@@ -127,10 +138,17 @@ __device__ __forceinline__ void logits_tile(const LogitArgs &a, float *Qs, float
   for (int i = 0; i < 8; ++i)
 #pragma unroll
     for (int jj = 0; jj < 8; ++jj) acc[i][jj] = 0.0f;
+  uint4 qv[Slice<T>::n], kv[Slice<T>::n];
+  load_chunk<T, D>(qv, Q, U * kTile, w, 0);
+  load_chunk<T, D>(kv, K, V * kTile, w, 0);
   for (int c0 = 0; c0 < D; c0 += kChunk) {
-    stage_chunk<T, D>(Qs, Q, U * kTile, w, c0);
-    stage_chunk<T, D>(Ks, K, V * kTile, w, c0);
+    store_chunk<T>(Qs, qv);
+    store_chunk<T>(Ks, kv);
     __syncthreads();
+    if (c0 + kChunk < D) {  // the next slice arrives while this one is used
+      load_chunk<T, D>(qv, Q, U * kTile, w, c0 + kChunk);
+      load_chunk<T, D>(kv, K, V * kTile, w, c0 + kChunk);
+    }
     chains<kFull>(acc, Qs, Ks, ty, tx, imax, jmax);
     __syncthreads();
   }
