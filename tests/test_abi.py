@@ -189,3 +189,67 @@ def test_group_selection_limits():
     st = _fake_step(st__select=S.SELECT_GROUP)
     n = C.c_size_t()
     assert S.lib().smallkv_workspace_size(C.byref(st), C.byref(n)) == 0 and n.value > 0
+
+
+def _fake_store(**over):
+    """A well-formed retained-store descriptor over fake 16-byte aligned
+    addresses (Qwen2-7B shapes, batch 2, N 8192); `over` replaces fields."""
+    b = S.Batch(batch=2, n_cap=8192, seq_len=0x1000, k_crit=0x1000, k_marg=0x1000, k_recent=None,
+                kc_cap=820, km_cap=1640)
+    st = S.Store(b, 28, 28, 4, 128, S.BF16, 0x1000, 336, S.SELECT_HEAD, 0x1000, 0x1000, 0x2000,
+                 0x3000, 4096, None, None, None, None, 0x4000, 0x5000, 0x6000, 0x7000, None)
+    for k, v in over.items():
+        if k.startswith("b__"):
+            setattr(st.batch, k[3:], v)
+        else:
+            setattr(st, k, v)
+    return st
+
+
+def test_header_declares_the_store_calls():
+    names = declared_functions()
+    assert "smallkv_store_update" in names and "smallkv_store_workspace_size" in names
+
+
+def test_store_workspace_size():
+    st = _fake_store()
+    n = C.c_size_t()
+    assert S.lib().smallkv_store_workspace_size(C.byref(st), C.byref(n)) == 0
+    units = 2 * 28 * 4
+    assert n.value == 2 * units * 4096 * 4 + 2 * units * 4  # both unions' row sources, sizes
+    assert S.lib().smallkv_store_workspace_size(C.byref(st), None) == S.EINVAL
+    # workspace checks come before any device call
+    assert S.lib().smallkv_store_update(C.byref(st), None, 0, None) == S.EWORKSPACE
+    assert S.lib().smallkv_store_update(C.byref(st), C.c_void_p(0x1000), n.value - 1,
+                                        None) == S.EWORKSPACE
+
+
+@pytest.mark.parametrize("over,status", [
+    ({"b__n_cap": 131073}, S.EUNSUPPORTED),   # past the index kernel's LDS bitmaps
+    ({"head_dim": 96}, S.EUNSUPPORTED),
+    ({"rows": 0}, S.EINVAL),
+    ({"n_q_heads": 30}, S.EINVAL),            # not a multiple of the kv heads
+    ({"dtype": 7}, S.EINVAL),
+    ({"select": 9}, S.EINVAL),
+    ({"head_map": None}, S.EINVAL),
+    ({"crit_idx": None}, S.EINVAL),
+    ({"marg_idx": None}, S.EINVAL),           # km_cap > 0 needs the marginal lists
+    ({"full_k": 0x2004}, S.EINVAL),           # not 16-byte aligned
+    ({"new_v": None}, S.EINVAL),
+    ({"k_slot": None}, S.EINVAL),
+    ({"old_k": 0x8000}, S.EINVAL),            # part of an old store only
+    ({"old_k": 0x4000, "old_v": 0x8000, "old_k_slot": 0x9000, "old_v_slot": 0xa000},
+     S.EINVAL),                               # the old store is the new one
+    ({"b__batch": 0}, S.EINVAL),
+])
+def test_store_rejects_before_launch(over, status):
+    st = _fake_store(**over)
+    n = C.c_size_t()
+    assert S.lib().smallkv_store_workspace_size(C.byref(st), C.byref(n)) == status
+    assert S.lib().smallkv_store_update(C.byref(st), C.c_void_p(0x1000), 1 << 40, None) == status
+
+
+def test_store_accepts_a_whole_old_store():
+    st = _fake_store(old_k=0x8000, old_v=0x9000, old_k_slot=0xa000, old_v_slot=0xb000)
+    n = C.c_size_t()
+    assert S.lib().smallkv_store_workspace_size(C.byref(st), C.byref(n)) == 0
