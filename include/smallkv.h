@@ -311,7 +311,25 @@ typedef struct {
   int32_t *counts;                    /* optional out [B][L][Hkv][2]: |U_K|, |U_V| */
 } smallkv_store_t;
 
+/* Bytes of device workspace smallkv_store_update needs for `store`:
+ * 2 * units * rows * 4 (each union row's source) + 2 * units * 4 (the union
+ * sizes, used when counts is null), units = B * n_layers * n_kv_heads.  Host
+ * only.  SMALLKV_EINVAL for a null or malformed descriptor (null required
+ * pointers, rows < 1, a group size that does not divide, part of an old
+ * store only, the old store passed as the new one, unaligned K/V);
+ * SMALLKV_EUNSUPPORTED for head_dim other than 64 or 128, n_cap > 131072 or
+ * rows > 2^30. */
 int smallkv_store_workspace_size(const smallkv_store_t *store, size_t *bytes);
+
+/* Enqueue the store maintenance on `stream` (a hipStream_t, null = the
+ * default stream).  Two launches: the unions, slot maps and row sources,
+ * then the row copies.  The caller owns every buffer, including `ws`
+ * (ws_bytes >= smallkv_store_workspace_size, else SMALLKV_EWORKSPACE); the
+ * library allocates nothing and does not synchronise.  The same errors as
+ * smallkv_store_workspace_size, and SMALLKV_EINVAL when full_k / full_v is
+ * host memory that is not pinned and mapped for the device, all returned
+ * before anything is enqueued; SMALLKV_EDEVICE if a launch fails.  Calls
+ * that share a workspace or outputs must not overlap. */
 int smallkv_store_update(const smallkv_store_t *store, void *ws, size_t ws_bytes, void *stream);
 
 /* ---------------------------------------------------------------------------
