@@ -318,7 +318,7 @@ typedef struct {
  * pointers, rows < 1, a group size that does not divide, part of an old
  * store only, the old store passed as the new one, unaligned K/V);
  * SMALLKV_EUNSUPPORTED for head_dim other than 64 or 128, n_cap > 131072 or
- * rows > 2^30. */
+ * rows >= 2^30. */
 int smallkv_store_workspace_size(const smallkv_store_t *store, size_t *bytes);
 
 /* Enqueue the store maintenance on `stream` (a hipStream_t, null = the
