@@ -227,3 +227,21 @@ def test_steps_through_a_host_backed_store():
         log(f"[store] step {t}: stage 3 through the host-backed store vs the full cache: {err:.3g}")
         assert err <= TOL[torch.bfloat16]
         old = sc
+
+
+def test_store_at_the_largest_n_cap():
+    """n_cap = 131072, the largest the store accepts (the index kernel's LDS
+    bitmaps and word ranks at their largest): one sequence at full length."""
+    S, W, prepare_step = modules()
+    w = W.Workload(140, "store-max", 1, 131072, "bf16", W.ModelShape(1, 2, 1, 64),
+                   W.ModelShape(1, 8, 2, 128), ("pct", 5), ("pct", 10))
+    x = W.make_step_inputs(w, DEV)
+    ps = prepare_step(x)
+    ps.run()
+    rows = capacity(x, 4)
+    log(f"[store] n_cap 131072: {rows} rows per kv head")
+    sc = S.prepare_store(ps.batch, ps.head_map, ps.buf.logits.shape[1], ps.buf.crit_idx,
+                         ps.buf.marg_idx, x["l_k"], x["l_v"], rows)
+    sc.run()
+    torch.cuda.synchronize()
+    check_store(sc, oracle_store(x, ps, rows, 0), x, "store at n_cap 131072")
