@@ -125,8 +125,8 @@ def stage3_kernels(w):
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py: this build runs on one GPU only; the multi-GPU sharding is a design "
-              "(see the sharding section of DESIGN.md), so --gpus must be 1", file=sys.stderr)
+        print("bench.py: the library runs on one GPU; sharding the step over several GPUs "
+              "is not implemented, so --gpus must be 1", file=sys.stderr)
         sys.exit(2)
 
     if args.match:
