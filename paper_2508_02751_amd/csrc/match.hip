@@ -16,8 +16,9 @@
 //                   64x64 tile, 8x8 independent FMA chains per lane over Q
 //                   and K slices staged in LDS as fp32 (one LDS byte read per
 //                   FMA), and each row's maximum over the tile;
-//   match_rowsum -- one thread per row of every head: the row's max from the
-//                   tile maxima and its sum Z_u, v ascending;
+//   match_rowsum -- one thread per pair of rows (u, w-1-u) of every head, so
+//                   that the lanes of a wave do equal work: each row's max
+//                   from the tile maxima and its sum Z_u, v ascending;
 //   match_scores -- one workgroup per head, one thread per token: the column
 //                   sum F_v, u ascending (a wave's lanes read each row of S
 //                   together), then the TopK set by counting, for each token,
@@ -219,11 +220,8 @@ constexpr int kInFlight = 8;  // loads each thread issues before using them
 // Row statistics: one thread per row u of every head (blockIdx.x covers 256
 // rows, blockIdx.y the head, blockIdx.z the sequence).  m_u from the tile
 // maxima; Z_u = e[u][0] + ... + e[u][u], one term at a time, v ascending.
-__global__ __launch_bounds__(kMatchThreads) void match_rowsum(ScoreArgs a) {
-  const int u = blockIdx.x * kMatchThreads + threadIdx.x, head = blockIdx.y, b = blockIdx.z;
-  const int w = clampi(a.win_len[b], 1, a.w_cap);
-  if (u >= w) return;
-  const int64_t hrow = (int64_t)b * a.H + head;
+// Row u's max (from the tile maxima) and its sum Z_u, v ascending.
+__device__ __forceinline__ void row_sum(const ScoreArgs &a, int64_t hrow, int u) {
   const float *pm = a.pmax + (hrow * a.w_cap + u) * a.nt;
   float m = pm[0];
   for (int V = 1; V <= u / kTile; ++V) m = pm[V] > m ? pm[V] : m;
@@ -244,6 +242,17 @@ __global__ __launch_bounds__(kMatchThreads) void match_rowsum(ScoreArgs a) {
     }
   }
   a.mz[hrow * a.w_cap + u] = make_float2(m, z);
+}
+
+// Thread p sums rows p and w-1-p (once when they coincide), so that every
+// lane of a wave adds about w terms whatever its rows.
+__global__ __launch_bounds__(kMatchThreads) void match_rowsum(ScoreArgs a) {
+  const int p = blockIdx.x * kMatchThreads + threadIdx.x, head = blockIdx.y, b = blockIdx.z;
+  const int w = clampi(a.win_len[b], 1, a.w_cap);
+  if (p >= (w + 1) / 2) return;
+  const int64_t hrow = (int64_t)b * a.H + head;
+  row_sum(a, hrow, p);
+  if (w - 1 - p != p) row_sum(a, hrow, w - 1 - p);
 }
 
 // Column sums and the TopK set: one workgroup per head, thread v adds
@@ -420,7 +429,7 @@ hipError_t launch_match(const smallkv_match_t &m, void *ws, hipStream_t st) {
   if (e != hipSuccess) return e;
   ScoreArgs sa{S, pmax, mz, m.w_cap, lay.ld, lay.nt, H, lay.nw, m.win_len, m.top_k, bits,
                m.scores, m.top_bits};
-  hipLaunchKernelGGL(match_rowsum, dim3((m.w_cap + kMatchThreads - 1) / kMatchThreads, H, m.batch),
+  hipLaunchKernelGGL(match_rowsum, dim3(((m.w_cap + 1) / 2 + kMatchThreads - 1) / kMatchThreads, H, m.batch),
                      dim3(kMatchThreads), 0, st, sa);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   hipLaunchKernelGGL(match_scores, dim3(H, m.batch), dim3(kMatchThreads), 0, st, sa);
