@@ -769,7 +769,8 @@ hipError_t launch_pt(const PartArgs &a, int rows, hipStream_t st) {
 }
 
 // Many rows (several per CU): 256 threads each, so that more rows are
-// resident at once; few rows: 512 threads, so that each finishes sooner.
+// resident at once; few rows: 512 threads, so that each finishes sooner;
+// at most one row per CU: 1024.
 constexpr int kManyRows = 4 * 256;
 
 template <bool kMerge, bool kProb = false>
@@ -779,6 +780,9 @@ hipError_t launch_rows(const PartArgs &a, int rows, hipStream_t st) {
     return launch_pt<kMerge, 512, true, kProb>(a, rows, st);
   }
   if (rows >= kManyRows) return launch_pt<kMerge, 256, false, kProb>(a, rows, st);
+  // at most one row per CU: 1024 threads shorten each row's passes
+  // (with more rows some CUs would run two of them in turn)
+  if (rows <= 256) return launch_pt<kMerge, 1024, false, kProb>(a, rows, st);
   return launch_pt<kMerge, 512, false, kProb>(a, rows, st);
 }
 
