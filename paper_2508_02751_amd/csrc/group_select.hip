@@ -207,13 +207,44 @@ __global__ __launch_bounds__(kGT) void group_weights(GroupSelArgs a) {
   const float *lg = a.logits + row * a.n_cap;
   const int32_t *crit = a.crit + grow * a.kc_cap, *marg = a.marg + grow * a.km_cap;
   const int last = sz.n - 1;
+  // four entries per thread per pass: their list loads, then their logit
+  // loads, are in flight together (each thread still adds in k order)
+  constexpr int kB = 4;
   float sc = 0.0f, sm = 0.0f;
-  for (int k = threadIdx.x; k < sz.nc; k += kGT) sc += __expf(lg[clampi(crit[k], 0, last)] - m) * zinv;
+  for (int k0 = threadIdx.x; k0 < sz.nc; k0 += kB * kGT) {
+    int t[kB];
+    float v[kB];
+#pragma unroll
+    for (int q = 0; q < kB; ++q) {
+      const int k = k0 + q * kGT;
+      t[q] = k < sz.nc ? clampi(crit[k], 0, last) : -1;
+    }
+#pragma unroll
+    for (int q = 0; q < kB; ++q) v[q] = t[q] >= 0 ? lg[t[q]] : 0.0f;
+#pragma unroll
+    for (int q = 0; q < kB; ++q)
+      if (t[q] >= 0) sc += __expf(v[q] - m) * zinv;
+  }
   float *mp = a.marg_prob + (int64_t)prow * a.km_cap;
-  for (int k = threadIdx.x; k < a.km_cap; k += kGT) {
-    const float p = k < sz.nm ? __expf(lg[clampi(marg[k], 0, last)] - m) * zinv : 0.0f;
-    mp[k] = p;
-    sm += p;
+  for (int k0 = threadIdx.x; k0 < a.km_cap; k0 += kB * kGT) {
+    int t[kB];
+    float v[kB];
+#pragma unroll
+    for (int q = 0; q < kB; ++q) {
+      const int k = k0 + q * kGT;
+      t[q] = k < sz.nm ? clampi(marg[k], 0, last) : -1;
+    }
+#pragma unroll
+    for (int q = 0; q < kB; ++q) v[q] = t[q] >= 0 ? lg[t[q]] : 0.0f;
+#pragma unroll
+    for (int q = 0; q < kB; ++q) {
+      const int k = k0 + q * kGT;
+      if (k < a.km_cap) {
+        const float p = t[q] >= 0 ? __expf(v[q] - m) * zinv : 0.0f;
+        mp[k] = p;
+        sm += p;
+      }
+    }
   }
   sc = wave_sum(sc);
   sm = wave_sum(sm);
