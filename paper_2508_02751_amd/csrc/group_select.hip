@@ -9,10 +9,10 @@
 //   Z_j    = fp32(Zq_j) * 2^-40
 //   F(t)   = ((e_j0/Z_j0 + e_j1/Z_j1) + ...)               (fp32, heads ascending)
 // Kernels, between stage 1 (logits and exact row maxima) and stage 3:
-//   group_init    -- zeroes the two atomically accumulated buffers;
-//   group_zq      -- per small head and 2048-token chunk: Zq_j by 64-bit
-//                    integer partial sums, added atomically (exact: integer
-//                    addition is associative);
+//   group_zq      -- per small head and 2048-token chunk: the chunk's part
+//                    of Zq_j as a 64-bit integer (the readers add the parts:
+//                    exact, integer addition is associative); it also zeroes
+//                    the row maxima that group_scores raises atomically;
 //   group_scores  -- per (sequence, large layer, kv head) and 1024-token
 //                    chunk: F(t) for every token, the row's largest F by an
 //                    atomic max on its bits;
@@ -34,7 +34,9 @@ struct GroupSelArgs {
   int n_cap, nsh, L, hq, hkv, gq, kc_cap, km_cap;
   const int32_t *seq_len, *k_crit, *k_marg, *k_recent, *head_map;
   const float *logits, *row_max, *row_sum;
-  uint64_t *zq_int;        // [B][nsh]: the exact integer sums
+  uint64_t *zq_int;        // [B][nsh][nzc]: the exact integer sums per token chunk
+  int nzc;                 // token chunks of group_zq per row
+  int n_keymax;            // entries of key_max, zeroed by group_zq
   float *keys, *key_max;   // [B][L*hkv][n_cap], [B][L*hkv]
   const int32_t *crit, *marg;  // group lists [B][L*hkv][cap]
   float *marg_prob, *mass;     // per large head [B][L*hq][km_cap], [B][L*hq][2]
@@ -59,21 +61,18 @@ constexpr int kScoreTok = 4 * kGT;  // tokens per group_scores workgroup (4 per 
 
 // Zeroes the integer sums and the key maxima that the next two kernels
 // accumulate with atomics (a kernel rather than a memset: graph-safe).
-__global__ __launch_bounds__(kGT) void group_init(GroupSelArgs a, int zrows, int grows) {
-  for (int i = blockIdx.x * kGT + threadIdx.x; i < zrows || i < grows; i += gridDim.x * kGT) {
-    if (i < zrows) a.zq_int[i] = 0ull;
-    if (i < grows) a.key_max[i] = 0.0f;
-  }
-}
-
-// blockIdx.x: small head row; blockIdx.y: a chunk of kZqTok tokens.
-// Integer addition is associative: the atomics give the exact sum.
+// blockIdx.x: small head row; blockIdx.y: a chunk of kZqTok tokens, whose
+// integer sum it writes (0 past the row's end): integer addition is
+// associative, so the readers' sum of the chunks is the exact sum.  The
+// workgroups also zero key_max, which group_scores / accum_scores then
+// raise with atomic maxima.
 __global__ __launch_bounds__(kGT) void group_zq(GroupSelArgs a) {
   __shared__ uint64_t part[kGT / kWave];
+  const int wg = blockIdx.x * gridDim.y + blockIdx.y, nwg = gridDim.x * gridDim.y;
+  for (int i = wg * kGT + threadIdx.x; i < a.n_keymax; i += nwg * kGT) a.key_max[i] = 0.0f;
   const int row = blockIdx.x, b = row / a.nsh;
   const int n = clampi(a.seq_len[b], 1, a.n_cap);
   const int t0 = blockIdx.y * kZqTok;
-  if (t0 >= n) return;
   const float m = a.row_max[row];
   const float *lg = a.logits + (int64_t)row * a.n_cap;
   uint64_t z = 0;
@@ -91,8 +90,16 @@ __global__ __launch_bounds__(kGT) void group_zq(GroupSelArgs a) {
   if (threadIdx.x == 0) {
     uint64_t s = 0;
     for (int w = 0; w < kGT / kWave; ++w) s += part[w];
-    atomicAdd(reinterpret_cast<unsigned long long *>(&a.zq_int[row]), (unsigned long long)s);
+    a.zq_int[(int64_t)row * a.nzc + blockIdx.y] = s;
   }
+}
+
+// Z of a small head row: the chunks' exact integer sums added, rounded once
+// to fp32 and scaled by 2^-40.
+__device__ __forceinline__ float zq_of(const GroupSelArgs &a, int64_t row) {
+  uint64_t z = 0;
+  for (int c = 0; c < a.nzc; ++c) z += a.zq_int[row * a.nzc + c];
+  return __fmul_rn(__ull2float_rn(z), 0x1p-40f);
 }
 
 // blockIdx.x: group row (b, layer, kv head); blockIdx.y: a chunk of
@@ -114,7 +121,7 @@ __global__ __launch_bounds__(kGT) void group_scores(GroupSelArgs a) {
     const int64_t row = (int64_t)b * a.nsh + j;
     lrow[h] = a.logits + row * a.n_cap;
     lm[h] = a.row_max[row];
-    lz[h] = __fmul_rn(__ull2float_rn(a.zq_int[row]), 0x1p-40f);
+    lz[h] = zq_of(a, row);
   }
   __syncthreads();
   float f[kQ];
@@ -160,7 +167,7 @@ __global__ __launch_bounds__(kGT) void accum_scores(GroupSelArgs a) {
   const int t0 = blockIdx.y * kScoreTok;
   if (t0 >= n) return;
   const float m = a.row_max[row];
-  const float z = __fmul_rn(__ull2float_rn(a.zq_int[row]), 0x1p-40f);
+  const float z = zq_of(a, row);
   const float *lg = a.logits + (int64_t)row * a.n_cap;
   float *acc = a.acc + (int64_t)row * a.n_cap;
   float fmx = 0.0f;
@@ -299,7 +306,8 @@ GroupLayout group_layout(const smallkv_batch_t &b, const smallkv_model_t &small,
                              : (size_t)b.batch * large.n_layers * large.n_kv_heads;
   GroupLayout l{};
   l.zq = r256(offset);
-  l.keys = l.zq + r256((size_t)b.batch * nsh * sizeof(uint64_t));
+  const size_t nzc = (size_t)(b.n_cap + kZqTok - 1) / kZqTok;
+  l.keys = l.zq + r256((size_t)b.batch * nsh * nzc * sizeof(uint64_t));
   l.key_max = l.keys + (accum ? 0 : r256(grows * b.n_cap * sizeof(float)));
   l.part_mp = l.key_max + r256(grows * sizeof(float));
   l.part_mass = l.part_mp + r256(grows * (b.km_cap > 0 ? b.km_cap : 1) * sizeof(float));
@@ -324,12 +332,11 @@ hipError_t launch_group_select(const smallkv_batch_t &b, const smallkv_model_t &
   const int nsh = small.n_layers * small.n_q_heads;
   const int grows_per = large.n_layers * large.n_kv_heads;
   const int zrows = b.batch * nsh, grows = b.batch * grows_per;
-  const int most = zrows > grows ? zrows : grows;
-  hipLaunchKernelGGL(group_init, dim3((most + kGT - 1) / kGT), dim3(kGT), 0, st, a, zrows, grows);
+  a.nzc = (b.n_cap + kZqTok - 1) / kZqTok;
+  a.n_keymax = grows;
+  hipLaunchKernelGGL(group_zq, dim3(zrows, a.nzc), dim3(kGT), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(group_zq, dim3(zrows, (b.n_cap + kZqTok - 1) / kZqTok), dim3(kGT), 0, st, a);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
   hipLaunchKernelGGL(group_scores, dim3(grows, (b.n_cap + kScoreTok - 1) / kScoreTok), dim3(kGT), 0,
                      st, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
@@ -361,11 +368,11 @@ hipError_t launch_accum_select(const smallkv_batch_t &b, const smallkv_model_t &
   a.marg_prob = marg_prob;
   a.mass = mass;
   const int nsh = small.n_layers * small.n_q_heads, rows = b.batch * nsh;
-  hipLaunchKernelGGL(group_init, dim3((rows + kGT - 1) / kGT), dim3(kGT), 0, st, a, rows, rows);
+  a.nzc = (b.n_cap + kZqTok - 1) / kZqTok;
+  a.n_keymax = rows;
+  hipLaunchKernelGGL(group_zq, dim3(rows, a.nzc), dim3(kGT), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(group_zq, dim3(rows, (b.n_cap + kZqTok - 1) / kZqTok), dim3(kGT), 0, st, a);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
   hipLaunchKernelGGL(accum_scores, dim3(rows, (b.n_cap + kScoreTok - 1) / kScoreTok), dim3(kGT), 0,
                      st, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
