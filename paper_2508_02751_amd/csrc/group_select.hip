@@ -340,9 +340,10 @@ hipError_t launch_group_select(const smallkv_batch_t &b, const smallkv_model_t &
   hipLaunchKernelGGL(group_scores, dim3(grows, (b.n_cap + kScoreTok - 1) / kScoreTok), dim3(kGT), 0,
                      st, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
+  // (64 bins per binade for the summed probabilities: 32 and 128 were slower)
   e = launch_group_partition(b, grows_per, a.keys, a.key_max, crit, marg,
                              reinterpret_cast<float *>(w + lay.part_mp),
-                             reinterpret_cast<float *>(w + lay.part_mass), st);
+                             reinterpret_cast<float *>(w + lay.part_mass), 64, st);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(group_weights, dim3(b.batch * large.n_layers * large.n_q_heads), dim3(kGT), 0,
                      st, a);
@@ -376,9 +377,10 @@ hipError_t launch_accum_select(const smallkv_batch_t &b, const smallkv_model_t &
   hipLaunchKernelGGL(accum_scores, dim3(rows, (b.n_cap + kScoreTok - 1) / kScoreTok), dim3(kGT), 0,
                      st, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
+  // (32 bins per binade for the running scores: 64 was slower)
   e = launch_group_partition(b, nsh, acc, a.key_max, crit, marg,
                              reinterpret_cast<float *>(w + lay.part_mp),
-                             reinterpret_cast<float *>(w + lay.part_mass), st);
+                             reinterpret_cast<float *>(w + lay.part_mass), 32, st);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(group_weights, dim3(rows), dim3(kGT), 0, st, a);
   return hipGetLastError();

@@ -104,7 +104,8 @@ hipError_t launch_group_select(const smallkv_batch_t &b, const smallkv_model_t &
 // The partition over group keys (rows [B][group_rows][n_cap], row maxima).
 hipError_t launch_group_partition(const smallkv_batch_t &b, int group_rows, const float *keys,
                                   const float *key_max, int32_t *crit, int32_t *marg,
-                                  float *marg_prob, float *mass, hipStream_t st);
+                                  float *marg_prob, float *mass, int bins_per_binade,
+                                  hipStream_t st);
 
 // Retained-store maintenance: workspace bytes (the unions' token lists and
 // sizes) and the two launches.

@@ -77,6 +77,7 @@ struct PartArgs {
   // tok_len[b]
   const int32_t *row_pos, *tok_len;
   int tok_cap;
+  float pscale;  // probability keys: the bin scale (see plog2)
 };
 
 __device__ __forceinline__ uint64_t lanemask_lt() {
@@ -236,20 +237,23 @@ __device__ __forceinline__ void row_stats(const PartArgs &a, PartShared<PT> &sh,
 // every token is ranked and the kernel carries no test for it.
 // Bin of a non-negative key that is a probability (or a sum of them) rather
 // than a logit: its bit pattern read as exponent + mantissa fraction, a
-// monotone stand-in for log2 with 64 bins per binade.  Exact (integer below
+// monotone stand-in for log2, in bins of a set fraction of a binade.  Exact (integer below
 // 2^24, power-of-2 scaling).
-__device__ __forceinline__ float plog2(float x) {
-  return (float)(__float_as_uint(x) >> 8) * (1.0f / 32768.0f);
+// pscale = bins per binade / (64 * 2^15): key bits >> 8 count 2^15 steps per
+// binade and logit_bin takes 64 bins per unit (2048 bins below the key).
+__device__ __forceinline__ float plog2(float x, float pscale) {
+  return (float)(__float_as_uint(x) >> 8) * pscale;
 }
 
 template <int R, int PT, bool kRecent, bool kProb = false>
 struct Row {
   static constexpr int kChunk = PC<PT>::chunk;
   // histogram bin of a key below the row's largest key M
-  __device__ static __forceinline__ int bin(float s, float M) {
-    if constexpr (kProb) return logit_bin(plog2(s), plog2(M));
+  __device__ __forceinline__ int bin(float s, float M) const {
+    if constexpr (kProb) return logit_bin(plog2(s, pscale), plog2(M, pscale));
     return logit_bin(s, M);
   }
+  float pscale;  // kProb: key bits >> 8 to bins of 1/64 (see plog2)
   float s[R > 0 ? R : 4];
   const float *lg;
   int n;
@@ -349,7 +353,7 @@ __device__ __forceinline__ Targets select_targets(PartShared<PT> &sh, const RowC
   if (tid < 2) sh.ncand[tid] = 0;
   __syncthreads();
   row.each([&](float s, bool valid) {
-    if (valid) atomicAdd(&sh.hist[0][Hist<PT>::idx(Row::bin(s, M))], 1u);
+    if (valid) atomicAdd(&sh.hist[0][Hist<PT>::idx(row.bin(s, M))], 1u);
   });
   __syncthreads();
   // every wave finds both targets' bins itself: no broadcast needed
@@ -370,7 +374,7 @@ __device__ __forceinline__ Targets select_targets(PartShared<PT> &sh, const RowC
   if (mode[0] < 2 || mode[1] < 2) {
     const uint64_t lt = lanemask_lt();
     row.each([&](float s, bool valid) {
-      const int bn = valid ? Row::bin(s, M) : -1;
+      const int bn = valid ? row.bin(s, M) : -1;
       const uint32_t u = logit_key(s);
 #pragma unroll
       for (int x = 0; x < 2; ++x) {
@@ -434,7 +438,7 @@ __device__ __forceinline__ Targets select_targets(PartShared<PT> &sh, const RowC
         }
       if (mode[0] == 2 || mode[1] == 2)
         row.each([&](float s, bool valid) {
-          const int bn = valid ? Row::bin(s, M) : -1;
+          const int bn = valid ? row.bin(s, M) : -1;
           const uint32_t u = logit_key(s);
           if (mode[0] == 2 && bn == bin[0] && (u & m0) == p0) atomicAdd(&sh.hist[0][Hist<PT>::idx((u >> shf) & dmask)], 1u);
           if (mode[1] == 2 && bn == bin[1] && (u & m1) == p1) atomicAdd(&sh.hist[1][Hist<PT>::idx((u >> shf) & dmask)], 1u);
@@ -585,6 +589,7 @@ void partition_kernel(PartArgs a) {
   row.lg = r.lg;
   row.n = r.n;
   row.nrank = r.older;
+  row.pscale = a.pscale;
   row.aligned = (reinterpret_cast<uintptr_t>(r.lg) & 15) == 0;
   row.load();  // in flight while the row's statistics arrive
   row_stats<kMerge>(a, sh, r);
@@ -839,11 +844,15 @@ namespace smallkv {
 
 hipError_t launch_group_partition(const smallkv_batch_t &b, int group_rows, const float *keys,
                                   const float *key_max, int32_t *crit, int32_t *marg,
-                                  float *marg_prob, float *mass, hipStream_t st) {
+                                  float *marg_prob, float *mass, int bins_per_binade,
+                                  hipStream_t st) {
   // keys are sums of probabilities: the row's largest key stands in for both
   // the row max and the normaliser (the p' this writes are not used)
-  const PartArgs a = base_args(b, group_rows, keys, const_cast<float *>(key_max),
-                               const_cast<float *>(key_max), crit, marg, marg_prob, mass);
+  PartArgs a = base_args(b, group_rows, keys, const_cast<float *>(key_max),
+                         const_cast<float *>(key_max), crit, marg, marg_prob, mass);
+  // key bits >> 8 hold 15 mantissa bits per binade; logit_bin takes 64 steps
+  // per unit, so a unit of 64 / bins_per_binade binades
+  a.pscale = (float)bins_per_binade / (64.0f * 32768.0f);
   return launch_rows<false, true>(a, b.batch * group_rows, st);
 }
 
