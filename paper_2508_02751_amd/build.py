@@ -6,6 +6,7 @@ from __future__ import annotations
 
 import concurrent.futures as cf
 import os
+import re
 import subprocess
 import sys
 
@@ -28,12 +29,34 @@ FLAGS = [
 ]
 
 
+def scratch_users(remarks: str) -> list:
+    """Kernels whose resource-usage remarks report private-segment (scratch)
+    bytes, i.e. register spills: [(kernel, bytes per lane)]."""
+    out, name = [], None
+    for line in remarks.splitlines():
+        m = re.search(r"Function Name: (\S+)", line)
+        if m:
+            name = m.group(1)
+            continue
+        m = re.search(r"ScratchSize \[bytes/lane\]: (\d+)", line)
+        if m and name and int(m.group(1)) > 0:
+            out.append((name, int(m.group(1))))
+    return out
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [HIPCC, *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [HIPCC, *FLAGS, "-Rpass-analysis=kernel-resource-usage", "-c",
+           os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stdout}\n{r.stderr}")
+    # no kernel may spill registers to scratch: the library is built and
+    # tested only in its spill-free form
+    spills = scratch_users(r.stderr)
+    if spills:
+        lines = "\n".join(f"  {k}: {n} bytes/lane" for k, n in spills)
+        raise RuntimeError(f"{src}: kernels use scratch (register spills):\n{lines}")
     return obj
 
 

@@ -755,6 +755,11 @@ PartArgs base_args(const smallkv_batch_t &b, int n_small_heads, const float *log
   return a;
 }
 
+// Rows of 1024 threads (16 waves, so at most 128 VGPRs per thread) exist
+// only with up to 8 logits per thread in registers: the 16-logit and
+// memory-path rows need more and would spill to scratch at that width.
+constexpr int kWideMaxR = 8;
+
 template <bool kMerge, int PT, bool kRecent, bool kProb>
 hipError_t launch_pt(const PartArgs &a, int rows, hipStream_t st) {
   const dim3 grid(rows), block(PT);
@@ -763,6 +768,8 @@ hipError_t launch_pt(const PartArgs &a, int rows, hipStream_t st) {
     hipLaunchKernelGGL((partition_kernel<kMerge, 4, PT, kRecent, kProb>), grid, block, 0, st, a);
   else if (n <= 8 * PT)
     hipLaunchKernelGGL((partition_kernel<kMerge, 8, PT, kRecent, kProb>), grid, block, 0, st, a);
+  else if constexpr (PT == 1024)
+    return hipErrorInvalidValue;  // the caller picks 1024 threads only for n <= 8 * 1024
   else if (n <= 16 * PT)
     hipLaunchKernelGGL((partition_kernel<kMerge, 16, PT, kRecent, kProb>), grid, block, 0, st, a);
   else if (PT == 256 && n <= 20 * PT)  // narrow rows: one more register chunk
@@ -787,7 +794,8 @@ hipError_t launch_rows(const PartArgs &a, int rows, hipStream_t st) {
   if (rows >= kManyRows) return launch_pt<kMerge, 256, false, kProb>(a, rows, st);
   // at most one row per CU: 1024 threads shorten each row's passes
   // (with more rows some CUs would run two of them in turn)
-  if (rows <= 256) return launch_pt<kMerge, 1024, false, kProb>(a, rows, st);
+  if (rows <= 256 && a.n_cap <= kWideMaxR * 1024)
+    return launch_pt<kMerge, 1024, false, kProb>(a, rows, st);
   return launch_pt<kMerge, 512, false, kProb>(a, rows, st);
 }
 
