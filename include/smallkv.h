@@ -24,7 +24,9 @@
  *   - Ownership: the caller allocates and owns every buffer, including the
  *     workspace.  The library allocates no device memory, keeps no state
  *     between calls and never synchronises: work is enqueued on `stream`
- *     (a hipStream_t; NULL is the null stream) and the call returns.
+ *     (a hipStream_t; NULL is the null stream) and the call returns.  The one
+ *     exception is smallkv_step_noalloc, which takes no workspace and runs on
+ *     a static device array of the library's (one per GPU, see there).
  *   - Errors: a negative status is returned, before anything is enqueued,
  *     for every condition visible on the host (null pointers, sizes, head
  *     dims, dtype, workspace too small, head counts).  A kernel launch
@@ -52,7 +54,7 @@
 extern "C" {
 #endif
 
-#define SMALLKV_ABI_VERSION 7
+#define SMALLKV_ABI_VERSION 8
 
 typedef enum { SMALLKV_F32 = 0, SMALLKV_BF16 = 1 } smallkv_dtype_t;
 
@@ -274,6 +276,27 @@ int smallkv_step(const smallkv_step_t *step, void *ws, size_t ws_bytes, void *st
 /* Bytes of workspace that smallkv_step needs for `step`; the single-stage
  * calls need no more than this for the same shapes.  Host only. */
 int smallkv_workspace_size(const smallkv_step_t *step, size_t *bytes);
+
+/* A whole step that allocates nothing and takes no workspace, for callers
+ * that cannot allocate device memory: code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc.  Same descriptor, kernels,
+ * results and errors as smallkv_step; the caller still owns every input,
+ * intermediate and output buffer the descriptor names.
+ *   - The workspace is a static device array of SMALLKV_NOALLOC_SCRATCH_BYTES
+ *     that the library holds on every GPU it runs on, from the first call
+ *     there until the process ends.  SMALLKV_EWORKSPACE (nothing enqueued)
+ *     when smallkv_workspace_size(step) exceeds it.  The first call on a GPU
+ *     (the device `stream` belongs to; the current device for the null
+ *     stream) looks the array's address up with that device current;
+ *     SMALLKV_EDEVICE if that fails.
+ *   - No hipMalloc, hipFree or other allocating call, on any call.
+ *   - Every call on one GPU uses that GPU's one array, which keeps the last
+ *     call's contents: calls that overlap on one GPU (two streams, two host
+ *     threads) race and must be serialised by the caller.  Nothing needs
+ *     clearing between calls: a step reads no byte of the array that it has
+ *     not written first. */
+#define SMALLKV_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+int smallkv_step_noalloc(const smallkv_step_t *step, void *stream);
 
 /* ---------------------------------------------------------------------------
  * Retained-store maintenance (Algorithm 1: the critical tokens keep K and V,

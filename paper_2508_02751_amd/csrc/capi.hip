@@ -2,6 +2,8 @@
 // and launches.  Nothing here touches device memory or synchronises.
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+
 #include "launch.h"
 #include "smallkv.h"
 
@@ -183,6 +185,50 @@ int device_view(const void *p, const void **out) {
   return SMALLKV_EINVAL;
 }
 
+int check_step(const smallkv_step_t *s);
+int run_step(const smallkv_step_t *s, void *ws, size_t ws_bytes, void *stream);
+
+}  // namespace
+
+// Workspace of smallkv_step_noalloc: one copy per GPU, held from the
+// library's load until the process ends.  Host code never passes this name
+// to a kernel or a copy (on the host it stands for no device address): it
+// uses the address hipGetSymbolAddress reports for the device.
+static __device__ __align__(256) unsigned char scratch[SMALLKV_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices];  // scratch's device address per device, once looked up
+
+// The scratch address on the device `stream` belongs to (the current device
+// for the null stream), looked up once per device with that device current.
+int device_scratch(hipStream_t stream, void **out) {
+  int dev = -1;
+  if ((stream ? hipStreamGetDevice(stream, &dev) : hipGetDevice(&dev)) != hipSuccess) {
+    (void)hipGetLastError();
+    return SMALLKV_EDEVICE;
+  }
+  if (dev < 0 || dev >= kMaxDevices) return SMALLKV_EUNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    int cur = -1;
+    if (hipGetDevice(&cur) != hipSuccess) return SMALLKV_EDEVICE;
+    if (cur != dev && hipSetDevice(dev) != hipSuccess) return SMALLKV_EDEVICE;
+    void *p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (cur != dev) (void)hipSetDevice(cur);
+    if (e != hipSuccess || !p) {
+      (void)hipGetLastError();
+      return SMALLKV_EDEVICE;
+    }
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return SMALLKV_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -360,6 +406,26 @@ int smallkv_match(const smallkv_match_t *m, void *ws, size_t ws_bytes, void *str
 }
 
 int smallkv_step(const smallkv_step_t *s, void *ws, size_t ws_bytes, void *stream) {
+  return run_step(s, ws, ws_bytes, stream);
+}
+
+int smallkv_step_noalloc(const smallkv_step_t *s, void *stream) {
+  int rc = check_step(s);
+  if (rc) return rc;
+  size_t need = 0;
+  if ((rc = smallkv_workspace_size(s, &need))) return rc;
+  if (need > SMALLKV_NOALLOC_SCRATCH_BYTES) return SMALLKV_EWORKSPACE;
+  void *ws = nullptr;
+  if ((rc = device_scratch(static_cast<hipStream_t>(stream), &ws))) return rc;
+  return run_step(s, ws, SMALLKV_NOALLOC_SCRATCH_BYTES, stream);
+}
+
+}  // extern "C"
+
+namespace {
+
+// Every host-visible check of a whole step, before anything is enqueued.
+int check_step(const smallkv_step_t *s) {
   if (!s) return SMALLKV_EINVAL;
   const int nsh = s->small.n_layers * s->small.n_q_heads;
   int rc = check_small(&s->batch, &s->small);
@@ -374,6 +440,15 @@ int smallkv_step(const smallkv_step_t *s, void *ws, size_t ws_bytes, void *strea
   if (accum && !s->acc_score) return SMALLKV_EINVAL;
   if ((group || accum) && s->small.held) return SMALLKV_EUNSUPPORTED;
   if (group && s->large.n_q_heads / s->large.n_kv_heads > 16) return SMALLKV_EUNSUPPORTED;
+  return SMALLKV_OK;
+}
+
+int run_step(const smallkv_step_t *s, void *ws, size_t ws_bytes, void *stream) {
+  const int rc = check_step(s);
+  if (rc) return rc;
+  const int nsh = s->small.n_layers * s->small.n_q_heads;
+  const bool group = s->select == SMALLKV_SELECT_GROUP;
+  const bool accum = s->select == SMALLKV_SELECT_ACCUM;
   const smallkv_batch_t sb = small_view(s->batch, s->small);
   const SmallPlan p = plan_small(sb, s->small);
   const StepLayout lay = step_layout(s->batch, s->small, s->large, nsh, s->select);
@@ -419,4 +494,4 @@ int smallkv_step(const smallkv_step_t *s, void *ws, size_t ws_bytes, void *strea
   return status_of(e);
 }
 
-}  // extern "C"
+}  // namespace

@@ -75,7 +75,7 @@ class Store(C.Structure):
 
 
 EXPORTS = ("smallkv_small_attn", "smallkv_partition", "smallkv_hybrid_attn", "smallkv_step",
-           "smallkv_workspace_size", "smallkv_match", "smallkv_match_workspace_size",
+           "smallkv_step_noalloc", "smallkv_workspace_size", "smallkv_match", "smallkv_match_workspace_size",
            "smallkv_group_select", "smallkv_group_select_workspace_size",
            "smallkv_accum_select", "smallkv_accum_select_workspace_size",
            "smallkv_store_update", "smallkv_store_workspace_size",
@@ -114,6 +114,7 @@ def lib():
         L.smallkv_store_update.argtypes = [P(Store), C.c_void_p, C.c_size_t, C.c_void_p]
         L.smallkv_store_workspace_size.argtypes = [P(Store), P(C.c_size_t)]
         L.smallkv_step.argtypes = [P(Step), C.c_void_p, C.c_size_t, C.c_void_p]
+        L.smallkv_step_noalloc.argtypes = [P(Step), C.c_void_p]
         L.smallkv_workspace_size.argtypes = [P(Step), P(C.c_size_t)]
         L.smallkv_match.argtypes = [P(Match), C.c_void_p, C.c_size_t, C.c_void_p]
         L.smallkv_match_workspace_size.argtypes = [P(Match), P(C.c_size_t)]
@@ -121,7 +122,7 @@ def lib():
         L.smallkv_status_string.restype = C.c_char_p
         L.smallkv_abi_version.argtypes = []
         for f in ("smallkv_small_attn", "smallkv_partition", "smallkv_hybrid_attn",
-                  "smallkv_step", "smallkv_workspace_size", "smallkv_abi_version",
+                  "smallkv_step", "smallkv_step_noalloc", "smallkv_workspace_size", "smallkv_abi_version",
                   "smallkv_match", "smallkv_match_workspace_size", "smallkv_group_select",
                   "smallkv_group_select_workspace_size", "smallkv_accum_select",
                   "smallkv_accum_select_workspace_size", "smallkv_store_update",
@@ -294,6 +295,15 @@ def make_step(batch: BatchSpec, small: ModelSpec, large: ModelSpec, head_map, mo
 def smallkv_step(step: Step, ws=None, stream=None):
     w, wb = _ws(ws)
     _check("smallkv_step", lib().smallkv_step(C.byref(step), w, wb, _stream(stream)))
+
+
+NOALLOC_SCRATCH_BYTES = 32 << 20  # SMALLKV_NOALLOC_SCRATCH_BYTES
+
+
+def smallkv_step_noalloc(step: Step, stream=None):
+    """smallkv_step on the library's own per-GPU scratch (no workspace, no
+    allocation); calls on one GPU must not overlap."""
+    _check("smallkv_step_noalloc", lib().smallkv_step_noalloc(C.byref(step), _stream(stream)))
 
 
 @dataclasses.dataclass

@@ -33,7 +33,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_abi_version_and_status_strings():
     L = S.lib()
-    assert L.smallkv_abi_version() == 7
+    assert L.smallkv_abi_version() == 8
     assert L.smallkv_status_string(0) == b"ok"
     assert L.smallkv_status_string(-3) == b"workspace too small"
     assert L.smallkv_status_string(123) == b"unknown status"
@@ -253,3 +253,25 @@ def test_store_accepts_a_whole_old_store():
     st = _fake_store(old_k=0x8000, old_v=0x9000, old_k_slot=0xa000, old_v_slot=0xb000)
     n = C.c_size_t()
     assert S.lib().smallkv_store_workspace_size(C.byref(st), C.byref(n)) == 0
+
+
+def test_noalloc_step_checks_before_touching_a_device():
+    """smallkv_step_noalloc validates like smallkv_step and refuses a step
+    whose workspace exceeds its static scratch, before any device call."""
+    L = S.lib()
+    assert L.smallkv_step_noalloc(None, None) == S.EINVAL
+    assert L.smallkv_step_noalloc(C.byref(_fake_step(**{"st__mode": 9})), None) == S.EINVAL
+    # one selection per kv group over 16 x 32768 tokens: ~590 MB of workspace
+    big = _fake_step(**{"b__batch": 16, "b__n_cap": 32768, "b__kc_cap": 1638, "b__km_cap": 4915,
+                        "s__n_layers": 16, "s__n_q_heads": 32, "s__n_kv_heads": 8,
+                        "s__n_rows": 32768, "l__n_layers": 32, "l__n_q_heads": 32,
+                        "l__n_kv_heads": 8, "l__n_rows": 32768, "st__select": S.SELECT_GROUP})
+    n = C.c_size_t()
+    assert L.smallkv_workspace_size(C.byref(big), C.byref(n)) == 0
+    assert n.value > S.NOALLOC_SCRATCH_BYTES
+    assert L.smallkv_step_noalloc(C.byref(big), None) == S.EWORKSPACE
+    # the header's limit and the binding's agree
+    text = open(os.path.join(ROOT, "include", "smallkv.h")).read()
+    assert "#define SMALLKV_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)" in text
+    assert S.NOALLOC_SCRATCH_BYTES == 32 << 20
+
