@@ -2,23 +2,39 @@
 
 A step is the whole hot path over one batch: stage 1 (small-model decode
 attention over all its layers), stage 2 (partition of every small head),
-stage 3 (hybrid attention of every large layer).  Workload: the Qwen2-7B
-(28 layers, 28q/4kv, d=128) + Qwen2-0.5B (24 layers, 14q/2kv, d=64) shapes,
-bf16, batch 1, context 8192, critical 10% / marginal 20%.
+stage 3 (hybrid attention of every large layer).  The default workload is
+the largest configuration: the LLaMA-3-8B (32 layers, 32q/8kv, d=128) +
+LLaMA-3.2-1B (16 layers, 32q/8kv, d=64) shapes, bf16, batch 16, context
+32768, critical 5% / marginal 15%, 5% heavy hitters.  `--workload N` selects
+another: 2 the Qwen2-7B + Qwen2-0.5B step at batch 1 and N = 8192; 4 the
+ragged batch-64 decode over 256 drifting steps (value = 64 * 256 / the time
+of all 256 steps); 5 the Qwen2-72B + Qwen2-0.5B step at N = 65536 whose large
+KV is held only for the retained tokens (the compact store is built from the
+step's own lists before timing, untimed, and the full cache freed).
 
-Timing: inputs are resident in HBM; the step is captured in one HIP graph per
-input copy, and consecutive steps rotate over `--rotate` copies so that a
-step never finds the previous step's operands in the 256 MB MALL.  W warm-up
-steps, then exactly K timed steps between two synchronisations.  A second
-pass with HIP events between the stages (enqueued behind a sleep kernel so
-the host never starves the GPU) gives per-stage kernel durations for the
-roofline.  The CPU baseline is the oracle on one host core over whole steps.
+Timing: inputs are resident in HBM; each step is a HIP-graph replay (the
+drifting workload launches its steps directly, each with its own queries and
+lengths).  W warm-up steps, then exactly K timed steps between two
+synchronisations (`value` and `ms_per_step`).  Small workloads rotate over
+`--rotate` input copies so that a step never finds the previous step's
+operands in the 256 MB MALL.  Then three timing passes with HIP events:
+  * per step, with the caches flushed before it (a 1 GiB write): the step's
+    own kernels through smallkv_step_events, which records events at the
+    stage boundaries -- median, p10 and p90 of the step, the stage means,
+    and the roofline of the dominant stage (its algorithmic bytes over its
+    event time against 8 TB/s);
+  * the same without the flush (warm);
+  * the per-layer-launch variant: stages 1 and 2 through their single-stage
+    calls, then stage 3 as one smallkv_hybrid_attn_layers call per large
+    layer, as a model that runs its layers one after another calls it.
+The CPU baseline is the oracle on one pinned host core over one sequence's
+whole step (the sample is named in the line).
 
 Prints one JSON line.
 
 `--match` benchmarks the prefill similarity matching instead (Eqs. 1-3: the
-step before decoding that computes the head map): the Qwen2-7B + Qwen2-0.5B
-shapes over a 200-token window, one JSON line of its own.
+step before decoding that computes the head map); `--store` the retained-store
+maintenance after a step.
 """
 from __future__ import annotations
 
@@ -26,27 +42,37 @@ import argparse
 import hashlib
 import json
 import os
+import statistics
 import sys
 import time
+import types
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, 8 TB/s
 FP32_VECTOR_PEAK_TFLOPS = 157.3  # MI355X fp32 vector (packed FMA counted as 4 flops)
+DEFAULT_STEPS = {2: 100, 4: 256}  # others: 20
+FLUSH_BYTES = 1 << 30  # written before each flushed step: above L2 and the 256 MB MALL
 
 
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=100)
-    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--steps", type=int, default=None,
+                   help="timed steps (default: 256 for the drifting workload, 100 for "
+                        "workload 2, else 20)")
+    p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--rotate", type=int, default=4, help="input copies cycled through")
-    p.add_argument("--workload", type=int, default=2,
-                   help="2: the Qwen2-7B + Qwen2-0.5B headline step; 3-5: the larger shapes")
+    p.add_argument("--workload", type=int, default=3,
+                   help="3: the LLaMA batch-16 step (default, the largest); 2: Qwen2-7B batch 1; "
+                        "4: ragged batch 64 over 256 drifting steps; 5: Qwen2-72B on a compact "
+                        "store; 1, 6-10: the other workloads")
     p.add_argument("--eager", action="store_true", help="launch without HIP graphs")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time budget")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-extra-passes", action="store_true",
+                   help="only the timed steps and the stage events (for profiler runs)")
     p.add_argument("--match", action="store_true",
                    help="benchmark the prefill head matching instead of the decode step")
     p.add_argument("--store", action="store_true",
@@ -57,7 +83,10 @@ def parse():
     p.add_argument("--match-window", type=int, default=200)
     p.add_argument("--copy-probe-mib", type=int, default=0,
                    help="first run a plain device copy of this many MiB (counter calibration)")
-    return p.parse_args()
+    a = p.parse_args()
+    if a.steps is None:
+        a.steps = 20 if (a.match or a.store) else DEFAULT_STEPS.get(a.workload, 20)
+    return a
 
 
 def source_hash(name: str) -> str:
@@ -65,11 +94,15 @@ def source_hash(name: str) -> str:
     return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
 
 
-def load_traffic(kernels, workload: str, name: str = "traffic.json"):
-    """HBM bytes of one stage call (the sum over its kernels) from the committed
-    rocprofv3 --pmc summary, or None when the counters were taken on another
-    workload, a kernel is missing, or its source changed since."""
-    path = os.path.join(ROOT, "profiles", name)
+def traffic_file(workload: str) -> str:
+    return os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+
+
+def load_traffic(kernels, workload: str, path: str = None):
+    """HBM bytes of one stage (the sum over its kernels) from the committed
+    rocprofv3 --pmc summary of this workload, or None when there is none, a
+    kernel is missing, or its source changed since the counters were taken."""
+    path = path or traffic_file(workload)
     if not os.path.exists(path):
         return None
     try:
@@ -109,18 +142,236 @@ def budget_text(spec) -> str:
     return f"{v}%" if kind == "pct" else f"{v} tokens"
 
 
-def stage3_kernels(w):
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def stage3_kernels(w, layers=None):
     """Kernels one stage-3 call launches for workload w: the grouped kernel for
     bf16, head_dim 128 and at most 8 query heads per kv head (plus the merge
-    of its token splits when there are fewer than 512 kv-head units, the
-    library's rule), the per-head kernel otherwise."""
+    of its token splits when it splits, the library's rule), the per-head
+    kernel otherwise."""
     L = w.large
     if w.dtype != "bf16" or L.head_dim != 128 or L.group > 8:
         return ["hybrid_kernel"]
-    units = w.batch * L.layers * L.kv_heads
-    splits = max(1, min(512 // units, (w.n_cap + 255) // 256))
-    return ["hybrid_group_kernel", "hybrid_group_merge"] if splits > 1 else ["hybrid_group_kernel"]
+    units = w.batch * (layers or L.layers) * L.kv_heads
+    n_cap = w.n_cap
+    cost = lambda c: -(-units * c // 512) * (-(-n_cap // c) + 384)
+    s = 1
+    for c in range(2, min(16, -(-n_cap // 256)) + 1):
+        if cost(c) < cost(s):
+            s = c
+    span = -(-(-(-n_cap // s)) // 256) * 256
+    return ["hybrid_group_kernel", "hybrid_group_merge"] if -(-n_cap // span) > 1 \
+        else ["hybrid_group_kernel"]
 
+
+def stage_kernels(w):
+    """The kernels inside each of smallkv_step_events' three windows."""
+    if w.select == 1:
+        return [["small_attn_mfma", "small_attn_merge"],
+                ["group_zq", "group_scores", "partition_kernel", "group_weights"],
+                stage3_kernels(w)]
+    if w.select == 2:
+        return [["small_attn_mfma", "small_attn_merge"],
+                ["group_zq", "accum_scores", "partition_kernel", "group_weights"],
+                stage3_kernels(w)]
+    s1 = "small_attn_valu" if w.dtype == "f32" else "small_attn_mfma"
+    return [[s1], ["partition_kernel"], stage3_kernels(w)]
+
+
+def pct(xs, q):
+    xs = sorted(xs)
+    k = (len(xs) - 1) * q
+    lo, hi = int(k), min(int(k) + 1, len(xs) - 1)
+    return xs[lo] + (xs[hi] - xs[lo]) * (k - lo)
+
+
+def host_cpu():
+    model = None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    try:
+        avail = len(os.sched_getaffinity(0))
+    except AttributeError:
+        avail = os.cpu_count()
+    return {"host_cpu": model, "host_nproc": os.cpu_count(), "host_cpus_available": avail}
+
+
+# ----------------------------------------------------------- inputs --------
+
+def compact_store(w, x, dev):
+    """The large model's KV held only for the retained tokens: the step's own
+    lists, the store built from them by smallkv_store_update (rows = the
+    largest union over the kv heads), the full cache freed.  Untimed."""
+    import torch
+    from paper_2508_02751_amd import smallkv as S
+    from paper_2508_02751_amd.pipeline import prepare_step
+
+    ps = prepare_step(x)
+    ps.run()
+    nsh = ps.buf.logits.shape[1]
+    probe = S.prepare_store(ps.batch, ps.head_map, nsh, ps.buf.crit_idx, ps.buf.marg_idx,
+                            x["l_k"], x["l_v"], 1)
+    probe.run()
+    torch.cuda.synchronize()
+    rows = int(probe.counts.max())
+    del probe
+    st = S.prepare_store(ps.batch, ps.head_map, nsh, ps.buf.crit_idx, ps.buf.marg_idx,
+                         x["l_k"], x["l_v"], rows)
+    st.run()
+    torch.cuda.synchronize()
+    k_union = st.counts[..., 0].to(torch.float64).mean().item() / w.n_cap
+    v_union = st.counts[..., 1].to(torch.float64).mean().item() / w.n_cap
+    store = {"l_k": st.new_k, "l_v": st.new_v, "k_slot": st.k_slot, "v_slot": st.v_slot}
+    del ps, st  # (both hold the full cache)
+    x.pop("l_k")
+    x.pop("l_v")
+    torch.cuda.empty_cache()
+    log(f"compact store: {rows} rows per kv head of {w.n_cap} (unions: critical "
+        f"{k_union:.3f}, critical+marginal {v_union:.3f} of the tokens); full cache freed")
+    info = {"large_store": "compact: retained rows only, read through slot maps",
+            "store_rows_per_kv_head": rows, "union_frac_k": k_union, "union_frac_v": v_union}
+    return store, info
+
+
+def prepare(x, store):
+    from paper_2508_02751_amd.pipeline import prepare_step
+    if store is None:
+        return prepare_step(x)
+    return prepare_step(x, k_slot=store["k_slot"], v_slot=store["v_slot"], l_k=store["l_k"],
+                        l_v=store["l_v"])
+
+
+def bytes_of(ps, store):
+    from paper_2508_02751_amd.bytes_model import step_bytes
+    x = dict(ps.inputs)
+    if store is not None:
+        x["l_k"] = store["l_k"]
+    return step_bytes(x, ps.buf.crit_idx, ps.buf.marg_idx, ps.batch.km_cap)
+
+
+# ----------------------------------------------------------- passes --------
+
+def event_pass(preps, K, stream, flush=None):
+    """Per step (preps cycled): events at the stage boundaries of the step's
+    own kernels; returns per-step stage and step times in ms."""
+    import torch
+    from paper_2508_02751_amd import smallkv as S
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    torch.cuda._sleep(50_000_000)  # keep the GPU busy while the host enqueues
+    for i in range(K):
+        ps = preps[i % len(preps)]
+        if flush is not None:
+            # read (not write) 1 GiB: L2 and the MALL end up holding clean
+            # lines of the flush buffer, so the step pays no write-backs
+            flush.sum(dtype=torch.int32)
+        S.smallkv_step_events(ps.desc, ps.buf.ws, ev[i], stream)
+    torch.cuda.synchronize()
+    stages = [[ev[i][s].elapsed_time(ev[i][s + 1]) for i in range(K)] for s in range(3)]
+    steps = [ev[i][0].elapsed_time(ev[i][3]) for i in range(K)]
+    return stages, steps
+
+
+def per_layer_variant(ps, K, W, use_graph):
+    """Stages 1-2 through the single-stage calls, stage 3 as one call per
+    large layer; mean ms per step over K graph replays."""
+    import torch
+    from paper_2508_02751_amd import smallkv as S
+    b = ps.buf
+    nsh = b.logits.shape[1]
+    L = ps.large.q.shape[1]
+    ws = torch.empty(max(1, S.smallkv_hybrid_attn_workspace_size(ps.batch, ps.large, 1, nsh),
+                         b.ws.numel() if b.ws is not None else 1), dtype=torch.uint8,
+                     device=b.logits.device)
+
+    def run():
+        S.smallkv_small_attn(ps.batch, ps.small, b.logits, b.row_max, b.row_sum, ws)
+        S.smallkv_partition(ps.batch, nsh, b.logits, b.row_max, b.row_sum, b.crit_idx,
+                            b.marg_idx, b.marg_prob, b.mass, None, small=ps.small)
+        for layer in range(L):
+            S.smallkv_hybrid_attn_layers(ps.batch, ps.large, layer, 1, ps.head_map, nsh,
+                                         b.crit_idx, b.marg_idx, b.marg_prob, b.mass, ps.mode,
+                                         ws)
+
+    for _ in range(max(W, 1)):
+        run()
+    torch.cuda.synchronize()
+    g = None
+    if use_graph:
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            run()
+        g.replay()
+        torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(K):
+        g.replay() if g is not None else run()
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) * 1e3 / K, L
+
+
+def cpu_baseline(args, w, ps, store):
+    """The oracle on one pinned host core over sequence 0's whole step (all
+    layers of both models): one token of the metric per run."""
+    import numpy as np
+    import torch
+    sys.path.insert(0, os.path.join(ROOT, "oracle"))
+    import oracle as O
+    from paper_2508_02751_amd.pipeline import softmax_scale
+
+    def h(t):
+        t = t[0:1]
+        return t.detach().float().cpu().numpy() if t.dtype == torch.bfloat16 else t.cpu().numpy()
+
+    x = ps.inputs
+    host = {k: h(x[k]) for k in ("seq_len", "k_crit", "k_marg", "s_q", "s_k", "s_v", "l_q")}
+    host["head_map"] = x["head_map"].cpu().numpy()
+    host["l_k"] = h(store["l_k"] if store else x["l_k"])
+    host["l_v"] = h(store["l_v"] if store else x["l_v"])
+    extra = {}
+    if store is not None:
+        extra["k_slot"], extra["v_slot"] = h(store["k_slot"]), h(store["v_slot"])
+    if x.get("k_recent") is not None:
+        extra["k_recent"] = h(x["k_recent"])
+    if x.get("s_held") is not None:
+        extra.update(s_held=h(x["s_held"]), s_row_pos=h(x["s_row_pos"]), n_cap=x["n_cap"])
+    if w.select == 1:
+        extra["select"] = O.SELECT_GROUP
+    if w.select == 2:
+        extra["select"] = O.SELECT_ACCUM
+        extra["acc"] = np.zeros((1,) + tuple(ps.buf.acc_score.shape[1:]), np.float32)
+    cpu_info = host_cpu()  # before pinning
+    try:
+        os.sched_setaffinity(0, {sorted(os.sched_getaffinity(0))[0]})
+    except (AttributeError, OSError):
+        pass
+    log("timing the CPU oracle")
+    reps, spent = 0, 0.0
+    while reps < 1 or spent < args.cpu_seconds:
+        c0 = time.perf_counter()
+        O.step(seq_len=host["seq_len"], k_crit=host["k_crit"], k_marg=host["k_marg"],
+               kc_cap=int(x["kc_cap"]), km_cap=int(x["km_cap"]), head_map=host["head_map"],
+               mode=O.NORM_REMAINING, s_q=host["s_q"], s_k=host["s_k"], s_v=host["s_v"],
+               s_scale=softmax_scale(w.small.head_dim), l_q=host["l_q"], l_k=host["l_k"],
+               l_v=host["l_v"], l_scale=softmax_scale(w.large.head_dim), **extra)
+        spent += time.perf_counter() - c0
+        reps += 1
+    n0 = int(host["seq_len"][0])
+    what = ("the whole decode step" if w.batch == 1 else
+            f"sequence 0 of {w.batch} (N = {n0}): its whole decode step, every layer of both "
+            f"models; the step's rate is {w.batch}x this sample's work")
+    return {"value": reps / spent, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": f"{reps} run(s) of {what}, single-threaded C oracle pinned to one core "
+                      f"({spent:.1f} s)", **cpu_info}
+
+
+# ----------------------------------------------------------- main ----------
 
 def main():
     args = parse()
@@ -128,38 +379,38 @@ def main():
         print("bench.py: the library runs on one GPU; sharding the step over several GPUs "
               "is not implemented, so --gpus must be 1", file=sys.stderr)
         sys.exit(2)
-
     if args.match:
         return bench_match(args)
     if args.store:
         return bench_store(args)
     import torch
-    from paper_2508_02751_amd import smallkv as S
     from paper_2508_02751_amd import workloads as W
-    from paper_2508_02751_amd.bytes_model import step_bytes
-    from paper_2508_02751_amd.pipeline import prepare_step
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     w = W.WORKLOADS[args.workload]
     copy_probe(args, dev)
-    print(f"[bench] generating {w.name}", file=sys.stderr, flush=True)
+    log(f"generating {w.name}")
+    if w.steps > 1:
+        return bench_drift(args, w, dev)
     x0 = W.make_step_inputs(w, dev)
+    store, store_info = (compact_store(w, x0, dev) if w.compact_large else (None, {}))
     copy_bytes = sum(v.numel() * v.element_size() for v in x0.values() if torch.is_tensor(v))
+    if store is not None:
+        copy_bytes += sum(v.numel() * v.element_size() for v in store.values())
     if copy_bytes > (16 << 30):  # far beyond the 256 MB MALL already; keep HBM free
         args.rotate = 1
     copies = [x0]
     for _ in range(args.rotate - 1):
         copies.append({k: (v.clone() if torch.is_tensor(v) else v) for k, v in x0.items()})
-    preps = [prepare_step(x) for x in copies]
+    preps = [prepare(x, store) for x in copies]
     stream = torch.cuda.current_stream()
 
     # warm-up (eager), also builds the partitions used for byte accounting
     for i in range(max(args.warmup, 1)):
         preps[i % len(preps)].run()
     torch.cuda.synchronize()
-
     graphs = None
     if not args.eager:
         graphs = []
@@ -174,6 +425,7 @@ def main():
 
     # ---- timed region: exactly K steps ------------------------------------
     K = args.steps
+    log(f"timing {K} steps")
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(K):
@@ -185,98 +437,42 @@ def main():
     t1 = time.perf_counter()
     ms_per_step = (t1 - t0) * 1e3 / K
 
-    # ---- per-stage kernel durations with HIP events -------------------------
-    nsh = w.small.layers * w.small.q_heads
-    group = w.select == 1
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
-    torch.cuda._sleep(50_000_000)  # keep the GPU busy while the host enqueues
-    for i in range(K):
-        ps = preps[i % len(preps)]
-        b = ps.buf
-        e = ev[i]
-        e[0].record(stream)
-        S.smallkv_small_attn(ps.batch, ps.small, b.logits, b.row_max, b.row_sum, b.ws, stream)
-        e[1].record(stream)
-        if group:
-            S.smallkv_group_select(ps.batch, ps.small, ps.large, ps.head_map, b.logits, b.row_max,
-                                   b.row_sum, b.crit_idx, b.marg_idx, b.marg_prob, b.mass, b.ws,
-                                   stream)
-        elif w.select == 2:
-            S.smallkv_accum_select(ps.batch, ps.small, b.logits, b.row_max, b.row_sum,
-                                   b.acc_score, b.crit_idx, b.marg_idx, b.marg_prob, b.mass, b.ws,
-                                   stream)
-        else:
-            S.smallkv_partition(ps.batch, nsh, b.logits, b.row_max, b.row_sum, b.crit_idx,
-                                b.marg_idx, b.marg_prob, b.mass, None, stream, small=ps.small)
-        e[2].record(stream)
-        S.smallkv_hybrid_attn(ps.batch, ps.large, ps.head_map, nsh, b.crit_idx, b.marg_idx,
-                              b.marg_prob, b.mass, ps.mode, b.ws, stream,
-                              select=S.SELECT_GROUP if group else S.SELECT_HEAD)
-        e[3].record(stream)
-    torch.cuda.synchronize()
-    stage_ms = [sum(ev[i][s].elapsed_time(ev[i][s + 1]) for i in range(K)) / K for s in range(3)]
+    # ---- the step's own kernels, by stage, with HIP events -----------------
+    flush = torch.zeros(FLUSH_BYTES, dtype=torch.uint8, device=dev)
+    stages, steps = event_pass(preps, K, stream, flush)
+    del flush
+    extra = {}
+    if not args.no_extra_passes:
+        _, warm = event_pass(preps[:1], K, stream)  # the same inputs step after step
+        extra["warm_no_flush_ms"] = {"median": statistics.median(warm), "p10": pct(warm, 0.1),
+                                     "p90": pct(warm, 0.9)}
+        del graphs
+        if w.select == 0:  # (the single-stage path of per-head selection)
+            ml, L = per_layer_variant(preps[0], K, args.warmup, not args.eager)
+            extra["per_layer_launch"] = {
+                "ms_per_step": ml, "tokens_per_s": w.batch * 1e3 / ml,
+                "launches": f"small attention, partition, then {L} stage-3 calls (one per "
+                            f"large layer)"}
 
-    # ---- bytes ------------------------------------------------------------
     ps = preps[0]
-    sb = step_bytes(ps.inputs, ps.buf.crit_idx, ps.buf.marg_idx, ps.batch.km_cap)
+    sb = bytes_of(ps, store)
+    out = result_line(args, w, K, ms_per_step, stages, steps, sb, store_info)
+    out["step"].update(extra)
+    out["cpu_baseline"] = None if args.no_cpu_baseline else cpu_baseline(args, w, ps, store)
+    print(json.dumps(out), flush=True)
+
+
+def result_line(args, w, K, ms_per_step, stages, steps, sb, store_info, value=None, n_tok=None):
+    stage_ms = [sum(x) / len(x) for x in stages]
     stage_bytes = [sb.stage1, sb.stage2, sb.stage3]
-    # kernels each single-stage call launches for this workload (bf16, large
-    # head_dim 128, 7 query heads per kv head, 112 kv-head units: stage 3 is
-    # the grouped kernel over token splits plus their merge)
-    stage_kernels = [["small_attn_mfma", "small_attn_merge"],
-                     ["group_zq", "group_scores", "partition_kernel", "group_weights"] if group
-                     else ["group_zq", "accum_scores", "partition_kernel", "group_weights"]
-                     if w.select == 2 else ["partition_kernel"], stage3_kernels(w)]
     dom = max(range(3), key=lambda s: stage_ms[s])
+    kern = stage_kernels(w)
     achieved = stage_bytes[dom] / (stage_ms[dom] * 1e-3) / 1e9
-    traffic = load_traffic(stage_kernels[dom], w.name)
     step_gbs = sb.step_compulsory / (ms_per_step * 1e-3) / 1e9
-
-    # ---- CPU baseline: the oracle on one core ------------------------------
-    cpu = None
-    if not args.no_cpu_baseline:
-        sys.path.insert(0, os.path.join(ROOT, "oracle"))
-        import numpy as np
-        import oracle as O
-        from paper_2508_02751_amd.pipeline import softmax_scale
-
-        def h(t):
-            return t.detach().float().cpu().numpy() if t.dtype == torch.bfloat16 else t.cpu().numpy()
-
-        x = ps.inputs
-        host = {k: h(x[k]) for k in ("seq_len", "k_crit", "k_marg", "head_map", "s_q", "s_k",
-                                     "s_v", "l_q", "l_k", "l_v")}
-        host["k_recent"] = h(x["k_recent"]) if x.get("k_recent") is not None else None
-        held = {} if x.get("s_held") is None else dict(
-            s_held=h(x["s_held"]), s_row_pos=h(x["s_row_pos"]), n_cap=x["n_cap"])
-        if group:
-            held["select"] = O.SELECT_GROUP
-        if w.select == 2:
-            held["select"] = O.SELECT_ACCUM
-            held["acc"] = np.zeros(tuple(ps.buf.acc_score.shape), np.float32)
-        try:
-            os.sched_setaffinity(0, {sorted(os.sched_getaffinity(0))[0]})
-        except (AttributeError, OSError):
-            pass
-        print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
-        reps, spent = 0, 0.0
-        while reps < 1 or spent < args.cpu_seconds:
-            c0 = time.perf_counter()
-            O.step(seq_len=host["seq_len"], k_crit=host["k_crit"], k_marg=host["k_marg"],
-                   kc_cap=x["kc_cap"], km_cap=x["km_cap"], head_map=host["head_map"],
-                   mode=O.NORM_REMAINING, s_q=host["s_q"], s_k=host["s_k"], s_v=host["s_v"],
-                   s_scale=softmax_scale(w.small.head_dim), l_q=host["l_q"], l_k=host["l_k"],
-                   l_v=host["l_v"], l_scale=softmax_scale(w.large.head_dim),
-                   k_recent=host["k_recent"], **held)
-            spent += time.perf_counter() - c0
-            reps += 1
-        cpu = {"value": w.batch * reps / spent, "unit": "tokens/s", "cores": 1, "kind": "oracle",
-               "sample": f"{reps} whole decode step(s) of the same workload, single-threaded C "
-                         f"oracle pinned to one core ({spent:.1f} s)"}
-
-    out = {
+    group = w.select == 1
+    return {
         "metric": "SmallKV decode-step attention tokens/s at 1 MI355X; % of HBM roofline",
-        "value": w.batch * 1e3 / ms_per_step,
+        "value": value if value is not None else w.batch * 1e3 / ms_per_step,
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": K,
@@ -285,42 +481,120 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": "bf16" if w.dtype == "bf16" else "f32",
         "data": "synthetic",
         "config": {
             "workload": w.name,
             "large": shape_text(w.large), "small": shape_text(w.small),
             "kv_dtype": w.dtype, "batch": w.batch, "context": w.n_ctx,
+            **({"context_range": f"{w.ragged_min}..{w.n_ctx} + {w.steps} decode steps"}
+               if w.ragged_min else {}),
             "critical": budget_text(w.crit), "marginal": budget_text(w.marg),
+            **({"heavy_hitters": f"{int(100 * w.heavy_frac)}%"} if w.heavy_frac else {}),
             **({"recent": budget_text(w.recent)} if w.recent != ("abs", 0) else {}),
             **({"small_cache_kept": f"{w.slm_keep}%"} if w.slm_keep else {}),
             **({"selection": "one per large kv head (summed)"} if group else {}),
             **({"selection": "accumulated scores (running state)"} if w.select == 2 else {}),
-            "launch": "eager" if args.eager else "hip-graph",
-            "rotated_input_copies": args.rotate,
+            **store_info,
+            "launch": "eager" if (args.eager or w.steps > 1) else "hip-graph",
+            "rotated_input_copies": 1 if w.steps > 1 else args.rotate,
         },
         "roofline": {
-            "kernel": "+".join(stage_kernels[dom]),
+            "kernel": "+".join(kern[dom]),
             "bound": "hbm",
             "achieved": achieved,
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS,
-            "traffic": traffic,
+            "traffic": load_traffic(kern[dom], w.name),
         },
         "step": {
             "compulsory_bytes": sb.step_compulsory,
             "achieved_GBs": step_gbs,
             "hbm_frac": step_gbs / HBM_PEAK_GBS,
+            "flushed_event_ms": {"median": statistics.median(steps), "p10": pct(steps, 0.1),
+                                 "p90": pct(steps, 0.9)},
             "stage_ms": stage_ms,
+            "stage_kernels": ["+".join(k) for k in kern],
             "stage_bytes": stage_bytes,
             "stage_GBs": [stage_bytes[s] / (stage_ms[s] * 1e-3) / 1e9 for s in range(3)],
             "large_rows_per_head_over_union": (sb.large_k_perhead + sb.large_v_perhead)
             / max(1, sb.large_k_union + sb.large_v_union),
             "index_metadata_bytes": sb.index_meta,
         },
-        "cpu_baseline": cpu,
     }
+
+
+def bench_drift(args, w, dev):
+    """The ragged batch over its consecutive drifting decode steps: every
+    step has its own queries and lengths (one descriptor each, sharing the
+    caches, the intermediates and the workspace); value = batch x steps / the
+    time of all the steps."""
+    import dataclasses
+
+    import torch
+    from paper_2508_02751_amd import smallkv as S
+    from paper_2508_02751_amd import workloads as W
+    from paper_2508_02751_amd.pipeline import prepare_step
+
+    z = W.latents(w, dev)
+    x = W.make_step_inputs(w, dev, 0, z=z)
+    base = prepare_step(x)
+    K = args.steps
+    n_steps = min(K, w.steps)
+    log(f"queries and lengths of {n_steps} steps")
+    descs = []
+    for t in range(n_steps):
+        s_q, l_q = W.step_queries(w, z, t, dev)
+        n, kc, km = W.budgets(w, t)
+        batch = dataclasses.replace(base.batch, seq_len=n.to(dev), k_crit=kc.to(dev),
+                                    k_marg=km.to(dev))
+        small = dataclasses.replace(base.small, q=s_q.contiguous())
+        large = dataclasses.replace(base.large, q=l_q.contiguous())
+        b = base.buf
+        desc = S.make_step(batch, small, large, base.head_map, base.mode, b.logits, b.row_max,
+                           b.row_sum, b.crit_idx, b.marg_idx, b.marg_prob, b.mass)
+        descs.append(dataclasses.replace(base, batch=batch, small=small, large=large, desc=desc))
+    stream = torch.cuda.current_stream()
+    for i in range(max(args.warmup, 1)):
+        descs[i % n_steps].run()
+    torch.cuda.synchronize()
+    log(f"timing {K} steps")
+    t0 = time.perf_counter()
+    for i in range(K):
+        descs[i % n_steps].run()
+    torch.cuda.synchronize()
+    total_ms = (time.perf_counter() - t0) * 1e3
+    ms_per_step = total_ms / K
+    stages, steps = event_pass(descs, K, stream)  # 9 GB per step: no cache holds it
+    # bytes: every step's own partition (recomputed, untimed)
+    log("byte accounting of every step")
+    comp = s1 = s2 = s3 = kper = kun = meta = 0
+    for t in range(n_steps):
+        d = descs[t]
+        d.run()
+        xi = dict(x)
+        xi["s_q"], xi["l_q"], xi["seq_len"] = d.small.q, d.large.q, d.batch.seq_len
+        sb = bytes_of(dataclasses.replace(d, inputs=xi), None)
+        comp += sb.step_compulsory
+        s1, s2, s3 = s1 + sb.stage1, s2 + sb.stage2, s3 + sb.stage3
+        kper += sb.large_k_perhead + sb.large_v_perhead
+        kun += sb.large_k_union + sb.large_v_union
+        meta += sb.index_meta
+    torch.cuda.synchronize()
+    mean = types.SimpleNamespace(
+        stage1=s1 / n_steps, stage2=s2 / n_steps, stage3=s3 / n_steps,
+        step_compulsory=comp / n_steps, large_k_perhead=kper / n_steps, large_v_perhead=0,
+        large_k_union=kun / n_steps, large_v_union=0, index_meta=meta / n_steps)
+    value = w.batch * K / (total_ms * 1e-3)
+    out = result_line(args, w, K, ms_per_step, stages, steps, mean, {}, value=value)
+    out["config"]["timed_steps"] = f"decode steps 0..{n_steps - 1}" + (
+        f", cycled to {K}" if K > n_steps else "")
+    out["step"]["lengths"] = {"first_step": [int(descs[0].batch.seq_len.min()),
+                                             int(descs[0].batch.seq_len.max())],
+                              "last_step": [int(descs[-1].batch.seq_len.min()),
+                                            int(descs[-1].batch.seq_len.max())]}
+    out["cpu_baseline"] = None if args.no_cpu_baseline else cpu_baseline(args, w, descs[0], None)
     print(json.dumps(out), flush=True)
 
 
@@ -380,7 +654,8 @@ def bench_store(args):
     lists = ps.buf.crit_idx.numel() * 4 + ps.buf.marg_idx.numel() * 4
     alg = 2 * moved + maps + lists
     achieved = alg / (ms_hbm * 1e-3) / 1e9
-    traffic = load_traffic(["store_index", "store_copy"], f"{w.name}-store", "traffic_store.json")
+    traffic = load_traffic(["store_index", "store_copy"], f"{w.name}-store",
+                           os.path.join(ROOT, "profiles", "traffic_store.json"))
     legs = None
     if not args.store_hbm_only:
         legs = store_legs(args, w, x, ps, store, timed, stream, moved, rows)

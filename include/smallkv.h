@@ -192,6 +192,28 @@ int smallkv_hybrid_attn(const smallkv_batch_t *batch, const smallkv_model_t *lar
                         const float *marg_prob, const float *mass, int32_t mode,
                         int32_t select, void *ws, size_t ws_bytes, void *stream);
 
+/* Stage 3 for the large layers [layer_begin, layer_begin + layer_count)
+ * only, as a model that runs its layers one after another calls it (one
+ * call per layer, each with that layer's queries in place).  `large`
+ * describes the whole stack exactly as for smallkv_hybrid_attn (n_layers =
+ * L, the same pointers and layouts); q, k, v, the slot maps and out are
+ * touched only in those layers' slices; head_map, the lists and the weights
+ * are the step's.  ws_bytes >= smallkv_hybrid_attn_workspace_size for
+ * layer_count.  SMALLKV_EINVAL for a range outside [0, L); the other errors
+ * as smallkv_hybrid_attn. */
+int smallkv_hybrid_attn_layers(const smallkv_batch_t *batch, const smallkv_model_t *large,
+                               int32_t layer_begin, int32_t layer_count, const int32_t *head_map,
+                               int32_t n_small_heads, const int32_t *crit_idx,
+                               const int32_t *marg_idx, const float *marg_prob,
+                               const float *mass, int32_t mode, int32_t select, void *ws,
+                               size_t ws_bytes, void *stream);
+
+/* Bytes of workspace a stage-3 call over layer_count layers needs
+ * (smallkv_hybrid_attn: layer_count = large->n_layers).  Host only. */
+int smallkv_hybrid_attn_workspace_size(const smallkv_batch_t *batch,
+                                       const smallkv_model_t *large, int32_t layer_count,
+                                       int32_t n_small_heads, size_t *bytes);
+
 /* Stage 2 of SMALLKV_SELECT_GROUP (see smallkv_select_t): from stage 1's
  * logits, row_max and row_sum, the lists of every (sequence, large layer, kv
  * head), crit_idx [B][L*Hkv][kc_cap] and marg_idx [B][L*Hkv][km_cap], and the
@@ -272,6 +294,17 @@ typedef struct {
 } smallkv_step_t;
 
 int smallkv_step(const smallkv_step_t *step, void *ws, size_t ws_bytes, void *stream);
+
+/* smallkv_step that also records the caller's hipEvents on `stream` at the
+ * step's stage boundaries, so that the kernels the step runs can be timed
+ * by stage: events[0] before stage 1; events[1] after stage 1's per-chunk
+ * kernel (per-head selection: stage 1's merge runs in the next kernel,
+ * fused with the partition; group and accumulated selection: after stage
+ * 1's merge); events[2] after stage 2; events[3] after stage 3.  `events`
+ * may be NULL and any entry may be NULL (not recorded).  Same checks,
+ * kernels and results as smallkv_step; SMALLKV_EDEVICE if a record fails. */
+int smallkv_step_events(const smallkv_step_t *step, void *ws, size_t ws_bytes, void *stream,
+                        void *const *events);
 
 /* Bytes of workspace that smallkv_step needs for `step`; the single-stage
  * calls need no more than this for the same shapes.  Host only. */

@@ -61,7 +61,9 @@ class StepBytes:
 
 
 def step_bytes(x: dict, crit_idx: torch.Tensor, marg_idx: torch.Tensor, km_cap: int) -> StepBytes:
-    """Count the bytes of one step from its inputs and the partition it produced."""
+    """Count the bytes of one step from its inputs and the partition it produced
+    (all sequences and large layers at once: one membership bitmap per
+    (sequence, layer, kv head) over its tokens)."""
     s_q, s_k = x["s_q"], x["s_k"]
     l_q = x["l_q"]
     esz = s_k.element_size()
@@ -80,32 +82,26 @@ def step_bytes(x: dict, crit_idx: torch.Tensor, marg_idx: torch.Tensor, km_cap: 
     part_out = B * l * hqs * (crit_idx.shape[-1] * 4 + km_cap * 8 + 8)
     large_qo = 2 * B * L * hq * d * esz
     dev = crit_idx.device
-    hm = x["head_map"].to(torch.int64).to(dev).view(L, hk, g)
     rowb = d * esz
-    k_union = v_union = k_per = v_per = meta = 0
-    group = x.get("select", 0) == 1  # lists per (large layer, kv head): the union is the list
-    for b in range(B):
-        c = crit_idx[b].to(torch.int64)          # [nsh][kc] (group selection: [L*hk][kc])
-        m = marg_idx[b, :, :km_cap].to(torch.int64) if km_cap else None
-        for li in range(L):
-            js = hm[li]                          # [hk][g]
-            if group:
-                js = (li * hk + torch.arange(hk, device=dev))[:, None].expand(hk, g)
-            cs = c[js.reshape(-1)].view(hk, -1)  # [hk][g*kc]
-            bm = torch.zeros((hk, n_cap + 1), dtype=torch.bool, device=dev)
-            bm.scatter_(1, torch.where(cs >= 0, cs, n_cap), True)
-            nk = int(bm[:, :n_cap].sum())
-            k_per += int((cs >= 0).sum()) * rowb
-            if m is not None:
-                ms = m[js.reshape(-1)].view(hk, -1)
-                bm.scatter_(1, torch.where(ms >= 0, ms, n_cap), True)
-                v_per += (int((cs >= 0).sum()) + int((ms >= 0).sum())) * rowb
-                meta += (int((cs >= 0).sum()) + 2 * int((ms >= 0).sum())) * 4
-            else:
-                v_per += int((cs >= 0).sum()) * rowb
-                meta += int((cs >= 0).sum()) * 4
-            nv = int(bm[:, :n_cap].sum())
-            k_union += nk * rowb
-            v_union += nv * rowb
+    if x.get("select", 0) == 1:  # lists per (large layer, kv head): the union is the list
+        rows = torch.arange(L * hk, device=dev)[:, None].expand(L * hk, g).reshape(-1)
+    else:  # each query head's lists are its small head's
+        rows = x["head_map"].to(torch.int64).to(dev)
+    cs = crit_idx.to(dev)[:, rows].view(B, L, hk, -1)           # [B][L][hk][g*kc]
+    n_c = int((cs >= 0).sum())
+    bm = torch.zeros((B, L, hk, n_cap + 1), dtype=torch.bool, device=dev)
+    bm.scatter_(3, torch.where(cs >= 0, cs, n_cap).to(torch.int64), True)
+    del cs
+    k_union = int(bm[..., :n_cap].sum()) * rowb
+    n_m = 0
+    if km_cap:
+        ms = marg_idx[..., :km_cap].to(dev)[:, rows].view(B, L, hk, -1)
+        n_m = int((ms >= 0).sum())
+        bm.scatter_(3, torch.where(ms >= 0, ms, n_cap).to(torch.int64), True)
+        del ms
+    v_union = int(bm[..., :n_cap].sum()) * rowb
+    k_per = n_c * rowb
+    v_per = (n_c + n_m) * rowb
+    meta = (n_c + 2 * n_m) * 4
     return StepBytes(small_kv, small_qo, logits, part_out, k_union, v_union, k_per, v_per,
                      large_qo, meta)

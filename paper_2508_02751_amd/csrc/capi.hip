@@ -101,15 +101,38 @@ StepLayout step_layout(const smallkv_batch_t &b, const smallkv_model_t &small,
 }
 
 // Stage 3: the grouped kernel where it applies, the per-head kernel otherwise.
+// Layers [layer0, layer0 + nl) of l (all of them by default).
 hipError_t launch_stage3(const smallkv_batch_t &b, const smallkv_model_t &l, const int32_t *head_map,
                          int nsh, const int32_t *crit, const int32_t *marg, const float *marg_prob,
                          const float *mass, int mode, void *ws, const int2 *tab, bool group_sel,
-                         hipStream_t st) {
-  const GroupPlan gp = plan_group(b, l, nsh);
+                         hipStream_t st, int layer0 = 0, int nl = -1) {
+  if (nl < 0) nl = l.n_layers;
+  const GroupPlan gp = plan_group(b, l, nsh, nl);
   if (gp.use)
     return launch_hybrid_group(b, l, head_map, nsh, crit, marg, marg_prob, mass, mode, gp,
-                               static_cast<float *>(ws), tab, group_sel, st);
-  return launch_hybrid(b, l, head_map, nsh, crit, marg, marg_prob, mass, mode, group_sel, st);
+                               static_cast<float *>(ws), tab, group_sel, layer0, nl, st);
+  return launch_hybrid(b, l, head_map, nsh, crit, marg, marg_prob, mass, mode, group_sel, layer0,
+                       nl, st);
+}
+
+// Host checks of a stage-3 call (whole stack or a layer range).
+int check_stage3(const smallkv_batch_t *batch, const smallkv_model_t *large,
+                 const int32_t *head_map, int32_t n_small_heads, const int32_t *crit_idx,
+                 const int32_t *marg_idx, const float *marg_prob, const float *mass, int32_t mode,
+                 int32_t select) {
+  int rc = check_large(batch, large, head_map, n_small_heads);
+  if (rc) return rc;
+  if ((rc = check_mode(mode))) return rc;
+  if (select != SMALLKV_SELECT_HEAD && select != SMALLKV_SELECT_GROUP) return SMALLKV_EINVAL;
+  if (!crit_idx || !mass) return SMALLKV_EINVAL;
+  if (batch->km_cap > 0 && (!marg_idx || !marg_prob)) return SMALLKV_EINVAL;
+  return SMALLKV_OK;
+}
+
+// Workspace of a stage-3 call over `nl` layers.
+size_t stage3_workspace(const smallkv_batch_t &b, const smallkv_model_t &l, int nsh, int nl) {
+  const GroupPlan gp = plan_group(b, l, nsh, nl);
+  return gp.use ? gp.ws_bytes : 0;
 }
 
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
@@ -186,7 +209,8 @@ int device_view(const void *p, const void **out) {
 }
 
 int check_step(const smallkv_step_t *s);
-int run_step(const smallkv_step_t *s, void *ws, size_t ws_bytes, void *stream);
+int run_step(const smallkv_step_t *s, void *ws, size_t ws_bytes, void *stream,
+             void *const *events);
 
 }  // namespace
 
@@ -303,18 +327,39 @@ int smallkv_hybrid_attn(const smallkv_batch_t *batch, const smallkv_model_t *lar
                         const int32_t *head_map, int32_t n_small_heads, const int32_t *crit_idx,
                         const int32_t *marg_idx, const float *marg_prob, const float *mass,
                         int32_t mode, int32_t select, void *ws, size_t ws_bytes, void *stream) {
-  int rc = check_large(batch, large, head_map, n_small_heads);
+  if (!large) return SMALLKV_EINVAL;
+  return smallkv_hybrid_attn_layers(batch, large, 0, large->n_layers, head_map, n_small_heads,
+                                    crit_idx, marg_idx, marg_prob, mass, mode, select, ws,
+                                    ws_bytes, stream);
+}
+
+int smallkv_hybrid_attn_workspace_size(const smallkv_batch_t *batch,
+                                       const smallkv_model_t *large, int32_t layer_count,
+                                       int32_t n_small_heads, size_t *bytes) {
+  if (!bytes || !batch || !large) return SMALLKV_EINVAL;
+  if (!batch_ok(batch) || !model_ok(large) || n_small_heads < 1) return SMALLKV_EINVAL;
+  if (layer_count < 1 || layer_count > large->n_layers) return SMALLKV_EINVAL;
+  *bytes = stage3_workspace(*batch, *large, n_small_heads, layer_count);
+  return SMALLKV_OK;
+}
+
+int smallkv_hybrid_attn_layers(const smallkv_batch_t *batch, const smallkv_model_t *large,
+                               int32_t layer_begin, int32_t layer_count, const int32_t *head_map,
+                               int32_t n_small_heads, const int32_t *crit_idx,
+                               const int32_t *marg_idx, const float *marg_prob,
+                               const float *mass, int32_t mode, int32_t select, void *ws,
+                               size_t ws_bytes, void *stream) {
+  const int rc = check_stage3(batch, large, head_map, n_small_heads, crit_idx, marg_idx,
+                              marg_prob, mass, mode, select);
   if (rc) return rc;
-  if ((rc = check_mode(mode))) return rc;
-  if (select != SMALLKV_SELECT_HEAD && select != SMALLKV_SELECT_GROUP) return SMALLKV_EINVAL;
-  if (!crit_idx || !mass) return SMALLKV_EINVAL;
-  if (batch->km_cap > 0 && (!marg_idx || !marg_prob)) return SMALLKV_EINVAL;
-  const GroupPlan gp = plan_group(*batch, *large, n_small_heads);
-  if (gp.use && gp.ws_bytes && (!ws || ws_bytes < gp.ws_bytes)) return SMALLKV_EWORKSPACE;
+  if (layer_begin < 0 || layer_count < 1 || layer_begin > large->n_layers - layer_count)
+    return SMALLKV_EINVAL;
+  const size_t need = stage3_workspace(*batch, *large, n_small_heads, layer_count);
+  if (need && (!ws || ws_bytes < need)) return SMALLKV_EWORKSPACE;
   return status_of(launch_stage3(*batch, *large, head_map, n_small_heads, crit_idx, marg_idx,
                                  marg_prob, mass, mode, ws, nullptr,
                                  select == SMALLKV_SELECT_GROUP,
-                                 static_cast<hipStream_t>(stream)));
+                                 static_cast<hipStream_t>(stream), layer_begin, layer_count));
 }
 
 int smallkv_accum_select_workspace_size(const smallkv_batch_t *batch,
@@ -406,7 +451,12 @@ int smallkv_match(const smallkv_match_t *m, void *ws, size_t ws_bytes, void *str
 }
 
 int smallkv_step(const smallkv_step_t *s, void *ws, size_t ws_bytes, void *stream) {
-  return run_step(s, ws, ws_bytes, stream);
+  return run_step(s, ws, ws_bytes, stream, nullptr);
+}
+
+int smallkv_step_events(const smallkv_step_t *s, void *ws, size_t ws_bytes, void *stream,
+                        void *const *events) {
+  return run_step(s, ws, ws_bytes, stream, events);
 }
 
 int smallkv_step_noalloc(const smallkv_step_t *s, void *stream) {
@@ -417,7 +467,7 @@ int smallkv_step_noalloc(const smallkv_step_t *s, void *stream) {
   if (need > SMALLKV_NOALLOC_SCRATCH_BYTES) return SMALLKV_EWORKSPACE;
   void *ws = nullptr;
   if ((rc = device_scratch(static_cast<hipStream_t>(stream), &ws))) return rc;
-  return run_step(s, ws, SMALLKV_NOALLOC_SCRATCH_BYTES, stream);
+  return run_step(s, ws, SMALLKV_NOALLOC_SCRATCH_BYTES, stream, nullptr);
 }
 
 }  // extern "C"
@@ -443,7 +493,11 @@ int check_step(const smallkv_step_t *s) {
   return SMALLKV_OK;
 }
 
-int run_step(const smallkv_step_t *s, void *ws, size_t ws_bytes, void *stream) {
+// events (optional, entries may be null): recorded on the stream before
+// stage 1, after stage 1's chunk kernel (after its merge too with group or
+// accumulated selection), after stage 2 and after stage 3.
+int run_step(const smallkv_step_t *s, void *ws, size_t ws_bytes, void *stream,
+             void *const *events) {
   const int rc = check_step(s);
   if (rc) return rc;
   const int nsh = s->small.n_layers * s->small.n_q_heads;
@@ -454,44 +508,46 @@ int run_step(const smallkv_step_t *s, void *ws, size_t ws_bytes, void *stream) {
   const StepLayout lay = step_layout(s->batch, s->small, s->large, nsh, s->select);
   if (lay.total && (!ws || ws_bytes < lay.total)) return SMALLKV_EWORKSPACE;
   hipStream_t st = static_cast<hipStream_t>(stream);
-  if (accum) {
-    // stage 1 with its own merge, the accumulated scores and their
-    // partition, stage 3 as for per-head selection
-    hipError_t e = launch_small_attn(sb, s->small, s->logits, s->row_max, s->row_sum,
-                                     static_cast<float *>(ws), p, st);
-    if (e != hipSuccess) return SMALLKV_EDEVICE;
-    e = launch_accum_select(s->batch, s->small, s->logits, s->row_max, s->row_sum, s->acc_score,
-                            s->crit_idx, s->marg_idx, s->marg_prob, s->mass, ws,
-                            group_layout(s->batch, s->small, s->large, 0, true), st);
-    if (e != hipSuccess) return SMALLKV_EDEVICE;
-    return status_of(launch_stage3(s->batch, s->large, s->head_map, nsh, s->crit_idx, s->marg_idx,
-                                   s->marg_prob, s->mass, s->mode, ws, nullptr, false, st));
-  }
-  if (group) {
-    // stage 1 with its own merge, the group selection, stage 3 on its sets
-    hipError_t e = launch_small_attn(sb, s->small, s->logits, s->row_max, s->row_sum,
-                                     static_cast<float *>(ws), p, st);
-    if (e != hipSuccess) return SMALLKV_EDEVICE;
-    e = launch_group_select(s->batch, s->small, s->large, s->head_map, s->logits, s->row_max,
-                            s->row_sum, s->crit_idx, s->marg_idx, s->marg_prob, s->mass, ws,
-                            group_layout(s->batch, s->small, s->large, 0), st);
-    if (e != hipSuccess) return SMALLKV_EDEVICE;
-    return status_of(launch_stage3(s->batch, s->large, s->head_map, nsh, s->crit_idx, s->marg_idx,
-                                   s->marg_prob, s->mass, s->mode, ws, nullptr, true, st));
+  auto mark = [&](int i) {
+    return events && events[i] ? hipEventRecord(static_cast<hipEvent_t>(events[i]), st)
+                               : hipSuccess;
+  };
+  if (mark(0) != hipSuccess) return SMALLKV_EDEVICE;
+  hipError_t e;
+  if (accum || group) {
+    // stage 1 with its own merge, the selection (accumulated scores and
+    // their partition, or the group sets), stage 3 on its lists
+    e = launch_small_attn(sb, s->small, s->logits, s->row_max, s->row_sum,
+                          static_cast<float *>(ws), p, st);
+    if (e != hipSuccess || mark(1) != hipSuccess) return SMALLKV_EDEVICE;
+    if (accum)
+      e = launch_accum_select(s->batch, s->small, s->logits, s->row_max, s->row_sum,
+                              s->acc_score, s->crit_idx, s->marg_idx, s->marg_prob, s->mass, ws,
+                              group_layout(s->batch, s->small, s->large, 0, true), st);
+    else
+      e = launch_group_select(s->batch, s->small, s->large, s->head_map, s->logits, s->row_max,
+                              s->row_sum, s->crit_idx, s->marg_idx, s->marg_prob, s->mass, ws,
+                              group_layout(s->batch, s->small, s->large, 0), st);
+    if (e != hipSuccess || mark(2) != hipSuccess) return SMALLKV_EDEVICE;
+    e = launch_stage3(s->batch, s->large, s->head_map, nsh, s->crit_idx, s->marg_idx,
+                      s->marg_prob, s->mass, s->mode, ws, nullptr, group, st);
+    if (e != hipSuccess || mark(3) != hipSuccess) return SMALLKV_EDEVICE;
+    return SMALLKV_OK;
   }
   int2 *tab = lay.tab_bytes ? reinterpret_cast<int2 *>(static_cast<char *>(ws) + lay.tab_offset)
                             : nullptr;
-  hipError_t e = launch_small_split(sb, s->small, s->logits, static_cast<float *>(ws), p, st);
-  if (e != hipSuccess) return SMALLKV_EDEVICE;
+  e = launch_small_split(sb, s->small, s->logits, static_cast<float *>(ws), p, st);
+  if (e != hipSuccess || mark(1) != hipSuccess) return SMALLKV_EDEVICE;
   e = launch_merge_partition(sb, s->small, p, static_cast<const float *>(ws), s->logits,
                              s->row_max, s->row_sum, s->crit_idx, s->marg_idx, s->marg_prob,
                              s->mass, tab, s->batch.seq_len, s->batch.n_cap, st);
-  if (e != hipSuccess) return SMALLKV_EDEVICE;
+  if (e != hipSuccess || mark(2) != hipSuccess) return SMALLKV_EDEVICE;
   // stage 1's records are consumed by now: stage 3 reuses the workspace
   // below the list offsets
   e = launch_stage3(s->batch, s->large, s->head_map, nsh, s->crit_idx, s->marg_idx, s->marg_prob,
                     s->mass, s->mode, ws, tab, false, st);
-  return status_of(e);
+  if (e != hipSuccess || mark(3) != hipSuccess) return SMALLKV_EDEVICE;
+  return SMALLKV_OK;
 }
 
 }  // namespace

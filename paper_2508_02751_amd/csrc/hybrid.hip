@@ -28,6 +28,7 @@ constexpr int kXcd = 8;
 
 struct HybArgs {
   int n_cap, layers, hq, hkv, g, nsh, kc_cap, km_cap, mode, units;
+  int layer0, nl;  // the large layers this launch runs: [layer0, layer0 + nl) of `layers`
   int64_t n_rows;
   float scale;
   const int32_t *seq_len, *k_crit, *k_marg, *k_recent, *head_map;
@@ -101,12 +102,14 @@ __global__ __launch_bounds__(kHT) void hybrid_kernel(HybArgs a) {
   const int rest = x / kXcd;
   const int u = (rest / a.g) * kXcd + x % kXcd, hh = rest % a.g;
   if (u >= a.units) return;
-  const int kvh = u % a.hkv, bl = u / a.hkv, layer = bl % a.layers, b = bl / a.layers;
+  const int kvh = u % a.hkv, bl = u / a.hkv, layer = a.layer0 + bl % a.nl, b = bl / a.nl;
+  // the (sequence, layer, kv head) in the whole stack's layout
+  const int64_t ua = ((int64_t)b * a.layers + layer) * a.hkv + kvh;
   const int h = kvh * a.g + hh;
   const int j = clampi(a.head_map[layer * a.hq + h], 0, a.nsh - 1);
   const int64_t qrow = ((int64_t)b * a.layers + layer) * a.hq + h;
   // lists of the small head f(i), or of the group; weights of f(i), or of the head
-  const int64_t lrow = a.group_sel ? (int64_t)u : (int64_t)b * a.nsh + j;
+  const int64_t lrow = a.group_sel ? ua : (int64_t)b * a.nsh + j;
   const int64_t row = a.group_sel ? qrow : lrow;
   const Sizes sz = set_sizes(a.seq_len, a.k_crit, a.k_marg, a.k_recent, b, a.n_cap, a.kc_cap, a.km_cap);
   const int nc = sz.nc, nm = sz.nm, ntot = sz.nc + sz.nm;
@@ -119,10 +122,10 @@ __global__ __launch_bounds__(kHT) void hybrid_kernel(HybArgs a) {
                                                    (qrow * D + sub * EPL) * (int64_t)sizeof(T)),
                   qv);
   const int64_t rowb = D * (int64_t)sizeof(T);
-  const unsigned char *kb = reinterpret_cast<const unsigned char *>(a.k) + (int64_t)u * a.n_rows * rowb + sub * 16;
-  const unsigned char *vb = reinterpret_cast<const unsigned char *>(a.v) + (int64_t)u * a.n_rows * rowb + sub * 16;
-  const int32_t *ks = a.k_slot ? a.k_slot + (int64_t)u * a.n_cap : nullptr;
-  const int32_t *vs = a.v_slot ? a.v_slot + (int64_t)u * a.n_cap : nullptr;
+  const unsigned char *kb = reinterpret_cast<const unsigned char *>(a.k) + ua * a.n_rows * rowb + sub * 16;
+  const unsigned char *vb = reinterpret_cast<const unsigned char *>(a.v) + ua * a.n_rows * rowb + sub * 16;
+  const int32_t *ks = a.k_slot ? a.k_slot + ua * a.n_cap : nullptr;
+  const int32_t *vs = a.v_slot ? a.v_slot + ua * a.n_cap : nullptr;
   const int last_row = (int)(a.n_rows - 1);
 
   // ---- phase 1: critical logits -----------------------------------------
@@ -238,8 +241,10 @@ __global__ __launch_bounds__(kHT) void hybrid_kernel(HybArgs a) {
 hipError_t launch_hybrid(const smallkv_batch_t &b, const smallkv_model_t &m,
                          const int32_t *head_map, int n_small_heads, const int32_t *crit,
                          const int32_t *marg, const float *marg_prob, const float *mass,
-                         int mode, bool group_sel, hipStream_t st) {
+                         int mode, bool group_sel, int layer0, int nl, hipStream_t st) {
   HybArgs a;
+  a.layer0 = layer0;
+  a.nl = nl;
   a.group_sel = group_sel ? 1 : 0;
   a.n_cap = b.n_cap;
   a.layers = m.n_layers;
@@ -250,7 +255,7 @@ hipError_t launch_hybrid(const smallkv_batch_t &b, const smallkv_model_t &m,
   a.kc_cap = b.kc_cap;
   a.km_cap = b.km_cap;
   a.mode = mode;
-  a.units = b.batch * m.n_layers * m.n_kv_heads;
+  a.units = b.batch * nl * m.n_kv_heads;
   a.n_rows = m.n_rows;
   a.scale = m.scale;
   a.seq_len = b.seq_len;

@@ -67,6 +67,7 @@ constexpr int64_t kMaxBuf = 0x7fffffff;
 
 struct GroupArgs {
   int n_cap, layers, hq, hkv, g, nsh, kc_cap, km_cap, mode, units, n_split, span;
+  int layer0, nl;  // the large layers this launch runs: [layer0, layer0 + nl) of `layers`
   int mp_bytes;  // size of marg_prob in bytes (< 2^31)
   int64_t n_rows;
   float scale;
@@ -242,7 +243,9 @@ __global__ __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2))) void h
   const int rest = x / kXcd;
   const int u = (rest / a.n_split) * kXcd + x % kXcd, sp = rest % a.n_split;
   if (u >= a.units) return;
-  const int kvh = u % a.hkv, bl = u / a.hkv, layer = bl % a.layers, b = bl / a.layers;
+  const int kvh = u % a.hkv, bl = u / a.hkv, layer = a.layer0 + bl % a.nl, b = bl / a.nl;
+  // the (sequence, layer, kv head) in the whole stack's layout
+  const int64_t ua = ((int64_t)b * a.layers + layer) * a.hkv + kvh;
   const Sizes sz = set_sizes(a.seq_len, a.k_crit, a.k_marg, a.k_recent, b, a.n_cap, a.kc_cap, a.km_cap);
   const int t_begin = sp * a.span;
   if (t_begin >= sz.n) return;
@@ -255,7 +258,7 @@ __global__ __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2))) void h
     const int j = clampi(a.head_map[layer * a.hq + kvh * g + tid], 0, a.nsh - 1);
     const int64_t row = (int64_t)b * a.nsh + j;
     const int64_t qrow = ((int64_t)b * a.layers + layer) * a.hq + (int64_t)kvh * g + tid;
-    sh.hrow[tid] = a.group_sel ? (int64_t)u : row;
+    sh.hrow[tid] = a.group_sel ? ua : row;
     const int64_t prow = a.group_sel ? qrow : row;
     sh.prow[tid] = prow;
     float ac, am;
@@ -308,13 +311,13 @@ __global__ __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2))) void h
                     : make_uint4(0u, 0u, 0u, 0u);
 
   const int64_t rowb = kRowB;
-  const unsigned char *kb = reinterpret_cast<const unsigned char *>(a.k) + (int64_t)u * a.n_rows * rowb;
-  const unsigned char *vb = reinterpret_cast<const unsigned char *>(a.v) + (int64_t)u * a.n_rows * rowb;
+  const unsigned char *kb = reinterpret_cast<const unsigned char *>(a.k) + ua * a.n_rows * rowb;
+  const unsigned char *vb = reinterpret_cast<const unsigned char *>(a.v) + ua * a.n_rows * rowb;
   const __amdgpu_buffer_rsrc_t kbuf = buffer_of(kb, (int)(a.n_rows * rowb));
   const __amdgpu_buffer_rsrc_t vbuf = buffer_of(vb, (int)(a.n_rows * rowb));
   const __amdgpu_buffer_rsrc_t mbuf = buffer_of(a.marg_prob, a.mp_bytes);
-  const int32_t *ksl = a.k_slot ? a.k_slot + (int64_t)u * a.n_cap : nullptr;
-  const int32_t *vsl = a.v_slot ? a.v_slot + (int64_t)u * a.n_cap : nullptr;
+  const int32_t *ksl = a.k_slot ? a.k_slot + ua * a.n_cap : nullptr;
+  const int32_t *vsl = a.v_slot ? a.v_slot + ua * a.n_cap : nullptr;
   const int last_row = (int)(a.n_rows - 1);
 
   f32x4_t acc[kD / 16];
@@ -677,7 +680,7 @@ __global__ __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2))) void h
 // One workgroup per query head, one thread per dim.
 __global__ __launch_bounds__(kD) void hybrid_group_merge(GroupArgs a) {
   const int u = blockIdx.x / a.g, h = blockIdx.x % a.g, d = threadIdx.x;
-  const int kvh = u % a.hkv, bl = u / a.hkv, layer = bl % a.layers, b = bl / a.layers;
+  const int kvh = u % a.hkv, bl = u / a.hkv, layer = a.layer0 + bl % a.nl, b = bl / a.nl;
   const int n = clampi(a.seq_len[b], 1, a.n_cap);
   const int ns = min(a.n_split, (n + a.span - 1) / a.span);
   const int g = a.g;
@@ -704,15 +707,17 @@ __global__ __launch_bounds__(kD) void hybrid_group_merge(GroupArgs a) {
 
 }  // namespace
 
-GroupPlan plan_group(const smallkv_batch_t &b, const smallkv_model_t &m, int n_small_heads) {
+GroupPlan plan_group(const smallkv_batch_t &b, const smallkv_model_t &m, int n_small_heads,
+                     int n_run) {
   GroupPlan p{};
+  if (n_run < 0) n_run = m.n_layers;
   const int g = m.n_q_heads / m.n_kv_heads;
   p.use = m.dtype == SMALLKV_BF16 && m.head_dim == kD && g <= kMaxG &&
           m.n_rows * kRowB <= kMaxBuf &&
           (int64_t)b.batch * std::max<int64_t>(n_small_heads, (int64_t)m.n_layers * m.n_q_heads) *
                   b.km_cap * (int64_t)sizeof(float) <= kMaxBuf;  // marg_prob of either selection
   if (!p.use) return p;
-  const int64_t units = (int64_t)b.batch * m.n_layers * m.n_kv_heads;
+  const int64_t units = (int64_t)b.batch * n_run * m.n_kv_heads;
   // splits per kv head: the fewest token-equivalents on the critical path,
   // rounds of resident workgroups (a partial last round costs a whole one) x
   // (span + the fixed per-workgroup setup); ties go to fewer splits
@@ -733,8 +738,10 @@ hipError_t launch_hybrid_group(const smallkv_batch_t &b, const smallkv_model_t &
                                const int32_t *head_map, int n_small_heads, const int32_t *crit,
                                const int32_t *marg, const float *marg_prob, const float *mass,
                                int mode, const GroupPlan &p, float *ws, const int2 *tab,
-                               bool group_sel, hipStream_t st) {
+                               bool group_sel, int layer0, int nl, hipStream_t st) {
   GroupArgs a;
+  a.layer0 = layer0;
+  a.nl = nl;
   a.n_cap = b.n_cap;
   a.layers = m.n_layers;
   a.hq = m.n_q_heads;
@@ -744,7 +751,7 @@ hipError_t launch_hybrid_group(const smallkv_batch_t &b, const smallkv_model_t &
   a.kc_cap = b.kc_cap;
   a.km_cap = b.km_cap;
   a.mode = mode;
-  a.units = b.batch * m.n_layers * m.n_kv_heads;
+  a.units = b.batch * nl * m.n_kv_heads;
   a.n_split = p.n_split;
   a.span = p.span;
   const int64_t prows = group_sel ? (int64_t)m.n_layers * m.n_q_heads : n_small_heads;

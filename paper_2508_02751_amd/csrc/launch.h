@@ -68,17 +68,20 @@ struct GroupPlan {
   size_t ws_bytes;
 };
 
-GroupPlan plan_group(const smallkv_batch_t &b, const smallkv_model_t &m, int n_small_heads);
+// n_run: the large layers one launch runs (-1: all of m's)
+GroupPlan plan_group(const smallkv_batch_t &b, const smallkv_model_t &m, int n_small_heads,
+                     int n_run = -1);
 
 // tab: the partition's list offsets, or null; with them the list cursors at
-// the start of each token range are read instead of searched.  group_sel:
+// the start of each token range are read instead of searched.  Layers
+// [layer0, layer0 + nl) of m run (m describes the whole stack).  group_sel:
 // the lists are per (sequence, layer, kv head) and marg_prob / mass per
 // large query head (group selection); otherwise all are per small head f(i).
 hipError_t launch_hybrid_group(const smallkv_batch_t &b, const smallkv_model_t &m,
                                const int32_t *head_map, int n_small_heads, const int32_t *crit,
                                const int32_t *marg, const float *marg_prob, const float *mass,
                                int mode, const GroupPlan &p, float *ws, const int2 *tab,
-                               bool group_sel, hipStream_t st);
+                               bool group_sel, int layer0, int nl, hipStream_t st);
 
 // Group selection (the query heads of a kv head share one selection):
 // workspace offsets of its intermediates, placed from `offset` on.
@@ -127,6 +130,6 @@ hipError_t launch_match(const smallkv_match_t &m, void *ws, hipStream_t st);
 hipError_t launch_hybrid(const smallkv_batch_t &b, const smallkv_model_t &m,
                          const int32_t *head_map, int n_small_heads, const int32_t *crit,
                          const int32_t *marg, const float *marg_prob, const float *mass,
-                         int mode, bool group_sel, hipStream_t st);
+                         int mode, bool group_sel, int layer0, int nl, hipStream_t st);
 
 }  // namespace smallkv

@@ -2,7 +2,10 @@
 
   python -m paper_2508_02751_amd.profiling stats DIR [--title T] [--cmd C]
       per-kernel call count and average / min / max duration from a
-      `rocprofv3 --kernel-trace --stats --output-format csv` run.
+      `rocprofv3 --kernel-trace --stats --output-format csv` run, one row
+      per kernel and launch grid (workgroups), from the per-dispatch trace:
+      a run that launches one kernel over different grids (the whole-stack
+      step and its per-layer variant) keeps them apart.
 
   python -m paper_2508_02751_amd.profiling traffic FETCH_DIR WRITE_DIR --copy-mib N --workload W
       HBM bytes per dispatch of each library kernel from two `--pmc` runs
@@ -71,16 +74,23 @@ def _one(pattern: str) -> str:
 
 
 def stats(d: str, title: str, cmd: str) -> str:
-    rows = list(csv.DictReader(open(_one(os.path.join(d, "**", "*kernel_stats.csv")))))
-    out = [f"# {title}", "", f"command: `{cmd}`", "",
-           "| kernel | calls | avg us | min us | max us | share of GPU time |",
-           "|---|---|---|---|---|---|"]
+    rows = list(csv.DictReader(open(_one(os.path.join(d, "**", "*kernel_trace.csv")))))
+    per = collections.defaultdict(list)
+    total = 0.0
     for r in rows:
-        if "smallkv" not in r["Name"]:
+        ns = float(r["End_Timestamp"]) - float(r["Start_Timestamp"])
+        total += ns
+        if "smallkv" not in r["Kernel_Name"]:
             continue
-        out.append(f"| {short_name(r['Name'])} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.1f} | "
-                   f"{float(r['MinNs']) / 1e3:.1f} | {float(r['MaxNs']) / 1e3:.1f} | "
-                   f"{float(r['Percentage']):.1f}% |")
+        wgs = int(r["Grid_Size_X"]) // max(1, int(r["Workgroup_Size_X"]))
+        per[(short_name(r["Kernel_Name"]), wgs)].append(ns)
+    out = [f"# {title}", "", f"command: `{cmd}`", "",
+           "| kernel | workgroups | calls | avg us | min us | max us | share of GPU time |",
+           "|---|---|---|---|---|---|---|"]
+    for (k, wgs), v in sorted(per.items(), key=lambda kv: -sum(kv[1])):
+        out.append(f"| {k} | {wgs} | {len(v)} | {sum(v) / len(v) / 1e3:.1f} | "
+                   f"{min(v) / 1e3:.1f} | {max(v) / 1e3:.1f} | "
+                   f"{100 * sum(v) / max(total, 1.0):.1f}% |")
     return "\n".join(out) + "\n"
 
 

@@ -75,7 +75,8 @@ class Store(C.Structure):
 
 
 EXPORTS = ("smallkv_small_attn", "smallkv_partition", "smallkv_hybrid_attn", "smallkv_step",
-           "smallkv_step_noalloc", "smallkv_workspace_size", "smallkv_match", "smallkv_match_workspace_size",
+           "smallkv_step_noalloc", "smallkv_step_events", "smallkv_hybrid_attn_layers",
+           "smallkv_hybrid_attn_workspace_size", "smallkv_workspace_size", "smallkv_match", "smallkv_match_workspace_size",
            "smallkv_group_select", "smallkv_group_select_workspace_size",
            "smallkv_accum_select", "smallkv_accum_select_workspace_size",
            "smallkv_store_update", "smallkv_store_workspace_size",
@@ -115,6 +116,14 @@ def lib():
         L.smallkv_store_workspace_size.argtypes = [P(Store), P(C.c_size_t)]
         L.smallkv_step.argtypes = [P(Step), C.c_void_p, C.c_size_t, C.c_void_p]
         L.smallkv_step_noalloc.argtypes = [P(Step), C.c_void_p]
+        L.smallkv_step_events.argtypes = [P(Step), C.c_void_p, C.c_size_t, C.c_void_p,
+                                          P(C.c_void_p)]
+        L.smallkv_hybrid_attn_layers.argtypes = [P(Batch), P(Model), C.c_int32, C.c_int32,
+                                                 C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p,
+                                                 C.c_void_p, C.c_void_p, C.c_int32, C.c_int32,
+                                                 C.c_void_p, C.c_size_t, C.c_void_p]
+        L.smallkv_hybrid_attn_workspace_size.argtypes = [P(Batch), P(Model), C.c_int32,
+                                                         C.c_int32, P(C.c_size_t)]
         L.smallkv_workspace_size.argtypes = [P(Step), P(C.c_size_t)]
         L.smallkv_match.argtypes = [P(Match), C.c_void_p, C.c_size_t, C.c_void_p]
         L.smallkv_match_workspace_size.argtypes = [P(Match), P(C.c_size_t)]
@@ -122,7 +131,9 @@ def lib():
         L.smallkv_status_string.restype = C.c_char_p
         L.smallkv_abi_version.argtypes = []
         for f in ("smallkv_small_attn", "smallkv_partition", "smallkv_hybrid_attn",
-                  "smallkv_step", "smallkv_step_noalloc", "smallkv_workspace_size", "smallkv_abi_version",
+                  "smallkv_step", "smallkv_step_noalloc", "smallkv_step_events",
+                  "smallkv_hybrid_attn_layers", "smallkv_hybrid_attn_workspace_size",
+                  "smallkv_workspace_size", "smallkv_abi_version",
                   "smallkv_match", "smallkv_match_workspace_size", "smallkv_group_select",
                   "smallkv_group_select_workspace_size", "smallkv_accum_select",
                   "smallkv_accum_select_workspace_size", "smallkv_store_update",
@@ -270,6 +281,28 @@ def smallkv_hybrid_attn(batch: BatchSpec, large: ModelSpec, head_map, n_small_he
         _ptr(marg_prob), _ptr(mass), int(mode), int(select), w, wb, _stream(stream)))
 
 
+def smallkv_hybrid_attn_layers(batch: BatchSpec, large: ModelSpec, layer_begin: int,
+                               layer_count: int, head_map, n_small_heads: int, crit_idx,
+                               marg_idx, marg_prob, mass, mode=NORM_REMAINING, ws=None,
+                               stream=None, select: int = SELECT_HEAD):
+    """Stage 3 over large layers [layer_begin, layer_begin + layer_count) only."""
+    b, m = batch.c(), large.c()
+    w, wb = _ws(ws)
+    _check("smallkv_hybrid_attn_layers", lib().smallkv_hybrid_attn_layers(
+        C.byref(b), C.byref(m), int(layer_begin), int(layer_count), _ptr(head_map),
+        n_small_heads, _ptr(crit_idx), _ptr(marg_idx), _ptr(marg_prob), _ptr(mass), int(mode),
+        int(select), w, wb, _stream(stream)))
+
+
+def smallkv_hybrid_attn_workspace_size(batch: BatchSpec, large: ModelSpec, layer_count: int,
+                                       n_small_heads: int) -> int:
+    b, m = batch.c(), large.c()
+    n = C.c_size_t()
+    _check("smallkv_hybrid_attn_workspace_size", lib().smallkv_hybrid_attn_workspace_size(
+        C.byref(b), C.byref(m), int(layer_count), int(n_small_heads), C.byref(n)))
+    return n.value
+
+
 def smallkv_group_select(batch: BatchSpec, small: ModelSpec, large: ModelSpec, head_map, logits,
                          row_max, row_sum, crit_idx, marg_idx, marg_prob, mass, ws, stream=None):
     """Stage 2 of group selection (lists per large kv head, weights per large head)."""
@@ -295,6 +328,20 @@ def make_step(batch: BatchSpec, small: ModelSpec, large: ModelSpec, head_map, mo
 def smallkv_step(step: Step, ws=None, stream=None):
     w, wb = _ws(ws)
     _check("smallkv_step", lib().smallkv_step(C.byref(step), w, wb, _stream(stream)))
+
+
+def smallkv_step_events(step: Step, ws, events, stream=None):
+    """smallkv_step recording the given torch.cuda.Event objects (4, or None
+    entries) at the stage boundaries: before stage 1, after stage 1's chunk
+    kernel, after stage 2, after stage 3."""
+    w, wb = _ws(ws)
+    ts = torch.cuda.current_stream() if stream is None else stream
+    for e in events:
+        if e is not None and not e.cuda_event:
+            e.record(ts)  # torch creates its HIP event at the first record
+    arr = (C.c_void_p * 4)(*[None if e is None else e.cuda_event for e in events])
+    _check("smallkv_step_events", lib().smallkv_step_events(C.byref(step), w, wb, _stream(stream),
+                                                            arr))
 
 
 NOALLOC_SCRATCH_BYTES = 32 << 20  # SMALLKV_NOALLOC_SCRATCH_BYTES

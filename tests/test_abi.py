@@ -275,3 +275,24 @@ def test_noalloc_step_checks_before_touching_a_device():
     assert "#define SMALLKV_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)" in text
     assert S.NOALLOC_SCRATCH_BYTES == 32 << 20
 
+
+
+def test_layer_range_and_its_workspace_checked_on_the_host():
+    L = S.lib()
+    b = S.Batch(batch=2, n_cap=512, seq_len=0x1000, k_crit=0x1000, k_marg=0x1000, k_recent=None,
+                kc_cap=64, km_cap=128)
+    lg = S.Model(4, 28, 4, 128, S.BF16, 0.088, 1, 1, 1, 512, None, None, 1)
+    n = C.c_size_t()
+    assert L.smallkv_hybrid_attn_workspace_size(C.byref(b), C.byref(lg), 1, 14, C.byref(n)) == 0
+    one = n.value
+    assert L.smallkv_hybrid_attn_workspace_size(C.byref(b), C.byref(lg), 4, 14, C.byref(n)) == 0
+    assert one > 0 and n.value > 0
+    for bad in (0, 5):
+        assert L.smallkv_hybrid_attn_workspace_size(C.byref(b), C.byref(lg), bad, 14,
+                                                    C.byref(n)) == S.EINVAL
+    for l0, cnt in ((-1, 1), (3, 2), (0, 0), (4, 1)):
+        assert L.smallkv_hybrid_attn_layers(C.byref(b), C.byref(lg), l0, cnt, 1, 14, 1, 1, 1, 1,
+                                            0, 0, C.c_void_p(0x1000), 1 << 30, None) == S.EINVAL
+    # a workspace below the layer call's own size
+    assert L.smallkv_hybrid_attn_layers(C.byref(b), C.byref(lg), 0, 1, 1, 14, 1, 1, 1, 1, 0, 0,
+                                        C.c_void_p(0x1000), one - 1, None) == S.EWORKSPACE

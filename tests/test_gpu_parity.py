@@ -520,3 +520,99 @@ def test_accumulated_single_stage_calls_match_step():
     for got, want in ((acc, b.acc_score), (ci, b.crit_idx), (mi, b.marg_idx), (mp, b.marg_prob),
                       (ms, b.mass), (large.out, b.large_out)):
         assert torch.equal(got, want)
+
+
+# ------------------------------------------- per-layer stage 3, step events --
+
+def _layered_stage3(ps, select=S.SELECT_HEAD, per=1):
+    """Stage 3 as a sequential model runs it: one smallkv_hybrid_attn_layers
+    call per `per` large layers, into a fresh output."""
+    b = ps.buf
+    nsh = ps.buf.logits.shape[1]
+    large = S.ModelSpec(ps.large.q, ps.large.k, ps.large.v, torch.empty_like(ps.large.out),
+                        ps.large.scale, ps.large.k_slot, ps.large.v_slot)
+    L = ps.large.q.shape[1]
+    ws = torch.empty(max(1, S.smallkv_hybrid_attn_workspace_size(ps.batch, large, per, nsh)),
+                     dtype=torch.uint8, device=DEV)
+    for l0 in range(0, L, per):
+        S.smallkv_hybrid_attn_layers(ps.batch, large, l0, min(per, L - l0), ps.head_map, nsh,
+                                     b.crit_idx, b.marg_idx, b.marg_prob, b.mass, ps.mode, ws,
+                                     select=select)
+    torch.cuda.synchronize()
+    return large.out
+
+
+def _check_layered(ps, ref, dtype, select=S.SELECT_HEAD, per=1):
+    """Per-layer stage 3 against the oracle (the launch over fewer kv heads
+    may split their tokens into more ranges than the whole-stack launch, so
+    its merge may round differently: the tolerance, not bit equality)."""
+    from parity import TOL, head_err
+    out = _layered_stage3(ps, select=select, per=per)
+    err = head_err(host(out), ref["large_out"])
+    assert err <= TOL[dtype], f"per-layer stage 3 error {err:.3g}"
+    return out
+
+
+@pytest.mark.parametrize("dtype,batch,per", [("bf16", 3, 1), ("bf16", 2, 2), ("f32", 3, 1)])
+def test_per_layer_stage3_matches_the_oracle(dtype, batch, per):
+    """One launch per large layer (grouped bf16 kernel, per-head fp32 kernel;
+    several sequences, so every layer slice is strided) within the
+    tolerance of the oracle; the per-head kernel does not split, so it also
+    equals the whole-stack call bit for bit."""
+    w = custom(f"layers-{dtype}", 121, batch, 1800, dtype, SMALL, LARGE, ("pct", 10),
+               ("pct", 20), ragged_min=600)
+    ps, x, ref = run_case(w)
+    out = _check_layered(ps, ref, w.torch_dtype, per=per)
+    if dtype == "f32":
+        assert torch.equal(out.view(torch.uint8), ps.buf.large_out.view(torch.uint8))
+
+
+def test_per_layer_stage3_qwen2_7b_and_group_selection():
+    ps, x, ref = run_case(W.WORKLOADS[2])
+    _check_layered(ps, ref, torch.bfloat16)
+    w = custom("layers-group", 122, 2, 2500, "bf16", SMALL, LARGE, ("pct", 10), ("pct", 20),
+               select=1)
+    ps, x, ref = run_case(w)
+    _check_layered(ps, ref, torch.bfloat16, select=S.SELECT_GROUP)
+
+
+def test_per_layer_stage3_rejects_ranges_outside_the_stack():
+    w = W.WORKLOADS[1]
+    x = W.make_step_inputs(w, DEV)
+    ps = prepare_step(x)
+    b = ps.buf
+    for l0, n in ((-1, 1), (0, 2), (1, 1), (0, 0)):
+        with pytest.raises(S.SmallKVError) as ei:
+            S.smallkv_hybrid_attn_layers(ps.batch, ps.large, l0, n, ps.head_map,
+                                         b.logits.shape[1], b.crit_idx, b.marg_idx, b.marg_prob,
+                                         b.mass, ps.mode, b.ws)
+        assert ei.value.status == S.EINVAL
+
+
+@pytest.mark.parametrize("select", [0, 1, 2])
+def test_step_events_time_the_step_without_changing_it(select):
+    w = custom(f"events-{select}", 123, 2, 3000, "bf16", SMALL, LARGE, ("pct", 10),
+               ("pct", 20), ragged_min=1000, select=select)
+    x = W.make_step_inputs(w, DEV)
+    ps = prepare_step(x)
+    ps.run()
+    torch.cuda.synchronize()
+    want = {f.name: getattr(ps.buf, f.name).clone() for f in dataclasses.fields(ps.buf)
+            if f.name not in ("ws", "acc_score", "logits") and getattr(ps.buf, f.name) is not None}
+    if select == 2:  # the running scores advance every step: start again from zero
+        ps.buf.acc_score.zero_()
+        ps.run()
+        torch.cuda.synchronize()
+        want = {k: getattr(ps.buf, k).clone() for k in want}
+        ps.buf.acc_score.zero_()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    S.smallkv_step_events(ps.desc, ps.buf.ws, ev)
+    torch.cuda.synchronize()
+    for k, v in want.items():
+        assert torch.equal(v.view(torch.uint8), getattr(ps.buf, k).view(torch.uint8)), k
+    ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(3)]
+    assert all(t > 0 for t in ms), ms
+    # entries may be left out
+    S.smallkv_step_events(ps.desc, ps.buf.ws, [None, ev[1], None, ev[3]])
+    torch.cuda.synchronize()
+    assert ev[1].elapsed_time(ev[3]) > 0
