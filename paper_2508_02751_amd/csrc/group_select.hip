@@ -59,8 +59,6 @@ __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
 constexpr int kZqTok = 8 * kGT;     // tokens per group_zq workgroup (8 per thread)
 constexpr int kScoreTok = 4 * kGT;  // tokens per group_scores workgroup (4 per thread)
 
-// Zeroes the integer sums and the key maxima that the next two kernels
-// accumulate with atomics (a kernel rather than a memset: graph-safe).
 // blockIdx.x: small head row; blockIdx.y: a chunk of kZqTok tokens, whose
 // integer sum it writes (0 past the row's end): integer addition is
 // associative, so the readers' sum of the chunks is the exact sum.  The

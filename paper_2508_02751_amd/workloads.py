@@ -85,7 +85,9 @@ class Workload:
 
     @property
     def n_cap(self) -> int:
-        return self.n_ctx + (self.steps - 1 if self.steps > 1 else 0)
+        # after decode step t a sequence holds its prompt (at most n_ctx
+        # tokens) and t + 1 decoded tokens
+        return self.n_ctx + (self.steps if self.steps > 1 else 0)
 
     @property
     def torch_dtype(self):

@@ -616,3 +616,50 @@ def test_step_events_time_the_step_without_changing_it(select):
     S.smallkv_step_events(ps.desc, ps.buf.ws, [None, ev[1], None, ev[3]])
     torch.cuda.synchronize()
     assert ev[1].elapsed_time(ev[3]) > 0
+
+
+# ----------------------------- selection kernels at every launch width --
+
+def test_accumulated_scores_at_the_qwen2_7b_shapes():
+    """The accumulated-score selection at the Qwen2-7B + Qwen2-0.5B shapes (336
+    rows of up to 8192 tokens: four Z chunks, 512-thread partition rows
+    holding 16 logits per thread, 32 bins per binade) over three drifting
+    steps: running scores, lists and outputs against the oracle."""
+    w = custom("accum-qwen2", 127, 1, 8189, "bf16", W.QWEN2_0_5B, W.QWEN2_7B, ("pct", 10),
+               ("pct", 20), ragged_min=8000, steps=3)
+    assert w.n_cap == 8192
+    ps, acc_ref = None, None
+    for step in range(3):
+        x = W.make_step_inputs(w, DEV, step)
+        x["select"] = S.SELECT_ACCUM
+        if ps is None:
+            ps = prepare_step(x)
+            acc_ref = np.zeros(tuple(ps.buf.acc_score.shape), np.float32)
+        else:
+            ps.with_query(x["s_q"], x["l_q"], x["seq_len"], x["k_crit"], x["k_marg"])
+        log(f"[parity] accumulated scores at the Qwen2 shapes, step {step}")
+        ps.run()
+        torch.cuda.synchronize()
+        ref = O.step(seq_len=host(x["seq_len"]), k_crit=host(x["k_crit"]), k_marg=host(x["k_marg"]),
+                     kc_cap=int(x["kc_cap"]), km_cap=int(x["km_cap"]), head_map=host(x["head_map"]),
+                     mode=O.NORM_REMAINING, s_q=host(x["s_q"]), s_k=host(x["s_k"]), s_v=host(x["s_v"]),
+                     s_scale=0.125, l_q=host(x["l_q"]), l_k=host(x["l_k"]), l_v=host(x["l_v"]),
+                     l_scale=1 / np.sqrt(128.0), select=O.SELECT_ACCUM, acc=acc_ref)
+        compare_step(ps.buf, ref, x, w.torch_dtype, f"accumulated (Qwen2 shapes) step {step}")
+        n = int(host(x["seq_len"])[0])
+        got = host(ps.buf.acc_score)
+        assert np.array_equal(got[0, :, :n].view(np.uint32), acc_ref[0, :, :n].view(np.uint32)), \
+            f"running scores differ at step {step}"
+
+
+@pytest.mark.parametrize("batch,n", [(22, 1500), (22, 9000), (86, 1200), (86, 5200)])
+def test_group_selection_at_every_partition_width(batch, n):
+    """Group rows (sequence, large layer, kv head): 264 rows run 512 threads
+    each, 1032 rows 256 each; the lengths give register rows of 4 and 8
+    logits per thread and the re-reading rows beyond 16 (512 threads) or 20
+    (256 threads) logits per thread."""
+    w = custom(f"gsel-rows{batch}-{n}", 128, batch, n, "bf16", SMALL, LARGE, ("pct", 10),
+               ("pct", 20), ragged_min=n - n // 8, select=1)
+    rows = batch * LARGE.layers * LARGE.kv_heads
+    assert (rows > 256) and ((rows >= 1024) == (batch == 86))
+    run_case(w)

@@ -32,13 +32,31 @@ def capacity(x, g):
     return min(x["l_k"].shape[3], g * (int(x["kc_cap"]) + int(x["km_cap"])))
 
 
+def oracle_lists(x, ps, select):
+    """The oracle's own step on the same inputs: its critical and marginal
+    lists, which must equal the library's (the store's expected rows are
+    built from the oracle's lists, not from the GPU's)."""
+    from parity import oracle_step
+    xs = dict(x)
+    xs["select"] = select
+    ref = oracle_step(xs, 0)
+    crit, marg = ref["crit"], ref["marg"]
+    assert np.array_equal(host(ps.buf.crit_idx)[..., : crit.shape[-1]], crit), "critical lists"
+    if marg.shape[-1]:
+        assert np.array_equal(host(ps.buf.marg_idx)[..., : marg.shape[-1]], marg), "marginal lists"
+    return crit, marg
+
+
 def oracle_store(x, ps, rows, select, old=None):
+    """The oracle's store after this step: from its own lists and, when given,
+    its own previous store `old` (a tuple as this function returns)."""
+    crit, marg = oracle_lists(x, ps, select)
     kw = {}
     if old is not None:
-        kw = dict(old_k=host(old.new_k), old_v=host(old.new_v), old_k_slot=host(old.k_slot),
-                  old_v_slot=host(old.v_slot))
+        kw = dict(old_k=old[0], old_v=old[1], old_k_slot=old[2], old_v_slot=old[3])
     return O.store_update(seq_len=host(x["seq_len"]), head_map=host(x["head_map"]),
-                          crit=host(ps.buf.crit_idx), marg=host(ps.buf.marg_idx),
+                          crit=crit, marg=marg if marg.shape[-1] else np.full(
+                              crit.shape[:-1] + (1,), -1, np.int32),
                           full_k=host(x["l_k"]), full_v=host(x["l_v"]), rows=rows,
                           n_small_heads=ps.buf.logits.shape[1],
                           select=O.SELECT_GROUP if select == 1 else O.SELECT_HEAD, **kw)
@@ -81,8 +99,9 @@ def test_store_from_a_step(select, dtype):
 
 
 def test_store_reuses_the_previous_store_across_steps():
-    """Two drifting steps; the previous store is altered so that the source of
-    every row (old store or full store) shows in the result."""
+    """Two drifting steps; the previous store (the library's and, separately,
+    the oracle's) is altered so that the source of every row (old store or
+    full store) shows in the result."""
     S, W, prepare_step = modules()
     w = workload("store-steps", 134, steps=2)
     x0 = W.make_step_inputs(w, DEV, 0)
@@ -93,8 +112,15 @@ def test_store_reuses_the_previous_store_across_steps():
                           ps.buf.marg_idx, x0["l_k"], x0["l_v"], rows)
     old.run()
     torch.cuda.synchronize()
+    ref0 = oracle_store(x0, ps, rows, 0)
+    check_store(old, ref0, x0, "first store")
     old.new_k += 1.0
     old.new_v -= 1.0
+
+    def shifted(a, by):  # the same change in the store's dtype (rounded as the library's store is)
+        return (torch.from_numpy(a).to(old.new_k.dtype) + by).float().numpy()
+
+    ref0 = (shifted(ref0[0], 1.0), shifted(ref0[1], -1.0)) + ref0[2:]
     x1 = W.make_step_inputs(w, DEV, 1)
     ps.with_query(x1["s_q"], x1["l_q"], x1["seq_len"], x1["k_crit"], x1["k_marg"])
     ps.run()
@@ -102,9 +128,9 @@ def test_store_reuses_the_previous_store_across_steps():
                          ps.buf.marg_idx, x1["l_k"], x1["l_v"], rows, old=old)
     sc.run()
     torch.cuda.synchronize()
-    ref = oracle_store(x1, ps, rows, 0, old=old)
+    ref = oracle_store(x1, ps, rows, 0, old=ref0)
     check_store(sc, ref, x1, "store from the previous store")
-    reused = int(((host(sc.k_slot) >= 0) & (host(old.k_slot) >= 0)).sum())
+    reused = int(((ref[2] >= 0) & (ref0[2] >= 0)).sum())
     log(f"[store] {reused} K rows reused from the previous store")
     assert reused > 0
 
@@ -143,6 +169,14 @@ def test_stage3_through_the_built_store_matches_the_full_cache():
     err = head_err(host(large.out), host(b.large_out).astype(np.float64))
     log(f"[store] stage 3 through the store vs the full cache: {err:.3g}")
     assert err <= TOL[torch.bfloat16]
+    # and against the oracle's step through the oracle's own store
+    from parity import oracle_step
+    nk, nv, ks, vs, _ = oracle_store(x, ps, rows, 0)
+    ref = oracle_step(x, 0, k_slot=torch.from_numpy(ks), v_slot=torch.from_numpy(vs),
+                      l_k=torch.from_numpy(nk), l_v=torch.from_numpy(nv))
+    err = head_err(host(large.out), ref["large_out"])
+    log(f"[store] stage 3 through the store vs the oracle through its store: {err:.3g}")
+    assert err <= TOL[torch.bfloat16]
 
 
 def test_store_from_pinned_host_memory():
@@ -163,7 +197,8 @@ def test_store_from_pinned_host_memory():
     old.run()
     torch.cuda.synchronize()
     assert old.new_k.is_cuda
-    check_store(old, oracle_store(x0, ps, rows, 0), x0, "rebuild from host memory")
+    ref0 = oracle_store(x0, ps, rows, 0)
+    check_store(old, ref0, x0, "rebuild from host memory")
     x1 = W.make_step_inputs(w, DEV, 1)
     ps.with_query(x1["s_q"], x1["l_q"], x1["seq_len"], x1["k_crit"], x1["k_marg"])
     ps.run()
@@ -175,7 +210,7 @@ def test_store_from_pinned_host_memory():
                               ps.buf.marg_idx, x1["l_k"], x1["l_v"], rows, old=old)
     dev_inc.run()
     torch.cuda.synchronize()
-    check_store(inc, oracle_store(x1, ps, rows, 0, old=old), x1, "update from host memory")
+    check_store(inc, oracle_store(x1, ps, rows, 0, old=ref0), x1, "update from host memory")
     for a, b in ((inc.new_k, dev_inc.new_k), (inc.new_v, dev_inc.new_v),
                  (inc.k_slot, dev_inc.k_slot), (inc.v_slot, dev_inc.v_slot)):
         assert torch.equal(a, b)
@@ -208,8 +243,9 @@ def test_steps_through_a_host_backed_store():
     ps = prepare_step(x)
     rows = capacity(x, 4)
     hk, hv = x["l_k"].cpu().pin_memory(), x["l_v"].cpu().pin_memory()
-    old = None
+    old = ref_old = None
     for t in range(3):
+        xt = x
         if t:
             xt = W.make_step_inputs(w, DEV, t)
             ps.with_query(xt["s_q"], xt["l_q"], xt["seq_len"], xt["k_crit"], xt["k_marg"])
@@ -226,7 +262,9 @@ def test_steps_through_a_host_backed_store():
         err = head_err(host(large.out), host(b.large_out).astype(np.float64))
         log(f"[store] step {t}: stage 3 through the host-backed store vs the full cache: {err:.3g}")
         assert err <= TOL[torch.bfloat16]
-        old = sc
+        ref = oracle_store(xt, ps, rows, 0, old=ref_old)
+        check_store(sc, ref, xt, f"host-backed store, step {t}")
+        old, ref_old = sc, ref
 
 
 def test_store_at_the_largest_n_cap():
