@@ -80,6 +80,16 @@ struct PartArgs {
   float pscale;  // probability keys: the bin scale (see plog2)
 };
 
+// Raw buffer views: an access at an offset at or past the view's size reads
+// zero / writes nothing, without touching memory, so masked lanes need no
+// branch (exec-mask regions around every conditional store cost more than
+// the stores).
+constexpr uint32_t kOOB = 0x80000000u;
+constexpr int kBufWord3 = 0x00020000;  // gfx9 raw buffer descriptor word 3 (32-bit data)
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_of(const void *p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), 0, (int)bytes, kBufWord3);
+}
+
 __device__ __forceinline__ uint64_t lanemask_lt() {
   const int lane = threadIdx.x & 63;
   return lane == 0 ? 0ull : (~0ull >> (64 - lane));
@@ -258,13 +268,16 @@ struct Row {
   const float *lg;
   int n;
   int nrank;     // tokens ranked: the first nrank (the rest, recent, are kept unranked)
-  bool aligned;  // 16-byte aligned row: whole chunks load as one float4
+  bool aligned;  // 16-byte aligned row of a multiple of 4 entries: whole chunks
+                 // load as one float4 through `buf`
+  __amdgpu_buffer_rsrc_t buf;  // the row's whole allocation (entries past n read
+                               // as whatever is there and are never ranked)
 
   __device__ __forceinline__ float4 fetch(int k) const {
     const int t = k * kChunk + 4 * (int)threadIdx.x;
     float4 v = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-    if (aligned && t + 3 < n) {
-      v = *reinterpret_cast<const float4 *>(lg + t);
+    if (aligned) {
+      v = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(buf, (uint32_t)t * 4u, 0, 0));
     } else {
       if (t < n) v.x = lg[t];
       if (t + 1 < n) v.y = lg[t + 1];
@@ -538,29 +551,38 @@ struct Compactor {
   const RowCtx &r;
   Targets t;
   float Zinv;
+  // the row's lists as raw buffers of exactly |C| and |M| entries: a store
+  // past them (or of a non-member, at kOOB) is dropped
+  __amdgpu_buffer_rsrc_t cbuf, mbuf, pbuf;
   float sc = 0.0f, sm = 0.0f;
+
+  __device__ Compactor(const RowCtx &rc, const Targets &tg, float zinv)
+      : r(rc), t(tg), Zinv(zinv), cbuf(buffer_of(rc.crit, 4u * (uint32_t)rc.nc)),
+        mbuf(buffer_of(rc.marg, 4u * (uint32_t)rc.nm)),
+        pbuf(buffer_of(rc.mp, 4u * (uint32_t)rc.nm)) {}
 
   // rC / rP: the value's rank (0-based, token order) among the row's ties at
   // T; recent tokens are critical whatever their key
   __device__ __forceinline__ void classify(uint32_t u, bool ranked, bool recent, uint32_t rC,
                                            uint32_t rP, bool &inC, bool &inM) const {
-    inC = recent || (ranked && (u > t.T[0] || (u == t.T[0] && rC < t.need[0])));
-    const bool inP = ranked && (u > t.T[1] || (u == t.T[1] && rP < t.need[1]));
-    inM = inP && !inC;
+    // bitwise, not short-circuit: every operand is cheap, and && / || would
+    // let the compiler branch around them
+    inC = recent | (ranked & ((u > t.T[0]) | ((u == t.T[0]) & (rC < t.need[0]))));
+    const bool inP = ranked & ((u > t.T[1]) | ((u == t.T[1]) & (rP < t.need[1])));
+    inM = inP & !inC;
   }
   __device__ __forceinline__ void emit(float s, int tok, bool inC, bool inM, uint32_t &pc,
                                        uint32_t &pm) {
-    const float p = (inC || inM) ? __expf(s - r.M) * Zinv : 0.0f;
+    const float p = __expf(s - r.M) * Zinv;
     sc += inC ? p : 0.0f;
     sm += inM ? p : 0.0f;
     // the small model's held rows name their token positions
     if (r.pos && (inC || inM)) tok = clampi(r.pos[tok], 0, r.last);
-    // the guards only matter if the select were wrong: never write past a row
-    if (inC && pc < (uint32_t)r.nc) r.crit[pc] = tok;
-    if (inM && pm < (uint32_t)r.nm) {
-      r.marg[pm] = tok;
-      r.mp[pm] = p;
-    }
+    // stores past a list (only if the select were wrong) are dropped by the
+    // buffer views, as are those of non-members
+    __builtin_amdgcn_raw_buffer_store_b32((uint32_t)tok, cbuf, inC ? pc * 4u : kOOB, 0, 0);
+    __builtin_amdgcn_raw_buffer_store_b32((uint32_t)tok, mbuf, inM ? pm * 4u : kOOB, 0, 0);
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(p), pbuf, inM ? pm * 4u : kOOB, 0, 0);
     pc += inC ? 1u : 0u;
     pm += inM ? 1u : 0u;
   }
@@ -590,10 +612,11 @@ void partition_kernel(PartArgs a) {
   row.n = r.n;
   row.nrank = r.older;
   row.pscale = a.pscale;
-  row.aligned = (reinterpret_cast<uintptr_t>(r.lg) & 15) == 0;
+  row.aligned = (reinterpret_cast<uintptr_t>(r.lg) & 15) == 0 && (a.n_cap & 3) == 0;
+  row.buf = buffer_of(r.lg, 4u * (uint32_t)a.n_cap);
   row.load();  // in flight while the row's statistics arrive
   row_stats<kMerge>(a, sh, r);
-  Compactor cp{r, select_targets(sh, r, row), 1.0f / r.Z};
+  Compactor cp(r, select_targets(sh, r, row), 1.0f / r.Z);
   // ties at a threshold split between two sets need their ranks in token order
   const bool split = cp.t.need[0] < cp.t.eq[0] || cp.t.need[1] < cp.t.eq[1];
 
@@ -612,7 +635,7 @@ void partition_kernel(PartArgs a) {
         for (int e = 0; e < 4; ++e) {
           const bool ok = row.ranked(k, e);
           const uint32_t u = logit_key(row.s[4 * k + e]);
-          v[k] += (ok && u == cp.t.T[0] ? 1u : 0u) + (ok && u == cp.t.T[1] ? 0x10000u : 0u);
+          v[k] += ((ok & (u == cp.t.T[0])) ? 1u : 0u) + ((ok & (u == cp.t.T[1])) ? 0x10000u : 0u);
         }
       }
       block_scan<NK>(sh, 0, v, ex, tot);
@@ -634,9 +657,9 @@ void partition_kernel(PartArgs a) {
         const int i = 4 * k + e;
         const bool ok = row.ranked(k, e);
         const uint32_t u = logit_key(row.s[i]);
-        cp.classify(u, ok, kRecent && row.valid(k, e) && !ok, rC, rP, inC[i], inM[i]);
-        rC += ok && u == cp.t.T[0] ? 1u : 0u;
-        rP += ok && u == cp.t.T[1] ? 1u : 0u;
+        cp.classify(u, ok, kRecent & row.valid(k, e) & !ok, rC, rP, inC[i], inM[i]);
+        rC += (ok & (u == cp.t.T[0])) ? 1u : 0u;
+        rP += (ok & (u == cp.t.T[1])) ? 1u : 0u;
         v[k] += (inC[i] ? 1u : 0u) + (inM[i] ? 0x10000u : 0u);
       }
     }
@@ -687,8 +710,11 @@ void partition_kernel(PartArgs a) {
           v[j] = 0;
 #pragma unroll
           for (int e = 0; e < 4; ++e)
-            v[j] += (row.ranked(k0 + j, e) && logit_key(sv[j][e]) == cp.t.T[0] ? 1u : 0u) +
-                    (row.ranked(k0 + j, e) && logit_key(sv[j][e]) == cp.t.T[1] ? 0x10000u : 0u);
+          {
+            const bool ok = row.ranked(k0 + j, e);
+            const uint32_t u = logit_key(sv[j][e]);
+            v[j] += ((ok & (u == cp.t.T[0])) ? 1u : 0u) + ((ok & (u == cp.t.T[1])) ? 0x10000u : 0u);
+          }
         }
         block_scan<NG>(sh, par, v, ex, tot);
         uint32_t in_group = 0;  // ties of the group's earlier chunks (packed, < 2^16 each)
@@ -709,9 +735,9 @@ void partition_kernel(PartArgs a) {
         for (int e = 0; e < 4; ++e) {
           const bool ok = row.ranked(k0 + j, e);
           const uint32_t u = logit_key(sv[j][e]);
-          cp.classify(u, ok, kRecent && row.valid(k0 + j, e) && !ok, rC, rP, inC[j][e], inM[j][e]);
-          rC += ok && u == cp.t.T[0] ? 1u : 0u;
-          rP += ok && u == cp.t.T[1] ? 1u : 0u;
+          cp.classify(u, ok, kRecent & row.valid(k0 + j, e) & !ok, rC, rP, inC[j][e], inM[j][e]);
+          rC += (ok & (u == cp.t.T[0])) ? 1u : 0u;
+          rP += (ok & (u == cp.t.T[1])) ? 1u : 0u;
           v[j] += (inC[j][e] ? 1u : 0u) + (inM[j][e] ? 0x10000u : 0u);
         }
       }
