@@ -158,7 +158,7 @@ def stage3_kernels(w, layers=None):
     n_cap = w.n_cap
     cost = lambda c: -(-units * c // 512) * (-(-n_cap // c) + 384)
     s = 1
-    for c in range(2, min(16, -(-n_cap // 256)) + 1):
+    for c in range(2, min(32, -(-n_cap // 256)) + 1):
         if cost(c) < cost(s):
             s = c
     span = -(-(-(-n_cap // s)) // 256) * 256

@@ -58,6 +58,7 @@ constexpr int kMaxG = 8;
 constexpr int kXcd = 8;
 constexpr int kRec = 2 * kD + 2;         // floats per (split, head) record
 constexpr int kTargetWgs = 512;          // two resident workgroups per CU
+constexpr int kMaxSplit = 32;            // token ranges per kv head (one per 256 tokens at most)
 constexpr int64_t kSetupTok = 384;       // per-workgroup setup, in streamed-token time
 // Raw buffer loads: an offset at or past the resource's size returns zero
 // without touching memory, so masked lanes need no branch.
@@ -682,7 +683,7 @@ __global__ __launch_bounds__(kD) void hybrid_group_merge(GroupArgs a) {
   const int u = blockIdx.x / a.g, h = blockIdx.x % a.g, d = threadIdx.x;
   const int kvh = u % a.hkv, bl = u / a.hkv, layer = a.layer0 + bl % a.nl, b = bl / a.nl;
   const int n = clampi(a.seq_len[b], 1, a.n_cap);
-  const int ns = min(a.n_split, (n + a.span - 1) / a.span);
+  const int ns = clampi((n + a.span - 1) / a.span, 1, min(a.n_split, kMaxSplit));
   const int g = a.g;
   const int64_t qrow = ((int64_t)b * a.layers + layer) * a.hq + (int64_t)kvh * g + h;
   const int j = clampi(a.head_map[layer * a.hq + kvh * g + h], 0, a.nsh - 1);
@@ -691,15 +692,37 @@ __global__ __launch_bounds__(kD) void hybrid_group_merge(GroupArgs a) {
   alphas(a.mode, a.mass[2 * row], a.mass[2 * row + 1], ac, am);
   const float *rec0 = a.rec + ((int64_t)u * a.n_split * g + h) * kRec;
   const int64_t sstride = (int64_t)g * kRec;
-  float M = -INFINITY;
-  for (int s = 0; s < ns; ++s) M = fmaxf(M, rec0[s * sstride]);
-  float Z = 0.0f, oc = 0.0f, om = 0.0f;
-  for (int s = 0; s < ns; ++s) {
-    const float *r = rec0 + s * sstride;
-    const float f = r[0] == -INFINITY ? 0.0f : __expf(r[0] - M);
-    Z = __builtin_fmaf(r[1], f, Z);
-    oc = __builtin_fmaf(r[2 + d], f, oc);
-    om += r[2 + kD + d];
+  // the records eight at a time, all eight in flight at once (past ns the
+  // last record is re-read and weighted 0), combined online
+  constexpr int kGroup = 8;
+  float M = -INFINITY, Z = 0.0f, oc = 0.0f, om = 0.0f;
+  for (int s0 = 0; s0 < ns; s0 += kGroup) {
+    float ms[kGroup], zs[kGroup], os[kGroup], oms[kGroup];
+#pragma unroll
+    for (int i = 0; i < kGroup; ++i) {
+      const float *r = rec0 + min(s0 + i, ns - 1) * sstride;
+      ms[i] = r[0];
+      zs[i] = r[1];
+      os[i] = r[2 + d];
+      oms[i] = r[2 + kD + d];
+    }
+    float mg = M;
+#pragma unroll
+    for (int i = 0; i < kGroup; ++i) mg = s0 + i < ns ? fmaxf(mg, ms[i]) : mg;
+    if (mg != M) {  // (uniform) rescale what the earlier groups added
+      const float f = M == -INFINITY ? 0.0f : __expf(M - mg);
+      Z *= f;
+      oc *= f;
+      M = mg;
+    }
+#pragma unroll
+    for (int i = 0; i < kGroup; ++i) {
+      const bool ok = s0 + i < ns;
+      const float f = (!ok || ms[i] == -INFINITY) ? 0.0f : __expf(ms[i] - M);
+      Z = __builtin_fmaf(zs[i], f, Z);
+      oc = __builtin_fmaf(os[i], f, oc);
+      om += ok ? oms[i] : 0.0f;
+    }
   }
   const float o = (Z > 0.0f ? ac * (oc / Z) : 0.0f) + om;
   elem<bf16_t>::store1(a.out, qrow * kD + d, o);
@@ -726,7 +749,7 @@ GroupPlan plan_group(const smallkv_batch_t &b, const smallkv_model_t &m, int n_s
     return (units * c + kTargetWgs - 1) / kTargetWgs * ((b.n_cap + c - 1) / c + kSetupTok);
   };
   int64_t s = 1;
-  for (int64_t c = 2; c <= 16 && c <= max_s; ++c)
+  for (int64_t c = 2; c <= kMaxSplit && c <= max_s; ++c)
     if (cost(c) < cost(s)) s = c;
   p.span = (int)(((b.n_cap + s - 1) / s + 255) / 256 * 256);  // range starts on list-offset blocks
   p.n_split = (int)((b.n_cap + p.span - 1) / p.span);
