@@ -556,10 +556,30 @@ struct Compactor {
   __amdgpu_buffer_rsrc_t cbuf, mbuf, pbuf;
   float sc = 0.0f, sm = 0.0f;
 
+  // the thresholds as the logits they are the keys of (the key above every
+  // logit's, of an empty set, becomes a NaN, which no logit reaches)
+  float Tf[2];
+
+  __device__ static float key_value(uint32_t k) {
+    return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
+  }
+
   __device__ Compactor(const RowCtx &rc, const Targets &tg, float zinv)
       : r(rc), t(tg), Zinv(zinv), cbuf(buffer_of(rc.crit, 4u * (uint32_t)rc.nc)),
         mbuf(buffer_of(rc.marg, 4u * (uint32_t)rc.nm)),
-        pbuf(buffer_of(rc.mp, 4u * (uint32_t)rc.nm)) {}
+        pbuf(buffer_of(rc.mp, 4u * (uint32_t)rc.nm)) {
+    Tf[0] = key_value(tg.T[0]);
+    Tf[1] = key_value(tg.T[1]);
+  }
+
+  // Membership when no threshold's ties are split between two sets (every
+  // token equal to a threshold is in its set): plain float compares, which
+  // order logits as their keys do (-0 equals +0).
+  __device__ __forceinline__ void classify_unsplit(float s, bool ranked, bool recent, bool &inC,
+                                                   bool &inM) const {
+    inC = recent | (ranked & (s >= Tf[0]));
+    inM = ranked & (s >= Tf[1]) & !inC;
+  }
 
   // rC / rP: the value's rank (0-based, token order) among the row's ties at
   // T; recent tokens are critical whatever their key
@@ -727,18 +747,32 @@ void partition_kernel(PartArgs a) {
       }
       bool inC[NG][4], inM[NG][4];
       uint32_t v[NG], ex[NG], tot[NG];
+      if (split) {
 #pragma unroll
-      for (int j = 0; j < NG; ++j) {
-        uint32_t rC = carry_eq_c + (rank[j] & 0xffffu), rP = carry_eq_p + (rank[j] >> 16);
-        v[j] = 0;
+        for (int j = 0; j < NG; ++j) {
+          uint32_t rC = carry_eq_c + (rank[j] & 0xffffu), rP = carry_eq_p + (rank[j] >> 16);
+          v[j] = 0;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const bool ok = row.ranked(k0 + j, e);
-          const uint32_t u = logit_key(sv[j][e]);
-          cp.classify(u, ok, kRecent & row.valid(k0 + j, e) & !ok, rC, rP, inC[j][e], inM[j][e]);
-          rC += (ok & (u == cp.t.T[0])) ? 1u : 0u;
-          rP += (ok & (u == cp.t.T[1])) ? 1u : 0u;
-          v[j] += (inC[j][e] ? 1u : 0u) + (inM[j][e] ? 0x10000u : 0u);
+          for (int e = 0; e < 4; ++e) {
+            const bool ok = row.ranked(k0 + j, e);
+            const uint32_t u = logit_key(sv[j][e]);
+            cp.classify(u, ok, kRecent & row.valid(k0 + j, e) & !ok, rC, rP, inC[j][e], inM[j][e]);
+            rC += (ok & (u == cp.t.T[0])) ? 1u : 0u;
+            rP += (ok & (u == cp.t.T[1])) ? 1u : 0u;
+            v[j] += (inC[j][e] ? 1u : 0u) + (inM[j][e] ? 0x10000u : 0u);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < NG; ++j) {
+          v[j] = 0;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const bool ok = row.ranked(k0 + j, e);
+            cp.classify_unsplit(sv[j][e], ok, kRecent & row.valid(k0 + j, e) & !ok, inC[j][e],
+                                inM[j][e]);
+            v[j] += (inC[j][e] ? 1u : 0u) + (inM[j][e] ? 0x10000u : 0u);
+          }
         }
       }
       block_scan<NG>(sh, par + 1, v, ex, tot);
