@@ -386,18 +386,22 @@ __device__ __forceinline__ Targets select_targets(PartShared<PT> &sh, const RowC
   for (int x = 0; x < 2; ++x) mode[x] = cnt[x] <= (uint32_t)PT ? 0 : (cnt[x] <= (uint32_t)kCap ? 1 : 2);
   if (mode[0] < 2 || mode[1] < 2) {
     const uint64_t lt = lanemask_lt();
+    const int gb0 = mode[0] < 2 ? bin[0] : -2, gb1 = mode[1] < 2 ? bin[1] : -2;  // bins gathered
     row.each([&](float s, bool valid) {
       const int bn = valid ? row.bin(s, M) : -1;
-      const uint32_t u = logit_key(s);
+      // one ballot for both targets: most waves hold no candidate of either
+      if (__ballot((bn == gb0) | (bn == gb1))) {
+        const uint32_t u = logit_key(s);
 #pragma unroll
-      for (int x = 0; x < 2; ++x) {
-        const bool take = mode[x] < 2 && bn == bin[x];
-        const uint64_t bal = __ballot(take);
-        if (bal) {  // one LDS atomic per wave
-          uint32_t off = 0;
-          if (lane == 0) off = atomicAdd(&sh.ncand[x], (uint32_t)__popcll(bal));
-          off = __shfl(off, 0, kWave);
-          if (take) sh.cand[x][off + __popcll(bal & lt)] = u;
+        for (int x = 0; x < 2; ++x) {
+          const bool take = bn == (x ? gb1 : gb0);
+          const uint64_t bal = __ballot(take);
+          if (bal) {  // one LDS atomic per wave
+            uint32_t off = 0;
+            if (lane == 0) off = atomicAdd(&sh.ncand[x], (uint32_t)__popcll(bal));
+            off = __shfl(off, 0, kWave);
+            if (take) sh.cand[x][off + __popcll(bal & lt)] = u;
+          }
         }
       }
     });
