@@ -587,12 +587,14 @@ struct Compactor {
 
   // rC / rP: the value's rank (0-based, token order) among the row's ties at
   // T; recent tokens are critical whatever their key
-  __device__ __forceinline__ void classify(uint32_t u, bool ranked, bool recent, uint32_t rC,
+  // s compared with the thresholds' logits orders as its key would (-0
+  // equals +0; the NaN of an empty set's threshold is never reached), so no
+  // key is formed.  Bitwise, not short-circuit: every operand is cheap, and
+  // && / || would let the compiler branch around them.
+  __device__ __forceinline__ void classify(float s, bool ranked, bool recent, uint32_t rC,
                                            uint32_t rP, bool &inC, bool &inM) const {
-    // bitwise, not short-circuit: every operand is cheap, and && / || would
-    // let the compiler branch around them
-    inC = recent | (ranked & ((u > t.T[0]) | ((u == t.T[0]) & (rC < t.need[0]))));
-    const bool inP = ranked & ((u > t.T[1]) | ((u == t.T[1]) & (rP < t.need[1])));
+    inC = recent | (ranked & ((s > Tf[0]) | ((s == Tf[0]) & (rC < t.need[0]))));
+    const bool inP = ranked & ((s > Tf[1]) | ((s == Tf[1]) & (rP < t.need[1])));
     inM = inP & !inC;
   }
   __device__ __forceinline__ void emit(float s, int tok, bool inC, bool inM, uint32_t &pc,
@@ -680,10 +682,10 @@ void partition_kernel(PartArgs a) {
       for (int e = 0; e < 4; ++e) {
         const int i = 4 * k + e;
         const bool ok = row.ranked(k, e);
-        const uint32_t u = logit_key(row.s[i]);
-        cp.classify(u, ok, kRecent & row.valid(k, e) & !ok, rC, rP, inC[i], inM[i]);
-        rC += (ok & (u == cp.t.T[0])) ? 1u : 0u;
-        rP += (ok & (u == cp.t.T[1])) ? 1u : 0u;
+        const float x = row.s[i];
+        cp.classify(x, ok, kRecent & row.valid(k, e) & !ok, rC, rP, inC[i], inM[i]);
+        rC += (ok & (x == cp.Tf[0])) ? 1u : 0u;
+        rP += (ok & (x == cp.Tf[1])) ? 1u : 0u;
         v[k] += (inC[i] ? 1u : 0u) + (inM[i] ? 0x10000u : 0u);
       }
     }
@@ -759,10 +761,10 @@ void partition_kernel(PartArgs a) {
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             const bool ok = row.ranked(k0 + j, e);
-            const uint32_t u = logit_key(sv[j][e]);
-            cp.classify(u, ok, kRecent & row.valid(k0 + j, e) & !ok, rC, rP, inC[j][e], inM[j][e]);
-            rC += (ok & (u == cp.t.T[0])) ? 1u : 0u;
-            rP += (ok & (u == cp.t.T[1])) ? 1u : 0u;
+            const float x = sv[j][e];
+            cp.classify(x, ok, kRecent & row.valid(k0 + j, e) & !ok, rC, rP, inC[j][e], inM[j][e]);
+            rC += (ok & (x == cp.Tf[0])) ? 1u : 0u;
+            rP += (ok & (x == cp.Tf[1])) ? 1u : 0u;
             v[j] += (inC[j][e] ? 1u : 0u) + (inM[j][e] ? 0x10000u : 0u);
           }
         }
