@@ -19,13 +19,16 @@
 //      workgroup prefix sums (DPP wave scans), computes p' for marginal
 //      tokens and the masses S'_C, S'_M.  Tie ranks are scanned only when a
 //      threshold's ties are split between two sets.
-// Rows of up to 16 (20 with 256 threads) logits per thread are read once,
-// 4 consecutive logits per thread per chunk, and kept in registers; their
-// compaction needs a single barrier.  Longer rows are re-read per pass, four
-// chunks in flight.  Many rows (several per CU) get 256 threads each, so
-// that more rows are resident; few rows get 512.  The fused variant first
-// combines stage 1's per-chunk records of its head (row max, row sum, the
-// head's output), so a step needs no separate merge launch.
+// The row is read in slots of PT consecutive tokens, one per thread, so that
+// each wave holds 64 consecutive tokens of a slot: a wave's members of a
+// slot are a ballot, and their list positions are the wave's base plus a
+// masked bit count (mbcnt), with one workgroup exchange of per-wave counts
+// per group of slots.  Rows of up to 16 (20 with 256 threads) slots are read
+// once and kept in registers (one exchange); longer rows are re-read per
+// pass, 16 slots in flight.  Many rows (several per CU) get 256 threads
+// each, so that more rows are resident; few rows get 512.  The fused variant
+// first combines stage 1's per-chunk records of its head (row max, row sum,
+// the head's output), so a step needs no separate merge launch.
 // The result depends only on the logits: deterministic.
 #include "common.h"
 #include "launch.h"
@@ -50,12 +53,15 @@ struct Hist {
   static __device__ __forceinline__ int idx(int b) { return pad ? b + (b >> 5) * 4 : b; }
 };
 constexpr int kCap = 2048;       // candidate keys per target kept in LDS
-constexpr int kMaxNK = 5;        // chunks of a register-cached row
 template <int PT>
 struct PC {
   static constexpr int waves = PT / kWave;
-  static constexpr int chunk = 4 * PT;  // tokens per chunk (4 per thread)
 };
+// Slots of a long row per workgroup exchange (and in flight while a group is
+// compacted)
+constexpr int kGroup = 16;
+// Slots per exchange at most: a register row's R, or kGroup
+constexpr int kMaxSlots = 20;
 
 struct PartArgs {
   int n_cap, nsh, kc_cap, km_cap;
@@ -90,18 +96,27 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_of(const void *p, uint3
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), 0, (int)bytes, kBufWord3);
 }
 
+// The lanes where p holds, straight from the compare that made p (HIP's
+// __ballot takes an int, which costs a select and a compare per use)
+__device__ __forceinline__ uint64_t ballot(bool p) { return __builtin_amdgcn_ballot_w64(p); }
+// This lane's bit of a wave-uniform lane mask, used as a lane predicate
+// without leaving the scalar unit
+__device__ __forceinline__ bool lane_in(uint64_t m) { return __builtin_amdgcn_inverse_ballot_w64(m); }
+
 __device__ __forceinline__ uint64_t lanemask_lt() {
   const int lane = threadIdx.x & 63;
   return lane == 0 ? 0ull : (~0ull >> (64 - lane));
 }
 
-// Monotone non-decreasing bin of a logit below the row max M: 2047 for the
-// top 1/64 of a logit unit, one bin per further 1/64, 0 for everything more
-// than 32 below.  Explicitly rounded ops so every pass computes the same bin.
-__device__ __forceinline__ int logit_bin(float s, float M) {
-  float d = __fmul_rn(__fsub_rn(M, s), 64.0f);
+// Distance of a key s below the row's largest key M in steps of 1/64 (M64 =
+// 64 M), clamped to 0..2047: the histogram bin 2047 - i holds the keys at
+// distance i, so the top 1/64 of a unit is bin 2047 and everything more than
+// 32 below is bin 0.  One correctly rounded fma: monotone in s, and the same
+// in every pass, which is all the select needs of it.
+__device__ __forceinline__ int bin_index(float s, float M64) {
+  float d = __fmaf_rn(s, -64.0f, M64);
   d = fminf(fmaxf(d, 0.0f), 2047.0f);
-  return 2047 - (int)d;
+  return (int)d;
 }
 
 template <int CTRL, int ROW_MASK>
@@ -169,7 +184,7 @@ struct alignas(16) PartShared {
   uint32_t sel[2][4];  // radix: prefix, mask, remaining rank, count of T
   uint32_t res[2][4];  // counting: key, ties taken, ties in all
   uint32_t ncand[2];
-  uint32_t wt[4][kMaxNK][PC<PT>::waves];  // wave totals of the block scans
+  uint32_t cnt[4][PC<PT>::waves][kMaxSlots];  // per-(wave, slot) counts of the exchanges
   float wsum[2][PC<PT>::waves];
   float mred[3 * PT + 2];
 };
@@ -239,109 +254,83 @@ __device__ __forceinline__ void row_stats(const PartArgs &a, PartShared<PT> &sh,
   }
 }
 
-// The row as seen by the passes: chunk k holds tokens [k*kChunk, (k+1)*kChunk),
-// 4 consecutive tokens per thread (token of value e = k*kChunk + 4*tid + e).
-// R > 0: the row sits in R registers per thread, read from memory once.
-// R == 0: every pass reads it from memory, four chunks in flight at a time.
-// kRecent: the row may end in recent tokens (kept unranked); without them
-// every token is ranked and the kernel carries no test for it.
+// The row as seen by the passes: slot q holds tokens [q*PT, (q+1)*PT), token
+// q*PT + tid in thread tid, so a wave holds 64 consecutive tokens of it.
+// R > 0: the row sits in R registers per thread (slots 0..R-1), read from
+// memory once.  R == 0: every pass reads it from memory, kGroup slots in
+// flight.  kRecent: the row may end in recent tokens (kept unranked); without
+// them every token is ranked and the kernel carries no test for it.
 // Bin of a non-negative key that is a probability (or a sum of them) rather
 // than a logit: its bit pattern read as exponent + mantissa fraction, a
 // monotone stand-in for log2, in bins of a set fraction of a binade.  Exact (integer below
 // 2^24, power-of-2 scaling).
 // pscale = bins per binade / (64 * 2^15): key bits >> 8 count 2^15 steps per
-// binade and logit_bin takes 64 bins per unit (2048 bins below the key).
+// binade and a bin is 1/64 of a unit (2048 bins below the key).
 __device__ __forceinline__ float plog2(float x, float pscale) {
   return (float)(__float_as_uint(x) >> 8) * pscale;
 }
 
 template <int R, int PT, bool kRecent, bool kProb = false>
 struct Row {
-  static constexpr int kChunk = PC<PT>::chunk;
-  // histogram bin of a key below the row's largest key M
-  __device__ __forceinline__ int bin(float s, float M) const {
-    if constexpr (kProb) return logit_bin(plog2(s, pscale), plog2(M, pscale));
-    return logit_bin(s, M);
-  }
   float pscale;  // kProb: key bits >> 8 to bins of 1/64 (see plog2)
-  float s[R > 0 ? R : 4];
-  const float *lg;
+  float M64;     // 64 x the row's largest key as the bins see it
+  float s[R > 0 ? R : 1];
   int n;
   int nrank;     // tokens ranked: the first nrank (the rest, recent, are kept unranked)
-  bool aligned;  // 16-byte aligned row of a multiple of 4 entries: whole chunks
-                 // load as one float4 through `buf`
   __amdgpu_buffer_rsrc_t buf;  // the row's whole allocation (entries past n read
                                // as whatever is there and are never ranked)
 
-  __device__ __forceinline__ float4 fetch(int k) const {
-    const int t = k * kChunk + 4 * (int)threadIdx.x;
-    float4 v = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-    if (aligned) {
-      v = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(buf, (uint32_t)t * 4u, 0, 0));
-    } else {
-      if (t < n) v.x = lg[t];
-      if (t + 1 < n) v.y = lg[t + 1];
-      if (t + 2 < n) v.z = lg[t + 2];
-      if (t + 3 < n) v.w = lg[t + 3];
-    }
-    return v;
+  __device__ __forceinline__ void set_max(float M) {
+    if constexpr (kProb) M64 = 64.0f * plog2(M, pscale);
+    else M64 = 64.0f * M;
+  }
+  // distance index of a key (0: the top bin; histogram bin 2047 - index)
+  __device__ __forceinline__ int bin_of(float s) const {
+    if constexpr (kProb) return bin_index(plog2(s, pscale), M64);
+    return bin_index(s, M64);
+  }
+  __device__ __forceinline__ int tok(int q) const { return q * PT + (int)threadIdx.x; }
+  // slots past the allocation read zero (raw buffer view)
+  __device__ __forceinline__ float fetch(int q) const {
+    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(buf, (uint32_t)tok(q) * 4u, 0, 0));
   }
   __device__ __forceinline__ void load() {
     if constexpr (R > 0) {
+      const int nq = slots();  // a short row of a wide variant reads only its own slots
 #pragma unroll
-      for (int k = 0; k < R / 4; ++k) {
-        const float4 v = fetch(k);
-        s[4 * k] = v.x;
-        s[4 * k + 1] = v.y;
-        s[4 * k + 2] = v.z;
-        s[4 * k + 3] = v.w;
-      }
+      for (int q = 0; q < R; ++q) s[q] = q < nq ? fetch(q) : 0.0f;
     }
   }
-  __device__ __forceinline__ float4 chunk(int k) const {
-    if constexpr (R > 0)
-      return make_float4(s[4 * k], s[4 * k + 1], s[4 * k + 2], s[4 * k + 3]);
-    else
-      return fetch(k);
+  __device__ __forceinline__ int slots() const { return (n + PT - 1) / PT; }
+  __device__ __forceinline__ bool valid(int q) const { return tok(q) < n; }
+  __device__ __forceinline__ bool ranked(int q) const {
+    if constexpr (!kRecent) return valid(q);
+    return tok(q) < nrank;
   }
-  __device__ __forceinline__ int chunks() const { return (n + kChunk - 1) / kChunk; }
-  __device__ __forceinline__ bool valid(int k, int e) const {
-    return k * kChunk + 4 * (int)threadIdx.x + e < n;
-  }
-  __device__ __forceinline__ bool ranked(int k, int e) const {
-    if constexpr (!kRecent) return valid(k, e);
-    return k * kChunk + 4 * (int)threadIdx.x + e < nrank;
-  }
-  // f(value, ranked) for every slot of every chunk holding ranked tokens,
-  // with the wave converged
+  // f(value, ranked) for every slot holding ranked tokens, with the wave
+  // converged
   template <typename F>
   __device__ __forceinline__ void each(F f) const {
+    const int nq = ((kRecent ? nrank : n) + PT - 1) / PT;
     if constexpr (R > 0) {
 #pragma unroll
-      for (int k = 0; k < R / 4; ++k) {
-        if (k * kChunk >= (kRecent ? nrank : n)) break;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) f(s[4 * k + e], ranked(k, e));
-      }
+      for (int q = 0; q < R; ++q)  // a fixed count (a break would keep s[] in memory)
+        if (q < nq) f(s[q], ranked(q));
     } else {
-      const int nk = ((kRecent ? nrank : n) + kChunk - 1) / kChunk;
-      float4 nx[4];  // the next four chunks, in flight while these are used
+      // the next slots, in flight while these are used (past the row's end
+      // too: past the allocation they read zero, and are not used)
+      float nx[kGroup];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) nx[j] = j < nk ? fetch(j) : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-      for (int k0 = 0; k0 < nk; k0 += 4) {
-        float4 v[4];
+      for (int j = 0; j < kGroup; ++j) nx[j] = fetch(j);
+      for (int q0 = 0; q0 < nq; q0 += kGroup) {
+        float v[kGroup];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) v[j] = nx[j];
+        for (int j = 0; j < kGroup; ++j) v[j] = nx[j];
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-          if (k0 + 4 + j < nk) nx[j] = fetch(k0 + 4 + j);
+        for (int j = 0; j < kGroup; ++j) nx[j] = fetch(q0 + kGroup + j);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          f(v[j].x, ranked(k0 + j, 0));
-          f(v[j].y, ranked(k0 + j, 1));
-          f(v[j].z, ranked(k0 + j, 2));
-          f(v[j].w, ranked(k0 + j, 3));
-        }
+        for (int j = 0; j < kGroup; ++j)
+          if (q0 + j < nq) f(v[j], ranked(q0 + j));
       }
     }
   }
@@ -361,12 +350,11 @@ __device__ __forceinline__ Targets select_targets(PartShared<PT> &sh, const RowC
   // ranked token in the set -- is resolved as rank 1 and then replaced by a
   // key above every logit's.
   if (r.ntop + r.nm == 0) return Targets{{~0u, ~0u}, {0u, 0u}, {0u, 0u}};
-  const float M = r.M;
   for (int x = tid; x < Hist<PT>::size; x += PT) sh.hist[0][x] = 0;
   if (tid < 2) sh.ncand[tid] = 0;
   __syncthreads();
   row.each([&](float s, bool valid) {
-    if (valid) atomicAdd(&sh.hist[0][Hist<PT>::idx(row.bin(s, M))], 1u);
+    if (valid) atomicAdd(&sh.hist[0][Hist<PT>::idx(2047 - row.bin_of(s))], 1u);
   });
   __syncthreads();
   // every wave finds both targets' bins itself: no broadcast needed
@@ -386,16 +374,19 @@ __device__ __forceinline__ Targets select_targets(PartShared<PT> &sh, const RowC
   for (int x = 0; x < 2; ++x) mode[x] = cnt[x] <= (uint32_t)PT ? 0 : (cnt[x] <= (uint32_t)kCap ? 1 : 2);
   if (mode[0] < 2 || mode[1] < 2) {
     const uint64_t lt = lanemask_lt();
-    const int gb0 = mode[0] < 2 ? bin[0] : -2, gb1 = mode[1] < 2 ? bin[1] : -2;  // bins gathered
+    // distance indices of the bins gathered (-1: none)
+    const int gb0 = mode[0] < 2 ? 2047 - bin[0] : -1, gb1 = mode[1] < 2 ? 2047 - bin[1] : -1;
     row.each([&](float s, bool valid) {
-      const int bn = valid ? row.bin(s, M) : -1;
-      // one ballot for both targets: most waves hold no candidate of either
-      if (__ballot((bn == gb0) | (bn == gb1))) {
+      const int bn = row.bin_of(s);
+      const uint64_t ok = ballot(valid);
+      const uint64_t h[2] = {ok & ballot(bn == gb0), ok & ballot(bn == gb1)};
+      // most waves hold no candidate of either target
+      if (h[0] | h[1]) {
         const uint32_t u = logit_key(s);
 #pragma unroll
         for (int x = 0; x < 2; ++x) {
-          const bool take = bn == (x ? gb1 : gb0);
-          const uint64_t bal = __ballot(take);
+          const uint64_t bal = h[x];
+          const bool take = lane_in(bal);
           if (bal) {  // one LDS atomic per wave
             uint32_t off = 0;
             if (lane == 0) off = atomicAdd(&sh.ncand[x], (uint32_t)__popcll(bal));
@@ -455,7 +446,7 @@ __device__ __forceinline__ Targets select_targets(PartShared<PT> &sh, const RowC
         }
       if (mode[0] == 2 || mode[1] == 2)
         row.each([&](float s, bool valid) {
-          const int bn = valid ? row.bin(s, M) : -1;
+          const int bn = valid ? 2047 - row.bin_of(s) : -1;
           const uint32_t u = logit_key(s);
           if (mode[0] == 2 && bn == bin[0] && (u & m0) == p0) atomicAdd(&sh.hist[0][Hist<PT>::idx((u >> shf) & dmask)], 1u);
           if (mode[1] == 2 && bn == bin[1] && (u & m1) == p1) atomicAdd(&sh.hist[1][Hist<PT>::idx((u >> shf) & dmask)], 1u);
@@ -494,32 +485,38 @@ __device__ __forceinline__ Targets select_targets(PartShared<PT> &sh, const RowC
   return t;
 }
 
-// Workgroup exclusive prefix of NK packed values (two 16-bit counts each;
-// per-chunk totals stay below 65536) with one barrier.
-template <int NK, int PT>
-__device__ __forceinline__ void block_scan(PartShared<PT> &sh, int slot, const uint32_t *v,
-                                           uint32_t *excl, uint32_t *total) {
+// One exchange of a group of G slots: each wave's count for each slot
+// (packed, two 16-bit counts; a group's totals stay below 65536) gives, in
+// lane j, the counts before (slot j, this wave) within the group (read back
+// per slot with readlane), and the group's totals.  Lane j sums slot j over
+// the waves; one wave scan orders the slots.  One barrier; `buf` alternates
+// so that the next exchange can write while slow waves still read this one.
+template <int G, int PT>
+__device__ __forceinline__ uint32_t exchange(PartShared<PT> &sh, int buf, const uint32_t *cnt,
+                                             uint32_t &total) {
   constexpr int kWaves = PC<PT>::waves;
+  static_assert(G <= kMaxSlots && G <= kWave, "slots per exchange");
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  uint32_t inc[NK];
+  if (lane == 0)
 #pragma unroll
-  for (int k = 0; k < NK; ++k) {
-    inc[k] = wave_incl_scan(v[k]);
-    if (lane == 63) sh.wt[slot][k][wave] = inc[k];
-  }
+    for (int j = 0; j < G; ++j) sh.cnt[buf][wave][j] = cnt[j];
   __syncthreads();
-#pragma unroll
-  for (int k = 0; k < NK; ++k) {
-    uint32_t off = 0, tot = 0;
+  uint32_t tot = 0, part = 0;
+  if (lane < G)
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) {
-      const uint32_t x = sh.wt[slot][k][w];
-      off += w < wave ? x : 0u;
-      tot += x;
+      const uint32_t v = sh.cnt[buf][w][lane];
+      tot += v;
+      part += w < wave ? v : 0u;
     }
-    excl[k] = off + inc[k] - v[k];
-    total[k] = tot;
-  }
+  const uint32_t inc = wave_incl_scan(tot);
+  total = __builtin_amdgcn_readlane(inc, G - 1);
+  return inc - tot + part;
+}
+
+// Positions of the set lanes of m below this lane, plus base
+__device__ __forceinline__ uint32_t mbcnt(uint64_t m, uint32_t base) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, base));
 }
 
 template <int PT>
@@ -576,225 +573,174 @@ struct Compactor {
     Tf[1] = key_value(tg.T[1]);
   }
 
-  // Membership when no threshold's ties are split between two sets (every
-  // token equal to a threshold is in its set): plain float compares, which
-  // order logits as their keys do (-0 equals +0).
-  __device__ __forceinline__ void classify_unsplit(float s, bool ranked, bool recent, bool &inC,
-                                                   bool &inM) const {
-    inC = recent | (ranked & (s >= Tf[0]));
-    inM = ranked & (s >= Tf[1]) & !inC;
-  }
-
-  // rC / rP: the value's rank (0-based, token order) among the row's ties at
-  // T; recent tokens are critical whatever their key
-  // s compared with the thresholds' logits orders as its key would (-0
-  // equals +0; the NaN of an empty set's threshold is never reached), so no
-  // key is formed.  Bitwise, not short-circuit: every operand is cheap, and
-  // && / || would let the compiler branch around them.
-  __device__ __forceinline__ void classify(float s, bool ranked, bool recent, uint32_t rC,
-                                           uint32_t rP, bool &inC, bool &inM) const {
-    inC = recent | (ranked & ((s > Tf[0]) | ((s == Tf[0]) & (rC < t.need[0]))));
-    const bool inP = ranked & ((s > Tf[1]) | ((s == Tf[1]) & (rP < t.need[1])));
-    inM = inP & !inC;
-  }
-  __device__ __forceinline__ void emit(float s, int tok, bool inC, bool inM, uint32_t &pc,
-                                       uint32_t &pm) {
+  // Writes the members of a wave's 64 consecutive tokens (lane masks mC,
+  // mM; the wave's first entries go to list positions bc, bm) and adds their
+  // p' to the masses.  Stores past a list (only if the select were wrong)
+  // are dropped by the buffer views, as are those of non-members.
+  template <bool kHeld>
+  __device__ __forceinline__ void emit(float s, int tok, uint64_t mC, uint64_t mM, uint32_t bc,
+                                       uint32_t bm) {
+    const bool inC = lane_in(mC), inM = lane_in(mM);
     const float p = __expf(s - r.M) * Zinv;
     sc += inC ? p : 0.0f;
     sm += inM ? p : 0.0f;
     // the small model's held rows name their token positions
-    if (r.pos && (inC || inM)) tok = clampi(r.pos[tok], 0, r.last);
-    // stores past a list (only if the select were wrong) are dropped by the
-    // buffer views, as are those of non-members
+    if constexpr (kHeld)
+      if (lane_in(mC | mM)) tok = clampi(r.pos[tok], 0, r.last);
+    const uint32_t pc = mbcnt(mC, bc), pm = mbcnt(mM, bm);
     __builtin_amdgcn_raw_buffer_store_b32((uint32_t)tok, cbuf, inC ? pc * 4u : kOOB, 0, 0);
     __builtin_amdgcn_raw_buffer_store_b32((uint32_t)tok, mbuf, inM ? pm * 4u : kOOB, 0, 0);
     __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(p), pbuf, inM ? pm * 4u : kOOB, 0, 0);
-    pc += inC ? 1u : 0u;
-    pm += inM ? 1u : 0u;
   }
 };
 
-// The list offsets at a 256-token boundary: the thread whose first token
-// starts the block (lane 0 of its wave: 64 threads x 4 tokens) records the
-// list positions it is about to write.
-__device__ __forceinline__ void offsets(const PartArgs &a, const RowCtx &r, int tok0, uint32_t pc,
+// The list offsets at 256-token boundaries, for a group of G slots from q0:
+// in every fourth wave (64 tokens each, so its first token starts a block),
+// lane j records the list positions before the wave's tokens of slot j.
+template <int G, int PT>
+__device__ __forceinline__ void offsets(const PartArgs &a, const RowCtx &r, int q0, uint32_t pc,
                                         uint32_t pm) {
-  if (a.tab && (threadIdx.x & 63) == 0 && tok0 < r.n)
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int tok0 = (q0 + lane) * PT + kWave * wave;
+  if ((wave & 3) == 0 && lane < G && tok0 < r.n)
     a.tab[(int64_t)r.row * a.nblk + (tok0 >> 8)] = make_int2((int)pc, (int)pm);
 }
 
 // ---------------------------------------------------------------- kernel --
 
+// Step 3 over a group of G slots x[0..G) starting at slot q0: membership,
+// one exchange of the per-wave counts (two with split ties: their ranks
+// first), then each wave writes its members at its base + mbcnt.
+template <int R, int PT, bool kRecent, bool kProb, bool kSplit, bool kHeld>
+struct Step3 {
+  PartShared<PT> &sh;
+  const PartArgs &a;
+  const RowCtx &r;
+  const Row<R, PT, kRecent, kProb> &row;
+  Compactor &cp;
+  bool offs;  // record the list offsets (a.tab)
+  // entries before the group: C, M, and the ties of T[0] / T[1]
+  uint32_t carry_c = 0, carry_m = 0, carry_eq_c = 0, carry_eq_p = 0;
+
+  // Lane masks of the critical and marginal members among slot q0 + j's
+  // tokens: C = recent | (ranked & above the critical threshold), M = ranked &
+  // above the marginal one, minus C.  Each mask is a ballot of one compare;
+  // the set algebra runs on the scalar unit.  A token equal to a threshold
+  // whose ties are split is in the set if its rank among the row's ties
+  // (token order) is below the set's share of them.
+  template <int G>
+  __device__ __forceinline__ void members(const float (&x)[G], int q0, int j, uint32_t tb,
+                                          uint64_t &mC, uint64_t &mM) const {
+    const int tid = threadIdx.x, q = q0 + j;
+    const uint64_t ok = ballot(tid < (kRecent ? row.nrank : row.n) - q * PT);
+    uint64_t rec = 0;
+    if constexpr (kRecent) rec = ballot(tid < row.n - q * PT) & ~ok;
+    if constexpr (kSplit) {
+      const uint32_t t = __builtin_amdgcn_readlane(tb, j);
+      const uint64_t e0 = ok & ballot(x[j] == cp.Tf[0]), e1 = ok & ballot(x[j] == cp.Tf[1]);
+      const uint64_t r0 = ballot(mbcnt(e0, carry_eq_c + (t & 0xffffu)) < cp.t.need[0]);
+      const uint64_t r1 = ballot(mbcnt(e1, carry_eq_p + (t >> 16)) < cp.t.need[1]);
+      mC = rec | (ok & ballot(x[j] > cp.Tf[0])) | (e0 & r0);
+      mM = ((ok & ballot(x[j] > cp.Tf[1])) | (e1 & r1)) & ~mC;
+    } else {
+      mC = rec | (ok & ballot(x[j] >= cp.Tf[0]));
+      mM = ok & ballot(x[j] >= cp.Tf[1]) & ~mC;
+    }
+  }
+
+  template <int G>
+  __device__ __forceinline__ void group(const float (&x)[G], int q0, int par) {
+    const int nq = min(G, row.slots() - q0);  // slots holding tokens
+    uint32_t tb = 0;  // lane j: ties (packed) before (slot j, this wave) within the group
+    uint32_t ttot = 0;
+    if constexpr (kSplit) {
+      uint32_t tc[G];
+#pragma unroll
+      for (int j = 0; j < G; ++j) {
+        tc[j] = 0;
+        if (j >= nq) continue;
+        const uint64_t ok = ballot((int)threadIdx.x < (kRecent ? row.nrank : row.n) - (q0 + j) * PT);
+        tc[j] = (uint32_t)__popcll(ok & ballot(x[j] == cp.Tf[0])) +
+                ((uint32_t)__popcll(ok & ballot(x[j] == cp.Tf[1])) << 16);
+      }
+      tb = exchange<G>(sh, par, tc, ttot);
+    }
+    uint32_t mc[G], mtot;
+#pragma unroll
+    for (int j = 0; j < G; ++j) {
+      mc[j] = 0;
+      if (j >= nq) continue;
+      uint64_t mC, mM;
+      members(x, q0, j, tb, mC, mM);
+      mc[j] = (uint32_t)__popcll(mC) + ((uint32_t)__popcll(mM) << 16);
+    }
+    const uint32_t mb = exchange<G>(sh, par + 1, mc, mtot);
+    if (offs) offsets<G, PT>(a, r, q0, carry_c + (mb & 0xffffu), carry_m + (mb >> 16));
+#pragma unroll
+    for (int j = 0; j < G; ++j) {
+      if (j >= nq) continue;
+      uint64_t mC, mM;
+      members(x, q0, j, tb, mC, mM);
+      const uint32_t m = __builtin_amdgcn_readlane(mb, j);
+      cp.template emit<kHeld>(x[j], row.tok(q0 + j), mC, mM, carry_c + (m & 0xffffu),
+                              carry_m + (m >> 16));
+    }
+    carry_c += mtot & 0xffffu;
+    carry_m += mtot >> 16;
+    carry_eq_c += ttot & 0xffffu;
+    carry_eq_p += ttot >> 16;
+  }
+
+  __device__ __forceinline__ void run() {
+    if constexpr (R > 0) {
+      group<R>(row.s, 0, 0);
+    } else {
+      // long rows: one exchange per kGroup slots, the next kGroup in flight
+      const int nq = row.slots();
+      // (slots past the row's end are read too: past the allocation they
+      // read zero, and no pass uses them)
+      float nx[kGroup];
+#pragma unroll
+      for (int j = 0; j < kGroup; ++j) nx[j] = row.fetch(j);
+      for (int q0 = 0, gi = 0; q0 < nq; q0 += kGroup, ++gi) {
+        float v[kGroup];
+#pragma unroll
+        for (int j = 0; j < kGroup; ++j) v[j] = nx[j];
+#pragma unroll
+        for (int j = 0; j < kGroup; ++j) nx[j] = row.fetch(q0 + kGroup + j);
+        group<kGroup>(v, q0, 2 * (gi & 1));
+      }
+    }
+  }
+};
+
 template <bool kMerge, int R, int PT, bool kRecent, bool kProb = false>
 __global__ __launch_bounds__(PT) __attribute__((amdgpu_waves_per_eu(4)))
 void partition_kernel(PartArgs a) {
-  constexpr int kChunk = PC<PT>::chunk;
   __shared__ PartShared<PT> sh;
   RowCtx r;
   row_setup(a, r);
-  const int tid = threadIdx.x;
   Row<R, PT, kRecent, kProb> row;
-  row.lg = r.lg;
   row.n = r.n;
   row.nrank = r.older;
   row.pscale = a.pscale;
-  row.aligned = (reinterpret_cast<uintptr_t>(r.lg) & 15) == 0 && (a.n_cap & 3) == 0;
   row.buf = buffer_of(r.lg, 4u * (uint32_t)a.n_cap);
   row.load();  // in flight while the row's statistics arrive
   row_stats<kMerge>(a, sh, r);
+  row.set_max(r.M);
   Compactor cp(r, select_targets(sh, r, row), 1.0f / r.Z);
   // ties at a threshold split between two sets need their ranks in token order
   const bool split = cp.t.need[0] < cp.t.eq[0] || cp.t.need[1] < cp.t.eq[1];
-
-  if constexpr (R > 0) {
-    constexpr int NK = R / 4;
-    static_assert(NK <= kMaxNK, "register row too long");
-    uint32_t rank_base[NK];  // tie ranks (C low, P high) before this thread's values
-#pragma unroll
-    for (int k = 0; k < NK; ++k) rank_base[k] = 0;
-    if (split) {
-      uint32_t v[NK], ex[NK], tot[NK];
-#pragma unroll
-      for (int k = 0; k < NK; ++k) {
-        v[k] = 0;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const bool ok = row.ranked(k, e);
-          const uint32_t u = logit_key(row.s[4 * k + e]);
-          v[k] += ((ok & (u == cp.t.T[0])) ? 1u : 0u) + ((ok & (u == cp.t.T[1])) ? 0x10000u : 0u);
-        }
-      }
-      block_scan<NK>(sh, 0, v, ex, tot);
-      uint32_t carry = 0;
-#pragma unroll
-      for (int k = 0; k < NK; ++k) {
-        rank_base[k] = carry + ex[k];
-        carry += tot[k];
-      }
-    }
-    bool inC[R], inM[R];
-    uint32_t v[NK], ex[NK], tot[NK];
-#pragma unroll
-    for (int k = 0; k < NK; ++k) {
-      uint32_t rC = rank_base[k] & 0xffffu, rP = rank_base[k] >> 16;
-      v[k] = 0;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int i = 4 * k + e;
-        const bool ok = row.ranked(k, e);
-        const float x = row.s[i];
-        cp.classify(x, ok, kRecent & row.valid(k, e) & !ok, rC, rP, inC[i], inM[i]);
-        rC += (ok & (x == cp.Tf[0])) ? 1u : 0u;
-        rP += (ok & (x == cp.Tf[1])) ? 1u : 0u;
-        v[k] += (inC[i] ? 1u : 0u) + (inM[i] ? 0x10000u : 0u);
-      }
-    }
-    block_scan<NK>(sh, 1, v, ex, tot);
-    uint32_t carry_c = 0, carry_m = 0;
-#pragma unroll
-    for (int k = 0; k < NK; ++k) {
-      uint32_t pc = carry_c + (ex[k] & 0xffffu), pm = carry_m + (ex[k] >> 16);
-      if constexpr (kMerge) offsets(a, r, k * kChunk + 4 * tid, pc, pm);
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-        cp.emit(row.s[4 * k + e], k * kChunk + 4 * tid + e, inC[4 * k + e], inM[4 * k + e], pc, pm);
-      carry_c += tot[k] & 0xffffu;
-      carry_m += tot[k] >> 16;
-    }
+  const bool offs = kMerge && a.tab;
+  if (r.pos) {
+    if (split)
+      Step3<R, PT, kRecent, kProb, true, true>{sh, a, r, row, cp, offs}.run();
+    else
+      Step3<R, PT, kRecent, kProb, false, true>{sh, a, r, row, cp, offs}.run();
+  } else if (split) {
+    Step3<R, PT, kRecent, kProb, true, false>{sh, a, r, row, cp, offs}.run();
   } else {
-    // Long rows: one workgroup scan per NG chunks, the next NG in flight.
-    constexpr int NG = 3;
-    static_assert(NG <= kMaxNK, "scan slots");
-    const int nk = row.chunks();
-    // tie ranks before the group, one 32-bit count per threshold: a row may
-    // hold more than 65535 ties (only a group's own counts are packed)
-    uint32_t carry_eq_c = 0, carry_eq_p = 0, carry_c = 0, carry_m = 0;
-    float4 nxt[NG];
-#pragma unroll
-    for (int j = 0; j < NG; ++j) nxt[j] = j < nk ? row.chunk(j) : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-    for (int k0 = 0, it = 0; k0 < nk; k0 += NG, ++it) {
-      float sv[NG][4];
-#pragma unroll
-      for (int j = 0; j < NG; ++j) {
-        sv[j][0] = nxt[j].x;
-        sv[j][1] = nxt[j].y;
-        sv[j][2] = nxt[j].z;
-        sv[j][3] = nxt[j].w;
-      }
-#pragma unroll
-      for (int j = 0; j < NG; ++j)
-        if (k0 + NG + j < nk) nxt[j] = row.chunk(k0 + NG + j);
-      const int par = 2 * (it & 1);
-      uint32_t rank[NG];  // keys are recomputed where used: fewer live registers
-#pragma unroll
-      for (int j = 0; j < NG; ++j) rank[j] = 0;
-      uint32_t group_eq = 0;  // the group's ties of T[0] (low half) and T[1] (high half)
-      if (split) {
-        uint32_t v[NG], ex[NG], tot[NG];
-#pragma unroll
-        for (int j = 0; j < NG; ++j) {
-          v[j] = 0;
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-          {
-            const bool ok = row.ranked(k0 + j, e);
-            const uint32_t u = logit_key(sv[j][e]);
-            v[j] += ((ok & (u == cp.t.T[0])) ? 1u : 0u) + ((ok & (u == cp.t.T[1])) ? 0x10000u : 0u);
-          }
-        }
-        block_scan<NG>(sh, par, v, ex, tot);
-        uint32_t in_group = 0;  // ties of the group's earlier chunks (packed, < 2^16 each)
-#pragma unroll
-        for (int j = 0; j < NG; ++j) {
-          rank[j] = in_group + ex[j];
-          in_group += tot[j];
-        }
-        group_eq = in_group;
-      }
-      bool inC[NG][4], inM[NG][4];
-      uint32_t v[NG], ex[NG], tot[NG];
-      if (split) {
-#pragma unroll
-        for (int j = 0; j < NG; ++j) {
-          uint32_t rC = carry_eq_c + (rank[j] & 0xffffu), rP = carry_eq_p + (rank[j] >> 16);
-          v[j] = 0;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const bool ok = row.ranked(k0 + j, e);
-            const float x = sv[j][e];
-            cp.classify(x, ok, kRecent & row.valid(k0 + j, e) & !ok, rC, rP, inC[j][e], inM[j][e]);
-            rC += (ok & (x == cp.Tf[0])) ? 1u : 0u;
-            rP += (ok & (x == cp.Tf[1])) ? 1u : 0u;
-            v[j] += (inC[j][e] ? 1u : 0u) + (inM[j][e] ? 0x10000u : 0u);
-          }
-        }
-      } else {
-#pragma unroll
-        for (int j = 0; j < NG; ++j) {
-          v[j] = 0;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const bool ok = row.ranked(k0 + j, e);
-            cp.classify_unsplit(sv[j][e], ok, kRecent & row.valid(k0 + j, e) & !ok, inC[j][e],
-                                inM[j][e]);
-            v[j] += (inC[j][e] ? 1u : 0u) + (inM[j][e] ? 0x10000u : 0u);
-          }
-        }
-      }
-      block_scan<NG>(sh, par + 1, v, ex, tot);
-#pragma unroll
-      for (int j = 0; j < NG; ++j) {
-        uint32_t pc = carry_c + (ex[j] & 0xffffu), pm = carry_m + (ex[j] >> 16);
-        if constexpr (kMerge) offsets(a, r, (k0 + j) * kChunk + 4 * tid, pc, pm);
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          cp.emit(sv[j][e], (k0 + j) * kChunk + 4 * tid + e, inC[j][e], inM[j][e], pc, pm);
-        carry_c += tot[j] & 0xffffu;
-        carry_m += tot[j] >> 16;
-      }
-      carry_eq_c += group_eq & 0xffffu;
-      carry_eq_p += group_eq >> 16;
-    }
+    Step3<R, PT, kRecent, kProb, false, false>{sh, a, r, row, cp, offs}.run();
   }
   finish_row(a, sh, r, cp.sc, cp.sm);
 }
@@ -924,7 +870,7 @@ hipError_t launch_group_partition(const smallkv_batch_t &b, int group_rows, cons
   // the row max and the normaliser (the p' this writes are not used)
   PartArgs a = base_args(b, group_rows, keys, const_cast<float *>(key_max),
                          const_cast<float *>(key_max), crit, marg, marg_prob, mass);
-  // key bits >> 8 hold 15 mantissa bits per binade; logit_bin takes 64 steps
+  // key bits >> 8 hold 15 mantissa bits per binade; a bin is 1/64 of a unit,
   // per unit, so a unit of 64 / bins_per_binade binades
   a.pscale = (float)bins_per_binade / (64.0f * 32768.0f);
   return launch_rows<false, true>(a, b.batch * group_rows, st);
