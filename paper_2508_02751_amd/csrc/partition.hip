@@ -308,8 +308,10 @@ struct Row {
     return tok(q) < nrank;
   }
   // f(value, ranked) for every slot holding ranked tokens, with the wave
-  // converged
-  template <typename F>
+  // converged.  kRev: from the row's end to its start, so that a pass that
+  // follows a forward one starts on what that one read last, which is still
+  // in L2 (order-free passes only).
+  template <bool kRev = false, typename F>
   __device__ __forceinline__ void each(F f) const {
     const int nq = ((kRecent ? nrank : n) + PT - 1) / PT;
     if constexpr (R > 0) {
@@ -320,17 +322,34 @@ struct Row {
       // the next slots, in flight while these are used (past the row's end
       // too: past the allocation they read zero, and are not used)
       float nx[kGroup];
+      if constexpr (kRev) {
+        const int last = (nq - 1) / kGroup * kGroup;  // first slot of the last group
 #pragma unroll
-      for (int j = 0; j < kGroup; ++j) nx[j] = fetch(j);
-      for (int q0 = 0; q0 < nq; q0 += kGroup) {
-        float v[kGroup];
+        for (int j = 0; j < kGroup; ++j) nx[j] = fetch(last + j);
+        for (int q0 = last; q0 >= 0; q0 -= kGroup) {
+          float v[kGroup];
 #pragma unroll
-        for (int j = 0; j < kGroup; ++j) v[j] = nx[j];
+          for (int j = 0; j < kGroup; ++j) v[j] = nx[j];
+          if (q0 >= kGroup)
 #pragma unroll
-        for (int j = 0; j < kGroup; ++j) nx[j] = fetch(q0 + kGroup + j);
+            for (int j = 0; j < kGroup; ++j) nx[j] = fetch(q0 - kGroup + j);
 #pragma unroll
-        for (int j = 0; j < kGroup; ++j)
-          if (q0 + j < nq) f(v[j], ranked(q0 + j));
+          for (int j = kGroup - 1; j >= 0; --j)
+            if (q0 + j < nq) f(v[j], ranked(q0 + j));
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < kGroup; ++j) nx[j] = fetch(j);
+        for (int q0 = 0; q0 < nq; q0 += kGroup) {
+          float v[kGroup];
+#pragma unroll
+          for (int j = 0; j < kGroup; ++j) v[j] = nx[j];
+#pragma unroll
+          for (int j = 0; j < kGroup; ++j) nx[j] = fetch(q0 + kGroup + j);
+#pragma unroll
+          for (int j = 0; j < kGroup; ++j)
+            if (q0 + j < nq) f(v[j], ranked(q0 + j));
+        }
       }
     }
   }
@@ -376,7 +395,8 @@ __device__ __forceinline__ Targets select_targets(PartShared<PT> &sh, const RowC
     const uint64_t lt = lanemask_lt();
     // distance indices of the bins gathered (-1: none)
     const int gb0 = mode[0] < 2 ? 2047 - bin[0] : -1, gb1 = mode[1] < 2 ? 2047 - bin[1] : -1;
-    row.each([&](float s, bool valid) {
+    // backwards: the histogram pass read the row forwards
+    row.template each<true>([&](float s, bool valid) {
       const int bn = row.bin_of(s);
       const uint64_t ok = ballot(valid);
       const uint64_t h[2] = {ok & ballot(bn == gb0), ok & ballot(bn == gb1)};
