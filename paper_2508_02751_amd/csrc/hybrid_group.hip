@@ -95,6 +95,7 @@ struct GroupShared {
   uint32_t uni[kWin];           // union rows: (bits << kPosBits) | position
   WaveTiles w[kGW];
   int cur[2 * kMaxG];           // list cursors (first entry not yet consumed)
+  int cend[2 * kMaxG];          // with list offsets: each list's end of the token range
   int mstart[kMaxG];            // M-list cursor at the window start
   int wcnt[kGW][kMaxG];         // marginal entries per head in each wave's rows
   int64_t hrow[kMaxG];          // row of each head's lists: small head (b, j), or its group
@@ -238,7 +239,10 @@ __device__ __forceinline__ void lower_bounds(const ListRef (&l)[kLPW], int targe
 
 __global__ __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2))) void hybrid_group_kernel(GroupArgs a) {
   __shared__ __align__(16) GroupShared sh;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  // the wave index, known to the compiler as wave-uniform: everything derived
+  // from it (the owned lists, their pointers and bits) stays in SGPRs
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   // XCD-aware numbering: x = ((u / 8) * n_split + sp) * 8 + u % 8
   const int x = blockIdx.x;
   const int rest = x / kXcd;
@@ -247,19 +251,41 @@ __global__ __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2))) void h
   const int kvh = u % a.hkv, bl = u / a.hkv, layer = a.layer0 + bl % a.nl, b = bl / a.nl;
   // the (sequence, layer, kv head) in the whole stack's layout
   const int64_t ua = ((int64_t)b * a.layers + layer) * a.hkv + kvh;
+  const int g = a.g;
+  // the heads' small heads, requested before the sequence's sizes arrive
+  // (the index is valid whatever they are)
+  const int hm = tid < g ? a.head_map[layer * a.hq + kvh * g + tid] : 0;
   const Sizes sz = set_sizes(a.seq_len, a.k_crit, a.k_marg, a.k_recent, b, a.n_cap, a.kc_cap, a.km_cap);
   const int t_begin = sp * a.span;
   if (t_begin >= sz.n) return;
   const int t_end = min(t_begin + a.span, sz.n);
-  const int g = a.g;
+  // With the partition's list offsets at both ends of a range of one window,
+  // every list's entries in it are known before any is read: they are
+  // loaded in one round instead of a scan that reads on until it passes the
+  // window's end.
+  const bool flat = a.tab && t_end - t_begin <= kWin;
   const int hc = lane & 15, lq = lane >> 4;  // MFMA column (head / slot) and lane quarter
   WaveTiles &wt = sh.w[wave];
 
   if (tid < g) {
-    const int j = clampi(a.head_map[layer * a.hq + kvh * g + tid], 0, a.nsh - 1);
+    const int j = clampi(hm, 0, a.nsh - 1);
     const int64_t row = (int64_t)b * a.nsh + j;
     const int64_t qrow = ((int64_t)b * a.layers + layer) * a.hq + (int64_t)kvh * g + tid;
-    sh.hrow[tid] = a.group_sel ? ua : row;
+    const int64_t hrow = a.group_sel ? ua : row;
+    sh.hrow[tid] = hrow;
+    if (a.tab) {
+      // the partition's offsets at the range's ends (multiples of 256 tokens,
+      // or the sequence's end): entries of each list below t_begin / t_end;
+      // clamped: no table content can move a cursor outside its list
+      const int2 *tb = a.tab + hrow * a.nblk;
+      const int2 v0 = tb[t_begin >> 8];
+      const int2 v1 = t_end < sz.n ? tb[t_end >> 8] : make_int2(sz.nc, sz.nm);
+      const int c0 = clampi(v0.x, 0, sz.nc), m0 = clampi(v0.y, 0, sz.nm);
+      sh.cur[tid] = c0;
+      sh.cur[g + tid] = m0;
+      sh.cend[tid] = clampi(v1.x, c0, sz.nc);
+      sh.cend[g + tid] = clampi(v1.y, m0, sz.nm);
+    }
     const int64_t prow = a.group_sel ? qrow : row;
     sh.prow[tid] = prow;
     float ac, am;
@@ -281,26 +307,50 @@ __global__ __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2))) void h
   ListRef lists[kLPW];
 #pragma unroll
   for (int i = 0; i < kLPW; ++i) lists[i] = list_ref(a, sh, wave + kGW * i, sz.nc, sz.nm);
-  if (a.tab) {
-    // the partition's offsets at the range start (a multiple of 256 tokens):
-    // entries of each list below t_begin
-    const int64_t blk = t_begin >> 8;
-    if (lane == 0)
-#pragma unroll
-      for (int i = 0; i < kLPW; ++i) {
-        const int L = wave + kGW * i;
-        if (!lists[i].on) continue;
-        const int2 v = a.tab[sh.hrow[L < g ? L : L - g] * a.nblk + blk];
-        // clamped: no table content can move a cursor outside its list
-        sh.cur[L] = clampi(L < g ? v.x : v.y, 0, lists[i].len);
-      }
-  } else {
+  if (!a.tab) {  // (with offsets the cursors are set above)
     int res[kLPW];
     lower_bounds(lists, t_begin, res);
     if (lane == 0)
 #pragma unroll
       for (int i = 0; i < kLPW; ++i)
         if (lists[i].on) sh.cur[wave + kGW * i] = res[i];
+  }
+
+  if (flat) {
+    // membership of the range's one window: each owned list's entries of
+    // the range, kF per lane per round, all lists' loads in flight together
+    // (before the queries and accumulators hold registers)
+    constexpr int kF = 8;
+    int c0[kLPW], ne[kLPW];
+#pragma unroll
+    for (int i = 0; i < kLPW; ++i) {
+      const int L = wave + kGW * i;
+      c0[i] = lists[i].on ? sh.cur[L] : 0;
+      ne[i] = lists[i].on ? sh.cend[L] - c0[i] : 0;
+      if (lists[i].on && L >= g && lane == 0) sh.mstart[L - g] = c0[i];
+    }
+    for (int k0 = 0;; k0 += kF * kWave) {
+      bool any = false;
+#pragma unroll
+      for (int i = 0; i < kLPW; ++i) any |= k0 < ne[i];
+      if (!any) break;
+      int e[kLPW][kF];
+#pragma unroll
+      for (int i = 0; i < kLPW; ++i)
+#pragma unroll
+        for (int k = 0; k < kF; ++k) {
+          const int pos = k0 + lane + kWave * k;
+          e[i][k] = pos < ne[i] ? lists[i].p[c0[i] + pos] : -1;
+        }
+#pragma unroll
+      for (int i = 0; i < kLPW; ++i)
+#pragma unroll
+        for (int k = 0; k < kF; ++k) {
+          // (an entry outside the window could come only from wrong offsets)
+          const int p = e[i][k] - t_begin;
+          if ((unsigned)p < (unsigned)(t_end - t_begin)) atomicOr(&sh.mem[p >> 1], lists[i].bit << (16 * (p & 1)));
+        }
+    }
   }
 
   // the group's queries as the B operand of QK: lane holds head hc, dims 32ks + 8lq .. +7
@@ -329,8 +379,9 @@ __global__ __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2))) void h
   for (int ws = t_begin; ws < t_end; ws += kWin) {
     const int we = min(ws + kWin, t_end);
 
-    // ---- membership: scan each owned list from its cursor up to we -------
-    {
+    // ---- membership (a single window with list offsets: above) -----------
+    if (!flat) {
+      // scan each owned list from its cursor up to we
       int c[kLPW];
       bool act[kLPW];
 #pragma unroll
