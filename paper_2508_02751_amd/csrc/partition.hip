@@ -277,8 +277,9 @@ struct Row {
   float s[R > 0 ? R : 1];
   int n;
   int nrank;     // tokens ranked: the first nrank (the rest, recent, are kept unranked)
-  __amdgpu_buffer_rsrc_t buf;  // the row's whole allocation (entries past n read
-                               // as whatever is there and are never ranked)
+  __amdgpu_buffer_rsrc_t buf;  // the row's n tokens: slots past them read zero
+                               // without a memory access (a short row of a
+                               // wide variant reads only its own tokens)
 
   __device__ __forceinline__ void set_max(float M) {
     if constexpr (kProb) M64 = 64.0f * plog2(M, pscale);
@@ -290,15 +291,14 @@ struct Row {
     return bin_index(s, M64);
   }
   __device__ __forceinline__ int tok(int q) const { return q * PT + (int)threadIdx.x; }
-  // slots past the allocation read zero (raw buffer view)
+  // slots past the row's tokens read zero (raw buffer view)
   __device__ __forceinline__ float fetch(int q) const {
     return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(buf, (uint32_t)tok(q) * 4u, 0, 0));
   }
   __device__ __forceinline__ void load() {
     if constexpr (R > 0) {
-      const int nq = slots();  // a short row of a wide variant reads only its own slots
 #pragma unroll
-      for (int q = 0; q < R; ++q) s[q] = q < nq ? fetch(q) : 0.0f;
+      for (int q = 0; q < R; ++q) s[q] = fetch(q);
     }
   }
   __device__ __forceinline__ int slots() const { return (n + PT - 1) / PT; }
@@ -320,7 +320,7 @@ struct Row {
         if (q < nq) f(s[q], ranked(q));
     } else {
       // the next slots, in flight while these are used (past the row's end
-      // too: past the allocation they read zero, and are not used)
+      // too: they read zero, and are not used)
       float nx[kGroup];
       if constexpr (kRev) {
         const int last = (nq - 1) / kGroup * kGroup;  // first slot of the last group
@@ -717,8 +717,8 @@ struct Step3 {
     } else {
       // long rows: one exchange per kGroup slots, the next kGroup in flight
       const int nq = row.slots();
-      // (slots past the row's end are read too: past the allocation they
-      // read zero, and no pass uses them)
+      // (slots past the row's end are read too: they read zero, and no
+      // pass uses them)
       float nx[kGroup];
 #pragma unroll
       for (int j = 0; j < kGroup; ++j) nx[j] = row.fetch(j);
@@ -744,7 +744,7 @@ void partition_kernel(PartArgs a) {
   row.n = r.n;
   row.nrank = r.older;
   row.pscale = a.pscale;
-  row.buf = buffer_of(r.lg, 4u * (uint32_t)a.n_cap);
+  row.buf = buffer_of(r.lg, 4u * (uint32_t)r.n);
   row.load();  // in flight while the row's statistics arrive
   row_stats<kMerge>(a, sh, r);
   row.set_max(r.M);
