@@ -15,17 +15,19 @@
 //      exceeds the LDS buffer).  This gives the target key T, how many
 //      tokens equal to T the set takes (the lowest indices) and how many
 //      tokens equal T in all;
-//   3. one ordered pass compacts C and M in ascending token order with
-//      workgroup prefix sums (DPP wave scans), computes p' for marginal
-//      tokens and the masses S'_C, S'_M.  Tie ranks are scanned only when a
-//      threshold's ties are split between two sets.
-// The row is read in slots of PT consecutive tokens, one per thread, so that
-// each wave holds 64 consecutive tokens of a slot: a wave's members of a
-// slot are a ballot, and their list positions are the wave's base plus a
-// masked bit count (mbcnt), with one workgroup exchange of per-wave counts
-// per group of slots.  Rows of up to 16 (20 with 256 threads) slots are read
-// once and kept in registers (one exchange); longer rows are re-read per
-// pass, 16 slots in flight.  Many rows (several per CU) get 256 threads
+//   3. one ordered pass compacts C and M in ascending token order and
+//      computes p' for marginal tokens and the masses S'_C, S'_M.  The row
+//      is read in slots of PT consecutive tokens, one per thread, so a wave
+//      holds 64 consecutive tokens of a slot: its members are lane masks
+//      (ballots of single compares, combined on the scalar unit), and their
+//      list positions are the wave's base plus a masked bit count (mbcnt);
+//      one workgroup exchange of per-(wave, slot) counts per group of slots
+//      gives the bases.  Tie ranks (also mbcnt over a ballot) are counted
+//      only when a threshold's ties are split between two sets.
+// Rows of up to 16 (20 with 256 threads) slots are read once and kept in
+// registers (one exchange); longer rows are re-read per pass, 16 slots in
+// flight, the candidate gather from the row's end (it starts on what the
+// histogram pass read last).  Many rows (several per CU) get 256 threads
 // each, so that more rows are resident; few rows get 512.  The fused variant
 // first combines stage 1's per-chunk records of its head (row max, row sum,
 // the head's output), so a step needs no separate merge launch.
@@ -567,7 +569,7 @@ __device__ __forceinline__ void finish_row(const PartArgs &a, PartShared<PT> &sh
   }
 }
 
-// Step 3 helpers: membership of one value and its output.
+// Step 3: the thresholds as logits, and the output of a wave's members.
 struct Compactor {
   const RowCtx &r;
   Targets t;
@@ -643,11 +645,12 @@ struct Step3 {
   uint32_t carry_c = 0, carry_m = 0, carry_eq_c = 0, carry_eq_p = 0;
 
   // Lane masks of the critical and marginal members among slot q0 + j's
-  // tokens: C = recent | (ranked & above the critical threshold), M = ranked &
-  // above the marginal one, minus C.  Each mask is a ballot of one compare;
-  // the set algebra runs on the scalar unit.  A token equal to a threshold
-  // whose ties are split is in the set if its rank among the row's ties
-  // (token order) is below the set's share of them.
+  // tokens: C = recent | (ranked & at or above the critical threshold), M =
+  // ranked & at or above the marginal one, minus C.  Each mask is a ballot
+  // of one compare; the set algebra runs on the scalar unit.  Where a
+  // threshold's ties are split between two sets, a token equal to it is in
+  // the set only if its rank among the row's ties (token order) is below
+  // the set's share of them.
   template <int G>
   __device__ __forceinline__ void members(const float (&x)[G], int q0, int j, uint32_t tb,
                                           uint64_t &mC, uint64_t &mM) const {
