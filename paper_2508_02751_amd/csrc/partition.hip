@@ -425,28 +425,37 @@ __device__ __forceinline__ Targets select_targets(PartShared<PT> &sh, const RowC
     sh.sel[tid][2] = rr[tid];
   }
   __syncthreads();  // candidates visible
+  // Counting: key k of target x's bin against all n of the bin's keys.
+  auto count = [&](int x, uint32_t k, uint32_t n, uint32_t rank) {
+    const uint32_t key = sh.cand[x][k];
+    uint32_t gt = 0, eq = 0;
+    for (uint32_t c0 = 0; c0 < n; c0 += 8) {  // 8 keys per step, two 16-byte reads
+      const uint4 a = *reinterpret_cast<const uint4 *>(&sh.cand[x][c0]);
+      const uint4 b = *reinterpret_cast<const uint4 *>(&sh.cand[x][c0 + 4]);
+      const uint32_t vs[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
 #pragma unroll
-  for (int x = 0; x < 2; ++x) {
-    if (mode[x] == 0 && (uint32_t)tid < cnt[x]) {
-      const uint32_t key = sh.cand[x][tid];
-      uint32_t gt = 0, eq = 0;
-      for (uint32_t c0 = 0; c0 < cnt[x]; c0 += 8) {  // 8 keys per step, two 16-byte reads
-        const uint4 a = *reinterpret_cast<const uint4 *>(&sh.cand[x][c0]);
-        const uint4 b = *reinterpret_cast<const uint4 *>(&sh.cand[x][c0 + 4]);
-        const uint32_t vs[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const bool ok = c0 + e < cnt[x];
-          gt += ok && vs[e] > key ? 1u : 0u;
-          eq += ok && vs[e] == key ? 1u : 0u;
-        }
-      }
-      if (gt < rr[x] && rr[x] <= gt + eq) {  // every tie of the target writes the same
-        sh.res[x][0] = key;
-        sh.res[x][1] = rr[x] - gt;
-        sh.res[x][2] = eq;
+      for (int e = 0; e < 8; ++e) {
+        const bool ok = c0 + e < n;
+        gt += ok && vs[e] > key ? 1u : 0u;
+        eq += ok && vs[e] == key ? 1u : 0u;
       }
     }
+    if (gt < rank && rank <= gt + eq) {  // every tie of the target writes the same
+      sh.res[x][0] = key;
+      sh.res[x][1] = rank - gt;
+      sh.res[x][2] = eq;
+    }
+  };
+  if (mode[0] == 0 && mode[1] == 0 && cnt[0] + cnt[1] <= (uint32_t)PT) {
+    // both targets at once: target 1's keys on the threads after target 0's
+    const bool second = (uint32_t)tid >= cnt[0];
+    const uint32_t k = second ? (uint32_t)tid - cnt[0] : (uint32_t)tid;
+    const uint32_t n = second ? cnt[1] : cnt[0];
+    if (k < n) count(second ? 1 : 0, k, n, second ? rr[1] : rr[0]);
+  } else {
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+      if (mode[x] == 0 && (uint32_t)tid < cnt[x]) count(x, tid, cnt[x], rr[x]);
   }
   if (mode[0] != 0 || mode[1] != 0) {
     for (int pass = 0; pass < 3; ++pass) {  // digits of 11, 11 and 10 bits
