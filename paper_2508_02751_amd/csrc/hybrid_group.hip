@@ -237,6 +237,8 @@ __device__ __forceinline__ void lower_bounds(const ListRef (&l)[kLPW], int targe
   }
 }
 
+// kResolved: slot maps into a store of at most 65536 rows (see below)
+template <bool kResolved>
 __global__ __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2))) void hybrid_group_kernel(GroupArgs a) {
   __shared__ __align__(16) GroupShared sh;
   const int tid = threadIdx.x, lane = tid & 63;
@@ -370,6 +372,14 @@ __global__ __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2))) void h
   const int32_t *ksl = a.k_slot ? a.k_slot + ua * a.n_cap : nullptr;
   const int32_t *vsl = a.v_slot ? a.v_slot + ua * a.n_cap : nullptr;
   const int last_row = (int)(a.n_rows - 1);
+  // With slot maps into a store of at most 65536 rows, each window's union
+  // rows are looked up before the rows stream: the K row replaces the
+  // position in the row's entry (membership bits above it), the V row goes
+  // to a 16-bit table in the membership words, so the streaming loop reads
+  // both from LDS instead of waiting on two dependent loads per block.
+  constexpr bool resolved = kResolved;
+  constexpr int bit0 = resolved ? 16 : kPosBits;  // membership bits' position in an entry
+  uint16_t *const vrow = reinterpret_cast<uint16_t *>(sh.mem);
 
   f32x4_t acc[kD / 16];
 #pragma unroll
@@ -490,6 +500,33 @@ __global__ __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2))) void h
         if (m) sh.uni[o++] = (m << kPosBits) | (uint32_t)(tid * pc + k);
       }
     }
+    if constexpr (resolved) {
+      // this wave's own rows (written by its own threads above); the
+      // membership words of its positions were cleared above, and no other
+      // wave touches them until the window's end
+      wave_lds_fence();
+      for (int i0 = r0; i0 < r1; i0 += 4 * kWave) {
+        uint32_t e[4];
+        int rk[4], rv[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int i = i0 + j * kWave + lane;
+          e[j] = i < r1 ? sh.uni[i] : 0u;
+          const int tok = ws + (int)(e[j] & (kWin - 1));
+          rk[j] = i < r1 ? ksl[tok] : 0;
+          rv[j] = i < r1 ? vsl[tok] : 0;
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int i = i0 + j * kWave + lane;
+          if (i < r1) {
+            sh.uni[i] = ((e[j] >> kPosBits) << 16) | (uint32_t)clampi(rk[j], 0, last_row);
+            vrow[i] = (uint16_t)clampi(rv[j], 0, last_row);
+          }
+        }
+      }
+      wave_lds_fence();
+    }
     // element index in marg_prob of the next marginal entry of each head
     // (wave-uniform: kept in SGPRs)
     int mpos[kMaxG];
@@ -516,6 +553,12 @@ __global__ __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2))) void h
       const int own = rb + (lane & 31);
       const bool valid = own < r1;
       const uint32_t e = valid ? sh.uni[own] : 0u;
+      if constexpr (resolved) {
+        bits = e >> 16;
+        rk = (int)(e & 0xffffu);
+        rv = valid ? (int)vrow[own] : 0;
+        return;
+      }
       bits = e >> kPosBits;
       const int tok = ws + (int)(e & (kWin - 1));
       rk = tok;
@@ -604,7 +647,7 @@ __global__ __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2))) void h
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const uint32_t uu = sh.uni[min(rr + i, kWin - 1)];
-          const bool cb = hc < g && rr + i < r1 && ((uu >> (kPosBits + hc)) & 1u);
+          const bool cb = hc < g && rr + i < r1 && ((uu >> (bit0 + hc)) & 1u);
           sv[h][i] = cb ? s[h][i] * a.scale : -INFINITY;
           bmax = fmaxf(bmax, sv[h][i]);
         }
@@ -679,6 +722,13 @@ __global__ __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2))) void h
           acc[nq + i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pl, B[i], acc[nq + i], 0, 0, 0);
       }
       wave_lds_fence();
+    }
+    if (resolved && we < t_end) {
+      // the next window's membership goes into the words the V rows used:
+      // each wave clears its own (only it reads them), then all wait, so
+      // that no wave's membership writes meet another's clearing
+      for (int i = (r0 >> 1) + lane; i < (r1 + 1) >> 1; i += kWave) sh.mem[i] = 0u;
+      __syncthreads();
     }
   }
 
@@ -852,7 +902,10 @@ hipError_t launch_hybrid_group(const smallkv_batch_t &b, const smallkv_model_t &
   a.nblk = list_blocks(b);
   a.out = m.out;
   const int groups = (a.units + kXcd - 1) / kXcd;
-  hipLaunchKernelGGL(hybrid_group_kernel, dim3(groups * kXcd * a.n_split), dim3(kGT), 0, st, a);
+  if (m.k_slot && m.n_rows <= 65536)
+    hipLaunchKernelGGL(hybrid_group_kernel<true>, dim3(groups * kXcd * a.n_split), dim3(kGT), 0, st, a);
+  else
+    hipLaunchKernelGGL(hybrid_group_kernel<false>, dim3(groups * kXcd * a.n_split), dim3(kGT), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.n_split == 1) return e;
   hipLaunchKernelGGL(hybrid_group_merge, dim3(a.units * a.g), dim3(kD), 0, st, a);
