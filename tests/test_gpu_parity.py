@@ -384,6 +384,27 @@ def test_compact_store_with_slot_maps(dtype):
     compare_step(ps.buf, ref, x, w.torch_dtype, f"compact-{dtype}")
 
 
+def test_compact_store_of_more_than_65536_rows():
+    """A store padded past 65536 rows per kv head: the grouped stage 3 then
+    looks its slot maps up per block instead of resolving them per window
+    into 16-bit LDS entries; both give the full-cache result."""
+    w = custom("compact-wide", 111, 2, 1200, "bf16", SMALL, LARGE, ("pct", 5), ("pct", 15),
+               ragged_min=600)
+    x = W.make_step_inputs(w, DEV)
+    ref_full = oracle_step(x, S.NORM_REMAINING)
+    ck, cv, ks, vs = compact_store(x, ref_full)
+    pad = 65600 - ck.shape[3]
+    zk = torch.zeros(ck.shape[:3] + (pad, ck.shape[4]), dtype=ck.dtype, device=ck.device)
+    wk, wv = torch.cat([ck, zk], 3), torch.cat([cv, zk], 3)
+    log(f"[parity] compact store rows {ck.shape[3]} padded to {wk.shape[3]}")
+    ps = prepare_step(x, k_slot=ks, v_slot=vs, l_k=wk, l_v=wv)
+    ps.run()
+    torch.cuda.synchronize()
+    ref = oracle_step(x, S.NORM_REMAINING, k_slot=ks, v_slot=vs, l_k=ck, l_v=cv)
+    np.testing.assert_array_equal(ref["large_out"], ref_full["large_out"])
+    compare_step(ps.buf, ref, x, w.torch_dtype, "compact-wide")
+
+
 # ------------------------------------------------------- group selection --
 
 def group_sel(x):
