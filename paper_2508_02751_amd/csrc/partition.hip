@@ -54,11 +54,18 @@ struct Hist {
   static constexpr int size = pad ? kBins + kBins / 8 : kBins;
   static __device__ __forceinline__ int idx(int b) { return pad ? b + (b >> 5) * 4 : b; }
 };
-constexpr int kCap = 2048;       // candidate keys per target kept in LDS
 template <int PT>
 struct PC {
   static constexpr int waves = PT / kWave;
+  // candidate keys per target kept in LDS: 1024 in the 256-thread rows, so
+  // that five long rows fit a CU's LDS
+  static constexpr int cap = PT == 256 ? 1024 : 2048;
 };
+// Rows resident per CU: five for the long 256-thread rows (the many-row
+// launches, where more rows in flight hide the passes' latency: 96 VGPRs),
+// four otherwise (the register rows need up to 128 VGPRs).
+template <int R, int PT>
+constexpr int rows_per_cu() { return R == 0 && PT == 256 ? 5 : 4; }
 // Slots of a long row per workgroup exchange (and in flight while a group is
 // compacted)
 constexpr int kGroup = 16;
@@ -182,7 +189,7 @@ __device__ __forceinline__ void find_digit(const uint32_t *hist, uint32_t rr, in
 template <int PT>
 struct alignas(16) PartShared {
   uint32_t hist[2][Hist<PT>::size];  // bin b at Hist<PT>::idx(b)
-  uint32_t cand[2][kCap];
+  uint32_t cand[2][PC<PT>::cap];
   uint32_t sel[2][4];  // radix: prefix, mask, remaining rank, count of T
   uint32_t res[2][4];  // counting: key, ties taken, ties in all
   uint32_t ncand[2];
@@ -392,7 +399,7 @@ __device__ __forceinline__ Targets select_targets(PartShared<PT> &sh, const RowC
   // 0: rank by counting, 1: radix over LDS candidates, 2: radix over the row
   int mode[2];
 #pragma unroll
-  for (int x = 0; x < 2; ++x) mode[x] = cnt[x] <= (uint32_t)PT ? 0 : (cnt[x] <= (uint32_t)kCap ? 1 : 2);
+  for (int x = 0; x < 2; ++x) mode[x] = cnt[x] <= (uint32_t)PT ? 0 : (cnt[x] <= (uint32_t)PC<PT>::cap ? 1 : 2);
   if (mode[0] < 2 || mode[1] < 2) {
     const uint64_t lt = lanemask_lt();
     // distance indices of the bins gathered (-1: none)
@@ -747,7 +754,7 @@ struct Step3 {
 };
 
 template <bool kMerge, int R, int PT, bool kRecent, bool kProb = false>
-__global__ __launch_bounds__(PT) __attribute__((amdgpu_waves_per_eu(4)))
+__global__ __launch_bounds__(PT) __attribute__((amdgpu_waves_per_eu(rows_per_cu<R, PT>())))
 void partition_kernel(PartArgs a) {
   __shared__ PartShared<PT> sh;
   RowCtx r;

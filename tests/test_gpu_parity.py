@@ -95,14 +95,26 @@ def test_ties_from_duplicated_keys(dtype):
 def test_constant_logits(n):
     """Every small key equal, so every logit of a row ties: the lowest indices
     fill C, then M.  One sub-bin holds the whole row, which sends the select
-    to its general path (candidates in LDS up to 2048 keys, else the row)."""
+    to its general path (candidates in LDS up to 2048 keys at this row
+    width, else the row)."""
     w = custom(f"const-{n}", 115, 2, n, "bf16", SMALL, LARGE, ("pct", 10), ("pct", 25))
+    run_case(w, mutate=flat_small_keys)
 
-    def flat(x):
-        k = x["s_k"]
-        x["s_k"] = k[:, :, :, :1].expand_as(k).contiguous()
 
-    run_case(w, mutate=flat)
+def flat_small_keys(x):
+    k = x["s_k"]
+    x["s_k"] = k[:, :, :, :1].expand_as(k).contiguous()
+
+
+@pytest.mark.parametrize("n", [800, 1500, 6000])
+def test_constant_logits_many_rows(n):
+    """The same ties over 1024 rows, so 256 threads per row, whose LDS holds
+    up to 1024 candidate keys: the whole-row bin is ranked in LDS at 800
+    tokens, over the row at 1500, and over a row re-read per pass (five rows
+    per CU) at 6000."""
+    small = W.ModelShape(4, 16, 4, 64)
+    w = custom(f"const-many-{n}", 117, 16, n, "bf16", small, LARGE, ("pct", 10), ("pct", 25))
+    run_case(w, mutate=flat_small_keys)
 
 
 @pytest.mark.parametrize("n", [1500, 3000])
