@@ -163,6 +163,14 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_of(const void *p, int b
 __device__ __forceinline__ uint4 bload16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
   return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
 }
+// The same, non-temporal (cache policy NT): for the V rows, which each
+// instruction reads whole and nothing reads again, so that they do not
+// evict lines still in use.  (The K rows are read half a line per
+// instruction, the other half by the next: those stay cached.)
+constexpr int kCpolNT = 2;
+__device__ __forceinline__ uint4 bload16_stream(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kCpolNT));
+}
 
 // The list a wave owns in slot i: L = wave + kGW * i; L < g is head L's
 // critical list, g <= L < 2g head (L - g)'s marginal list.
@@ -602,7 +610,7 @@ __global__ __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2))) void h
       for (int k = 0; k < 8; ++k) {
         const int src = lq * 8 + k;
         const int row = __shfl(rv, src, kWave);
-        vr[k] = bload16(vbuf, rb + src < r1 ? (uint32_t)row * kRowB + hc * 16 : kOOB);
+        vr[k] = bload16_stream(vbuf, rb + src < r1 ? (uint32_t)row * kRowB + hc * 16 : kOOB);
       }
     };
     if (r0 < r1) {

@@ -167,6 +167,16 @@ constexpr int head_shift() {
   return GP == 4 ? 4 : (GP == 8 ? 3 : 2);
 }
 
+// A 16-byte piece of the small cache, which a step reads exactly once:
+// loaded non-temporally, so that streaming 17 GB of K and V through the
+// caches does not evict the logits this kernel writes for the partition
+// (LLaMA step: stage 1 3.73 -> 3.49 ms with the same pages).
+typedef __attribute__((ext_vector_type(4))) unsigned int u32x4_t;
+__device__ __forceinline__ uint4 stream16(const unsigned char *p) {
+  const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(p));
+  return make_uint4(v[0], v[1], v[2], v[3]);
+}
+
 template <typename T, int D>
 __device__ __forceinline__ void stage_k(unsigned char *tile, const unsigned char *src, int nr) {
   using C = SmallCfg<T, D>;
@@ -175,8 +185,7 @@ __device__ __forceinline__ void stage_k(unsigned char *tile, const unsigned char
     const int x = threadIdx.x + r * kThreads;
     const int row = x / C::V16, w = x % C::V16;
     if (row < nr)
-      *reinterpret_cast<uint4 *>(tile + row * C::ROWS + w * 16) =
-          *reinterpret_cast<const uint4 *>(src + (int64_t)row * C::ROWB + w * 16);
+      *reinterpret_cast<uint4 *>(tile + row * C::ROWS + w * 16) = stream16(src + (int64_t)row * C::ROWB + w * 16);
   }
 }
 
@@ -235,7 +244,7 @@ __global__ __launch_bounds__(kThreads) void small_attn_mfma(SmallArgs a) {
     for (int r = 0; r < KR; ++r) {
       const int x = tid + r * kThreads;
       const int row = x / C::V16, w = x % C::V16;
-      kpre[r] = row < n ? *reinterpret_cast<const uint4 *>(kb + (int64_t)(t + row) * C::ROWB + w * 16)
+      kpre[r] = row < n ? stream16(kb + (int64_t)(t + row) * C::ROWB + w * 16)
                         : make_uint4(0u, 0u, 0u, 0u);
     }
   };
@@ -341,7 +350,7 @@ __global__ __launch_bounds__(kThreads) void small_attn_mfma(SmallArgs a) {
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
       const int tok = tb8 * 8 + k;
-      vr[k] = tok < nr ? *reinterpret_cast<const uint4 *>(vb + (int64_t)(tb + tok) * C::ROWB + dc * 16)
+      vr[k] = tok < nr ? stream16(vb + (int64_t)(tb + tok) * C::ROWB + dc * 16)
                        : make_uint4(0u, 0u, 0u, 0u);
     }
     __syncthreads();  // K tile no longer read; red visible
