@@ -681,14 +681,15 @@ SmallPlan plan_small(const smallkv_batch_t &b, const smallkv_model_t &m) {
   // chunks pipeline their tiles, more of them only add merge records; at
   // least four tiles per chunk when that still gives every CU a workgroup,
   // so that the next tile's K loads overlap the current tile's arithmetic
-  // (a one-tile chunk loads, then computes); and at most 64 tiles, so that
-  // long rows give enough workgroups that the last round of them is a small
-  // part of the launch
+  // (a one-tile chunk loads, then computes); and rows of more than 32 tiles
+  // in chunks of at most 16, so that long rows give enough workgroups that
+  // the last round of them is a small part of the launch (rows of up to 17
+  // tiles, as in a batch of many short sequences, are fastest unsplit)
   const int want = (int)((1536 + units - 1) / units);
   int ns = want < 1 ? 1 : (want > max_split ? max_split : want);
   const int four = max_split / 4 < 1 ? 1 : max_split / 4;
   if (units * four >= 256 && ns > four) ns = four;
-  const int least = (max_split + 63) / 64;
+  const int least = max_split > 32 ? (max_split + 15) / 16 : 1;
   if (ns < least) ns = least;
   if (ns > kMaxChunks) ns = kMaxChunks;
   const int per = (b.n_cap + ns - 1) / ns;
