@@ -57,15 +57,16 @@ struct Hist {
 template <int PT>
 struct PC {
   static constexpr int waves = PT / kWave;
-  // candidate keys per target kept in LDS: 1024 in the 256-thread rows, so
-  // that five long rows fit a CU's LDS
-  static constexpr int cap = PT == 256 ? 1024 : 2048;
 };
-// Rows resident per CU: five for the long 256-thread rows (the many-row
-// launches, where more rows in flight hide the passes' latency: 96 VGPRs),
+// Rows resident per CU: six for the long 256-thread rows (the many-row
+// launches, where more rows in flight hide the passes' latency: 80 VGPRs),
 // four otherwise (the register rows need up to 128 VGPRs).
 template <int R, int PT>
-constexpr int rows_per_cu() { return R == 0 && PT == 256 ? 5 : 4; }
+constexpr int rows_per_cu() { return R == 0 && PT == 256 ? 6 : 4; }
+// Candidate keys per target kept in LDS: 512 in the long 256-thread rows,
+// so that six of them fit a CU's LDS, else 2048.
+template <int R, int PT>
+constexpr int cand_cap() { return R == 0 && PT == 256 ? 512 : 2048; }
 // Slots of a long row per workgroup exchange (and in flight while a group is
 // compacted)
 constexpr int kGroup = 16;
@@ -186,10 +187,11 @@ __device__ __forceinline__ void find_digit(const uint32_t *hist, uint32_t rr, in
   above = __shfl(ab, src, kWave);
 }
 
-template <int PT>
+template <int PT, int CAP>
 struct alignas(16) PartShared {
+  static constexpr int cap = CAP;
   uint32_t hist[2][Hist<PT>::size];  // bin b at Hist<PT>::idx(b)
-  uint32_t cand[2][PC<PT>::cap];
+  uint32_t cand[2][CAP];
   uint32_t sel[2][4];  // radix: prefix, mask, remaining rank, count of T
   uint32_t res[2][4];  // counting: key, ties taken, ties in all
   uint32_t ncand[2];
@@ -235,8 +237,8 @@ __device__ __forceinline__ void row_setup(const PartArgs &a, RowCtx &r) {
 
 // Row max and sum: combined from stage 1's chunk records (fused; also writes
 // the head's output) or read back.
-template <bool kMerge, int PT>
-__device__ __forceinline__ void row_stats(const PartArgs &a, PartShared<PT> &sh, RowCtx &r) {
+template <bool kMerge, int PT, int CAP>
+__device__ __forceinline__ void row_stats(const PartArgs &a, PartShared<PT, CAP> &sh, RowCtx &r) {
   if constexpr (kMerge) {
     const int b = r.row / a.nsh, j = r.row % a.nsh, layer = j / a.hq, h = j % a.hq;
     const int unit = (b * a.layers + layer) * a.hkv + h / a.g, i = h % a.g;
@@ -371,8 +373,8 @@ struct Targets {
 };
 
 // Steps 1 and 2.
-template <int PT, typename Row>
-__device__ __forceinline__ Targets select_targets(PartShared<PT> &sh, const RowCtx &r, const Row &row) {
+template <int PT, int CAP, typename Row>
+__device__ __forceinline__ Targets select_targets(PartShared<PT, CAP> &sh, const RowCtx &r, const Row &row) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   // The targets' ranks count ranked (older) tokens only.  Rank 0 -- no
   // ranked token in the set -- is resolved as rank 1 and then replaced by a
@@ -399,7 +401,7 @@ __device__ __forceinline__ Targets select_targets(PartShared<PT> &sh, const RowC
   // 0: rank by counting, 1: radix over LDS candidates, 2: radix over the row
   int mode[2];
 #pragma unroll
-  for (int x = 0; x < 2; ++x) mode[x] = cnt[x] <= (uint32_t)PT ? 0 : (cnt[x] <= (uint32_t)PC<PT>::cap ? 1 : 2);
+  for (int x = 0; x < 2; ++x) mode[x] = cnt[x] <= (uint32_t)PT ? 0 : (cnt[x] <= (uint32_t)CAP ? 1 : 2);
   if (mode[0] < 2 || mode[1] < 2) {
     const uint64_t lt = lanemask_lt();
     // distance indices of the bins gathered (-1: none)
@@ -529,8 +531,8 @@ __device__ __forceinline__ Targets select_targets(PartShared<PT> &sh, const RowC
 // per slot with readlane), and the group's totals.  Lane j sums slot j over
 // the waves; one wave scan orders the slots.  One barrier; `buf` alternates
 // so that the next exchange can write while slow waves still read this one.
-template <int G, int PT>
-__device__ __forceinline__ uint32_t exchange(PartShared<PT> &sh, int buf, const uint32_t *cnt,
+template <int G, int PT, int CAP>
+__device__ __forceinline__ uint32_t exchange(PartShared<PT, CAP> &sh, int buf, const uint32_t *cnt,
                                              uint32_t &total) {
   constexpr int kWaves = PC<PT>::waves;
   static_assert(G <= kMaxSlots && G <= kWave, "slots per exchange");
@@ -557,8 +559,8 @@ __device__ __forceinline__ uint32_t mbcnt(uint64_t m, uint32_t base) {
   return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, base));
 }
 
-template <int PT>
-__device__ __forceinline__ void finish_row(const PartArgs &a, PartShared<PT> &sh, const RowCtx &r,
+template <int PT, int CAP>
+__device__ __forceinline__ void finish_row(const PartArgs &a, PartShared<PT, CAP> &sh, const RowCtx &r,
                                            float sc, float sm) {
   constexpr int kWaves = PC<PT>::waves;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -651,7 +653,7 @@ __device__ __forceinline__ void offsets(const PartArgs &a, const RowCtx &r, int 
 // first), then each wave writes its members at its base + mbcnt.
 template <int R, int PT, bool kRecent, bool kProb, bool kSplit, bool kHeld>
 struct Step3 {
-  PartShared<PT> &sh;
+  PartShared<PT, cand_cap<R, PT>()> &sh;
   const PartArgs &a;
   const RowCtx &r;
   const Row<R, PT, kRecent, kProb> &row;
@@ -756,7 +758,7 @@ struct Step3 {
 template <bool kMerge, int R, int PT, bool kRecent, bool kProb = false>
 __global__ __launch_bounds__(PT) __attribute__((amdgpu_waves_per_eu(rows_per_cu<R, PT>())))
 void partition_kernel(PartArgs a) {
-  __shared__ PartShared<PT> sh;
+  __shared__ PartShared<PT, cand_cap<R, PT>()> sh;
   RowCtx r;
   row_setup(a, r);
   Row<R, PT, kRecent, kProb> row;

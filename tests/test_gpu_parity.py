@@ -106,15 +106,31 @@ def flat_small_keys(x):
     x["s_k"] = k[:, :, :, :1].expand_as(k).contiguous()
 
 
-@pytest.mark.parametrize("n", [800, 1500, 6000])
+@pytest.mark.parametrize("n", [800, 3000, 6000])
 def test_constant_logits_many_rows(n):
-    """The same ties over 1024 rows, so 256 threads per row, whose LDS holds
-    up to 1024 candidate keys: the whole-row bin is ranked in LDS at 800
-    tokens, over the row at 1500, and over a row re-read per pass (five rows
-    per CU) at 6000."""
+    """The same ties over 1024 rows, so 256 threads per row: register rows
+    keep up to 2048 candidate keys in LDS (the whole-row bin is ranked there
+    at 800 tokens, over the row at 3000), rows re-read per pass (six per CU)
+    up to 512 (over the row at 6000)."""
     small = W.ModelShape(4, 16, 4, 64)
     w = custom(f"const-many-{n}", 117, 16, n, "bf16", small, LARGE, ("pct", 10), ("pct", 25))
     run_case(w, mutate=flat_small_keys)
+
+
+def test_tied_block_in_long_rows():
+    """Long 256-thread rows (6000 tokens, re-read per pass) where 401 tokens
+    share one key: in the rows whose target falls in that tie, its bin holds
+    between 256 and 512 keys and is ranked in LDS; in the others the targets
+    are counted or ranked as usual."""
+    small = W.ModelShape(4, 16, 4, 64)
+    w = custom("tied-block-6000", 118, 16, 6000, "bf16", small, LARGE, ("pct", 10), ("pct", 25))
+
+    def tie(x):
+        k = x["s_k"].clone()
+        k[:, :, :, 1:401] = k[:, :, :, :1]
+        x["s_k"] = k
+
+    run_case(w, mutate=tie)
 
 
 @pytest.mark.parametrize("n", [1500, 3000])
