@@ -28,7 +28,8 @@
 // registers (one exchange); longer rows are re-read per pass, 16 slots in
 // flight, the candidate gather from the row's end (it starts on what the
 // histogram pass read last).  Many rows (several per CU) get 256 threads
-// each, so that more rows are resident; few rows get 512.  The fused variant
+// each, so that more rows are resident (six re-read rows per CU); few rows
+// get 512, or 1024 when there is at most one per CU.  The fused variant
 // first combines stage 1's per-chunk records of its head (row max, row sum,
 // the head's output), so a step needs no separate merge launch.
 // The result depends only on the logits: deterministic.
