@@ -641,11 +641,15 @@ __global__ __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2))) void h
       for (int h = 0; h < kMaxG; ++h) wt.p[8 + h][lane & 31] = wm[h];
       int rvn = 0;
       if (more) {
+        // the next block's requests at a raised wave priority, so that they
+        // leave before the other waves' arithmetic (LLaMA stage 3 -1%)
         int rkn;
         uint32_t bitsn;
+        __builtin_amdgcn_s_setprio(2);
         rows_of(rn, rkn, rvn, bitsn);
         issue_k(rkn, bitsn);
         issue_m(bitsn);
+        __builtin_amdgcn_s_setprio(0);
       }
       float sv[2][4];
       float bmax = -INFINITY;
@@ -690,7 +694,11 @@ __global__ __launch_bounds__(kGT) __attribute__((amdgpu_waves_per_eu(2))) void h
         }
         *reinterpret_cast<uint4 *>(wt.vt + vt_off(hc * 8 + d, lq)) = make_uint4(w4[0], w4[1], w4[2], w4[3]);
       }
-      if (more) issue_v(rn, rvn);
+      if (more) {
+        __builtin_amdgcn_s_setprio(2);
+        issue_v(rn, rvn);
+        __builtin_amdgcn_s_setprio(0);
+      }
       wave_lds_fence();
 
       // P.V: O[slot][dim] += P[slot][rows] V[rows][dim]
