@@ -163,11 +163,12 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_of(const void *p, int b
 __device__ __forceinline__ uint4 bload16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
   return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
 }
-// The same, non-temporal (cache policy NT): for the V rows, which each
-// instruction reads whole and nothing reads again, so that they do not
-// evict lines still in use.  (The K rows are read half a line per
-// instruction, the other half by the next: those stay cached.)
-constexpr int kCpolNT = 2;
+// The same, non-temporal and past the first-level cache (cache policy
+// SC0 | NT): for the V rows, which each instruction reads whole and nothing
+// reads again, so that they do not evict lines still in use.  (The K rows
+// are read half a line per instruction, the other half by the next: those
+// stay cached.)
+constexpr int kCpolNT = 3;
 __device__ __forceinline__ uint4 bload16_stream(__amdgpu_buffer_rsrc_t r, uint32_t off) {
   return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kCpolNT));
 }
